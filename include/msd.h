@@ -1,0 +1,218 @@
+/*
+ * msd.h -- C ABI of the MI355X (gfx950) multimodal speculative decoding
+ * (MSD) decode path.
+ *
+ * One decode cycle of MSD (arXiv 2505.14260) at temperature 0:
+ *   msd_draft_tree      the one-layer draft head builds a token tree from the
+ *                       decoupled draft input (Sec. 4.1, Eq. decouple) with
+ *                       tree-structured drafting (Sec. 3.2);
+ *   msd_verify          the target runs one tree-masked forward over the tree
+ *                       (Sec. 3.2, verification phase);
+ *   msd_accept_compact  greedy longest-path acceptance plus the bonus token
+ *                       (Sec. 3.2 acceptance rule with a one-hot target) and
+ *                       in-place compaction of the target KV cache.
+ * msd_prefill processes the interleaved visual + text prompt (Sec. 3.1).
+ *
+ * Conventions
+ *  - Every pointer named *_d is device memory owned by the caller; the
+ *    library never allocates or frees device memory.  *_h pointers are host.
+ *  - Weights are bfloat16 (raw 16-bit patterns), row-major [out][in], no
+ *    biases.  Norm gains are bfloat16 [d].
+ *  - All device work is enqueued on the stream given to msd_create, in order.
+ *    Only msd_prefill and msd_accept_compact wait for the stream (to return
+ *    host outputs).  A context serves one stream and is not thread-safe.
+ *  - Return value: MSD_OK (0) or a negative MSD_ERR_*; msd_last_error()
+ *    returns a message for the last failure on that context (or of
+ *    msd_create when ctx is NULL).
+ */
+#ifndef MSD_H
+#define MSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  MSD_OK = 0,
+  MSD_ERR_INVALID_ARG = -1, /* null pointer, shape beyond limits, bad tree  */
+  MSD_ERR_CAPACITY = -2,    /* the KV cache cannot hold the request          */
+  MSD_ERR_STATE = -3,       /* call out of order (e.g. verify before prefill)*/
+  MSD_ERR_HIP = -4          /* a HIP runtime call failed                     */
+};
+
+/* Llama-style decoder shape (the target; the draft layer uses the same). */
+typedef struct msd_model_desc {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;     /* query heads */
+  int32_t n_kv_heads;  /* key/value heads (n_heads % n_kv_heads == 0) */
+  int32_t head_dim;    /* must be 128 or 64 */
+  int32_t ffn_dim;
+  int32_t vocab;
+  float rope_theta;
+  float norm_eps;
+} msd_model_desc;
+
+typedef struct msd_limits {
+  int32_t max_batch;   /* sequences decoded together (<= 8) */
+  int32_t max_seq;     /* KV slots per sequence: prompt + generated + tree */
+  int32_t max_tree;    /* nodes per tree including the root (<= 64) */
+  int32_t max_prompt;  /* rows of one prefill */
+} msd_limits;
+
+typedef struct msd_layer_weights {
+  const void *wq, *wk, *wv, *wo;   /* [H*hd][d], [KV*hd][d] x2, [d][H*hd] */
+  const void *w_gate, *w_up;       /* [F][d] */
+  const void *w_down;              /* [d][F] */
+  const void *attn_norm, *ffn_norm;/* [d] */
+} msd_layer_weights;
+
+typedef struct msd_target_weights {
+  const void* embed;                 /* [V][d] token embedding E_t */
+  const msd_layer_weights* layers;   /* host array of n_layers entries */
+  const void* final_norm;            /* [d] */
+  const void* lm_head;               /* [V][d] projection head */
+} msd_target_weights;
+
+/* One-layer draft head: f_down [d][2d] acting on Concat(h, e) (h first),
+ * one decoder layer, then the target's LM head. */
+typedef struct msd_draft_weights {
+  const void* fc;
+  msd_layer_weights layer;
+} msd_draft_weights;
+
+/*
+ * Caller-owned device buffers (sizes from msd_buffer_sizes).
+ *  target_k: per layer, per sequence, per kv head: [max_seq][head_dim] bf16
+ *            i.e. index ((layer*B + b)*KV + g)*max_seq*hd + slot*hd + e
+ *  target_v: same blocks, transposed: [head_dim][max_seq] bf16
+ *            i.e. index ((layer*B + b)*KV + g)*hd*max_seq + e*max_seq + slot
+ *  draft_k / draft_v: the same layouts with one layer.
+ *  workspace: scratch, contents undefined between calls except the library's
+ *            own per-sequence state that it keeps there.
+ */
+typedef struct msd_buffers {
+  void *target_k, *target_v, *draft_k, *draft_v, *workspace;
+} msd_buffers;
+
+/* Draft-tree shape for one decode cycle.
+ *  STATIC: n_nodes drafted nodes (root excluded) given in canonical order
+ *          (depth ascending); node i (1-based) has parent parent[i-1]
+ *          (0 = root) and is the rank[i-1]-th best token of its parent's
+ *          draft distribution.  Siblings have distinct ranks.
+ *  DYNAMIC: depth levels, topk children per expanded node, topk frontier
+ *          nodes per depth ranked by cumulative draft log-probability,
+ *          n_nodes best candidates of the pool kept (Sec. 3.2 tree drafting,
+ *          breadth-wise expansion).  Ties: score descending, then creation
+ *          order.  Requires topk*(depth-1) <= 64 and n_nodes + 1 <= max_tree. */
+enum { MSD_TREE_STATIC = 0, MSD_TREE_DYNAMIC = 1 };
+typedef struct msd_tree_spec {
+  int32_t kind;
+  int32_t n_nodes;
+  int32_t depth;
+  int32_t topk;            /* DYNAMIC only */
+  const int32_t* parent;   /* STATIC only, host, [n_nodes] */
+  const int32_t* rank;     /* STATIC only, host, [n_nodes] */
+} msd_tree_spec;
+
+/* Device-resident token tree of one sequence.  Node 0 is the root (the last
+ * emitted token, not yet in the cache); nodes are in canonical order so
+ * parent[i] < i.  anc[i] has bit j set iff node j is node i or an ancestor. */
+#define MSD_MAX_TREE 64
+typedef struct msd_tree {
+  int32_t n_nodes;                 /* including the root */
+  int32_t token[MSD_MAX_TREE];
+  int32_t parent[MSD_MAX_TREE];    /* -1 for the root */
+  int32_t depth[MSD_MAX_TREE];
+  float score[MSD_MAX_TREE];       /* cumulative draft log-prob (DYNAMIC) */
+  uint64_t anc[MSD_MAX_TREE];
+} msd_tree;
+
+typedef struct msd_ctx msd_ctx;
+
+/* Byte sizes of the caller-owned buffers for this shape and these limits. */
+int msd_buffer_sizes(const msd_model_desc* m, const msd_limits* lim,
+                     size_t* target_kv_bytes /* each of K and V */,
+                     size_t* draft_kv_bytes /* each of K and V */,
+                     size_t* workspace_bytes);
+
+/* Creates a context over caller-owned weights and buffers (device pointers
+ * must stay valid until msd_destroy).  stream: a hipStream_t (NULL = the
+ * null stream).  Initialises the workspace and zeroes the four KV caches
+ * (enqueued on the stream, waited for before returning). */
+int msd_create(const msd_model_desc* m, const msd_limits* lim,
+               const msd_target_weights* tw, const msd_draft_weights* dw,
+               const msd_buffers* bufs, void* stream, msd_ctx** out);
+void msd_destroy(msd_ctx* ctx);
+const char* msd_last_error(const msd_ctx* ctx);
+
+/*
+ * Prompt processing for sequence `seq` (Sec. 3.1): n rows, row i is the text
+ * token tokens_h[i] (embedded with E_t) when is_visual_h[i] == 0, otherwise
+ * the next unused row of visual_d ([n_visual][d] bf16, in prompt order).
+ * The prompt must end in a text token (the draft's text rows need the next
+ * token's embedding).  Runs the target over the prompt (causal), fills the
+ * target KV slots [0, n), stores the features of every row as pending draft
+ * inputs and returns the first generated token (greedy) in *first_token_h.
+ * Waits for the stream.  Resets the sequence.
+ */
+int msd_prefill(msd_ctx* ctx, int seq, int n, const int32_t* tokens_h,
+                const uint8_t* is_visual_h, const void* visual_d,
+                int32_t* first_token_h);
+
+/*
+ * Draft phase for sequences seqs_h[0..n_seq): runs the pending rows through
+ * the draft head (text: f_down(Concat(h_i, e_{i+1})); visual: e_i), then
+ * builds the tree of `spec` depth by depth.  Writes one msd_tree per
+ * sequence to trees_d[0..n_seq).  All sequences use the same spec.
+ */
+int msd_draft_tree(msd_ctx* ctx, int n_seq, const int32_t* seqs_h,
+                   const msd_tree_spec* spec, msd_tree* trees_d);
+
+/*
+ * Verification: the target runs over the n_nodes tree tokens of each
+ * sequence (node i at position L + depth[i], cache slot L + i) with the
+ * ancestor mask, L being the sequence's committed length.  Writes the greedy
+ * token of every node to argmax_d [n_seq][n_nodes] (lowest id on ties) and,
+ * when logits_d is not NULL, the logits to logits_d [n_seq][n_nodes][V]
+ * float32.  The tree rows' KV stay in slots [L, L+n_nodes) until
+ * msd_accept_compact.
+ */
+int msd_verify(msd_ctx* ctx, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,
+               int n_nodes, int32_t* argmax_d, float* logits_d);
+
+/*
+ * Acceptance and compaction: for each sequence, the deepest node whose every
+ * token on the root path equals its parent's argmax is accepted; emitted
+ * tokens are the accepted drafted tokens followed by the bonus token (the
+ * argmax of the deepest accepted node).  KV rows L+path[j] move to L+j for
+ * every layer (all reads before any write); slot_map_d [n_seq][MSD_MAX_TREE]
+ * receives L+path[j] (-1 past the path).  The accepted nodes' target
+ * features become the next pending draft rows and L grows by len(path).
+ * emitted_h [n_seq][MSD_MAX_TREE] and n_emitted_h [n_seq] are host outputs;
+ * waits for the stream.
+ */
+int msd_accept_compact(msd_ctx* ctx, int n_seq, const int32_t* seqs_h,
+                       const msd_tree* trees_d, int n_nodes, const int32_t* argmax_d,
+                       int32_t* emitted_h, int32_t* n_emitted_h, int32_t* slot_map_d);
+
+/* Committed KV length of a sequence (host-side bookkeeping), or < 0. */
+int msd_seq_len(const msd_ctx* ctx, int seq);
+
+/*
+ * Sets a sequence's committed length without running the prompt, for callers
+ * that filled the target KV cache slots [0, L) themselves (cache import).
+ * The pending draft rows become the single text row (h_d [d] bf16, the
+ * target feature of position L-1; next_token = the token at position L, which
+ * is also the next tree root).  The draft cache is not touched: the caller
+ * fills draft slots [0, L-1) as well, or accepts whatever they hold.
+ */
+int msd_set_state(msd_ctx* ctx, int seq, int L, const void* h_d, int32_t next_token);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MSD_H */

@@ -357,16 +357,21 @@ def msd_generate(m: Models, prompt, shape, n_new, static_arrays=None, max_slots=
     return out[:n_new], cycles
 
 
-def greedy_generate(m: Models, prompt, n_new, max_slots=None):
-    """Plain greedy decoding of the target: the sequence MSD must reproduce."""
+def greedy_generate(m: Models, prompt, n_new, max_slots=None, return_logits=False):
+    """Plain greedy decoding of the target: the sequence MSD must reproduce.
+
+    With return_logits, also returns the logits row each token was chosen from.
+    """
     tokens, is_visual, visual = prompt
     max_slots = max_slots or (len(tokens) + n_new + 8)
-    st, first, _, _ = prefill(m, tokens, is_visual, visual, max_slots)
+    st, first, _, lg = prefill(m, tokens, is_visual, visual, max_slots)
     out = [first]
+    rows = [lg[-1]]
     while len(out) < n_new:
         x = M.embed_rows(m.w, [out[-1]])
         pos = np.array([st.L], dtype=np.int32)
         _, logits = M.target_forward(m.dims, m.w, st.kv, x, pos, pos, st.L, 1, None)
         st.L += 1
         out.append(int(np.argmax(logits[0])))
-    return out
+        rows.append(logits[0])
+    return (out, np.stack(rows)) if return_logits else out

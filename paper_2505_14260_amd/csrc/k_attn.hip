@@ -1,0 +1,285 @@
+// Attention over the KV cache on gfx950 MFMA.
+//
+// Tree mode (verification and draft expansion): every query row sees the
+// whole prefix [0, P) of its sequence and the slots of region [P, P+R) whose
+// bit is set in its 64-bit ancestor mask (tree-structured attention of the
+// draft/verify phases).  Keys are split into chunks; one wave handles one
+// (sequence, kv head, 32-row query tile, key chunk) with an online softmax,
+// and a combine kernel merges the chunks in fixed order.  Query rows of a
+// tile are (node, head-in-group) pairs so a GQA group shares every K/V load.
+// Causal mode (prompt processing): one wave per (sequence, head, 32
+// consecutive query rows) over all keys up to the diagonal.
+//
+// Per 32-key block: S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows,
+// B = Q^T), then O^T += V^T P^T (A = V^T rows of the transposed V cache,
+// B = P^T).  The K rows feeding MFMA row i are key pi(i) (bits 2 and 3 of i
+// swapped), which makes each lane's eight P values of the second product
+// correspond to eight consecutive keys, i.e. one 16-byte load of V^T.
+#include "msd_internal.h"
+
+namespace msd {
+
+namespace {
+
+MSD_DEV int perm_key(int x) { return (x & ~12) | ((x & 4) << 1) | ((x & 8) >> 1); }
+
+MSD_DEV float wave_xor32_max(float v) { return fmaxf(v, __shfl_xor(v, 32)); }
+MSD_DEV float wave_xor32_sum(float v) { return v + __shfl_xor(v, 32); }
+
+template <int HD>
+struct AttnState {
+  f32x16 o[HD / 32];
+  float m, l;
+};
+
+// Processes keys [k_begin, k_end) (k_begin multiple of 32) for the wave's 32
+// query columns.  vis(key, j-specific data) decides visibility.
+template <int HD, typename Vis>
+MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qf)[HD / 16],
+                          const uint16_t* kbase, const uint16_t* vbase, int S,
+                          int k_begin, int k_end, int k_valid, float scale, Vis vis) {
+  const int lane = threadIdx.x & 63;
+  const int i = lane & 31, h = lane >> 5;
+  for (int kb = k_begin; kb < k_end; kb += 32) {
+    // ---- S^T tile: rows = keys, columns = query rows
+    const int krow = kb + perm_key(i);
+    const bool kval = krow < k_valid;
+    const uint16_t* kp = kbase + (size_t)(kval ? krow : 0) * HD + (HD / 2) * h;
+    f32x16 s = {};
+#pragma unroll
+    for (int c = 0; c < HD / 16; ++c) {
+      uint4 kv = kval ? *reinterpret_cast<const uint4*>(kp + 8 * c) : make_uint4(0, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[c], s, 0, 0, 0);
+    }
+    float bm = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = kb + perm_key(8 * (r >> 2) + 4 * h + (r & 3));
+      const bool ok = key < k_end && vis(key);
+      s[r] = ok ? s[r] * scale : -INFINITY;
+      bm = fmaxf(bm, s[r]);
+    }
+    bm = wave_xor32_max(bm);
+    const float m_new = fmaxf(st.m, bm);
+    float p[16];
+    float rs = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p[r] = (m_new == -INFINITY) ? 0.f : __expf(s[r] - m_new);
+      rs += p[r];
+    }
+    rs = wave_xor32_sum(rs);
+    const float alpha = (st.m == -INFINITY) ? 0.f : __expf(st.m - m_new);
+    st.l = st.l * alpha + rs;
+    st.m = m_new;
+    uint4 pb[2];
+#pragma unroll
+    for (int pk = 0; pk < 2; ++pk) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)f2bf(p[pk * 8 + 2 * e]) | ((uint32_t)f2bf(p[pk * 8 + 2 * e + 1]) << 16);
+      pb[pk] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    // ---- O^T += V^T P^T
+#pragma unroll
+    for (int dt = 0; dt < HD / 32; ++dt) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
+      const uint16_t* vp = vbase + (size_t)(dt * 32 + i) * S;
+#pragma unroll
+      for (int pk = 0; pk < 2; ++pk) {
+        const int k0 = kb + 16 * pk + 8 * h;
+        uint4 vv;
+        if (k0 + 8 <= k_valid) {
+          vv = *reinterpret_cast<const uint4*>(vp + k0);
+        } else {
+          uint16_t t[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) t[e] = (k0 + e < k_valid) ? vp[k0 + e] : (uint16_t)0;
+          vv = make_uint4(t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4] | (t[5] << 16),
+                          t[6] | (t[7] << 16));
+        }
+        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), as_bf16x8(pb[pk]),
+                                                           st.o[dt], 0, 0, 0);
+      }
+    }
+  }
+}
+
+template <int HD>
+MSD_DEV void load_q(bf16x8 (&qf)[HD / 16], const uint16_t* qrow) {
+  const int h = (threadIdx.x & 63) >> 5;
+#pragma unroll
+  for (int c = 0; c < HD / 16; ++c)
+    qf[c] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + (HD / 2) * h + 8 * c));
+}
+
+template <int HD>
+MSD_DEV void init_state(AttnState<HD>& st) {
+#pragma unroll
+  for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) st.o[dt][r] = 0.f;
+  st.m = -INFINITY;
+  st.l = 0.f;
+}
+
+// O^T C layout: lane holds query column (lane & 31), register r of dim tile
+// dt holds dim dt*32 + 8*(r/4) + 4*(lane/32) + r%4.
+template <int HD>
+MSD_DEV void store_final(const AttnState<HD>& st, uint16_t* orow, bool valid) {
+  if (!valid) return;
+  const int h = (threadIdx.x & 63) >> 5;
+  const float inv = st.l > 0.f ? 1.f / st.l : 0.f;
+#pragma unroll
+  for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      orow[dt * 32 + 8 * (r >> 2) + 4 * h + (r & 3)] = f2bf(st.o[dt][r] * inv);
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int n_items = a.n_seq * a.KV * a.qtiles * a.n_chunks;
+  if (wid >= n_items) return;
+  int t = wid;
+  const int c = t % a.n_chunks; t /= a.n_chunks;
+  const int qt = t % a.qtiles; t /= a.qtiles;
+  const int g = t % a.KV;
+  const int sidx = t / a.KV;
+  const int b = a.seq_ids[sidx];
+  const int P = a.prefix[sidx];
+  const int Ltot = P + a.R;
+  const int G = a.H / a.KV;
+  const int j = lane & 31;
+  const int qr = qt * 32 + j;
+  int node = qr / G;
+  const int head = g * G + (qr - node * G);
+  const bool valid = node < a.nq;
+  if (!valid) node = 0;
+  const uint16_t* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)(valid ? head : g * G) * HD;
+  bf16x8 qf[HD / 16];
+  load_q<HD>(qf, qrow);
+  const uint64_t msk = a.mask[sidx * a.nq + node];
+  const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
+  const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
+  AttnState<HD> st;
+  init_state<HD>(st);
+  const int k0 = c * a.chunk_keys;
+  const int k1 = min(k0 + a.chunk_keys, Ltot);
+  attend_range<HD>(st, qf, kbase, vbase, a.S, k0, k1, Ltot, a.scale, [&](int key) {
+    return key < P || ((msk >> (key - P)) & 1ull);
+  });
+  if (a.n_chunks == 1) {
+    store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD, valid);
+    return;
+  }
+  float* po = a.part_o + (size_t)wid * 32 * HD;
+#pragma unroll
+  for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) po[(dt * 16 + r) * 64 + lane] = st.o[dt][r];
+  if (lane < 32) {
+    a.part_ml[(size_t)wid * 64 + 2 * lane] = st.m;
+    a.part_ml[(size_t)wid * 64 + 2 * lane + 1] = st.l;
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
+  int t = blockIdx.x;
+  const int qt = t % a.qtiles; t /= a.qtiles;
+  const int g = t % a.KV;
+  const int sidx = t / a.KV;
+  const int G = a.H / a.KV;
+  const size_t item0 = (size_t)blockIdx.x * a.n_chunks;
+  for (int o = threadIdx.x; o < 32 * HD; o += 256) {
+    const int j = o / HD, dim = o % HD;
+    const int qr = qt * 32 + j;
+    const int node = qr / G;
+    if (node >= a.nq) continue;
+    const int head = g * G + (qr - node * G);
+    const int dt = dim >> 5, dd = dim & 31;
+    const int hh = (dd >> 2) & 1, r = (dd >> 3) * 4 + (dd & 3);
+    const int idx = (dt * 16 + r) * 64 + j + 32 * hh;
+    float M = -INFINITY;
+    for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
+    float num = 0.f, den = 0.f;
+    if (M != -INFINITY) {
+      for (int c = 0; c < a.n_chunks; ++c) {
+        const float mc = a.part_ml[(item0 + c) * 64 + 2 * j];
+        const float w = (mc == -INFINITY) ? 0.f : __expf(mc - M);
+        den += w * a.part_ml[(item0 + c) * 64 + 2 * j + 1];
+        num += w * a.part_o[(item0 + c) * 32 * HD + idx];
+      }
+    }
+    a.out[(size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD + dim] =
+        f2bf(den > 0.f ? num / den : 0.f);
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int n_items = a.n_seq * a.H * a.qtiles;
+  if (wid >= n_items) return;
+  int t = wid;
+  const int qt = t % a.qtiles; t /= a.qtiles;
+  const int head = t % a.H;
+  const int sidx = t / a.H;
+  const int b = a.seq_ids[sidx];
+  const int P = a.prefix[sidx];
+  const int g = head / (a.H / a.KV);
+  const int j = lane & 31;
+  int node = qt * 32 + j;
+  const bool valid = node < a.nq;
+  if (!valid) node = a.nq - 1;
+  const uint16_t* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD;
+  bf16x8 qf[HD / 16];
+  load_q<HD>(qf, qrow);
+  const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
+  const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
+  AttnState<HD> st;
+  init_state<HD>(st);
+  const int last = min(qt * 32 + 32, a.nq);
+  const int k1 = P + last;
+  const int my_last = P + node;
+  attend_range<HD>(st, qf, kbase, vbase, a.S, 0, k1, k1, a.scale,
+                   [&](int key) { return key <= my_last; });
+  store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD, valid);
+}
+
+}  // namespace
+
+size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd) {
+  return (size_t)n_seq * KV * qtiles * n_chunks * 32 * hd;
+}
+
+void launch_tree_attention(AttnArgs a, hipStream_t st) {
+  const int items = a.n_seq * a.KV * a.qtiles * a.n_chunks;
+  dim3 grid((items + 3) / 4);
+  if (a.hd == 128) {
+    hipLaunchKernelGGL(k_tree_attn<128>, grid, dim3(256), 0, st, a);
+    if (a.n_chunks > 1)
+      hipLaunchKernelGGL(k_tree_combine<128>, dim3(a.n_seq * a.KV * a.qtiles), dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL(k_tree_attn<64>, grid, dim3(256), 0, st, a);
+    if (a.n_chunks > 1)
+      hipLaunchKernelGGL(k_tree_combine<64>, dim3(a.n_seq * a.KV * a.qtiles), dim3(256), 0, st, a);
+  }
+}
+
+void launch_causal_attention(AttnArgs a, hipStream_t st) {
+  const int items = a.n_seq * a.H * a.qtiles;
+  dim3 grid((items + 3) / 4);
+  if (a.hd == 128)
+    hipLaunchKernelGGL(k_causal_attn<128>, grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_causal_attn<64>, grid, dim3(256), 0, st, a);
+}
+
+}  // namespace msd

@@ -1,0 +1,449 @@
+// Tree bookkeeping kernels: per-step row descriptors, static and dynamic
+// draft-tree construction, greedy acceptance and in-place KV compaction.
+// All of this is integer / selection work on at most a few hundred entries
+// per sequence, so the kernels use one block (or one thread) per sequence.
+#include "../../include/msd.h"
+#include "msd_internal.h"
+
+namespace msd {
+
+namespace {
+
+MSD_DEV bool better_score(float sa, int ia, float sb, int ib) {
+  return sa > sb || (sa == sb && ia < ib);
+}
+
+__global__ void k_tree_init_static(msd_tree* trees, const int* seq_ids, const int* d_root,
+                                   StaticSpec sp, int T) {
+  const int sidx = blockIdx.x;
+  msd_tree* t = trees + sidx;
+  const int b = seq_ids[sidx];
+  for (int i = threadIdx.x; i < MSD_MAX_TREE; i += blockDim.x) {
+    const bool in = i < T;
+    t->token[i] = (i == 0) ? d_root[b] : 0;
+    t->parent[i] = in ? sp.parent[i] : -1;
+    t->depth[i] = in ? sp.depth[i] : 0;
+    t->anc[i] = in ? sp.anc[i] : 0ull;
+    t->score[i] = 0.f;
+  }
+  if (threadIdx.x == 0) t->n_nodes = T;
+}
+
+__global__ void k_static_rows(const msd_tree* trees, const int* seq_ids, const int* d_len,
+                              StaticSpec sp, int round_off, int n_round, int depth,
+                              int feat_stride, Rows r, int* prefix) {
+  const int sidx = blockIdx.x;
+  const int j = threadIdx.x;
+  const int b = seq_ids[sidx];
+  const int L = d_len[b];
+  if (j == 0) prefix[sidx] = L;
+  if (j >= n_round) return;
+  const int u = sp.round_nodes[round_off + j];
+  const int row = sidx * n_round + j;
+  r.tok[row] = trees[sidx].token[u];
+  r.vis[row] = -1;
+  r.hrow[row] = b * feat_stride + sp.pslot[u];
+  r.pos[row] = L + depth - 1;
+  r.slot[row] = L + sp.exp_idx[u];
+  r.seq[row] = b;
+  r.mask[row] = sp.exp_mask[u];
+  r.dst[row] = b * feat_stride + 1 + sp.exp_idx[u];
+}
+
+// Children of the round's nodes: node c with parent p takes the rank[c]-th
+// best token of p's draft distribution.
+__global__ void k_static_assign(msd_tree* trees, StaticSpec sp, int T, int parent_depth,
+                                const int* topk_idx, int k, int n_round) {
+  const int sidx = blockIdx.x;
+  for (int c = 1 + threadIdx.x; c < T; c += blockDim.x) {
+    if (sp.depth[c] != parent_depth + 1) continue;
+    const int p = sp.parent[c];
+    const int row = sidx * n_round + sp.round_pos[p];
+    trees[sidx].token[c] = topk_idx[(size_t)row * k + sp.rank[c]];
+  }
+}
+
+// Dynamic tree, depth 1: the root's top-K with scores log q.
+__global__ void k_dyn_root(DynPool pool, const int* topk_idx, const float* topk_val,
+                           const float* lse, int K) {
+  const int sidx = blockIdx.x;
+  const int j = threadIdx.x;
+  if (j >= K) return;
+  const size_t o = (size_t)sidx * pool.cap + j;
+  pool.parent[o] = -1;
+  pool.tok[o] = topk_idx[sidx * K + j];
+  pool.depth[o] = 1;
+  pool.score[o] = topk_val[sidx * K + j] - lse[sidx];
+  pool.exp_idx[o] = j;
+  pool.mask[o] = 1ull << j;
+  pool.frontier[sidx * K + j] = j;
+}
+
+// Rows for expanding the current frontier (nodes of depth depth-1 at draft
+// position L + depth - 2).
+__global__ void k_dyn_rows(DynPool pool, const int* seq_ids, const int* d_len, int K,
+                           int depth, int feat_stride, Rows r, int* prefix) {
+  const int sidx = blockIdx.x;
+  const int j = threadIdx.x;
+  const int b = seq_ids[sidx];
+  const int L = d_len[b];
+  if (j == 0) prefix[sidx] = L;
+  if (j >= K) return;
+  const size_t base = (size_t)sidx * pool.cap;
+  const int u = pool.frontier[sidx * K + j];
+  const int p = pool.parent[base + u];
+  const int row = sidx * K + j;
+  r.tok[row] = pool.tok[base + u];
+  r.vis[row] = -1;
+  r.hrow[row] = b * feat_stride + (p < 0 ? 0 : 1 + pool.exp_idx[base + p]);
+  r.pos[row] = L + depth - 2;
+  r.slot[row] = L + pool.exp_idx[base + u];
+  r.seq[row] = b;
+  r.mask[row] = pool.mask[base + u];
+  r.dst[row] = b * feat_stride + 1 + pool.exp_idx[base + u];
+}
+
+// Adds the K*K children of the frontier (frontier order, then rank order),
+// picks the best K as the next frontier and gives them expansion indices
+// exp_base + position in creation order.
+__global__ void k_dyn_expand(DynPool pool, const int* topk_idx, const float* topk_val,
+                             const float* lse, int K, int n_pool, int exp_base) {
+  __shared__ float sc[256];
+  __shared__ int sel[16];
+  const int sidx = blockIdx.x;
+  const size_t base = (size_t)sidx * pool.cap;
+  const int KK = K * K;
+  const int t = threadIdx.x;
+  if (t < KK) {
+    const int j = t / K;
+    const int row = sidx * K + j;
+    const int u = pool.frontier[sidx * K + j];
+    const int id = n_pool + t;
+    const float lq = topk_val[(size_t)row * K + (t - j * K)] - lse[row];
+    const float s = pool.score[base + u] + lq;
+    pool.parent[base + id] = u;
+    pool.tok[base + id] = topk_idx[(size_t)row * K + (t - j * K)];
+    pool.depth[base + id] = pool.depth[base + u] + 1;
+    pool.score[base + id] = s;
+    pool.exp_idx[base + id] = -1;
+    pool.mask[base + id] = 0ull;
+    sc[t] = s;
+  }
+  __syncthreads();
+  if (t < KK) {
+    int rank = 0;
+    for (int q = 0; q < KK; ++q) rank += better_score(sc[q], q, sc[t], t) ? 1 : 0;
+    if (rank < K) sel[rank] = t;
+  }
+  __syncthreads();
+  if (t < K) {
+    // position in creation order among the selected
+    const int me = sel[t];
+    int pos = 0;
+    for (int q = 0; q < K; ++q) pos += (sel[q] < me) ? 1 : 0;
+    const int id = n_pool + me;
+    const int e = exp_base + pos;
+    if (e < 64) {  // the last depth's frontier is never expanded
+      pool.exp_idx[base + id] = e;
+      pool.mask[base + id] = pool.mask[base + pool.parent[base + id]] | (1ull << e);
+    }
+    pool.frontier[sidx * K + pos] = id;
+  }
+}
+
+// Final tree: best N of the pool (score desc, creation asc), laid out by
+// (depth, creation) with the root as node 0.
+__global__ void k_dyn_finalize(DynPool pool, msd_tree* trees, const int* seq_ids,
+                               const int* d_root, int n_pool, int N) {
+  __shared__ int node_of[1024];
+  __shared__ int keep[MSD_MAX_TREE];
+  const int sidx = blockIdx.x;
+  const size_t base = (size_t)sidx * pool.cap;
+  for (int i = threadIdx.x; i < n_pool; i += blockDim.x) {
+    const float si = pool.score[base + i];
+    int rank = 0;
+    for (int q = 0; q < n_pool; ++q) rank += better_score(pool.score[base + q], q, si, i) ? 1 : 0;
+    node_of[i] = (rank < N) ? 1 : 0;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < n_pool; i += blockDim.x) {
+    if (!node_of[i]) continue;
+    const int di = pool.depth[base + i];
+    int pos = 0;
+    for (int q = 0; q < n_pool; ++q)
+      if (node_of[q] && (pool.depth[base + q] < di || (pool.depth[base + q] == di && q < i)))
+        ++pos;
+    keep[pos] = i;
+  }
+  __syncthreads();
+  for (int n = threadIdx.x; n < N; n += blockDim.x) node_of[keep[n]] = 2 + n;
+  __syncthreads();
+  msd_tree* t = trees + sidx;
+  if (threadIdx.x == 0) {
+    t->n_nodes = N + 1;
+    t->token[0] = d_root[seq_ids[sidx]];
+    t->parent[0] = -1;
+    t->depth[0] = 0;
+    t->score[0] = 0.f;
+    t->anc[0] = 1ull;
+    for (int n = 1; n <= N; ++n) {
+      const int i = keep[n - 1];
+      const int p = pool.parent[base + i];
+      // a kept node's parent is always kept (scores never increase along a
+      // path); the guard only keeps a malformed pool inside the tree arrays
+      const int pn = (p < 0 || node_of[p] < 2) ? 0 : node_of[p] - 1;
+      t->token[n] = pool.tok[base + i];
+      t->parent[n] = pn;
+      t->depth[n] = pool.depth[base + i];
+      t->score[n] = pool.score[base + i];
+      t->anc[n] = t->anc[pn] | (1ull << n);
+    }
+    for (int n = N + 1; n < MSD_MAX_TREE; ++n) {
+      t->token[n] = 0;
+      t->parent[n] = -1;
+      t->depth[n] = 0;
+      t->score[n] = 0.f;
+      t->anc[n] = 0ull;
+    }
+  }
+}
+
+__global__ void k_verify_rows(const msd_tree* trees, const int* seq_ids, const int* d_len,
+                              int T, int vocab, Rows r, int* prefix) {
+  const int sidx = blockIdx.x;
+  const int i = threadIdx.x;
+  const int b = seq_ids[sidx];
+  const int L = d_len[b];
+  if (i == 0) prefix[sidx] = L;
+  if (i >= T) return;
+  const msd_tree* t = trees + sidx;
+  const int row = sidx * T + i;
+  // caller-supplied trees: keep ids and positions inside their tables
+  r.tok[row] = min(max(t->token[i], 0), vocab - 1);
+  r.vis[row] = -1;
+  r.pos[row] = L + min(max(t->depth[i], 0), T - 1);
+  r.slot[row] = L + i;
+  r.seq[row] = b;
+  r.mask[row] = t->anc[i];
+}
+
+// Pending draft rows of each sequence, padded to r_max rows per sequence.
+__global__ void k_catchup_rows(const int* seq_ids, const int* d_len, const int* pend_n,
+                               const int* pend_next, int r_max, int pend_stride,
+                               int feat_stride, Rows r, int* prefix) {
+  const int sidx = blockIdx.x;
+  const int j = threadIdx.x;
+  const int b = seq_ids[sidx];
+  const int rb = pend_n[b];
+  const int P = d_len[b] - rb;
+  if (j == 0) prefix[sidx] = P;
+  if (j >= r_max) return;
+  const bool valid = j < rb;
+  const int jj = valid ? j : (rb > 0 ? rb - 1 : 0);
+  const int row = sidx * r_max + j;
+  r.tok[row] = pend_next[b * pend_stride + jj];
+  r.vis[row] = -1;
+  r.hrow[row] = b * pend_stride + jj;
+  r.pos[row] = P + jj;
+  r.slot[row] = valid ? P + j : -1;
+  r.seq[row] = b;
+  r.mask[row] = 0ull;
+  r.dst[row] = (j == rb - 1) ? b * feat_stride : -1;
+}
+
+__global__ void k_store_feat(const float* x, const int* dst, int d, float* feat) {
+  const int row = blockIdx.x;
+  const int o = dst[row];
+  if (o < 0) return;
+  for (int e = threadIdx.x; e < d; e += blockDim.x)
+    feat[(size_t)o * d + e] = x[(size_t)row * d + e];
+}
+
+// Greedy acceptance: node j is accepted iff its parent is and its token is
+// the parent's argmax; the deepest accepted node ends the path (unique since
+// siblings carry distinct tokens).
+__global__ void k_accept(const msd_tree* trees, const int* seq_ids, int T, const int* amax,
+                         int* path, int* n_path, int* emitted, int* slot_map, const int* d_len) {
+  const int sidx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (sidx >= gridDim.x * blockDim.x) return;
+  const msd_tree* t = trees + sidx;
+  const int* am = amax + (size_t)sidx * T;
+  uint64_t ok = 1ull;
+  int best = 0;
+  for (int j = 1; j < T; ++j) {
+    const int p = t->parent[j];
+    if (p < 0 || p >= j) continue;  // malformed: parents must precede children
+    if (((ok >> p) & 1ull) && t->token[j] == am[p]) {
+      ok |= 1ull << j;
+      if (t->depth[j] > t->depth[best]) best = j;
+    }
+  }
+  int tmp[MSD_MAX_TREE];
+  int n = 0;
+  for (int u = best; u >= 0 && n < MSD_MAX_TREE; u = (t->parent[u] < u) ? t->parent[u] : -1)
+    tmp[n++] = u;
+  const int L = d_len[seq_ids[sidx]];
+  for (int j = 0; j < MSD_MAX_TREE; ++j) {
+    const int u = (j < n) ? tmp[n - 1 - j] : -1;
+    path[sidx * MSD_MAX_TREE + j] = u;
+    slot_map[sidx * MSD_MAX_TREE + j] = (j < n) ? L + u : -1;
+    emitted[sidx * MSD_MAX_TREE + j] =
+        (j + 1 < n) ? t->token[tmp[n - 2 - j]] : ((j + 1 == n) ? am[best] : -1);
+  }
+  n_path[sidx] = n;
+}
+
+// In place: K rows L + path[j] -> L + j and the matching V^T columns, for
+// one (layer, sequence, kv head) per block; every read lands in LDS before
+// the first write.
+__global__ __launch_bounds__(256) void k_compact(uint16_t* kc, uint16_t* vc, int B, int KV,
+                                                 int S, int hd, int n_seq, const int* seq_ids,
+                                                 const int* path, const int* n_path,
+                                                 const int* d_len) {
+  __shared__ uint16_t ks[MSD_MAX_TREE * 128];
+  __shared__ uint16_t vs[MSD_MAX_TREE * 128];
+  int t = blockIdx.x;
+  const int g = t % KV; t /= KV;
+  const int sidx = t % n_seq;
+  const int layer = t / n_seq;
+  const int b = seq_ids[sidx];
+  const int n = n_path[sidx];
+  const int L = d_len[b];
+  const int* pth = path + sidx * MSD_MAX_TREE;
+  uint16_t* kb = kc + ((size_t)(layer * B + b) * KV + g) * S * hd;
+  uint16_t* vb = vc + ((size_t)(layer * B + b) * KV + g) * hd * S;
+  for (int idx = threadIdx.x; idx < n * hd; idx += 256) {
+    const int j = idx / hd, e = idx - j * hd;
+    const int src = L + pth[j];
+    ks[idx] = kb[(size_t)src * hd + e];
+    vs[idx] = vb[(size_t)e * S + src];
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < n * hd; idx += 256) {
+    const int j = idx / hd, e = idx - j * hd;
+    if (pth[j] == j) continue;
+    kb[(size_t)(L + j) * hd + e] = ks[idx];
+    vb[(size_t)e * S + L + j] = vs[idx];
+  }
+}
+
+// Accepted nodes become the next pending draft rows; the committed length
+// grows by the path length and the bonus token becomes the next root.
+__global__ void k_commit(const int* seq_ids, const int* path, const int* n_path,
+                         const int* emitted, const uint16_t* h_tree, int T, int d,
+                         uint16_t* pend_h, int* pend_next, int* pend_n, int pend_stride,
+                         int* d_len, int* d_root) {
+  const int sidx = blockIdx.x;
+  const int j = blockIdx.y;
+  const int b = seq_ids[sidx];
+  const int n = n_path[sidx];
+  if (j >= n) return;
+  const int u = path[sidx * MSD_MAX_TREE + j];
+  const uint16_t* src = h_tree + (size_t)(sidx * T + u) * d;
+  uint16_t* dst = pend_h + (size_t)(b * pend_stride + j) * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) dst[e] = src[e];
+  if (threadIdx.x == 0) {
+    pend_next[b * pend_stride + j] = emitted[sidx * MSD_MAX_TREE + j];
+    if (j == 0) {
+      pend_n[b] = n;
+      d_len[b] += n;
+      d_root[b] = emitted[sidx * MSD_MAX_TREE + n - 1];
+    }
+  }
+}
+
+__global__ void k_set_int(int* p, int idx, const int* src, int src_idx) {
+  p[idx] = src[src_idx];
+}
+
+}  // namespace
+
+void launch_tree_init_static(void* trees, int n_seq, const int* seq_ids, const int* d_root,
+                             StaticSpec sp, int T, hipStream_t st) {
+  hipLaunchKernelGGL(k_tree_init_static, dim3(n_seq), dim3(64), 0, st, (msd_tree*)trees,
+                     seq_ids, d_root, sp, T);
+}
+
+void launch_static_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
+                        StaticSpec sp, int round_off, int n_round, int depth, int feat_stride,
+                        Rows r, int* prefix, hipStream_t st) {
+  hipLaunchKernelGGL(k_static_rows, dim3(n_seq), dim3(64), 0, st, (const msd_tree*)trees,
+                     seq_ids, d_len, sp, round_off, n_round, depth, feat_stride, r, prefix);
+}
+
+void launch_static_assign(void* trees, int n_seq, StaticSpec sp, int T, int parent_depth,
+                          const int* topk_idx, int k, int n_round, hipStream_t st) {
+  hipLaunchKernelGGL(k_static_assign, dim3(n_seq), dim3(64), 0, st, (msd_tree*)trees, sp, T,
+                     parent_depth, topk_idx, k, n_round);
+}
+
+void launch_dyn_root(DynPool pool, int n_seq, const int* topk_idx, const float* topk_val,
+                     const float* lse, int K, hipStream_t st) {
+  hipLaunchKernelGGL(k_dyn_root, dim3(n_seq), dim3(64), 0, st, pool, topk_idx, topk_val, lse, K);
+}
+
+void launch_dyn_rows(DynPool pool, int n_seq, const int* seq_ids, const int* d_len, int K,
+                     int depth, int feat_stride, Rows r, int* prefix, hipStream_t st) {
+  hipLaunchKernelGGL(k_dyn_rows, dim3(n_seq), dim3(64), 0, st, pool, seq_ids, d_len, K, depth,
+                     feat_stride, r, prefix);
+}
+
+void launch_dyn_expand(DynPool pool, int n_seq, const int* topk_idx, const float* topk_val,
+                       const float* lse, int K, int n_pool, int exp_base, hipStream_t st) {
+  hipLaunchKernelGGL(k_dyn_expand, dim3(n_seq), dim3(256), 0, st, pool, topk_idx, topk_val, lse,
+                     K, n_pool, exp_base);
+}
+
+void launch_dyn_finalize(DynPool pool, void* trees, int n_seq, const int* seq_ids,
+                         const int* d_root, int n_pool, int N, hipStream_t st) {
+  hipLaunchKernelGGL(k_dyn_finalize, dim3(n_seq), dim3(256), 0, st, pool, (msd_tree*)trees,
+                     seq_ids, d_root, n_pool, N);
+}
+
+void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
+                        int T, int vocab, Rows r, int* prefix, hipStream_t st) {
+  hipLaunchKernelGGL(k_verify_rows, dim3(n_seq), dim3(64), 0, st, (const msd_tree*)trees,
+                     seq_ids, d_len, T, vocab, r, prefix);
+}
+
+void launch_catchup_rows(int n_seq, const int* seq_ids, const int* d_len, const int* pend_n,
+                         const int* pend_next, int r_max, int pend_stride, int feat_stride,
+                         Rows r, int* prefix, hipStream_t st) {
+  hipLaunchKernelGGL(k_catchup_rows, dim3(n_seq), dim3(64), 0, st, seq_ids, d_len, pend_n,
+                     pend_next, r_max, pend_stride, feat_stride, r, prefix);
+}
+
+void launch_store_feat(const float* x, int rows, const int* dst, int d, float* feat,
+                       hipStream_t st) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(k_store_feat, dim3(rows), dim3(256), 0, st, x, dst, d, feat);
+}
+
+void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,
+                   int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,
+                   hipStream_t st) {
+  hipLaunchKernelGGL(k_accept, dim3(n_seq), dim3(1), 0, st, (const msd_tree*)trees, seq_ids, T,
+                     amax, path, n_path, emitted, slot_map, d_len);
+}
+
+void launch_compact(uint16_t* kc, uint16_t* vc, int n_layers, int B, int KV, int S, int hd,
+                    int n_seq, const int* seq_ids, const int* path, const int* n_path,
+                    const int* d_len, hipStream_t st) {
+  hipLaunchKernelGGL(k_compact, dim3(n_layers * n_seq * KV), dim3(256), 0, st, kc, vc, B, KV, S,
+                     hd, n_seq, seq_ids, path, n_path, d_len);
+}
+
+void launch_commit(int n_seq, const int* seq_ids, const int* path, const int* n_path,
+                   const int* emitted, const uint16_t* h_tree, int T, int d, uint16_t* pend_h,
+                   int* pend_next, int* pend_n, int pend_stride, int* d_len, int* d_root,
+                   hipStream_t st) {
+  hipLaunchKernelGGL(k_commit, dim3(n_seq, MSD_MAX_TREE), dim3(256), 0, st, seq_ids, path,
+                     n_path, emitted, h_tree, T, d, pend_h, pend_next, pend_n, pend_stride,
+                     d_len, d_root);
+}
+
+void launch_set_int(int* p, int idx, const int* src, int src_idx, hipStream_t st) {
+  hipLaunchKernelGGL(k_set_int, dim3(1), dim3(1), 0, st, p, idx, src, src_idx);
+}
+
+}  // namespace msd

@@ -1,0 +1,808 @@
+// C ABI of the MSD decode path (see include/msd.h): buffer planning, the
+// per-call orchestration of the HIP kernels and the host-side sequence state.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <initializer_list>
+#include <string>
+#include <vector>
+
+#include "../../include/msd.h"
+#include "msd_internal.h"
+
+using namespace msd;
+
+namespace {
+
+struct LayerW {
+  const uint16_t *wq, *wk, *wv, *wo, *wg, *wu, *wd, *n1, *n2;
+};
+
+LayerW to_layer(const msd_layer_weights& l) {
+  return {(const uint16_t*)l.wq, (const uint16_t*)l.wk, (const uint16_t*)l.wv,
+          (const uint16_t*)l.wo, (const uint16_t*)l.w_gate, (const uint16_t*)l.w_up,
+          (const uint16_t*)l.w_down, (const uint16_t*)l.attn_norm, (const uint16_t*)l.ffn_norm};
+}
+
+constexpr int PEND = MSD_MAX_TREE;      // pending draft rows per sequence
+constexpr int FEAT = MSD_MAX_TREE + 1;  // draft feature slots per sequence
+constexpr int TOPK = 16;
+constexpr int POOL = 1024;              // dynamic-tree candidates per sequence
+constexpr int STAGE_INTS = 1 << 16;
+
+// Bump allocator over the workspace (also used to size it).
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <typename T>
+  T* take(size_t n) {
+    off = (off + 255) & ~(size_t)255;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+
+struct Plan {
+  int rows_max, lrows, ld_qkv;
+  size_t gemm_floats, attn_floats;
+  int counters;
+};
+
+Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
+  Plan p;
+  p.rows_max = std::max(lim.max_prompt, lim.max_batch * MSD_MAX_TREE);
+  p.lrows = lim.max_batch * MSD_MAX_TREE;
+  p.ld_qkv = (m.n_heads + 2 * m.n_kv_heads) * m.head_dim;
+  p.gemm_floats = gemm_partial_floats(0, 0, 1024);
+  const int G = m.n_heads / m.n_kv_heads;
+  const int qtiles = (MSD_MAX_TREE * G + 31) / 32;
+  p.attn_floats = attn_partial_floats(lim.max_batch, m.n_kv_heads, qtiles, 64, m.head_dim);
+  p.counters = 8192;
+  return p;
+}
+
+}  // namespace
+
+struct msd_ctx {
+  msd_model_desc m;
+  msd_limits lim;
+  Plan plan;
+  hipStream_t st;
+  std::vector<LayerW> layers;
+  LayerW dlayer;
+  const uint16_t *embed, *final_norm, *lm_head, *fc;
+  uint16_t *tk, *tv, *dk, *dv;
+  // workspace
+  float* x;
+  uint16_t *xn, *q, *ao, *act, *h;
+  float *qkv, *logits;
+  Rows rows;
+  int *nxt, *prefix, *seq_ids;
+  int *d_len, *d_root, *pend_n, *pend_next;
+  uint16_t* pend_h;
+  float* dfeat;
+  int *acc_path, *acc_n, *acc_emit, *acc_slot, *feat_idx;
+  int* tk_idx;
+  float *tk_val, *tk_lse;
+  StaticSpec sp;
+  DynPool pool;
+  GemmScratch gs;
+  float *att_po, *att_ml;
+  float2* rope;
+  // host
+  int* stage;  // pinned staging
+  std::vector<int> L, pend, ready;
+  std::string err;
+  // static spec cache
+  std::vector<int> sp_parent, sp_rank;
+  std::vector<int> round_off, round_n, round_k, round_exp_end;
+  int sp_T = 0, sp_D = 0;
+  int verified_T = 0, verified_nseq = 0;
+};
+
+namespace {
+
+std::string g_err;
+
+int fail(msd_ctx* c, int code, const std::string& msg) {
+  if (c)
+    c->err = msg;
+  else
+    g_err = msg;
+  return code;
+}
+
+#define HIPC(c, expr)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess)                                                          \
+      return fail(c, MSD_ERR_HIP, std::string(#expr ": ") + hipGetErrorString(e_)); \
+  } while (0)
+
+#define LAUNCHED(c)                                                                   \
+  do {                                                                                \
+    hipError_t e_ = hipGetLastError();                                                \
+    if (e_ != hipSuccess)                                                             \
+      return fail(c, MSD_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e_)); \
+  } while (0)
+
+size_t kv_bytes(const msd_model_desc& m, const msd_limits& lim, int layers) {
+  return (size_t)layers * lim.max_batch * m.n_kv_heads * (size_t)lim.max_seq * m.head_dim * 2;
+}
+
+// Lays out the workspace (base == nullptr: only measures it).
+size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* base) {
+  const Plan p = make_plan(m, lim);
+  Carver cv{base};
+  const int d = m.d_model, R = p.rows_max, B = lim.max_batch;
+  msd_ctx tmp;
+  msd_ctx* t = c ? c : &tmp;
+  t->x = cv.take<float>((size_t)R * d);
+  t->xn = cv.take<uint16_t>((size_t)R * 2 * d);
+  t->qkv = cv.take<float>((size_t)R * p.ld_qkv);
+  t->q = cv.take<uint16_t>((size_t)R * m.n_heads * m.head_dim);
+  t->ao = cv.take<uint16_t>((size_t)R * m.n_heads * m.head_dim);
+  t->act = cv.take<uint16_t>((size_t)R * m.ffn_dim);
+  t->h = cv.take<uint16_t>((size_t)R * d);
+  t->logits = cv.take<float>((size_t)p.lrows * m.vocab);
+  t->rows.tok = cv.take<int>(R);
+  t->rows.vis = cv.take<int>(R);
+  t->rows.pos = cv.take<int>(R);
+  t->rows.slot = cv.take<int>(R);
+  t->rows.seq = cv.take<int>(R);
+  t->rows.hrow = cv.take<int>(R);
+  t->rows.dst = cv.take<int>(R);
+  t->rows.mask = cv.take<uint64_t>(R);
+  t->nxt = cv.take<int>(R);
+  t->prefix = cv.take<int>(B);
+  t->seq_ids = cv.take<int>(B);
+  t->d_len = cv.take<int>(B);
+  t->d_root = cv.take<int>(B);
+  t->pend_n = cv.take<int>(B);
+  t->pend_next = cv.take<int>((size_t)B * PEND);
+  t->pend_h = cv.take<uint16_t>((size_t)B * PEND * d);
+  t->dfeat = cv.take<float>((size_t)B * FEAT * d);
+  t->acc_path = cv.take<int>((size_t)B * MSD_MAX_TREE);
+  t->acc_n = cv.take<int>(B);
+  t->acc_emit = cv.take<int>((size_t)B * MSD_MAX_TREE);
+  t->acc_slot = cv.take<int>((size_t)B * MSD_MAX_TREE);
+  t->feat_idx = cv.take<int>(B);
+  t->tk_idx = cv.take<int>((size_t)p.lrows * TOPK);
+  t->tk_val = cv.take<float>((size_t)p.lrows * TOPK);
+  t->tk_lse = cv.take<float>(p.lrows);
+  t->sp.parent = cv.take<int>(MSD_MAX_TREE);
+  t->sp.rank = cv.take<int>(MSD_MAX_TREE);
+  t->sp.depth = cv.take<int>(MSD_MAX_TREE);
+  t->sp.anc = cv.take<uint64_t>(MSD_MAX_TREE);
+  t->sp.exp_idx = cv.take<int>(MSD_MAX_TREE);
+  t->sp.exp_mask = cv.take<uint64_t>(MSD_MAX_TREE);
+  t->sp.pslot = cv.take<int>(MSD_MAX_TREE);
+  t->sp.round_nodes = cv.take<int>(MSD_MAX_TREE);
+  t->sp.round_pos = cv.take<int>(MSD_MAX_TREE);
+  t->pool.cap = POOL;
+  t->pool.parent = cv.take<int>((size_t)B * POOL);
+  t->pool.tok = cv.take<int>((size_t)B * POOL);
+  t->pool.depth = cv.take<int>((size_t)B * POOL);
+  t->pool.score = cv.take<float>((size_t)B * POOL);
+  t->pool.exp_idx = cv.take<int>((size_t)B * POOL);
+  t->pool.mask = cv.take<uint64_t>((size_t)B * POOL);
+  t->pool.frontier = cv.take<int>((size_t)B * TOPK);
+  t->gs.partial = cv.take<float>(p.gemm_floats);
+  t->gs.partial_floats = p.gemm_floats;
+  t->gs.counters = cv.take<int>(p.counters);
+  t->gs.n_counters = p.counters;
+  t->att_po = cv.take<float>(p.attn_floats);
+  t->att_ml = cv.take<float>(p.attn_floats / m.head_dim * 2 + 64);
+  t->rope = cv.take<float2>((size_t)lim.max_seq * (m.head_dim / 2));
+  return cv.off + 256;
+}
+
+int check_desc(const msd_model_desc* m, const msd_limits* lim, msd_ctx* c) {
+  if (!m || !lim) return fail(c, MSD_ERR_INVALID_ARG, "null model or limits");
+  if (m->n_layers <= 0 || m->d_model <= 0 || m->n_heads <= 0 || m->n_kv_heads <= 0 ||
+      m->n_heads % m->n_kv_heads || m->ffn_dim <= 0 || m->vocab <= 0)
+    return fail(c, MSD_ERR_INVALID_ARG, "bad model shape");
+  if (m->head_dim != 128 && m->head_dim != 64)
+    return fail(c, MSD_ERR_INVALID_ARG, "head_dim must be 64 or 128");
+  if (m->d_model % 8 || m->ffn_dim % 8)
+    return fail(c, MSD_ERR_INVALID_ARG, "d_model and ffn_dim must be multiples of 8");
+  if (m->n_heads / m->n_kv_heads > 16)
+    return fail(c, MSD_ERR_INVALID_ARG, "query group larger than 16");
+  if (lim->max_batch <= 0 || lim->max_batch > 8 || lim->max_tree <= 0 ||
+      lim->max_tree > MSD_MAX_TREE || lim->max_prompt <= 0 || lim->max_seq <= 0 ||
+      lim->max_seq % 8)
+    return fail(c, MSD_ERR_INVALID_ARG, "bad limits (max_seq must be a multiple of 8)");
+  return MSD_OK;
+}
+
+struct Up {
+  void* dst;
+  const void* src;
+  size_t bytes;
+};
+
+// Copies host arrays to the device through the pinned staging buffer (the
+// stream is drained first because the previous upload may still read it).
+int upload_many(msd_ctx* c, std::initializer_list<Up> ups) {
+  size_t total = 0;
+  for (const Up& u : ups) total += (u.bytes + 255) & ~(size_t)255;
+  if (total > sizeof(int) * (size_t)STAGE_INTS) return fail(c, MSD_ERR_INVALID_ARG, "upload too large");
+  HIPC(c, hipStreamSynchronize(c->st));
+  size_t off = 0;
+  for (const Up& u : ups) {
+    if (!u.bytes) continue;
+    char* s = reinterpret_cast<char*>(c->stage) + off;
+    std::memcpy(s, u.src, u.bytes);
+    HIPC(c, hipMemcpyAsync(u.dst, s, u.bytes, hipMemcpyHostToDevice, c->st));
+    off += (u.bytes + 255) & ~(size_t)255;
+  }
+  return MSD_OK;
+}
+
+int upload(msd_ctx* c, int* dst, const int* src, int n) {
+  return upload_many(c, {{dst, src, sizeof(int) * (size_t)n}});
+}
+
+int gemm(msd_ctx* c, int epi, const uint16_t* X, int ldx, int M, const uint16_t* W,
+         const uint16_t* W2, int N, int K, float* of, uint16_t* ob, int ldo) {
+  launch_gemm(epi, X, ldx, M, W, W2, N, K, of, ob, ldo, c->gs, c->st);
+  LAUNCHED(c);
+  return MSD_OK;
+}
+
+#define TRY(x)              \
+  do {                      \
+    int r_ = (x);           \
+    if (r_ != MSD_OK) return r_; \
+  } while (0)
+
+// One decoder stack (the target's layers or the draft's single layer) over
+// n_seq * nq rows of c->x described by c->rows; tree_R < 0 selects causal
+// attention, otherwise tree attention over a region of tree_R slots.
+int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int max_ltot) {
+  const msd_model_desc& m = c->m;
+  const int rows = n_seq * nq;
+  const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim;
+  const int ld = c->plan.ld_qkv;
+  const int nl = draft ? 1 : m.n_layers;
+  const int B = c->lim.max_batch, S = c->lim.max_seq;
+  const size_t layer_kv = (size_t)B * KV * S * hd;
+  for (int l = 0; l < nl; ++l) {
+    const LayerW& w = draft ? c->dlayer : c->layers[l];
+    uint16_t* kc = (draft ? c->dk : c->tk) + (size_t)l * layer_kv;
+    uint16_t* vc = (draft ? c->dv : c->tv) + (size_t)l * layer_kv;
+    launch_rmsnorm(c->x, w.n1, rows, d, m.norm_eps, c->xn, c->st);
+    LAUNCHED(c);
+    TRY(gemm(c, EPI_F32, c->xn, d, rows, w.wq, nullptr, H * hd, d, c->qkv, nullptr, ld));
+    TRY(gemm(c, EPI_F32, c->xn, d, rows, w.wk, nullptr, KV * hd, d, c->qkv + H * hd, nullptr, ld));
+    TRY(gemm(c, EPI_F32, c->xn, d, rows, w.wv, nullptr, KV * hd, d, c->qkv + (H + KV) * hd,
+             nullptr, ld));
+    launch_rope_kv(c->qkv, rows, H, KV, hd, c->rows.pos, c->rows.seq, c->rows.slot, c->rope,
+                   c->q, kc, vc, S, c->st);
+    LAUNCHED(c);
+    AttnArgs a{};
+    a.q = c->q;
+    a.kc = kc;
+    a.vc = vc;
+    a.seq_ids = c->seq_ids;
+    a.prefix = c->prefix;
+    a.mask = c->rows.mask;
+    a.S = S;
+    a.H = H;
+    a.KV = KV;
+    a.hd = hd;
+    a.nq = nq;
+    a.n_seq = n_seq;
+    a.out = c->ao;
+    a.scale = 1.0f / std::sqrt((float)hd);
+    a.part_o = c->att_po;
+    a.part_ml = c->att_ml;
+    if (tree_R < 0) {
+      a.qtiles = (nq + 31) / 32;
+      a.n_chunks = 1;
+      launch_causal_attention(a, c->st);
+    } else {
+      const int G = H / KV;
+      a.R = tree_R;
+      a.qtiles = (nq * G + 31) / 32;
+      const int base_items = n_seq * KV * a.qtiles;
+      int chunks = std::max(1, 1024 / std::max(1, base_items));
+      chunks = std::min(chunks, (max_ltot + 63) / 64);
+      chunks = std::max(chunks, 1);
+      while (chunks > 1 && attn_partial_floats(n_seq, KV, a.qtiles, chunks, hd) >
+                               c->plan.attn_floats)
+        --chunks;
+      int ck = (max_ltot + chunks - 1) / chunks;
+      ck = (ck + 31) / 32 * 32;
+      a.chunk_keys = ck;
+      a.n_chunks = (max_ltot + ck - 1) / ck;
+      launch_tree_attention(a, c->st);
+    }
+    LAUNCHED(c);
+    TRY(gemm(c, EPI_RESID, c->ao, H * hd, rows, w.wo, nullptr, d, H * hd, c->x, nullptr, d));
+    launch_rmsnorm(c->x, w.n2, rows, d, m.norm_eps, c->xn, c->st);
+    LAUNCHED(c);
+    TRY(gemm(c, EPI_SILU, c->xn, d, rows, w.wg, w.wu, m.ffn_dim, d, nullptr, c->act, m.ffn_dim));
+    TRY(gemm(c, EPI_RESID, c->act, m.ffn_dim, rows, w.wd, nullptr, d, m.ffn_dim, c->x, nullptr,
+             d));
+  }
+  return MSD_OK;
+}
+
+// Draft head on rows whose fc input is already in c->xn ([rows][2d]):
+// f = f_down(concat) -> decoder layer -> features in c->x.
+int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const uint16_t* visual) {
+  const int d = c->m.d_model;
+  const int rows = n_seq * nq;
+  TRY(gemm(c, EPI_F32, c->xn, 2 * d, rows, c->fc, nullptr, d, 2 * d, c->x, nullptr, d));
+  if (visual) {
+    launch_visual_rows(visual, c->rows.vis, rows, d, c->x, c->st);
+    LAUNCHED(c);
+  }
+  return forward_layers(c, true, n_seq, nq, tree_R, max_ltot);
+}
+
+// LM head + top-k over rows of c->x (draft features, f32): no final norm.
+int draft_head(msd_ctx* c, int rows, int k) {
+  const int d = c->m.d_model, V = c->m.vocab;
+  launch_to_bf16(c->x, rows * d, c->xn, c->st);
+  LAUNCHED(c);
+  TRY(gemm(c, EPI_F32, c->xn, d, rows, c->lm_head, nullptr, V, d, c->logits, nullptr, V));
+  launch_topk(c->logits, rows, V, k, c->tk_idx, c->tk_val, c->tk_lse, c->st);
+  LAUNCHED(c);
+  return MSD_OK;
+}
+
+int check_seqs(msd_ctx* c, int n_seq, const int32_t* seqs) {
+  if (n_seq <= 0 || n_seq > c->lim.max_batch || !seqs)
+    return fail(c, MSD_ERR_INVALID_ARG, "bad sequence list");
+  for (int i = 0; i < n_seq; ++i) {
+    if (seqs[i] < 0 || seqs[i] >= c->lim.max_batch)
+      return fail(c, MSD_ERR_INVALID_ARG, "sequence index out of range");
+    for (int j = 0; j < i; ++j)
+      if (seqs[j] == seqs[i]) return fail(c, MSD_ERR_INVALID_ARG, "duplicate sequence");
+    if (!c->ready[seqs[i]]) return fail(c, MSD_ERR_STATE, "sequence has no prompt");
+  }
+  return MSD_OK;
+}
+
+// Validates a static spec and rebuilds the device template when it changes.
+int prepare_static(msd_ctx* c, const msd_tree_spec* s) {
+  const int N = s->n_nodes, T = N + 1;
+  if (!s->parent || !s->rank || N <= 0 || T > c->lim.max_tree)
+    return fail(c, MSD_ERR_INVALID_ARG, "bad static tree");
+  std::vector<int> par(T, -1), rk(T, 0), dep(T, 0);
+  for (int i = 1; i < T; ++i) {
+    par[i] = s->parent[i - 1];
+    rk[i] = s->rank[i - 1];
+    if (par[i] < 0 || par[i] >= i) return fail(c, MSD_ERR_INVALID_ARG, "parent must precede child");
+    if (rk[i] < 0 || rk[i] >= TOPK) return fail(c, MSD_ERR_INVALID_ARG, "rank out of range");
+    dep[i] = dep[par[i]] + 1;
+    if (dep[i] < dep[i - 1]) return fail(c, MSD_ERR_INVALID_ARG, "nodes not ordered by depth");
+    for (int j = 1; j < i; ++j)
+      if (par[j] == par[i] && rk[j] == rk[i])
+        return fail(c, MSD_ERR_INVALID_ARG, "siblings share a rank");
+  }
+  if (T == c->sp_T && par == c->sp_parent && rk == c->sp_rank) return MSD_OK;
+  const int D = dep[T - 1];
+  std::vector<int> has(T, 0);
+  for (int i = 1; i < T; ++i) has[par[i]] = 1;
+  std::vector<int> exp_idx(T, -1), pslot(T, 0), rnodes, rpos(T, 0);
+  std::vector<uint64_t> anc(T, 0), emask(T, 0);
+  c->round_off.assign(D, 0);
+  c->round_n.assign(D, 0);
+  c->round_k.assign(D, 0);
+  c->round_exp_end.assign(D, 0);
+  int ne = 0;
+  for (int dd = 0; dd < D; ++dd) {
+    c->round_off[dd] = (int)rnodes.size();
+    for (int u = 0; u < T; ++u) {
+      if (dep[u] != dd || !has[u]) continue;
+      rpos[u] = c->round_n[dd]++;
+      if (dd > 0) {
+        rnodes.push_back(u);
+        exp_idx[u] = ne++;
+      }
+    }
+    if (dd == 0) c->round_n[dd] = 1;
+    c->round_exp_end[dd] = ne;
+  }
+  for (int i = 0; i < T; ++i) {
+    anc[i] = (i ? anc[par[i]] : 0ull) | (1ull << i);
+    if (i > 0) {
+      const int p = par[i];
+      pslot[i] = (p == 0) ? 0 : 1 + exp_idx[p];
+      c->round_k[dep[p]] = std::max(c->round_k[dep[p]], rk[i] + 1);
+    }
+    if (exp_idx[i] >= 0) emask[i] = (par[i] > 0 ? emask[par[i]] : 0ull) | (1ull << exp_idx[i]);
+  }
+  if (ne > MSD_MAX_TREE) return fail(c, MSD_ERR_INVALID_ARG, "too many expanded nodes");
+  rnodes.resize(MSD_MAX_TREE, 0);
+  std::vector<int> packed;
+  auto put = [&](const std::vector<int>& v) { packed.insert(packed.end(), v.begin(), v.end()); packed.resize(packed.size() + (MSD_MAX_TREE - v.size()), 0); };
+  put(par); put(rk); put(dep); put(exp_idx); put(pslot); put(rnodes); put(rpos);
+  std::vector<int> anc_i(2 * MSD_MAX_TREE, 0), em_i(2 * MSD_MAX_TREE, 0);
+  std::memcpy(anc_i.data(), anc.data(), sizeof(uint64_t) * T);
+  std::memcpy(em_i.data(), emask.data(), sizeof(uint64_t) * T);
+  TRY(upload(c, c->sp.parent, packed.data(), MSD_MAX_TREE));
+  TRY(upload(c, c->sp.rank, packed.data() + MSD_MAX_TREE, MSD_MAX_TREE));
+  TRY(upload(c, c->sp.depth, packed.data() + 2 * MSD_MAX_TREE, MSD_MAX_TREE));
+  TRY(upload(c, c->sp.exp_idx, packed.data() + 3 * MSD_MAX_TREE, MSD_MAX_TREE));
+  TRY(upload(c, c->sp.pslot, packed.data() + 4 * MSD_MAX_TREE, MSD_MAX_TREE));
+  TRY(upload(c, c->sp.round_nodes, packed.data() + 5 * MSD_MAX_TREE, MSD_MAX_TREE));
+  TRY(upload(c, c->sp.round_pos, packed.data() + 6 * MSD_MAX_TREE, MSD_MAX_TREE));
+  TRY(upload(c, (int*)c->sp.anc, anc_i.data(), 2 * MSD_MAX_TREE));
+  TRY(upload(c, (int*)c->sp.exp_mask, em_i.data(), 2 * MSD_MAX_TREE));
+  c->sp_T = T;
+  c->sp_D = D;
+  c->sp_parent = par;
+  c->sp_rank = rk;
+  return MSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int msd_buffer_sizes(const msd_model_desc* m, const msd_limits* lim, size_t* target_kv_bytes,
+                     size_t* draft_kv_bytes, size_t* workspace_bytes) {
+  int r = check_desc(m, lim, nullptr);
+  if (r != MSD_OK) return r;
+  if (target_kv_bytes) *target_kv_bytes = kv_bytes(*m, *lim, m->n_layers);
+  if (draft_kv_bytes) *draft_kv_bytes = kv_bytes(*m, *lim, 1);
+  if (workspace_bytes) *workspace_bytes = carve(nullptr, *m, *lim, nullptr);
+  return MSD_OK;
+}
+
+int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_weights* tw,
+               const msd_draft_weights* dw, const msd_buffers* bufs, void* stream,
+               msd_ctx** out) {
+  if (!out) return fail(nullptr, MSD_ERR_INVALID_ARG, "null output pointer");
+  *out = nullptr;
+  int r = check_desc(m, lim, nullptr);
+  if (r != MSD_OK) return r;
+  if (!tw || !dw || !bufs || !tw->embed || !tw->layers || !tw->final_norm || !tw->lm_head ||
+      !dw->fc || !bufs->target_k || !bufs->target_v || !bufs->draft_k || !bufs->draft_v ||
+      !bufs->workspace)
+    return fail(nullptr, MSD_ERR_INVALID_ARG, "null weight or buffer pointer");
+  for (int l = 0; l < m->n_layers; ++l) {
+    const msd_layer_weights& w = tw->layers[l];
+    if (!w.wq || !w.wk || !w.wv || !w.wo || !w.w_gate || !w.w_up || !w.w_down || !w.attn_norm ||
+        !w.ffn_norm)
+      return fail(nullptr, MSD_ERR_INVALID_ARG, "null layer weight");
+  }
+  msd_ctx* c = new msd_ctx();
+  c->m = *m;
+  c->lim = *lim;
+  c->plan = make_plan(*m, *lim);
+  c->st = (hipStream_t)stream;
+  for (int l = 0; l < m->n_layers; ++l) c->layers.push_back(to_layer(tw->layers[l]));
+  c->dlayer = to_layer(dw->layer);
+  c->embed = (const uint16_t*)tw->embed;
+  c->final_norm = (const uint16_t*)tw->final_norm;
+  c->lm_head = (const uint16_t*)tw->lm_head;
+  c->fc = (const uint16_t*)dw->fc;
+  c->tk = (uint16_t*)bufs->target_k;
+  c->tv = (uint16_t*)bufs->target_v;
+  c->dk = (uint16_t*)bufs->draft_k;
+  c->dv = (uint16_t*)bufs->draft_v;
+  carve(c, *m, *lim, (char*)bufs->workspace);
+  c->gs.target_wgs = 512;
+  if (const char* e = std::getenv("MSD_GEMM_WGS")) c->gs.target_wgs = std::max(1, atoi(e));
+  c->L.assign(lim->max_batch, 0);
+  c->pend.assign(lim->max_batch, 0);
+  c->ready.assign(lim->max_batch, 0);
+  hipError_t e = hipHostMalloc((void**)&c->stage, sizeof(int) * STAGE_INTS, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    delete c;
+    return fail(nullptr, MSD_ERR_HIP, std::string("hipHostMalloc: ") + hipGetErrorString(e));
+  }
+  auto init = [&]() -> int {
+    HIPC(c, hipMemsetAsync(c->gs.counters, 0, sizeof(int) * c->gs.n_counters, c->st));
+    // never-written cache slots may be read (with zero weight) by padded rows
+    const size_t tkv = kv_bytes(*m, *lim, m->n_layers), dkv = kv_bytes(*m, *lim, 1);
+    HIPC(c, hipMemsetAsync(c->tk, 0, tkv, c->st));
+    HIPC(c, hipMemsetAsync(c->tv, 0, tkv, c->st));
+    HIPC(c, hipMemsetAsync(c->dk, 0, dkv, c->st));
+    HIPC(c, hipMemsetAsync(c->dv, 0, dkv, c->st));
+    HIPC(c, hipMemsetAsync(c->d_len, 0, sizeof(int) * lim->max_batch, c->st));
+    HIPC(c, hipMemsetAsync(c->pend_n, 0, sizeof(int) * lim->max_batch, c->st));
+    HIPC(c, hipMemsetAsync(c->d_root, 0, sizeof(int) * lim->max_batch, c->st));
+    launch_rope_table(c->rope, lim->max_seq, m->head_dim, (double)m->rope_theta, c->st);
+    LAUNCHED(c);
+    HIPC(c, hipStreamSynchronize(c->st));
+    return MSD_OK;
+  };
+  r = init();
+  if (r != MSD_OK) {
+    g_err = c->err;
+    (void)hipHostFree(c->stage);
+    delete c;
+    return r;
+  }
+  *out = c;
+  return MSD_OK;
+}
+
+void msd_destroy(msd_ctx* c) {
+  if (!c) return;
+  (void)hipStreamSynchronize(c->st);
+  (void)hipHostFree(c->stage);
+  delete c;
+}
+
+const char* msd_last_error(const msd_ctx* c) { return c ? c->err.c_str() : g_err.c_str(); }
+
+int msd_seq_len(const msd_ctx* c, int seq) {
+  if (!c || seq < 0 || seq >= c->lim.max_batch) return -1;
+  return c->L[seq];
+}
+
+int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8_t* is_visual_h,
+                const void* visual_d, int32_t* first_token_h) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  const msd_model_desc& m = c->m;
+  if (seq < 0 || seq >= c->lim.max_batch) return fail(c, MSD_ERR_INVALID_ARG, "bad sequence");
+  if (n <= 0 || n > c->lim.max_prompt || !tokens_h || !is_visual_h || !first_token_h)
+    return fail(c, MSD_ERR_INVALID_ARG, "bad prompt");
+  if (n + c->lim.max_tree > c->lim.max_seq)
+    return fail(c, MSD_ERR_CAPACITY, "prompt does not fit the KV cache");
+  if (is_visual_h[n - 1]) return fail(c, MSD_ERR_INVALID_ARG, "prompt must end in a text token");
+  int n_vis = 0;
+  for (int i = 0; i < n; ++i) {
+    if (!is_visual_h[i] && (tokens_h[i] < 0 || tokens_h[i] >= m.vocab))
+      return fail(c, MSD_ERR_INVALID_ARG, "token id out of range");
+    n_vis += is_visual_h[i] ? 1 : 0;
+  }
+  if (n_vis && !visual_d) return fail(c, MSD_ERR_INVALID_ARG, "visual rows missing");
+  const int d = m.d_model;
+  // row descriptors: tok, vis, pos, slot, seq, hrow, dst, nxt
+  std::vector<int> a(8 * (size_t)n);
+  int* tok = a.data();
+  int* vis = tok + n;
+  int* pos = vis + n;
+  int* slot = pos + n;
+  int* sq = slot + n;
+  int* hrow = sq + n;
+  int* dst = hrow + n;
+  int* nxt = dst + n;
+  for (int i = 0, v = 0; i < n; ++i) {
+    tok[i] = is_visual_h[i] ? 0 : tokens_h[i];
+    vis[i] = is_visual_h[i] ? v++ : -1;
+    pos[i] = slot[i] = i;
+    sq[i] = seq;
+    hrow[i] = i;
+    dst[i] = (i == n - 1) ? seq * FEAT : -1;
+  }
+  for (int i = 0; i < n; ++i)
+    nxt[i] = (i + 1 < n) ? (is_visual_h[i + 1] ? -1 - vis[i + 1] : tokens_h[i + 1]) : 0;
+  int hdr[2] = {0, seq};
+  const size_t nb = sizeof(int) * (size_t)n;
+  TRY(upload_many(c, {{c->rows.tok, tok, nb}, {c->rows.vis, vis, nb}, {c->rows.pos, pos, nb},
+                      {c->rows.slot, slot, nb}, {c->rows.seq, sq, nb}, {c->rows.hrow, hrow, nb},
+                      {c->rows.dst, dst, nb}, {c->nxt, nxt, nb}, {c->prefix, hdr, sizeof(int)},
+                      {c->seq_ids, hdr + 1, sizeof(int)}}));
+  // target over the prompt
+  launch_embed(c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, c->x, c->st);
+  LAUNCHED(c);
+  TRY(forward_layers(c, false, 1, n, -1, n));
+  launch_rmsnorm(c->x, c->final_norm, n, d, m.norm_eps, c->h, c->st);
+  LAUNCHED(c);
+  TRY(gemm(c, EPI_F32, c->h + (size_t)(n - 1) * d, d, 1, c->lm_head, nullptr, m.vocab, d,
+           c->logits, nullptr, m.vocab));
+  launch_topk(c->logits, 1, m.vocab, 1, c->tk_idx, c->tk_val, nullptr, c->st);
+  LAUNCHED(c);
+  launch_set_int(c->d_root, seq, c->tk_idx, 0, c->st);
+  launch_set_int(c->nxt, n - 1, c->tk_idx, 0, c->st);
+  LAUNCHED(c);
+  // draft over the prompt: text rows f_down(Concat(h_i, e_{i+1})), visual rows e_i
+  launch_fc_input(c->h, nullptr, c->rows.hrow, c->embed, c->nxt, (const uint16_t*)visual_d, n, d,
+                  c->xn, c->st);
+  LAUNCHED(c);
+  TRY(draft_pass(c, 1, n, -1, n, n_vis ? (const uint16_t*)visual_d : nullptr));
+  launch_store_feat(c->x, n, c->rows.dst, d, c->dfeat, c->st);
+  LAUNCHED(c);
+  int st_len[2] = {n, 0};
+  TRY(upload_many(c, {{c->d_len + seq, st_len, sizeof(int)}, {c->pend_n + seq, st_len + 1, sizeof(int)}}));
+  int* back = c->stage + STAGE_INTS - 64;
+  HIPC(c, hipMemcpyAsync(back, c->d_root + seq, sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIPC(c, hipStreamSynchronize(c->st));
+  *first_token_h = back[0];
+  c->L[seq] = n;
+  c->pend[seq] = 0;
+  c->ready[seq] = 1;
+  return MSD_OK;
+}
+
+int msd_set_state(msd_ctx* c, int seq, int L, const void* h_d, int32_t next_token) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  if (seq < 0 || seq >= c->lim.max_batch || !h_d) return fail(c, MSD_ERR_INVALID_ARG, "bad argument");
+  if (L < 1 || L + c->lim.max_tree > c->lim.max_seq) return fail(c, MSD_ERR_CAPACITY, "length does not fit");
+  if (next_token < 0 || next_token >= c->m.vocab) return fail(c, MSD_ERR_INVALID_ARG, "token out of range");
+  int v[4] = {L, next_token, 1, next_token};
+  TRY(upload_many(c, {{c->d_len + seq, v, sizeof(int)}, {c->d_root + seq, v + 1, sizeof(int)},
+                      {c->pend_n + seq, v + 2, sizeof(int)},
+                      {c->pend_next + (size_t)seq * PEND, v + 3, sizeof(int)}}));
+  HIPC(c, hipMemcpyAsync(c->pend_h + (size_t)seq * PEND * c->m.d_model, h_d,
+                         sizeof(uint16_t) * c->m.d_model, hipMemcpyDeviceToDevice, c->st));
+  HIPC(c, hipStreamSynchronize(c->st));
+  c->L[seq] = L;
+  c->pend[seq] = 1;
+  c->ready[seq] = 1;
+  return MSD_OK;
+}
+
+int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_spec* spec,
+                   msd_tree* trees_d) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  TRY(check_seqs(c, n_seq, seqs_h));
+  if (!spec || !trees_d) return fail(c, MSD_ERR_INVALID_ARG, "null spec or tree buffer");
+  const msd_model_desc& m = c->m;
+  const int d = m.d_model;
+  int T = 0, D = 0, K = 0;
+  if (spec->kind == MSD_TREE_STATIC) {
+    TRY(prepare_static(c, spec));
+    T = c->sp_T;
+    D = c->sp_D;
+  } else if (spec->kind == MSD_TREE_DYNAMIC) {
+    K = spec->topk;
+    D = spec->depth;
+    T = spec->n_nodes + 1;
+    if (K < 1 || K > TOPK || D < 1 || T < 2 || T > c->lim.max_tree || K * (D - 1) > MSD_MAX_TREE ||
+        K + (D - 1) * K * K > POOL || spec->n_nodes > K + (D - 1) * K * K)
+      return fail(c, MSD_ERR_INVALID_ARG, "bad dynamic tree");
+  } else {
+    return fail(c, MSD_ERR_INVALID_ARG, "unknown tree kind");
+  }
+  int max_l = 0, r_max = 0;
+  const int region = std::max(T, spec->kind == MSD_TREE_DYNAMIC ? K * (D - 1) : T);
+  for (int i = 0; i < n_seq; ++i) {
+    const int b = seqs_h[i];
+    if (c->L[b] + region > c->lim.max_seq) return fail(c, MSD_ERR_CAPACITY, "KV cache full");
+    max_l = std::max(max_l, c->L[b]);
+    r_max = std::max(r_max, c->pend[b]);
+  }
+  TRY(upload(c, c->seq_ids, seqs_h, n_seq));
+  // 1. catch-up: pending rows through the draft head
+  if (r_max > 0) {
+    launch_catchup_rows(n_seq, c->seq_ids, c->d_len, c->pend_n, c->pend_next, r_max, PEND, FEAT,
+                        c->rows, c->prefix, c->st);
+    LAUNCHED(c);
+    launch_fc_input(c->pend_h, nullptr, c->rows.hrow, c->embed, c->rows.tok, nullptr,
+                    n_seq * r_max, d, c->xn, c->st);
+    LAUNCHED(c);
+    TRY(draft_pass(c, n_seq, r_max, -1, max_l, nullptr));
+    launch_store_feat(c->x, n_seq * r_max, c->rows.dst, d, c->dfeat, c->st);
+    LAUNCHED(c);
+    for (int i = 0; i < n_seq; ++i) c->pend[seqs_h[i]] = 0;
+  }
+  // 2. draft distribution at the root: the last catch-up feature of each
+  //    sequence goes through the LM head
+  for (int i = 0; i < n_seq; ++i)
+    HIPC(c, hipMemcpyAsync(c->x + (size_t)i * d, c->dfeat + (size_t)seqs_h[i] * FEAT * d,
+                           sizeof(float) * d, hipMemcpyDeviceToDevice, c->st));
+  if (spec->kind == MSD_TREE_STATIC) {
+    TRY(draft_head(c, n_seq, c->round_k[0]));
+    launch_tree_init_static(trees_d, n_seq, c->seq_ids, c->d_root, c->sp, T, c->st);
+    LAUNCHED(c);
+    launch_static_assign(trees_d, n_seq, c->sp, T, 0, c->tk_idx, c->round_k[0], 1, c->st);
+    LAUNCHED(c);
+    for (int dd = 1; dd < D; ++dd) {
+      const int nr = c->round_n[dd];
+      if (nr == 0) continue;
+      launch_static_rows(trees_d, n_seq, c->seq_ids, c->d_len, c->sp, c->round_off[dd], nr, dd,
+                         FEAT, c->rows, c->prefix, c->st);
+      LAUNCHED(c);
+      launch_fc_input(nullptr, c->dfeat, c->rows.hrow, c->embed, c->rows.tok, nullptr, n_seq * nr,
+                      d, c->xn, c->st);
+      LAUNCHED(c);
+      const int R = c->round_exp_end[dd];
+      TRY(draft_pass(c, n_seq, nr, R, max_l + R, nullptr));
+      launch_store_feat(c->x, n_seq * nr, c->rows.dst, d, c->dfeat, c->st);
+      LAUNCHED(c);
+      TRY(draft_head(c, n_seq * nr, c->round_k[dd]));
+      launch_static_assign(trees_d, n_seq, c->sp, T, dd, c->tk_idx, c->round_k[dd], nr, c->st);
+      LAUNCHED(c);
+    }
+  } else {
+    TRY(draft_head(c, n_seq, K));
+    launch_dyn_root(c->pool, n_seq, c->tk_idx, c->tk_val, c->tk_lse, K, c->st);
+    LAUNCHED(c);
+    int n_pool = K, exp_base = K;
+    for (int dd = 2; dd <= D; ++dd) {
+      launch_dyn_rows(c->pool, n_seq, c->seq_ids, c->d_len, K, dd, FEAT, c->rows, c->prefix, c->st);
+      LAUNCHED(c);
+      launch_fc_input(nullptr, c->dfeat, c->rows.hrow, c->embed, c->rows.tok, nullptr, n_seq * K,
+                      d, c->xn, c->st);
+      LAUNCHED(c);
+      const int R = exp_base;
+      TRY(draft_pass(c, n_seq, K, R, max_l + R, nullptr));
+      launch_store_feat(c->x, n_seq * K, c->rows.dst, d, c->dfeat, c->st);
+      LAUNCHED(c);
+      TRY(draft_head(c, n_seq * K, K));
+      launch_dyn_expand(c->pool, n_seq, c->tk_idx, c->tk_val, c->tk_lse, K, n_pool, exp_base, c->st);
+      LAUNCHED(c);
+      n_pool += K * K;
+      exp_base += K;
+    }
+    launch_dyn_finalize(c->pool, trees_d, n_seq, c->seq_ids, c->d_root, n_pool, T - 1, c->st);
+    LAUNCHED(c);
+  }
+  return MSD_OK;
+}
+
+int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d, int n_nodes,
+               int32_t* argmax_d, float* logits_d) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  TRY(check_seqs(c, n_seq, seqs_h));
+  const int T = n_nodes;
+  if (!trees_d || !argmax_d || T < 1 || T > c->lim.max_tree)
+    return fail(c, MSD_ERR_INVALID_ARG, "bad tree");
+  const msd_model_desc& m = c->m;
+  const int d = m.d_model, V = m.vocab;
+  int max_l = 0;
+  for (int i = 0; i < n_seq; ++i) {
+    const int b = seqs_h[i];
+    if (c->L[b] + T > c->lim.max_seq) return fail(c, MSD_ERR_CAPACITY, "KV cache full");
+    max_l = std::max(max_l, c->L[b]);
+  }
+  TRY(upload(c, c->seq_ids, seqs_h, n_seq));
+  const int rows = n_seq * T;
+  launch_verify_rows(trees_d, n_seq, c->seq_ids, c->d_len, T, V, c->rows, c->prefix, c->st);
+  LAUNCHED(c);
+  launch_embed(c->embed, c->rows.tok, nullptr, nullptr, rows, d, c->x, c->st);
+  LAUNCHED(c);
+  TRY(forward_layers(c, false, n_seq, T, T, max_l + T));
+  launch_rmsnorm(c->x, c->final_norm, rows, d, m.norm_eps, c->h, c->st);
+  LAUNCHED(c);
+  float* lg = logits_d ? logits_d : c->logits;
+  TRY(gemm(c, EPI_F32, c->h, d, rows, c->lm_head, nullptr, V, d, lg, nullptr, V));
+  launch_topk(lg, rows, V, 1, argmax_d, nullptr, nullptr, c->st);
+  LAUNCHED(c);
+  c->verified_T = T;
+  c->verified_nseq = n_seq;
+  return MSD_OK;
+}
+
+int msd_accept_compact(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,
+                       int n_nodes, const int32_t* argmax_d, int32_t* emitted_h,
+                       int32_t* n_emitted_h, int32_t* slot_map_d) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  TRY(check_seqs(c, n_seq, seqs_h));
+  if (!trees_d || !argmax_d || !emitted_h || !n_emitted_h)
+    return fail(c, MSD_ERR_INVALID_ARG, "null argument");
+  if (n_nodes != c->verified_T || n_seq != c->verified_nseq)
+    return fail(c, MSD_ERR_STATE, "accept must follow msd_verify of the same trees");
+  const int T = n_nodes, d = c->m.d_model;
+  TRY(upload(c, c->seq_ids, seqs_h, n_seq));
+  int* slots = slot_map_d ? slot_map_d : c->acc_slot;
+  launch_accept(trees_d, n_seq, c->seq_ids, T, argmax_d, c->acc_path, c->acc_n, c->acc_emit, slots,
+                c->d_len, c->st);
+  LAUNCHED(c);
+  launch_compact(c->tk, c->tv, c->m.n_layers, c->lim.max_batch, c->m.n_kv_heads, c->lim.max_seq,
+                 c->m.head_dim, n_seq, c->seq_ids, c->acc_path, c->acc_n, c->d_len, c->st);
+  LAUNCHED(c);
+  launch_commit(n_seq, c->seq_ids, c->acc_path, c->acc_n, c->acc_emit, c->h, T, d, c->pend_h,
+                c->pend_next, c->pend_n, PEND, c->d_len, c->d_root, c->st);
+  LAUNCHED(c);
+  int* back = c->stage + STAGE_INTS - (MSD_MAX_TREE + 1) * 8 - 64;
+  HIPC(c, hipMemcpyAsync(back, c->acc_emit, sizeof(int) * MSD_MAX_TREE * n_seq,
+                         hipMemcpyDeviceToHost, c->st));
+  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8, c->acc_n, sizeof(int) * n_seq,
+                         hipMemcpyDeviceToHost, c->st));
+  HIPC(c, hipStreamSynchronize(c->st));
+  for (int i = 0; i < n_seq; ++i) {
+    const int n = back[MSD_MAX_TREE * 8 + i];
+    n_emitted_h[i] = n;
+    for (int j = 0; j < MSD_MAX_TREE; ++j) emitted_h[i * MSD_MAX_TREE + j] = back[i * MSD_MAX_TREE + j];
+    c->L[seqs_h[i]] += n;
+    c->pend[seqs_h[i]] = n;
+  }
+  c->verified_T = 0;
+  return MSD_OK;
+}
+
+}  // extern "C"

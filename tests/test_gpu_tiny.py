@@ -1,0 +1,275 @@
+"""GPU parity on the tiny Llama-style workload (4 layers, d=256, vocab 4096):
+the HIP path through the C ABI against the float64 oracle on the same seeded
+weights and prompt.
+
+Tolerances (see tests/parity.py): logits and KV within 2e-2 of the row's
+max magnitude; tokens identical wherever the oracle's margin exceeds that;
+tree structure, accepted paths and slot maps bit-exact.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+import synth
+from synth.configs import TINY, TreeShape, chain_paths
+from oracle import model as M
+from oracle import msd as O
+from parity import RTOL, decided, rank_decided, row_close
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def bits_to_f64(t):
+    """int16 tensor of bf16 bits -> float64 numpy."""
+    a = t.cpu().numpy().astype(np.int16).view(np.uint16)
+    return M.widen(a)
+
+
+@pytest.fixture(scope="module")
+def setup():
+    from paper_2505_14260_amd.msd import Engine
+    wl = TINY
+    dims = wl.dims
+    w = synth.make_target_weights(dims, wl.seed)
+    dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
+    prompt = synth.make_prompt(wl)
+    eng = Engine(dims, w, dr, max_batch=2, max_seq=256, max_tree=64, max_prompt=128)
+    m = O.Models(dims, w, dr)
+    yield wl, eng, m, prompt
+    eng.close()
+
+
+def static_spec(paths):
+    from paper_2505_14260_amd.msd import make_static_spec
+    parent, rank, depth = synth.static_tree_arrays(paths)
+    return make_static_spec(parent[1:], rank[1:]), (parent, rank, depth)
+
+
+def upload_tree(eng, tree: O.Tree):
+    from paper_2505_14260_amd.msd import Tree
+    t = Tree()
+    t.n_nodes = tree.n
+    anc = tree.anc
+    for i in range(tree.n):
+        t.token[i] = int(tree.token[i])
+        t.parent[i] = int(tree.parent[i])
+        t.depth[i] = int(tree.depth[i])
+        t.anc[i] = int(anc[i])
+    raw = bytes(t)
+    dev = eng.new_trees(1)
+    dev.copy_(torch.frombuffer(bytearray(raw), dtype=torch.uint8))
+    return dev
+
+
+def test_prefill_kv_and_first_token(setup):
+    wl, eng, m, prompt = setup
+    print(f"case: prefill tiny seq 0 n={wl.prompt_len}", flush=True)
+    first = eng.prefill(0, *prompt)
+    st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=256)
+    if decided(logits[-1]):
+        assert first == f_ref
+    n = wl.prompt_len
+    tk, tv, dk, dv = eng.kv_views()
+    torch.cuda.synchronize()
+    for l in range(wl.dims.n_layers):
+        kg = bits_to_f64(tk[l, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        vg = bits_to_f64(tv[l, 0, :, :, :n].permute(2, 0, 1).reshape(n, -1))
+        ok, err = row_close(kg, st.kv.k[l, :n].reshape(n, -1))
+        assert ok, (l, "K", err)
+        ok, err = row_close(vg, st.kv.v[l, :n].reshape(n, -1))
+        assert ok, (l, "V", err)
+    # draft cache after the draft has consumed the prompt (Eq. decouple inputs)
+    O.draft_catch_up(m, st)
+    kg = bits_to_f64(dk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+    ok, err = row_close(kg, st.dkv.k[0, :n].reshape(n, -1))
+    assert ok, ("draft K", err)
+
+
+def test_verify_logits_on_fixed_tree(setup):
+    wl, eng, m, prompt = setup
+    print("case: verify tiny fixed tree", flush=True)
+    eng.prefill(0, *prompt)
+    st, first, _, _ = O.prefill(m, *prompt, max_slots=256)
+    parent, rank, depth = synth.static_tree_arrays(wl.tree.paths)
+    toks = synth.ids(len(parent), wl.seed, synth.TID_TEST, wl.dims.vocab)
+    toks[0] = first
+    tree = O.Tree(toks.astype(np.int32), parent, depth, np.zeros(len(parent)))
+    dev = upload_tree(eng, tree)
+    amax, logits = eng.verify([0], dev, tree.n, want_logits=True)
+    h_ref, lg_ref = O.verify(m, st, tree)
+    lg = logits.cpu().numpy()
+    ok, err = row_close(lg, lg_ref)
+    print(f"verify logits max rel err {err:.2e}")
+    assert ok, err
+    am = amax.cpu().numpy()
+    for i in range(tree.n):
+        if decided(lg_ref[i]):
+            assert am[i] == int(np.argmax(lg_ref[i])), i
+
+
+def test_accept_compact_bit_exact(setup):
+    wl, eng, m, prompt = setup
+    print("case: accept/compact tiny synthetic", flush=True)
+    eng.prefill(1, *prompt)
+    L = wl.prompt_len
+    parent, rank, depth = synth.static_tree_arrays(wl.tree.paths)
+    T = len(parent)
+    rng = np.random.default_rng(7)
+    for trial in range(4):
+        toks = np.zeros(T, dtype=np.int32)
+        for c in range(1, T):
+            toks[c] = 100 + c  # siblings distinct
+        toks[0] = 5
+        tree = O.Tree(toks, parent, depth, np.zeros(T))
+        dev = upload_tree(eng, tree)
+        eng.verify([1], dev, T)
+        # argmax chosen so a random branch is accepted to a random depth
+        amax = rng.integers(0, 50, T).astype(np.int32)
+        leaf = int(rng.integers(1, T))
+        path = []
+        u = leaf
+        while u > 0:
+            path.append(u)
+            u = int(parent[u])
+        path.reverse()
+        stop = int(rng.integers(0, len(path) + 1))
+        prev = 0
+        for u in path[:stop]:
+            amax[prev] = toks[u]
+            prev = u
+        tk, tv, _, _ = eng.kv_views()
+        Lc = eng_len = __import__("paper_2505_14260_amd.msd", fromlist=["x"]).msd_seq_len(eng.ctx, 1)
+        kv_bits = torch.from_numpy(rng.integers(-30000, 30000, size=tk[:, 1, :, Lc:Lc + T, :].shape,
+                                                dtype=np.int16)).cuda()
+        vv_bits = torch.from_numpy(rng.integers(-30000, 30000, size=tv[:, 1, :, :, Lc:Lc + T].shape,
+                                                dtype=np.int16)).cuda()
+        tk[:, 1, :, Lc:Lc + T, :] = kv_bits
+        tv[:, 1, :, :, Lc:Lc + T] = vv_bits
+        before_k = tk[:, 1].clone()
+        am_dev = torch.from_numpy(amax).cuda()
+        em, slots = eng.accept([1], dev, T, am_dev, want_slots=True)
+        ref_path, ref_emit = O.greedy_accept(tree, amax)
+        assert em[0] == ref_emit
+        sl = slots.cpu().numpy()[:len(ref_path)]
+        assert list(sl) == [Lc + j for j in ref_path]
+        # compaction against an out-of-place copy of the same bits
+        k_after = tk[:, 1].cpu().numpy()
+        k_before = before_k.cpu().numpy()
+        for j, u in enumerate(ref_path):
+            assert np.array_equal(k_after[:, :, Lc + j, :], k_before[:, :, Lc + u, :])
+        assert np.array_equal(k_after[:, :, :Lc, :], k_before[:, :, :Lc, :])
+        v_after = tv[:, 1].cpu().numpy()
+        vb = vv_bits.cpu().numpy()
+        for j, u in enumerate(ref_path):
+            assert np.array_equal(v_after[:, :, :, Lc + j], vb[:, :, :, u])
+        assert eng_len + len(ref_path) == __import__(
+            "paper_2505_14260_amd.msd", fromlist=["x"]).msd_seq_len(eng.ctx, 1)
+
+
+def oracle_static_with_logits(m, st, paths):
+    parent, rank, depth = synth.static_tree_arrays(paths)
+    root_feat = O.draft_catch_up(m, st)
+    root_logits = M.linear(root_feat[None, :], m.w["lm_head"])[0]
+    ex = O._DraftExpander(m, st, root_feat)
+    logs = {0: root_logits}
+
+    def expand(nodes, tokens, d):
+        pk = [None if parent[u] == 0 else int(parent[u]) for u in nodes]
+        rows = ex(list(nodes), pk, tokens, d)
+        for u, r in zip(nodes, rows):
+            logs[u] = r
+        return rows
+    tree = O.select_static_tree(parent, rank, depth, st.root, root_logits, expand)
+    return tree, logs, rank
+
+
+@pytest.mark.parametrize("paths", [TINY.tree.paths, tuple(chain_paths(4))], ids=["binary3", "chain4"])
+def test_static_draft_tree_matches_oracle(setup, paths):
+    wl, eng, m, prompt = setup
+    print(f"case: static draft tree tiny {len(paths)} nodes", flush=True)
+    eng.prefill(0, *prompt)
+    st, first, _, _ = O.prefill(m, *prompt, max_slots=256)
+    spec, _ = static_spec(paths)
+    dev = eng.new_trees(1)
+    eng.draft_tree([0], spec, dev)
+    g = eng.trees_to_host(dev, 1)[0]
+    ref, logs, rank = oracle_static_with_logits(m, st, paths)
+    assert g.n_nodes == ref.n
+    assert list(g.parent[:ref.n]) == list(ref.parent)
+    assert list(g.depth[:ref.n]) == list(ref.depth)
+    assert [int(x) for x in g.anc[:ref.n]] == [int(x) for x in ref.anc]
+    assert g.token[0] == ref.token[0] == first
+    skip = set()
+    checked = 0
+    for c in range(1, ref.n):
+        p = int(ref.parent[c])
+        if p in skip:
+            skip.add(c)
+            continue
+        if g.token[c] != ref.token[c]:
+            assert not rank_decided(logs[p], int(rank[c])), (c, g.token[c], ref.token[c])
+            skip.add(c)
+        else:
+            checked += 1
+    print(f"draft tree: {checked}/{ref.n - 1} nodes compared equal")
+    assert checked >= (ref.n - 1) // 2
+
+
+def test_speculative_decode_matches_greedy(setup):
+    wl, eng, m, prompt = setup
+    print("case: e2e tiny static tree", flush=True)
+    spec, _ = static_spec(wl.tree.paths)
+    toks, cycles = eng.generate(0, prompt, spec, wl.new_tokens)
+    ref, rows = O.greedy_generate(m, prompt, wl.new_tokens, return_logits=True)
+    first_bad = next((i for i in range(len(ref)) if toks[i] != ref[i]), None)
+    print(f"e2e: {first_bad if first_bad is not None else len(ref)}/{len(ref)} tokens equal; "
+          f"tau={np.mean(cycles):.2f}")
+    if first_bad is not None:
+        assert not decided(rows[first_bad]), (first_bad, toks[first_bad], ref[first_bad])
+
+
+def test_dynamic_tree_decode(setup):
+    wl, eng, m, prompt = setup
+    print("case: e2e tiny dynamic tree", flush=True)
+    from paper_2505_14260_amd.msd import make_dynamic_spec
+    shape = TreeShape("dynamic", 4, topk=3, n_nodes=12)
+    spec = make_dynamic_spec(shape.topk, shape.depth, shape.n_nodes)
+    eng.prefill(0, *prompt)
+    dev = eng.new_trees(1)
+    eng.draft_tree([0], spec, dev)
+    g = eng.trees_to_host(dev, 1)[0]
+    assert g.n_nodes == 13
+    for c in range(1, 13):
+        assert 0 <= g.parent[c] < c
+        assert g.depth[c] == g.depth[g.parent[c]] + 1
+        assert g.score[c] <= g.score[g.parent[c]] + 1e-6
+        assert int(g.anc[c]) == int(g.anc[g.parent[c]]) | (1 << c)
+    for p in range(13):
+        kids = [g.token[c] for c in range(1, 13) if g.parent[c] == p]
+        assert len(kids) == len(set(kids))
+    toks, cycles = eng.generate(0, prompt, spec, wl.new_tokens)
+    ref, rows = O.greedy_generate(m, prompt, wl.new_tokens, return_logits=True)
+    first_bad = next((i for i in range(len(ref)) if toks[i] != ref[i]), None)
+    print(f"e2e dynamic: {first_bad if first_bad is not None else len(ref)}/{len(ref)} equal")
+    if first_bad is not None:
+        assert not decided(rows[first_bad])
+
+
+def test_errors_and_capacity(setup):
+    wl, eng, m, prompt = setup
+    from paper_2505_14260_amd import msd as B
+    tokens, is_visual, visual = prompt
+    with pytest.raises(B.MSDError) as e:
+        eng.prefill(0, tokens[:10], is_visual[:10], visual)  # ends in a visual row
+    assert e.value.code == B.MSD_ERR_INVALID_ARG
+    with pytest.raises(B.MSDError) as e:
+        eng.prefill(0, np.zeros(200, np.int32), np.zeros(200, np.uint8), None)
+    assert e.value.code == B.MSD_ERR_INVALID_ARG  # beyond max_prompt
+    spec, _ = static_spec(wl.tree.paths)
+    dev = eng.new_trees(1)
+    with pytest.raises(B.MSDError) as e:
+        B.msd_accept_compact(eng.ctx, [0], dev.data_ptr(), 15, dev.data_ptr())
+    assert e.value.code == B.MSD_ERR_STATE

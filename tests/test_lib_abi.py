@@ -1,0 +1,56 @@
+"""The C ABI library loads and exports every entry point of include/msd.h
+(no compute: runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "msd.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(msd_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for n in ("msd_prefill", "msd_draft_tree", "msd_verify", "msd_accept_compact"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2505_14260_amd import msd
+    if not os.path.exists(msd.LIB_PATH):
+        pytest.skip("libmsd.so not built")
+    lib = ctypes.CDLL(msd.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_struct_sizes_match_header_layout():
+    from paper_2505_14260_amd import msd
+    # msd_tree: int32 + 3*64 int32 + 64 float, padded to 8, + 64 uint64
+    assert ctypes.sizeof(msd.Tree) == 4 + 3 * 256 + 256 + 4 + 512
+    assert ctypes.sizeof(msd.ModelDesc) == 9 * 4
+
+
+def test_buffer_sizes_and_errors_without_gpu():
+    from paper_2505_14260_amd import msd
+    if not os.path.exists(msd.LIB_PATH):
+        pytest.skip("libmsd.so not built")
+    d = msd.ModelDesc(2, 128, 4, 2, 64, 256, 512, 1e4, 1e-5)
+    lim = msd.Limits(1, 256, 16, 64)
+    tkv, dkv, ws = msd.msd_buffer_sizes(d, lim)
+    assert tkv == 2 * 1 * 2 * 256 * 64 * 2 and dkv == tkv // 2 and ws > 0
+    bad = msd.ModelDesc(2, 128, 4, 3, 64, 256, 512, 1e4, 1e-5)
+    with pytest.raises(msd.MSDError) as e:
+        msd.msd_buffer_sizes(bad, lim)
+    assert e.value.code == msd.MSD_ERR_INVALID_ARG
+    with pytest.raises(msd.MSDError):
+        msd.msd_buffer_sizes(msd.ModelDesc(2, 128, 4, 2, 96, 256, 512, 1e4, 1e-5), lim)
+    with pytest.raises(msd.MSDError):
+        msd.msd_buffer_sizes(d, msd.Limits(1, 256, 65, 64))
