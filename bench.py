@@ -1,0 +1,264 @@
+#!/usr/bin/env python3
+"""Decode benchmark of the MSD hot path on one MI355X.
+
+One step = one full MSD cycle of the LLaVA-1.5-7B-shaped workload (32 layers,
+d=4096, 32 heads x 128, FFN 11008, vocab 32000, bf16, random-init N(0,0.02)):
+draft tree (one-layer draft head, static 26-node depth-5 tree), tree-masked
+verification over a KV cache whose prefix holds the 576-row visual prompt plus
+64 text tokens, greedy acceptance and KV compaction.  All inputs are seeded
+synthetic tensors resident in HBM before timing starts.
+
+Prints one JSON line: value = decoded tokens/s over the timed cycles, plus the
+verify-step latency, the roofline of the dominant kernel (the gate/up GEMM,
+timed with events on the library's stream) and the CPU oracle timed on the
+host's cores on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verify-step ms + decoded tokens/sec, bs=1, 7B-shaped; % HBM roofline"
+HBM_PEAK_GBS = 8000.0
+SILU_KIND = 3
+
+
+def weight_bytes(dims):
+    d, H, KV, hd, F, V, nl = (dims.d_model, dims.n_heads, dims.n_kv_heads, dims.head_dim,
+                              dims.ffn_dim, dims.vocab, dims.n_layers)
+    return 2 * (nl * (d * (H + 2 * KV) * hd + H * hd * d + 3 * d * F + 2 * d) + V * d + d)
+
+
+def verify_bytes(dims, L, T, B=1):
+    """Algorithmic bytes of one verification: bf16 weights + the KV prefix and
+    tree rows read + the tree's embedding rows."""
+    kv = B * (L + T) * dims.n_layers * 2 * dims.n_kv_heads * dims.head_dim * 2
+    return weight_bytes(dims) + kv + B * T * dims.d_model * 2
+
+
+def silu_launch_bytes(dims, m):
+    """Algorithmic bytes of one gate/up launch: both weights, the input rows
+    and the bf16 output rows."""
+    d, F = dims.d_model, dims.ffn_dim
+    return 2 * F * d * 2 + m * d * 2 + m * F * 2
+
+
+def traffic_from_profile(kernel_src):
+    """HBM bytes per gate/up launch from the committed rocprofv3 counter
+    summary, or None when the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "k_gemm_silu_llava7b_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    sha = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+    if rec.get("k_gemm_sha256") != sha:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, w, dr, budget_s):
+    """The float64 oracle on a bounded sample: MSD cycles from a seeded
+    mid-generation state (target and draft caches filled for the prompt
+    length, one pending text row), as many as fit the time budget (>= 1)."""
+    from oracle import model as M
+    from oracle import msd as O
+    import synth
+    dims = wl.dims
+    L = wl.prompt_len
+    T = wl.tree.n_draft + 1
+    m = O.Models(dims, w, dr)
+    slots = L + 8 * T
+    kv = M.KVCache(dims.n_layers, slots, dims.n_kv_heads, dims.head_dim)
+    dkv = M.KVCache(1, slots, dims.n_kv_heads, dims.head_dim)
+    rng = np.random.default_rng(wl.seed)
+    kv.k[:, :L] = rng.standard_normal(kv.k[:, :L].shape)
+    kv.v[:, :L] = rng.standard_normal(kv.v[:, :L].shape)
+    dkv.k[:, :L] = rng.standard_normal(dkv.k[:, :L].shape)
+    dkv.v[:, :L] = rng.standard_normal(dkv.v[:, :L].shape)
+    tok = synth.ids(2, wl.seed, synth.TID_TEST, dims.vocab)
+    h = rng.standard_normal(dims.d_model)
+    st = O.SeqState(kv=kv, dkv=dkv, L=L, root=int(tok[1]),
+                    pending=[O.PendingRow(False, h=h, e_next=m.embed(tok[1]))])
+    st.L = L
+    arrays = None
+    if wl.tree.kind == "static":
+        arrays = synth.static_tree_arrays(wl.tree.paths)
+    st.L = L  # pending row sits at position L-1
+    emitted, cycles = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        tree = O.draft_tree(m, st, wl.tree, arrays)
+        h_t, logits = O.verify(m, st, tree)
+        amax = np.argmax(logits, axis=1)
+        _, em, _ = O.accept_and_compact(m, st, tree, h_t, amax)
+        emitted += len(em)
+        cycles += 1
+        el = time.perf_counter() - t0
+        if el > budget_s or st.L + 2 * T >= slots:
+            break
+    threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    return {"value": emitted / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{cycles} MSD cycle(s) of the same workload (draft tree + tree verify "
+                      f"at L={L} + accept) from a seeded synthetic cache state; "
+                      f"{el:.1f} s, {el / cycles * 1e3:.0f} ms/cycle"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=48)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--workload", default="llava-1.5-7b-shaped")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the decode path would shard).", file=sys.stderr)
+        sys.exit(2)
+    if int(os.environ.get("RANK", "0")) != 0:
+        return
+
+    import torch
+    import synth
+    from synth.configs import WORKLOADS
+    from paper_2505_14260_amd import msd as B
+
+    wl = WORKLOADS[args.workload]
+    dims = wl.dims
+    t_gen = time.perf_counter()
+    w = synth.make_target_weights(dims, wl.seed, wl.weight_sigma)
+    dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
+    prompt = synth.make_prompt(wl)
+    print(f"[bench] weights generated in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr,
+          flush=True)
+    T = wl.tree.n_draft + 1
+    max_seq = wl.prompt_len + (args.steps + args.warmup + 2) * (wl.tree.depth + 1) + 2 * T
+    max_seq = (max_seq + 255) // 256 * 256
+    eng = B.Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64,
+                   max_prompt=wl.prompt_len)
+    if wl.tree.kind == "static":
+        parent, rank, _ = synth.static_tree_arrays(wl.tree.paths)
+        spec = B.make_static_spec(parent[1:], rank[1:])
+    else:
+        spec = B.make_dynamic_spec(wl.tree.topk, wl.tree.depth, wl.tree.n_nodes)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    eng.prefill(0, *prompt)
+    prefill_ms = (time.perf_counter() - t0) * 1e3
+    print(f"[bench] prefill {prefill_ms:.1f} ms", file=sys.stderr, flush=True)
+    trees = eng.new_trees(1)
+    stream = torch.cuda.current_stream()
+
+    def cycle(ev=None):
+        if ev:
+            ev[0].record(stream)
+        eng.draft_tree([0], spec, trees)
+        if ev:
+            ev[1].record(stream)
+        amax, _ = eng.verify([0], trees, T)
+        if ev:
+            ev[2].record(stream)
+        em, _ = eng.accept([0], trees, T, amax)
+        if ev:
+            ev[3].record(stream)
+        return len(em[0])
+
+    for _ in range(args.warmup):
+        cycle()
+    torch.cuda.synchronize()
+    L_start = B.msd_seq_len(eng.ctx, 0)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    B.msd_trace_enable(eng.ctx, 64 * args.steps, 1 << SILU_KIND)
+    emitted = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        emitted.append(cycle(evs[i]))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    L_end = B.msd_seq_len(eng.ctx, 0)
+    recs = B.msd_trace_read(eng.ctx, 64 * args.steps)
+    B.msd_trace_enable(eng.ctx, 0)
+    draft_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    verify_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    accept_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    tokens = int(np.sum(emitted))
+    value = tokens / wall
+    L_mid = (L_start + L_end) // 2
+    vb = verify_bytes(dims, L_mid, T)
+    v_med = float(np.median(verify_ms))
+    silu = [r for r in recs if r[0] == SILU_KIND]
+    silu_ms = float(np.mean([r[4] for r in silu]))
+    silu_bytes = float(np.mean([silu_launch_bytes(dims, r[1]) for r in silu]))
+    achieved = silu_bytes / (silu_ms * 1e-3) / 1e9
+    traffic = traffic_from_profile(os.path.join(ROOT, "paper_2505_14260_amd", "csrc",
+                                                "k_gemm.hip"))
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights and prompt)",
+        "config": {
+            "workload": wl.name,
+            "layers": dims.n_layers, "d_model": dims.d_model, "heads": dims.n_heads,
+            "kv_heads": dims.n_kv_heads, "ffn": dims.ffn_dim, "vocab": dims.vocab,
+            "prompt": f"{wl.n_visual} visual + {wl.n_text} text",
+            "tree": (f"static {wl.tree.n_draft} nodes depth {wl.tree.depth}"
+                     if wl.tree.kind == "static" else
+                     f"dynamic top-{wl.tree.topk} depth {wl.tree.depth} {wl.tree.n_nodes} nodes"),
+            "batch": 1, "draft_fc_init": wl.draft_fc_mode,
+        },
+        "roofline": {
+            "kernel": "k_gemm<MT=1, SwiGLU> (gate+up projection)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "launches": len(silu),
+            "avg_launch_ms": round(silu_ms, 5),
+            "algorithmic_bytes_per_launch": int(silu_bytes),
+        },
+        "verify": {
+            "ms_median": round(v_med, 4),
+            "ms_p10": round(float(np.percentile(verify_ms, 10)), 4),
+            "ms_p90": round(float(np.percentile(verify_ms, 90)), 4),
+            "L_start": L_start, "L_end": L_end, "tree_nodes": T,
+            "algorithmic_bytes": int(vb),
+            "achieved_GBs": round(vb / (v_med * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(vb / (v_med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        },
+        "draft_ms_median": round(float(np.median(draft_ms)), 4),
+        "accept_ms_median": round(float(np.median(accept_ms)), 4),
+        "tau": round(tokens / args.steps, 3),
+        "prefill_ms": round(prefill_ms, 2),
+        "cpu_baseline": None,
+    }
+    eng.close()
+    del eng
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, w, dr, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

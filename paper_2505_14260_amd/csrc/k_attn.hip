@@ -32,25 +32,63 @@ struct AttnState {
   float m, l;
 };
 
+// K rows of the 32-key block starting at kb for the S^T product (A operand).
+template <int HD>
+MSD_DEV void load_k(uint4 (&kf)[HD / 16], const uint16_t* kbase, int kb, int k_valid) {
+  const int lane = threadIdx.x & 63;
+  const int krow = kb + perm_key(lane & 31);
+  const bool kval = krow < k_valid;
+  const uint16_t* kp = kbase + (size_t)(kval ? krow : 0) * HD + (HD / 2) * (lane >> 5);
+#pragma unroll
+  for (int c = 0; c < HD / 16; ++c)
+    kf[c] = kval ? *reinterpret_cast<const uint4*>(kp + 8 * c) : make_uint4(0, 0, 0, 0);
+}
+
+// V^T columns of the block for the O^T product (A operand), zero past k_valid.
+template <int HD>
+MSD_DEV void load_v(uint4 (&vf)[HD / 32][2], const uint16_t* vbase, int S, int kb, int k_valid) {
+  const int lane = threadIdx.x & 63;
+  const int i = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int dt = 0; dt < HD / 32; ++dt) {
+    const uint16_t* vp = vbase + (size_t)(dt * 32 + i) * S;
+#pragma unroll
+    for (int pk = 0; pk < 2; ++pk) {
+      const int k0 = kb + 16 * pk + 8 * h;
+      if (k0 + 8 <= k_valid) {
+        vf[dt][pk] = *reinterpret_cast<const uint4*>(vp + k0);
+      } else {
+        uint16_t t[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t[e] = (k0 + e < k_valid) ? vp[k0 + e] : (uint16_t)0;
+        vf[dt][pk] = make_uint4(t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4] | (t[5] << 16),
+                                t[6] | (t[7] << 16));
+      }
+    }
+  }
+}
+
 // Processes keys [k_begin, k_end) (k_begin multiple of 32) for the wave's 32
-// query columns.  vis(key, j-specific data) decides visibility.
+// query columns; vis(key) decides visibility.  The next block's K rows and
+// the current block's V columns are loaded while the scores are computed.
 template <int HD, typename Vis>
 MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qf)[HD / 16],
                           const uint16_t* kbase, const uint16_t* vbase, int S,
                           int k_begin, int k_end, int k_valid, float scale, Vis vis) {
   const int lane = threadIdx.x & 63;
-  const int i = lane & 31, h = lane >> 5;
+  const int h = lane >> 5;
+  if (k_begin >= k_end) return;
+  uint4 kf[HD / 16];
+  load_k<HD>(kf, kbase, k_begin, k_valid);
   for (int kb = k_begin; kb < k_end; kb += 32) {
+    uint4 vf[HD / 32][2];
+    load_v<HD>(vf, vbase, S, kb, k_valid);
     // ---- S^T tile: rows = keys, columns = query rows
-    const int krow = kb + perm_key(i);
-    const bool kval = krow < k_valid;
-    const uint16_t* kp = kbase + (size_t)(kval ? krow : 0) * HD + (HD / 2) * h;
     f32x16 s = {};
 #pragma unroll
-    for (int c = 0; c < HD / 16; ++c) {
-      uint4 kv = kval ? *reinterpret_cast<const uint4*>(kp + 8 * c) : make_uint4(0, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[c], s, 0, 0, 0);
-    }
+    for (int c = 0; c < HD / 16; ++c)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), qf[c], s, 0, 0, 0);
+    if (kb + 32 < k_end) load_k<HD>(kf, kbase, kb + 32, k_valid);
     float bm = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -86,23 +124,10 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qf)[HD / 16],
     for (int dt = 0; dt < HD / 32; ++dt) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
-      const uint16_t* vp = vbase + (size_t)(dt * 32 + i) * S;
 #pragma unroll
-      for (int pk = 0; pk < 2; ++pk) {
-        const int k0 = kb + 16 * pk + 8 * h;
-        uint4 vv;
-        if (k0 + 8 <= k_valid) {
-          vv = *reinterpret_cast<const uint4*>(vp + k0);
-        } else {
-          uint16_t t[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) t[e] = (k0 + e < k_valid) ? vp[k0 + e] : (uint16_t)0;
-          vv = make_uint4(t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4] | (t[5] << 16),
-                          t[6] | (t[7] << 16));
-        }
-        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), as_bf16x8(pb[pk]),
+      for (int pk = 0; pk < 2; ++pk)
+        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[dt][pk]), as_bf16x8(pb[pk]),
                                                            st.o[dt], 0, 0, 0);
-      }
     }
   }
 }
@@ -188,37 +213,38 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
   }
 }
 
+// One block per query column of a tile: merges the chunks' partial softmax
+// states in chunk order.
 template <int HD>
-__global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
+__global__ __launch_bounds__(HD) void k_tree_combine(AttnArgs a) {
   int t = blockIdx.x;
+  const int j = t & 31; t >>= 5;
   const int qt = t % a.qtiles; t /= a.qtiles;
   const int g = t % a.KV;
   const int sidx = t / a.KV;
   const int G = a.H / a.KV;
-  const size_t item0 = (size_t)blockIdx.x * a.n_chunks;
-  for (int o = threadIdx.x; o < 32 * HD; o += 256) {
-    const int j = o / HD, dim = o % HD;
-    const int qr = qt * 32 + j;
-    const int node = qr / G;
-    if (node >= a.nq) continue;
-    const int head = g * G + (qr - node * G);
-    const int dt = dim >> 5, dd = dim & 31;
-    const int hh = (dd >> 2) & 1, r = (dd >> 3) * 4 + (dd & 3);
-    const int idx = (dt * 16 + r) * 64 + j + 32 * hh;
-    float M = -INFINITY;
-    for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
-    float num = 0.f, den = 0.f;
-    if (M != -INFINITY) {
-      for (int c = 0; c < a.n_chunks; ++c) {
-        const float mc = a.part_ml[(item0 + c) * 64 + 2 * j];
-        const float w = (mc == -INFINITY) ? 0.f : __expf(mc - M);
-        den += w * a.part_ml[(item0 + c) * 64 + 2 * j + 1];
-        num += w * a.part_o[(item0 + c) * 32 * HD + idx];
-      }
+  const int qr = qt * 32 + j;
+  const int node = qr / G;
+  if (node >= a.nq) return;
+  const int head = g * G + (qr - node * G);
+  const size_t item0 = (size_t)(blockIdx.x >> 5) * a.n_chunks;
+  const int dim = threadIdx.x;
+  const int dt = dim >> 5, dd = dim & 31;
+  const int hh = (dd >> 2) & 1, r = (dd >> 3) * 4 + (dd & 3);
+  const int idx = (dt * 16 + r) * 64 + j + 32 * hh;
+  float M = -INFINITY;
+  for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
+  float num = 0.f, den = 0.f;
+  if (M != -INFINITY) {
+    for (int c = 0; c < a.n_chunks; ++c) {
+      const float mc = a.part_ml[(item0 + c) * 64 + 2 * j];
+      const float w = (mc == -INFINITY) ? 0.f : __expf(mc - M);
+      den += w * a.part_ml[(item0 + c) * 64 + 2 * j + 1];
+      num += w * a.part_o[(item0 + c) * 32 * HD + idx];
     }
-    a.out[(size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD + dim] =
-        f2bf(den > 0.f ? num / den : 0.f);
   }
+  a.out[(size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD + dim] =
+      f2bf(den > 0.f ? num / den : 0.f);
 }
 
 template <int HD>
@@ -265,11 +291,13 @@ void launch_tree_attention(AttnArgs a, hipStream_t st) {
   if (a.hd == 128) {
     hipLaunchKernelGGL(k_tree_attn<128>, grid, dim3(256), 0, st, a);
     if (a.n_chunks > 1)
-      hipLaunchKernelGGL(k_tree_combine<128>, dim3(a.n_seq * a.KV * a.qtiles), dim3(256), 0, st, a);
+      hipLaunchKernelGGL(k_tree_combine<128>, dim3(a.n_seq * a.KV * a.qtiles * 32), dim3(128), 0,
+                         st, a);
   } else {
     hipLaunchKernelGGL(k_tree_attn<64>, grid, dim3(256), 0, st, a);
     if (a.n_chunks > 1)
-      hipLaunchKernelGGL(k_tree_combine<64>, dim3(a.n_seq * a.KV * a.qtiles), dim3(256), 0, st, a);
+      hipLaunchKernelGGL(k_tree_combine<64>, dim3(a.n_seq * a.KV * a.qtiles * 32), dim3(64), 0, st,
+                         a);
   }
 }
 

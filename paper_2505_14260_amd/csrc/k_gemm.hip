@@ -3,241 +3,265 @@
 // The decode path multiplies a few dozen activation rows (tree nodes) by
 // large weight matrices, so the kernel is bound by streaming W from HBM once.
 // Layout of the work:
-//  - a workgroup is 4 waves; wave w owns 32 rows of W (n0 = 128*tile + 32*w)
-//    and all M rows of X (MT tiles of 32), over a range of K blocks of 64;
-//  - v_mfma_f32_32x32x16_bf16 with A = W rows, B = X^T columns.  The K
-//    index inside one MFMA may be any permutation shared by A and B, so each
-//    lane loads 32 physically contiguous bf16 of its W row (lanes l and l+32
-//    cover one 128-byte line of a row) and the same 32 columns of its X row;
-//  - split-K across workgroups with a deterministic reduction: partial tiles
-//    go to scratch, the last workgroup of a tile (integer atomic counter)
-//    sums them in split order and runs the epilogue, then resets the counter.
+//  - one workgroup of 8 waves owns 16*NT consecutive rows of W (and of W2 for
+//    the SwiGLU pair) and all M rows of X (MT tiles of 16); the 8 waves split
+//    K into contiguous ranges of 128-element blocks, and their partial tiles
+//    are summed through LDS in wave order, so no workgroup ever waits for
+//    another and the result does not depend on timing;
+//  - v_mfma_f32_16x16x32_bf16 with A = W rows and B = X^T columns.  The K
+//    index inside one MFMA may be any permutation shared by A and B, so a
+//    lane loads 32 physically contiguous bf16 of its W row (the four lanes of
+//    a row cover 256 contiguous bytes per block) and the same 32 columns of
+//    its X row;
+//  - the loads of the next P-1 blocks are in flight while a block's MFMAs
+//    run (a ring of P register stages), which keeps enough bytes outstanding
+//    per CU to cover HBM latency;
+//  - the weight may be given as up to three row segments (e.g. the q, k and v
+//    projections) that behave as one matrix of the summed height.
 #include "msd_internal.h"
 
 namespace msd {
 
 namespace {
 
-constexpr int KB = 64;  // K elements per block
+constexpr int KB = 128;     // K elements per block
+constexpr int WAVES = 8;
 
-template <int MT, int NW>
+template <int MT, int NT, int NW>
 struct Frag {
-  uint4 w[NW][4];
+  uint4 w[NW][NT][4];
   uint4 x[MT][4];
 };
 
-template <int MT, int NW>
-MSD_DEV void load_block(Frag<MT, NW>& f, const uint16_t* const* wrow, bool nvalid,
-                        const uint16_t* const* xrow, const bool* mvalid, int k, int K) {
+// Block load.  Rows past N or M were clamped to row 0 by the caller (they
+// only feed output rows that are never stored).  Full blocks (GUARD false)
+// load without any per-lane condition, which is what lets the compiler keep
+// several blocks in flight; the single partial block at the end of K
+// (K % 128 != 0) uses GUARD and zeroes the W columns past K.
+template <int MT, int NT, int NW, bool GUARD>
+MSD_DEV void load_block(Frag<MT, NT, NW>& f, const uint16_t* const (&wrow)[NW][NT],
+                        const uint16_t* const (&xrow)[MT], int k, int K) {
+  // k is this lane's first column of the block; K % 8 == 0
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     const int kk = k + 8 * c;
-    const bool ok = kk < K;
+    const bool ok = !GUARD || kk < K;
+    const int kc = ok ? kk : K - 8;
 #pragma unroll
     for (int w = 0; w < NW; ++w)
-      f.w[w][c] = (ok && nvalid) ? *reinterpret_cast<const uint4*>(wrow[w] + kk)
-                                 : make_uint4(0, 0, 0, 0);
 #pragma unroll
-    for (int t = 0; t < MT; ++t)
-      f.x[t][c] = (ok && mvalid[t]) ? *reinterpret_cast<const uint4*>(xrow[t] + kk)
-                                    : make_uint4(0, 0, 0, 0);
+      for (int s = 0; s < NT; ++s) {
+        const uint4 v = *reinterpret_cast<const uint4*>(wrow[w][s] + kc);
+        f.w[w][s][c] = ok ? v : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+    for (int t = 0; t < MT; ++t) f.x[t][c] = *reinterpret_cast<const uint4*>(xrow[t] + kc);
   }
 }
 
-template <int MT, int NW>
-MSD_DEV void mma_block(f32x16 (&acc)[NW][MT], const Frag<MT, NW>& f) {
+template <int MT, int NT, int NW>
+MSD_DEV void mma_block(f32x4 (&acc)[NW][NT][MT], const Frag<MT, NT, NW>& f) {
 #pragma unroll
   for (int c = 0; c < 4; ++c)
 #pragma unroll
     for (int w = 0; w < NW; ++w)
 #pragma unroll
-      for (int t = 0; t < MT; ++t)
-        acc[w][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(f.w[w][c]),
-                                                            as_bf16x8(f.x[t][c]),
-                                                            acc[w][t], 0, 0, 0);
+      for (int s = 0; s < NT; ++s)
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+          acc[w][s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              as_bf16x8(f.w[w][s][c]), as_bf16x8(f.x[t][c]), acc[w][s][t], 0, 0, 0);
 }
 
-template <int MT, int EPI>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+template <int MT, int NT, int EPI, int P>
+__global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int NW = (EPI == EPI_SILU) ? 2 : 1;
+  constexpr int TILE = NW * NT * MT * 4;  // floats per lane per wave
+  __shared__ float red[WAVES / 2][TILE][64];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int tile = blockIdx.x / a.splits;
-  const int split = blockIdx.x - tile * a.splits;
-  const int i = lane & 31, h = lane >> 5;
-  const int n0 = tile * 128 + wave * 32;
-  const int kb0 = split * a.kb_per_split;
-  const int kb1 = min(kb0 + a.kb_per_split, a.n_kblocks);
+  const int i = lane & 15, g = lane >> 4;
+  const int n0 = blockIdx.x * 16 * NT;
 
-  const int nrow = n0 + i;
-  const bool nvalid = nrow < a.N;
-  const uint16_t* wrow[NW];
-  wrow[0] = a.W + (size_t)(nvalid ? nrow : 0) * a.K;
-  if (NW == 2) wrow[NW - 1] = a.W2 + (size_t)(nvalid ? nrow : 0) * a.K;
+  const uint16_t* wrow[NW][NT];
+#pragma unroll
+  for (int s = 0; s < NT; ++s) {
+    const int n = n0 + 16 * s + i;
+    const int nn = n < a.N ? n : 0;
+    // 16-row tiles never straddle a segment (segment heights are multiples of 16)
+    const int seg = (nn < a.seg_end[0]) ? 0 : (nn < a.seg_end[1] ? 1 : 2);
+    const int base = seg == 0 ? 0 : a.seg_end[seg - 1];
+    wrow[0][s] = a.Wseg[seg] + (size_t)(nn - base) * a.K;
+    if (NW == 2) wrow[NW - 1][s] = a.W2 + (size_t)nn * a.K;
+  }
   const uint16_t* xrow[MT];
-  bool mvalid[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) {
-    const int m = t * 32 + i;
-    mvalid[t] = m < a.M;
-    xrow[t] = a.X + (size_t)(mvalid[t] ? m : 0) * a.ldx;
+    const int m = t * 16 + i;
+    xrow[t] = a.X + (size_t)(m < a.M ? m : 0) * a.ldx;
   }
 
-  f32x16 acc[NW][MT];
+  f32x4 acc[NW][NT][MT];
 #pragma unroll
   for (int w = 0; w < NW; ++w)
 #pragma unroll
-    for (int t = 0; t < MT; ++t)
+    for (int s = 0; s < NT; ++s)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[w][t][r] = 0.f;
+      for (int t = 0; t < MT; ++t) acc[w][s][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // contiguous, balanced range of full blocks for this wave; the trip count
+  // is uniform across the wave and the prefetch index is clamped rather than
+  // guarded
+  const int nkb = a.K / KB;
+  const int kb0 = (nkb * wave) / WAVES;
+  const int kb1 = (nkb * (wave + 1)) / WAVES;
   if (kb0 < kb1) {
-    Frag<MT, NW> cur;
-    load_block<MT, NW>(cur, wrow, nvalid, xrow, mvalid, kb0 * KB + 32 * h, a.K);
-    for (int kb = kb0; kb < kb1; ++kb) {
-      Frag<MT, NW> nxt;
-      if (kb + 1 < kb1)
-        load_block<MT, NW>(nxt, wrow, nvalid, xrow, mvalid, (kb + 1) * KB + 32 * h, a.K);
-      mma_block<MT, NW>(acc, cur);
-      cur = nxt;
-    }
-  }
-
-  if (a.splits > 1) {
-    constexpr int TILE_FLOATS = NW * MT * 16 * 64;
-    float* mine = a.partial + ((size_t)blockIdx.x * 4 + wave) * TILE_FLOATS;
+    const int last = kb1 - 1;
+    Frag<MT, NT, NW> ring[P];
 #pragma unroll
-    for (int w = 0; w < NW; ++w)
+    for (int p = 0; p < P; ++p)
+      load_block<MT, NT, NW, false>(ring[p], wrow, xrow, min(kb0 + p, last) * KB + 32 * g, a.K);
+    int kb = kb0;
+    for (; kb + P <= kb1; kb += P) {
 #pragma unroll
-      for (int t = 0; t < MT; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          __hip_atomic_store(mine + ((w * MT + t) * 16 + r) * 64 + lane, acc[w][t][r],
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __threadfence();
-    __syncthreads();
-    __shared__ int s_last;
-    if (threadIdx.x == 0) {
-      const int prev = atomicAdd(a.counters + tile, 1);
-      s_last = (prev == a.splits - 1);
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    const float* base = a.partial + ((size_t)tile * a.splits * 4 + wave) * TILE_FLOATS;
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-#pragma unroll
-      for (int t = 0; t < MT; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float s = 0.f;
-          const int off = ((w * MT + t) * 16 + r) * 64 + lane;
-          for (int sp = 0; sp < a.splits; ++sp) {
-            const float v = (sp == split)
-                                ? acc[w][t][r]
-                                : __hip_atomic_load(base + (size_t)sp * 4 * TILE_FLOATS + off,
-                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s += v;
-          }
-          acc[w][t][r] = s;
-        }
-    if (threadIdx.x == 0) a.counters[tile] = 0;
-  }
-
-  // C layout of the 32x32 MFMA: lane holds column (lane & 31) = output row m,
-  // register r holds W row n0 + 8*(r/4) + 4*(lane/32) + r%4.
-#pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    const int m = t * 32 + i;
-    if (m >= a.M) continue;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int n = n0 + 8 * (r >> 2) + 4 * h + (r & 3);
-      if (n >= a.N) continue;
-      const size_t o = (size_t)m * a.ldo + n;
-      if (EPI == EPI_F32) {
-        a.out_f32[o] = acc[0][t][r];
-      } else if (EPI == EPI_RESID) {
-        a.out_f32[o] += acc[0][t][r];
-      } else if (EPI == EPI_BF16) {
-        a.out_bf16[o] = f2bf(acc[0][t][r]);
-      } else {
-        const float g = acc[0][t][r], u = acc[NW - 1][t][r];
-        a.out_bf16[o] = f2bf(g / (1.f + __expf(-g)) * u);
+      for (int p = 0; p < P; ++p) {
+        mma_block<MT, NT, NW>(acc, ring[p]);
+        load_block<MT, NT, NW, false>(ring[p], wrow, xrow, min(kb + p + P, last) * KB + 32 * g,
+                                      a.K);
       }
     }
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+      if (p < kb1 - kb) mma_block<MT, NT, NW>(acc, ring[p]);
   }
+  if (wave == WAVES - 1 && nkb * KB < a.K) {
+    Frag<MT, NT, NW> f;
+    load_block<MT, NT, NW, true>(f, wrow, xrow, nkb * KB + 32 * g, a.K);
+    mma_block<MT, NT, NW>(acc, f);
+  }
+
+  // pairwise reduction over the 8 waves through LDS:
+  // ((w0 + w4) + (w2 + w6)) + ((w1 + w5) + (w3 + w7))
+#pragma unroll
+  for (int half = 4; half >= 1; half >>= 1) {
+    if (wave >= half && wave < 2 * half) {
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int s = 0; s < NT; ++s)
+#pragma unroll
+          for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              red[wave - half][((w * NT + s) * MT + t) * 4 + r][lane] = acc[w][s][t][r];
+    }
+    __syncthreads();
+    if (wave < half) {
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int s = 0; s < NT; ++s)
+#pragma unroll
+          for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              acc[w][s][t][r] += red[wave][((w * NT + s) * MT + t) * 4 + r][lane];
+    }
+    __syncthreads();
+  }
+  if (wave != 0) return;
+
+  // C layout of the 16x16 MFMA: lane holds column (lane & 15) = output row
+  // m, register r holds W row 4*(lane/16) + r of the 16-row tile.
+#pragma unroll
+  for (int s = 0; s < NT; ++s)
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = t * 16 + i;
+        const int n = n0 + 16 * s + 4 * g + r;
+        if (m >= a.M || n >= a.N) continue;
+        const float v0 = acc[0][s][t][r];
+        const size_t o = (size_t)m * a.ldo + n;
+        if (EPI == EPI_F32) {
+          a.out_f32[o] = v0;
+        } else if (EPI == EPI_RESID) {
+          a.out_f32[o] += v0;
+        } else if (EPI == EPI_BF16) {
+          a.out_bf16[o] = f2bf(v0);
+        } else {
+          const float v1 = acc[NW - 1][s][t][r];
+          a.out_bf16[o] = f2bf(v0 / (1.f + __expf(-v0)) * v1);
+        }
+      }
 }
 
-template <int MT>
+// ring depth: three stages when a stage is at most 64 VGPRs, else two
+template <int MT, int NT, int NW>
+constexpr int ring_depth() { return (16 * NT * NW + 16 * MT) <= 64 ? 3 : 2; }
+
+template <int MT, int NT>
 void dispatch_epi(int epi, dim3 grid, const GemmArgs& a, hipStream_t st) {
+  constexpr int P1 = ring_depth<MT, NT, 1>();
+  constexpr int P2 = ring_depth<MT, NT, 2>();
   switch (epi) {
-    case EPI_F32: hipLaunchKernelGGL((k_gemm<MT, EPI_F32>), grid, dim3(256), 0, st, a); break;
-    case EPI_BF16: hipLaunchKernelGGL((k_gemm<MT, EPI_BF16>), grid, dim3(256), 0, st, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((k_gemm<MT, EPI_RESID>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((k_gemm<MT, EPI_SILU>), grid, dim3(256), 0, st, a); break;
+    case EPI_F32: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_F32, P1>), grid, dim3(512), 0, st, a); break;
+    case EPI_BF16: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_BF16, P1>), grid, dim3(512), 0, st, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_RESID, P1>), grid, dim3(512), 0, st, a); break;
+    default: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_SILU, P2>), grid, dim3(512), 0, st, a); break;
   }
 }
 
 }  // namespace
 
-size_t gemm_partial_floats(int max_m, int max_n, int target_wgs) {
-  (void)max_n;
-  // splits * tiles <= max(target_wgs, tiles) and each split-K workgroup
-  // stores 4 waves * NW(<=2) * MT(<=2) * 16 * 64 floats.
-  (void)max_m;
-  const size_t per_wg = 4 * 2 * 2 * 16 * 64;
-  return per_wg * (size_t)(target_wgs * 2 + 64);
+void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
+                 const int* seg_rows, int n_seg, const uint16_t* W2, int K, float* out_f32,
+                 uint16_t* out_bf16, int ldo, const GemmScratch& s, hipStream_t st) {
+  int N = 0;
+  GemmArgs base{};
+  for (int q = 0; q < 3; ++q) {
+    if (q < n_seg) {
+      N += seg_rows[q];
+      base.Wseg[q] = Wseg[q];
+    } else {
+      base.Wseg[q] = Wseg[0];
+    }
+    base.seg_end[q] = N;
+  }
+  // wider row tiles for wide matrices (fewer re-reads of X) as long as the
+  // grid still covers every CU
+  const int tiles16 = (N + 15) / 16;
+  int nt = 1;
+  if (tiles16 >= 2 * s.target_wgs) nt = 2;
+  if (M > 32) nt = 1;
+  for (int m0 = 0; m0 < M; m0 += 64) {
+    const int mc = (M - m0) < 64 ? (M - m0) : 64;
+    GemmArgs a = base;
+    a.X = X + (size_t)m0 * ldx;
+    a.ldx = ldx;
+    a.M = mc;
+    a.W2 = W2;
+    a.N = N;
+    a.K = K;
+    a.out_f32 = out_f32 ? out_f32 + (size_t)m0 * ldo : nullptr;
+    a.out_bf16 = out_bf16 ? out_bf16 + (size_t)m0 * ldo : nullptr;
+    a.ldo = ldo;
+    dim3 grid((N + 16 * nt - 1) / (16 * nt));
+    if (mc <= 16) {
+      if (nt == 2) dispatch_epi<1, 2>(epi, grid, a, st); else dispatch_epi<1, 1>(epi, grid, a, st);
+    } else if (mc <= 32) {
+      if (nt == 2) dispatch_epi<2, 2>(epi, grid, a, st); else dispatch_epi<2, 1>(epi, grid, a, st);
+    } else {
+      dispatch_epi<4, 1>(epi, grid, a, st);
+    }
+  }
 }
 
 void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* W,
                  const uint16_t* W2, int N, int K, float* out_f32, uint16_t* out_bf16,
                  int ldo, const GemmScratch& s, hipStream_t st) {
-  const int n_tiles = (N + 127) / 128;
-  const int n_kblocks = (K + KB - 1) / KB;
-  const int mt_cap = 2;
-  for (int m0 = 0; m0 < M; m0 += 32 * mt_cap) {
-    const int mc = (M - m0) < 32 * mt_cap ? (M - m0) : 32 * mt_cap;
-    const int MT = mc <= 32 ? 1 : 2;
-    int splits = 1;
-    if (n_tiles < s.target_wgs) {
-      splits = (s.target_wgs + n_tiles - 1) / n_tiles;
-      if (splits > n_kblocks) splits = n_kblocks;
-      if (splits > 64) splits = 64;
-    }
-    int kb_per = (n_kblocks + splits - 1) / splits;
-    splits = (n_kblocks + kb_per - 1) / kb_per;
-    const int NW = (epi == EPI_SILU) ? 2 : 1;
-    if (splits > 1) {
-      const size_t need = (size_t)n_tiles * splits * 4 * NW * MT * 16 * 64;
-      if (need > s.partial_floats || n_tiles > s.n_counters) {
-        splits = 1;
-        kb_per = n_kblocks;
-      }
-    }
-    GemmArgs a;
-    a.X = X + (size_t)m0 * ldx;
-    a.ldx = ldx;
-    a.M = mc;
-    a.W = W;
-    a.W2 = W2;
-    a.N = N;
-    a.K = K;
-    a.splits = splits;
-    a.kb_per_split = kb_per;
-    a.n_kblocks = n_kblocks;
-    a.partial = s.partial;
-    a.counters = s.counters;
-    a.out_f32 = out_f32 ? out_f32 + (size_t)m0 * ldo : nullptr;
-    a.out_bf16 = out_bf16 ? out_bf16 + (size_t)m0 * ldo : nullptr;
-    a.ldo = ldo;
-    dim3 grid(n_tiles * splits);
-    if (MT == 1)
-      dispatch_epi<1>(epi, grid, a, st);
-    else
-      dispatch_epi<2>(epi, grid, a, st);
-  }
+  launch_gemm(epi, X, ldx, M, &W, &N, 1, W2, K, out_f32, out_bf16, ldo, s, st);
 }
 
 }  // namespace msd

@@ -124,57 +124,20 @@ __global__ __launch_bounds__(256) void k_fc_input(const uint16_t* h, const float
 }
 
 // Per-row top-k over the vocabulary (value descending, then id ascending)
-// and the row's logsumexp.  One block of 256 threads per row, k <= 16.
+// and the row's logsumexp, in two phases: every (row, slice) block reduces a
+// slice of the vocabulary to its own top-k and (max, sum of exp) pair; one
+// block per row then merges the slices in slice order.
 constexpr int TOPK_MAX = 16;
+constexpr int TOPK_SLICE = 2048;
 
 MSD_DEV bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
-__global__ __launch_bounds__(256) void k_topk(const float* logits, int V, int k, int* out_idx,
-                                              float* out_val, float* out_lse) {
-  __shared__ float sv[256];
-  __shared__ int si[256];
-  __shared__ float sm[4];
-  const int row = blockIdx.x;
-  const float* x = logits + (size_t)row * V;
-  float lv[TOPK_MAX];
-  int li[TOPK_MAX];
-  int n = 0;
-  float mloc = -INFINITY, sloc = 0.f;
-  for (int v = threadIdx.x; v < V; v += 256) {
-    const float val = x[v];
-    if (val > mloc) {
-      sloc = sloc * __expf(mloc - val) + 1.f;
-      mloc = val;
-    } else {
-      sloc += __expf(val - mloc);
-    }
-    // insert keeping (value desc, id asc); ids arrive in increasing order
-    if (n < k || val > lv[k - 1]) {
-      int p = (n < k) ? n : k - 1;
-      while (p > 0 && val > lv[p - 1]) {
-        lv[p] = lv[p - 1];
-        li[p] = li[p - 1];
-        --p;
-      }
-      lv[p] = val;
-      li[p] = v;
-      if (n < k) ++n;
-    }
-  }
-  // logsumexp: block max then fixed-order sum of rescaled partial sums
-  float mm = mloc;
-  for (int o = 32; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
-  if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = mm;
-  __syncthreads();
-  const float M = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
-  __syncthreads();
-  __shared__ float ssum[4];
-  const float part = (mloc == -INFINITY) ? 0.f : sloc * __expf(mloc - M);
-  const float tot = block_sum_256(part, ssum);
-  if (threadIdx.x == 0 && out_lse) out_lse[row] = M + __logf(tot);
-  // k rounds: each thread offers its best remaining candidate
+// Block-wide selection of the k best (value, id) pairs offered by each
+// thread's sorted local list (lv, li of length n).
+MSD_DEV void block_select(const float* lv, const int* li, int n, int k, float* sv, int* si,
+                          float* out_v, int* out_i) {
   int head = 0;
   for (int q = 0; q < k; ++q) {
     sv[threadIdx.x] = (head < n) ? lv[head] : -INFINITY;
@@ -196,9 +159,90 @@ __global__ __launch_bounds__(256) void k_topk(const float* logits, int V, int k,
     __syncthreads();
     if (head < n && li[head] == win) ++head;
     if (threadIdx.x == 0) {
-      out_idx[(size_t)row * k + q] = win;
-      if (out_val) out_val[(size_t)row * k + q] = wv;
+      out_i[q] = win;
+      out_v[q] = wv;
     }
+  }
+}
+
+MSD_DEV void insert_sorted(float* lv, int* li, int& n, int k, float val, int id) {
+  if (n < k || better(val, id, lv[k - 1], li[k - 1])) {
+    int p = (n < k) ? n : k - 1;
+    while (p > 0 && better(val, id, lv[p - 1], li[p - 1])) {
+      lv[p] = lv[p - 1];
+      li[p] = li[p - 1];
+      --p;
+    }
+    lv[p] = val;
+    li[p] = id;
+    if (n < k) ++n;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_topk_slice(const float* logits, int V, int k, int n_slices,
+                                                    float* cand_v, int* cand_i, float2* stats) {
+  __shared__ float sv[256];
+  __shared__ int si[256];
+  __shared__ float sm[4];
+  __shared__ float ssum[4];
+  const int row = blockIdx.x / n_slices;
+  const int sl = blockIdx.x - row * n_slices;
+  const float* x = logits + (size_t)row * V;
+  const int v0 = sl * TOPK_SLICE, v1 = min(V, v0 + TOPK_SLICE);
+  float lv[TOPK_MAX];
+  int li[TOPK_MAX];
+  int n = 0;
+  float mloc = -INFINITY, sloc = 0.f;
+  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
+    const float val = x[v];
+    if (val > mloc) {
+      sloc = sloc * __expf(mloc - val) + 1.f;
+      mloc = val;
+    } else {
+      sloc += __expf(val - mloc);
+    }
+    insert_sorted(lv, li, n, k, val, v);
+  }
+  float mm = mloc;
+  for (int o = 32; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
+  if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = mm;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
+  const float part = (mloc == -INFINITY) ? 0.f : sloc * __expf(mloc - M);
+  const float tot = block_sum_256(part, ssum);
+  if (threadIdx.x == 0) stats[blockIdx.x] = make_float2(M, tot);
+  block_select(lv, li, n, k, sv, si, cand_v + (size_t)blockIdx.x * k,
+               cand_i + (size_t)blockIdx.x * k);
+}
+
+__global__ __launch_bounds__(256) void k_topk_merge(int k, int n_slices, const float* cand_v,
+                                                    const int* cand_i, const float2* stats,
+                                                    int* out_idx, float* out_val, float* out_lse) {
+  __shared__ float sv[256];
+  __shared__ int si[256];
+  __shared__ float ov[TOPK_MAX];
+  __shared__ int oi[TOPK_MAX];
+  const int row = blockIdx.x;
+  const size_t c0 = (size_t)row * n_slices * k;
+  float lv[TOPK_MAX];
+  int li[TOPK_MAX];
+  int n = 0;
+  for (int c = threadIdx.x; c < n_slices * k; c += 256)
+    insert_sorted(lv, li, n, k, cand_v[c0 + c], cand_i[c0 + c]);
+  block_select(lv, li, n, k, sv, si, ov, oi);
+  __syncthreads();
+  if (threadIdx.x < k) {
+    out_idx[(size_t)row * k + threadIdx.x] = oi[threadIdx.x];
+    if (out_val) out_val[(size_t)row * k + threadIdx.x] = ov[threadIdx.x];
+  }
+  if (threadIdx.x == 0 && out_lse) {
+    const float2* st = stats + (size_t)row * n_slices;
+    float M = -INFINITY;
+    for (int q = 0; q < n_slices; ++q) M = fmaxf(M, st[q].x);
+    float tot = 0.f;
+    for (int q = 0; q < n_slices; ++q)
+      tot += (st[q].x == -INFINITY) ? 0.f : st[q].y * __expf(st[q].x - M);
+    out_lse[row] = M + __logf(tot);
   }
 }
 
@@ -249,10 +293,22 @@ void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const
                      visual, d, out);
 }
 
+size_t topk_scratch_floats(int rows, int V) {
+  const int n_slices = (V + TOPK_SLICE - 1) / TOPK_SLICE;
+  return (size_t)rows * n_slices * (2 * TOPK_MAX + 2);
+}
+
 void launch_topk(const float* logits, int rows, int V, int k, int* idx, float* val, float* lse,
-                 hipStream_t st) {
+                 float* scratch, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_topk, dim3(rows), dim3(256), 0, st, logits, V, k, idx, val, lse);
+  const int n_slices = (V + TOPK_SLICE - 1) / TOPK_SLICE;
+  float* cand_v = scratch;
+  int* cand_i = reinterpret_cast<int*>(cand_v + (size_t)rows * n_slices * TOPK_MAX);
+  float2* stats = reinterpret_cast<float2*>(cand_i + (size_t)rows * n_slices * TOPK_MAX);
+  hipLaunchKernelGGL(k_topk_slice, dim3(rows * n_slices), dim3(256), 0, st, logits, V, k, n_slices,
+                     cand_v, cand_i, stats);
+  hipLaunchKernelGGL(k_topk_merge, dim3(rows), dim3(256), 0, st, k, n_slices, cand_v, cand_i,
+                     stats, idx, val, lse);
 }
 
 }  // namespace msd

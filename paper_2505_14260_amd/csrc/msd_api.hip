@@ -47,8 +47,7 @@ struct Carver {
 
 struct Plan {
   int rows_max, lrows, ld_qkv;
-  size_t gemm_floats, attn_floats;
-  int counters;
+  size_t attn_floats;
 };
 
 Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
@@ -56,11 +55,9 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
   p.rows_max = std::max(lim.max_prompt, lim.max_batch * MSD_MAX_TREE);
   p.lrows = lim.max_batch * MSD_MAX_TREE;
   p.ld_qkv = (m.n_heads + 2 * m.n_kv_heads) * m.head_dim;
-  p.gemm_floats = gemm_partial_floats(0, 0, 1024);
   const int G = m.n_heads / m.n_kv_heads;
   const int qtiles = (MSD_MAX_TREE * G + 31) / 32;
   p.attn_floats = attn_partial_floats(lim.max_batch, m.n_kv_heads, qtiles, 64, m.head_dim);
-  p.counters = 8192;
   return p;
 }
 
@@ -90,7 +87,7 @@ struct msd_ctx {
   StaticSpec sp;
   DynPool pool;
   GemmScratch gs;
-  float *att_po, *att_ml;
+  float *att_po, *att_ml, *tk_scratch;
   float2* rope;
   // host
   int* stage;  // pinned staging
@@ -101,6 +98,16 @@ struct msd_ctx {
   std::vector<int> round_off, round_n, round_k, round_exp_end;
   int sp_T = 0, sp_D = 0;
   int verified_T = 0, verified_nseq = 0;
+  // optional per-GEMM event trace (msd_trace_enable)
+  struct TraceRec {
+    int epi, M, N, K;
+    hipEvent_t a, b;
+  };
+  std::vector<TraceRec> trace;
+  std::vector<hipEvent_t> ev_pool;
+  size_t trace_cap = 0;
+  bool tracing = false;
+  int trace_kinds = 0;  // bit per epilogue kind
 };
 
 namespace {
@@ -190,13 +197,10 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->pool.exp_idx = cv.take<int>((size_t)B * POOL);
   t->pool.mask = cv.take<uint64_t>((size_t)B * POOL);
   t->pool.frontier = cv.take<int>((size_t)B * TOPK);
-  t->gs.partial = cv.take<float>(p.gemm_floats);
-  t->gs.partial_floats = p.gemm_floats;
-  t->gs.counters = cv.take<int>(p.counters);
-  t->gs.n_counters = p.counters;
   t->att_po = cv.take<float>(p.attn_floats);
   t->att_ml = cv.take<float>(p.attn_floats / m.head_dim * 2 + 64);
   t->rope = cv.take<float2>((size_t)lim.max_seq * (m.head_dim / 2));
+  t->tk_scratch = cv.take<float>(topk_scratch_floats(p.lrows, m.vocab));
   return cv.off + 256;
 }
 
@@ -248,8 +252,37 @@ int upload(msd_ctx* c, int* dst, const int* src, int n) {
 
 int gemm(msd_ctx* c, int epi, const uint16_t* X, int ldx, int M, const uint16_t* W,
          const uint16_t* W2, int N, int K, float* of, uint16_t* ob, int ldo) {
+  const bool tr = c->tracing && ((c->trace_kinds >> epi) & 1) && c->trace.size() < c->trace_cap;
+  if (tr) {
+    msd_ctx::TraceRec r{epi, M, N, K, c->ev_pool[2 * c->trace.size()],
+                        c->ev_pool[2 * c->trace.size() + 1]};
+    HIPC(c, hipEventRecord(r.a, c->st));
+    c->trace.push_back(r);
+  }
   launch_gemm(epi, X, ldx, M, W, W2, N, K, of, ob, ldo, c->gs, c->st);
   LAUNCHED(c);
+  if (tr) HIPC(c, hipEventRecord(c->trace.back().b, c->st));
+  return MSD_OK;
+}
+
+// q, k and v projections as one launch over the row-concatenated weight.
+int gemm_qkv(msd_ctx* c, const LayerW& w, int rows) {
+  const msd_model_desc& m = c->m;
+  const uint16_t* seg[3] = {w.wq, w.wk, w.wv};
+  const int hd = m.head_dim;
+  const int nrow[3] = {m.n_heads * hd, m.n_kv_heads * hd, m.n_kv_heads * hd};
+  const int N = nrow[0] + nrow[1] + nrow[2];
+  const bool tr = c->tracing && ((c->trace_kinds >> EPI_F32) & 1) && c->trace.size() < c->trace_cap;
+  if (tr) {
+    msd_ctx::TraceRec r{EPI_F32, rows, N, m.d_model, c->ev_pool[2 * c->trace.size()],
+                        c->ev_pool[2 * c->trace.size() + 1]};
+    HIPC(c, hipEventRecord(r.a, c->st));
+    c->trace.push_back(r);
+  }
+  launch_gemm(EPI_F32, c->xn, m.d_model, rows, seg, nrow, 3, nullptr, m.d_model, c->qkv, nullptr,
+              c->plan.ld_qkv, c->gs, c->st);
+  LAUNCHED(c);
+  if (tr) HIPC(c, hipEventRecord(c->trace.back().b, c->st));
   return MSD_OK;
 }
 
@@ -266,7 +299,6 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
   const msd_model_desc& m = c->m;
   const int rows = n_seq * nq;
   const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim;
-  const int ld = c->plan.ld_qkv;
   const int nl = draft ? 1 : m.n_layers;
   const int B = c->lim.max_batch, S = c->lim.max_seq;
   const size_t layer_kv = (size_t)B * KV * S * hd;
@@ -276,10 +308,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     uint16_t* vc = (draft ? c->dv : c->tv) + (size_t)l * layer_kv;
     launch_rmsnorm(c->x, w.n1, rows, d, m.norm_eps, c->xn, c->st);
     LAUNCHED(c);
-    TRY(gemm(c, EPI_F32, c->xn, d, rows, w.wq, nullptr, H * hd, d, c->qkv, nullptr, ld));
-    TRY(gemm(c, EPI_F32, c->xn, d, rows, w.wk, nullptr, KV * hd, d, c->qkv + H * hd, nullptr, ld));
-    TRY(gemm(c, EPI_F32, c->xn, d, rows, w.wv, nullptr, KV * hd, d, c->qkv + (H + KV) * hd,
-             nullptr, ld));
+    TRY(gemm_qkv(c, w, rows));
     launch_rope_kv(c->qkv, rows, H, KV, hd, c->rows.pos, c->rows.seq, c->rows.slot, c->rope,
                    c->q, kc, vc, S, c->st);
     LAUNCHED(c);
@@ -308,15 +337,18 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       const int G = H / KV;
       a.R = tree_R;
       a.qtiles = (nq * G + 31) / 32;
+      // key chunks: enough waves to spread the cache over the chip, but at
+      // least 128 keys per wave so the partial results stay small
       const int base_items = n_seq * KV * a.qtiles;
-      int chunks = std::max(1, 1024 / std::max(1, base_items));
-      chunks = std::min(chunks, (max_ltot + 63) / 64);
-      chunks = std::max(chunks, 1);
+      int chunks = std::max(1, 512 / std::max(1, base_items));
       while (chunks > 1 && attn_partial_floats(n_seq, KV, a.qtiles, chunks, hd) >
                                c->plan.attn_floats)
         --chunks;
       int ck = (max_ltot + chunks - 1) / chunks;
-      ck = (ck + 31) / 32 * 32;
+      ck = std::max(128, (ck + 31) / 32 * 32);
+      while (attn_partial_floats(n_seq, KV, a.qtiles, (max_ltot + ck - 1) / ck, hd) >
+             c->plan.attn_floats)
+        ck += 128;
       a.chunk_keys = ck;
       a.n_chunks = (max_ltot + ck - 1) / ck;
       launch_tree_attention(a, c->st);
@@ -351,7 +383,7 @@ int draft_head(msd_ctx* c, int rows, int k) {
   launch_to_bf16(c->x, rows * d, c->xn, c->st);
   LAUNCHED(c);
   TRY(gemm(c, EPI_F32, c->xn, d, rows, c->lm_head, nullptr, V, d, c->logits, nullptr, V));
-  launch_topk(c->logits, rows, V, k, c->tk_idx, c->tk_val, c->tk_lse, c->st);
+  launch_topk(c->logits, rows, V, k, c->tk_idx, c->tk_val, c->tk_lse, c->tk_scratch, c->st);
   LAUNCHED(c);
   return MSD_OK;
 }
@@ -490,7 +522,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   c->dk = (uint16_t*)bufs->draft_k;
   c->dv = (uint16_t*)bufs->draft_v;
   carve(c, *m, *lim, (char*)bufs->workspace);
-  c->gs.target_wgs = 512;
+  c->gs.target_wgs = 256;
   if (const char* e = std::getenv("MSD_GEMM_WGS")) c->gs.target_wgs = std::max(1, atoi(e));
   c->L.assign(lim->max_batch, 0);
   c->pend.assign(lim->max_batch, 0);
@@ -501,7 +533,6 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     return fail(nullptr, MSD_ERR_HIP, std::string("hipHostMalloc: ") + hipGetErrorString(e));
   }
   auto init = [&]() -> int {
-    HIPC(c, hipMemsetAsync(c->gs.counters, 0, sizeof(int) * c->gs.n_counters, c->st));
     // never-written cache slots may be read (with zero weight) by padded rows
     const size_t tkv = kv_bytes(*m, *lim, m->n_layers), dkv = kv_bytes(*m, *lim, 1);
     HIPC(c, hipMemsetAsync(c->tk, 0, tkv, c->st));
@@ -530,6 +561,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
 void msd_destroy(msd_ctx* c) {
   if (!c) return;
   (void)hipStreamSynchronize(c->st);
+  for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   (void)hipHostFree(c->stage);
   delete c;
 }
@@ -593,7 +625,7 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
   LAUNCHED(c);
   TRY(gemm(c, EPI_F32, c->h + (size_t)(n - 1) * d, d, 1, c->lm_head, nullptr, m.vocab, d,
            c->logits, nullptr, m.vocab));
-  launch_topk(c->logits, 1, m.vocab, 1, c->tk_idx, c->tk_val, nullptr, c->st);
+  launch_topk(c->logits, 1, m.vocab, 1, c->tk_idx, c->tk_val, nullptr, c->tk_scratch, c->st);
   LAUNCHED(c);
   launch_set_int(c->d_root, seq, c->tk_idx, 0, c->st);
   launch_set_int(c->nxt, n - 1, c->tk_idx, 0, c->st);
@@ -760,7 +792,7 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
   LAUNCHED(c);
   float* lg = logits_d ? logits_d : c->logits;
   TRY(gemm(c, EPI_F32, c->h, d, rows, c->lm_head, nullptr, V, d, lg, nullptr, V));
-  launch_topk(lg, rows, V, 1, argmax_d, nullptr, nullptr, c->st);
+  launch_topk(lg, rows, V, 1, argmax_d, nullptr, nullptr, c->tk_scratch, c->st);
   LAUNCHED(c);
   c->verified_T = T;
   c->verified_nseq = n_seq;
@@ -803,6 +835,42 @@ int msd_accept_compact(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_t
   }
   c->verified_T = 0;
   return MSD_OK;
+}
+
+int msd_trace_enable(msd_ctx* c, int capacity, int kinds) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  HIPC(c, hipStreamSynchronize(c->st));
+  c->trace.clear();
+  if (capacity <= 0) {
+    c->tracing = false;
+    return MSD_OK;
+  }
+  while (c->ev_pool.size() < 2 * (size_t)capacity) {
+    hipEvent_t e;
+    HIPC(c, hipEventCreate(&e));
+    c->ev_pool.push_back(e);
+  }
+  c->trace_cap = (size_t)capacity;
+  c->trace_kinds = kinds;
+  c->tracing = true;
+  return MSD_OK;
+}
+
+int msd_trace_read(msd_ctx* c, int max_recs, msd_trace_rec* out) {
+  if (!c || (max_recs > 0 && !out)) return fail(c, MSD_ERR_INVALID_ARG, "bad argument");
+  HIPC(c, hipStreamSynchronize(c->st));
+  const int n = std::min((int)c->trace.size(), max_recs);
+  for (int i = 0; i < n; ++i) {
+    const msd_ctx::TraceRec& r = c->trace[i];
+    float ms = 0.f;
+    HIPC(c, hipEventElapsedTime(&ms, r.a, r.b));
+    out[i].kind = r.epi;
+    out[i].m = r.M;
+    out[i].n = r.N;
+    out[i].k = r.K;
+    out[i].ms = ms;
+  }
+  return n;
 }
 
 }  // extern "C"

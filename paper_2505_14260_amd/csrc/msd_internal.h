@@ -30,31 +30,29 @@ namespace msd {
 enum Epilogue { EPI_F32 = 0, EPI_BF16 = 1, EPI_RESID = 2, EPI_SILU = 3 };
 
 struct GemmArgs {
-  const uint16_t* X;   // [M][ldx] bf16
+  const uint16_t* X;        // [M][ldx] bf16
   int ldx, M;
-  const uint16_t* W;   // [N][K] bf16
-  const uint16_t* W2;  // second weight (EPI_SILU: up projection), same shape
+  const uint16_t* Wseg[3];  // [N][K] bf16 given as up to three row segments
+  int seg_end[3];           // cumulative segment heights (multiples of 16)
+  const uint16_t* W2;       // second weight (EPI_SILU: up projection), [N][K]
   int N, K;
-  int splits, kb_per_split, n_kblocks;
-  float* partial;      // split-K partial tiles
-  int* counters;       // one per N tile, zero between launches
-  float* out_f32;      // EPI_F32 / EPI_RESID
-  uint16_t* out_bf16;  // EPI_BF16 / EPI_SILU
+  float* out_f32;           // EPI_F32 / EPI_RESID
+  uint16_t* out_bf16;       // EPI_BF16 / EPI_SILU
   int ldo;
 };
 
 struct GemmScratch {
-  float* partial;
-  size_t partial_floats;
-  int* counters;
-  int n_counters;
-  int target_wgs;
+  int target_wgs;  // workgroups that keep every CU busy (tile-width choice)
 };
 
 void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* W,
                  const uint16_t* W2, int N, int K, float* out_f32, uint16_t* out_bf16,
                  int ldo, const GemmScratch& s, hipStream_t st);
-size_t gemm_partial_floats(int max_m, int max_n, int target_wgs);
+// Segmented form: the weight is the row concatenation of n_seg (<= 3)
+// matrices Wseg[q] of seg_rows[q] rows each (multiples of 16).
+void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
+                 const int* seg_rows, int n_seg, const uint16_t* W2, int K, float* out_f32,
+                 uint16_t* out_bf16, int ldo, const GemmScratch& s, hipStream_t st);
 
 // ----------------------------------------------------------- attention ----
 struct AttnArgs {
@@ -93,8 +91,10 @@ void launch_visual_rows(const uint16_t* visual, const int* vis_idx, int rows, in
                         float* x, hipStream_t st);
 
 // -------------------------------------------------------- selection ----
+// scratch: topk_scratch_floats(rows, V) floats (8-byte aligned)
+size_t topk_scratch_floats(int rows, int V);
 void launch_topk(const float* logits, int rows, int V, int k, int* idx, float* val,
-                 float* lse, hipStream_t st);
+                 float* lse, float* scratch, hipStream_t st);
 
 // ---------------------------------------------------- tree / accept ----
 // Row descriptors of one forward step (device arrays, one entry per row).

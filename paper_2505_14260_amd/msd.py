@@ -53,6 +53,10 @@ class TreeSpec(ctypes.Structure):
                 ("parent", ctypes.POINTER(c_i32)), ("rank", ctypes.POINTER(c_i32))]
 
 
+class TraceRec(ctypes.Structure):
+    _fields_ = [("kind", c_i32), ("m", c_i32), ("n", c_i32), ("k", c_i32), ("ms", c_f32)]
+
+
 class Tree(ctypes.Structure):
     _fields_ = [("n_nodes", c_i32), ("token", c_i32 * MAX_TREE), ("parent", c_i32 * MAX_TREE),
                 ("depth", c_i32 * MAX_TREE), ("score", c_f32 * MAX_TREE),
@@ -84,6 +88,8 @@ def lib():
                                          P(c_i32), P(c_i32), c_vp]
         L.msd_seq_len.argtypes = [c_vp, ctypes.c_int]
         L.msd_set_state.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, c_vp, c_i32]
+        L.msd_trace_enable.argtypes = [c_vp, ctypes.c_int, ctypes.c_int]
+        L.msd_trace_read.argtypes = [c_vp, ctypes.c_int, P(TraceRec)]
         _lib = L
     return _lib
 
@@ -167,6 +173,18 @@ def msd_seq_len(ctx, seq):
 
 def msd_set_state(ctx, seq, L, h_ptr, next_token):
     _check(ctx, lib().msd_set_state(ctx, seq, L, h_ptr, next_token))
+
+
+def msd_trace_enable(ctx, capacity, kinds=0xF):
+    _check(ctx, lib().msd_trace_enable(ctx, capacity, kinds))
+
+
+def msd_trace_read(ctx, max_recs=4096):
+    recs = (TraceRec * max_recs)()
+    n = lib().msd_trace_read(ctx, max_recs, recs)
+    if n < 0:
+        _check(ctx, n)
+    return [(r.kind, r.m, r.n, r.k, r.ms) for r in recs[:n]]
 
 
 # --- convenience wrapper over device memory held in torch tensors --------------------
