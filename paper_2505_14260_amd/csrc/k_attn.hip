@@ -232,15 +232,20 @@ __global__ __launch_bounds__(HD) void k_tree_combine(AttnArgs a) {
   const int dt = dim >> 5, dd = dim & 31;
   const int hh = (dd >> 2) & 1, r = (dd >> 3) * 4 + (dd & 3);
   const int idx = (dt * 16 + r) * 64 + j + 32 * hh;
+  // chunk order is fixed; the loads of different chunks are independent
   float M = -INFINITY;
+#pragma unroll 8
   for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
   float num = 0.f, den = 0.f;
   if (M != -INFINITY) {
+#pragma unroll 8
     for (int c = 0; c < a.n_chunks; ++c) {
       const float mc = a.part_ml[(item0 + c) * 64 + 2 * j];
+      const float lc = a.part_ml[(item0 + c) * 64 + 2 * j + 1];
+      const float oc = a.part_o[(item0 + c) * 32 * HD + idx];
       const float w = (mc == -INFINITY) ? 0.f : __expf(mc - M);
-      den += w * a.part_ml[(item0 + c) * 64 + 2 * j + 1];
-      num += w * a.part_o[(item0 + c) * 32 * HD + idx];
+      den += w * lc;
+      num += w * oc;
     }
   }
   a.out[(size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD + dim] =

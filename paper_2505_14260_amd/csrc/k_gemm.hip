@@ -1,223 +1,228 @@
-// Thin-M bf16 GEMM on gfx950 MFMA: Y[m][n] = sum_k X[m][k] * W[n][k].
+// Thin-M bf16 GEMM on gfx950 MFMA: P_s[m][n] = sum_{k in chunk s} X[m][k] * W[n][k].
 //
 // The decode path multiplies a few dozen activation rows (tree nodes) by
 // large weight matrices, so the kernel is bound by streaming W from HBM once.
 // Layout of the work:
-//  - one workgroup of 8 waves owns 16*NT consecutive rows of W (and of W2 for
-//    the SwiGLU pair) and all M rows of X (MT tiles of 16); the 8 waves split
-//    K into contiguous ranges of 128-element blocks, and their partial tiles
-//    are summed through LDS in wave order, so no workgroup ever waits for
-//    another and the result does not depend on timing;
-//  - v_mfma_f32_16x16x32_bf16 with A = W rows and B = X^T columns.  The K
-//    index inside one MFMA may be any permutation shared by A and B, so a
-//    lane loads 32 physically contiguous bf16 of its W row (the four lanes of
-//    a row cover 256 contiguous bytes per block) and the same 32 columns of
-//    its X row;
-//  - the loads of the next P-1 blocks are in flight while a block's MFMAs
-//    run (a ring of P register stages), which keeps enough bytes outstanding
-//    per CU to cover HBM latency;
-//  - the weight may be given as up to three row segments (e.g. the q, k and v
-//    projections) that behave as one matrix of the summed height.
+//  - K is cut into S chunks.  A workgroup (4 waves) owns one chunk s and a
+//    strided set of 64-row tiles of W (and of W2 for the SwiGLU pair); it
+//    stages its X chunk into LDS once and then streams the W rows of all its
+//    tiles, each wave owning 16 rows of a tile, with a ring of P register
+//    stages whose prefetch runs across tile boundaries.  No workgroup or wave
+//    ever waits for another one.
+//  - v_mfma_f32_16x16x32_bf16 with A = W rows (from HBM) and B = X^T (from
+//    LDS).  The K index inside one MFMA may be any permutation shared by A and
+//    B, so a lane loads 32 physically contiguous bf16 of its W row (the four
+//    lanes of a row cover 256 contiguous bytes per block).
+//  - Each chunk's partial product is stored in float32 as part[s][m][n]; the
+//    kernel that consumes the product (residual + RMSNorm, RoPE + KV write,
+//    SwiGLU, vocabulary top-k) sums the S partials in chunk order, so the
+//    result is deterministic.
 #include "msd_internal.h"
 
 namespace msd {
 
 namespace {
 
-constexpr int KB = 128;     // K elements per block
-constexpr int WAVES = 8;
+constexpr int KB = 128;  // K elements per block
+constexpr int WAVES = 4;
+constexpr int TILE_ROWS = 16 * WAVES;
 
-template <int MT, int NT, int NW>
-struct Frag {
-  uint4 w[NW][NT][4];
-  uint4 x[MT][4];
+template <int NW>
+struct WFrag {
+  uint4 w[NW][4];
 };
 
-// Block load.  Rows past N or M were clamped to row 0 by the caller (they
-// only feed output rows that are never stored).  Full blocks (GUARD false)
-// load without any per-lane condition, which is what lets the compiler keep
-// several blocks in flight; the single partial block at the end of K
-// (K % 128 != 0) uses GUARD and zeroes the W columns past K.
-template <int MT, int NT, int NW, bool GUARD>
-MSD_DEV void load_block(Frag<MT, NT, NW>& f, const uint16_t* const (&wrow)[NW][NT],
-                        const uint16_t* const (&xrow)[MT], int k, int K) {
-  // k is this lane's first column of the block; K % 8 == 0
+// W block load for one lane: 32 contiguous bf16 of its row starting at k.
+// TAIL: the chunk may end inside the block; columns past kend read a clamped
+// address and are zeroed.
+template <int NW, bool TAIL>
+MSD_DEV void load_w(WFrag<NW>& f, const uint16_t* const (&wrow)[NW], int k, int kend) {
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     const int kk = k + 8 * c;
-    const bool ok = !GUARD || kk < K;
-    const int kc = ok ? kk : K - 8;
+    const bool ok = !TAIL || kk < kend;
+    const int kc = ok ? kk : kend - 8;
 #pragma unroll
-    for (int w = 0; w < NW; ++w)
-#pragma unroll
-      for (int s = 0; s < NT; ++s) {
-        const uint4 v = *reinterpret_cast<const uint4*>(wrow[w][s] + kc);
-        f.w[w][s][c] = ok ? v : make_uint4(0, 0, 0, 0);
-      }
-#pragma unroll
-    for (int t = 0; t < MT; ++t) f.x[t][c] = *reinterpret_cast<const uint4*>(xrow[t] + kc);
+    for (int w = 0; w < NW; ++w) {
+      const uint4 v = *reinterpret_cast<const uint4*>(wrow[w] + kc);
+      f.w[w][c] = ok ? v : make_uint4(0, 0, 0, 0);
+    }
   }
 }
 
-template <int MT, int NT, int NW>
-MSD_DEV void mma_block(f32x4 (&acc)[NW][NT][MT], const Frag<MT, NT, NW>& f) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c)
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-#pragma unroll
-      for (int s = 0; s < NT; ++s)
-#pragma unroll
-        for (int t = 0; t < MT; ++t)
-          acc[w][s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              as_bf16x8(f.w[w][s][c]), as_bf16x8(f.x[t][c]), acc[w][s][t], 0, 0, 0);
+// LDS X chunk: row m holds the chunk's columns in 16-byte units; unit u of
+// row m is stored at u ^ (m & 15) so that the 16 rows read by one MFMA
+// operand load hit different banks.
+MSD_DEV int xs_index(int m, int u, int units_per_row) { return m * units_per_row + (u ^ (m & 15)); }
+
+// Row pointers of W (and W2) for 16-row group `row0` of a tile; only
+// constant indices into the argument block are used: a runtime index would
+// become a memory load whose wait drains every outstanding weight load.
+template <int NW>
+MSD_DEV void row_ptrs(const uint16_t* (&wrow)[NW], int n, int N, int K, const uint16_t* w0,
+                      const uint16_t* w1, const uint16_t* w2, int e0, int e1,
+                      const uint16_t* wb2) {
+  const int nn = n < N ? n : 0;
+  const uint16_t* wb = nn < e0 ? w0 : (nn < e1 ? w1 : w2);
+  const int base = nn < e0 ? 0 : (nn < e1 ? e0 : e1);
+  wrow[0] = wb + (size_t)(nn - base) * K;
+  if (NW == 2) wrow[NW - 1] = wb2 + (size_t)nn * K;
 }
 
-template <int MT, int NT, int EPI, int P>
-__global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
-  constexpr int NW = (EPI == EPI_SILU) ? 2 : 1;
-  constexpr int TILE = NW * NT * MT * 4;  // floats per lane per wave
-  __shared__ float red[WAVES / 2][TILE][64];
+template <int MT, int NW, int P, bool TAIL>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+  extern __shared__ uint4 xs[];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
-  const int n0 = blockIdx.x * 16 * NT;
+  // scalar copies of the arguments
+  const int N = a.N, K = a.K, M = a.M, G = a.G, S = a.S, Kc = a.Kc;
+  const uint16_t* const w0 = a.Wseg[0];
+  const uint16_t* const w1 = a.Wseg[1];
+  const uint16_t* const w2 = a.Wseg[2];
+  const uint16_t* const wb2 = a.W2;
+  const int e0 = a.seg_end[0], e1 = a.seg_end[1];
+  float* const part = a.part;
+  const size_t part_split = a.part_split;
+  const int ldp = a.ldp;
 
-  const uint16_t* wrow[NW][NT];
-#pragma unroll
-  for (int s = 0; s < NT; ++s) {
-    const int n = n0 + 16 * s + i;
-    const int nn = n < a.N ? n : 0;
-    // 16-row tiles never straddle a segment (segment heights are multiples of 16)
-    const int seg = (nn < a.seg_end[0]) ? 0 : (nn < a.seg_end[1] ? 1 : 2);
-    const int base = seg == 0 ? 0 : a.seg_end[seg - 1];
-    wrow[0][s] = a.Wseg[seg] + (size_t)(nn - base) * a.K;
-    if (NW == 2) wrow[NW - 1][s] = a.W2 + (size_t)nn * a.K;
+  const int s = blockIdx.x % S;
+  const int gi = blockIdx.x / S;
+  const int k0 = s * Kc;
+  const int kend = min(K, k0 + Kc);
+  const int nkb = (kend - k0 + KB - 1) / KB;
+  const int upr = Kc / 8;  // 16-byte units per LDS row
+  const int n_tiles = (N + TILE_ROWS - 1) / TILE_ROWS;
+  const int n_my = gi < n_tiles ? (n_tiles - gi + G - 1) / G : 0;
+  const int total = n_my * nkb;
+  const int row_in_tile = wave * 16 + i;
+
+  // stage X[0:MT*16, k0:k0+nkb*128) into LDS (rows past M and columns past
+  // kend are zero).  Issued before the weight prefetch: loads complete in
+  // order, so staging first does not wait for the first weight blocks.
+  const int units = nkb * (KB / 8);
+  for (int e = threadIdx.x; e < MT * 16 * units; e += 256) {
+    const int m = e / units, u = e - m * units;
+    const int col = k0 + 8 * u;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (m < M && col < kend) v = *reinterpret_cast<const uint4*>(a.X + (size_t)m * a.ldx + col);
+    xs[xs_index(m, u, upr)] = v;
   }
-  const uint16_t* xrow[MT];
+  WFrag<NW> ring[P];
+  if (total > 0) {
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    const int m = t * 16 + i;
-    xrow[t] = a.X + (size_t)(m < a.M ? m : 0) * a.ldx;
+    for (int p = 0; p < P; ++p) {
+      const int f = min(p, total - 1);
+      const uint16_t* wr[NW];
+      row_ptrs<NW>(wr, (gi + (f / nkb) * G) * TILE_ROWS + row_in_tile, N, K, w0, w1, w2, e0, e1,
+                   wb2);
+      load_w<NW, TAIL>(ring[p], wr, k0 + (f % nkb) * KB + 32 * g, kend);
+    }
   }
 
-  f32x4 acc[NW][NT][MT];
+  __syncthreads();
+  if (total == 0) return;
+
+  f32x4 acc[NW][MT];
 #pragma unroll
   for (int w = 0; w < NW; ++w)
 #pragma unroll
-    for (int s = 0; s < NT; ++s)
-#pragma unroll
-      for (int t = 0; t < MT; ++t) acc[w][s][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < MT; ++t) acc[w][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // contiguous, balanced range of full blocks for this wave; the trip count
-  // is uniform across the wave and the prefetch index is clamped rather than
-  // guarded
-  const int nkb = a.K / KB;
-  const int kb0 = (nkb * wave) / WAVES;
-  const int kb1 = (nkb * (wave + 1)) / WAVES;
-  if (kb0 < kb1) {
-    const int last = kb1 - 1;
-    Frag<MT, NT, NW> ring[P];
+  // flattened (tile, block) sequence; the prefetch index is clamped, and a
+  // tile's partial is stored after its last block
+  for (int f0 = 0; f0 < total; f0 += P) {
 #pragma unroll
-    for (int p = 0; p < P; ++p)
-      load_block<MT, NT, NW, false>(ring[p], wrow, xrow, min(kb0 + p, last) * KB + 32 * g, a.K);
-    int kb = kb0;
-    for (; kb + P <= kb1; kb += P) {
+    for (int p = 0; p < P; ++p) {
+      const int f = f0 + p;
+      if (f < total) {
+        const int kb = f % nkb;
+        uint4 xf[MT][4];
 #pragma unroll
-      for (int p = 0; p < P; ++p) {
-        mma_block<MT, NT, NW>(acc, ring[p]);
-        load_block<MT, NT, NW, false>(ring[p], wrow, xrow, min(kb + p + P, last) * KB + 32 * g,
-                                      a.K);
-      }
-    }
+        for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int p = 0; p < P; ++p)
-      if (p < kb1 - kb) mma_block<MT, NT, NW>(acc, ring[p]);
-  }
-  if (wave == WAVES - 1 && nkb * KB < a.K) {
-    Frag<MT, NT, NW> f;
-    load_block<MT, NT, NW, true>(f, wrow, xrow, nkb * KB + 32 * g, a.K);
-    mma_block<MT, NT, NW>(acc, f);
-  }
-
-  // pairwise reduction over the 8 waves through LDS:
-  // ((w0 + w4) + (w2 + w6)) + ((w1 + w5) + (w3 + w7))
+          for (int c = 0; c < 4; ++c) xf[t][c] = xs[xs_index(t * 16 + i, kb * 16 + 4 * g + c, upr)];
 #pragma unroll
-  for (int half = 4; half >= 1; half >>= 1) {
-    if (wave >= half && wave < 2 * half) {
+        for (int c = 0; c < 4; ++c)
 #pragma unroll
-      for (int w = 0; w < NW; ++w)
+          for (int w = 0; w < NW; ++w)
 #pragma unroll
-        for (int s = 0; s < NT; ++s)
+            for (int t = 0; t < MT; ++t)
+              acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(ring[p].w[w][c]), as_bf16x8(xf[t][c]), acc[w][t], 0, 0, 0);
+        const int fn = min(f + P, total - 1);
+        const uint16_t* wr[NW];
+        row_ptrs<NW>(wr, (gi + (fn / nkb) * G) * TILE_ROWS + row_in_tile, N, K, w0, w1, w2, e0, e1,
+                     wb2);
+        load_w<NW, TAIL>(ring[p], wr, k0 + (fn % nkb) * KB + 32 * g, kend);
+        if (kb == nkb - 1) {
+          // C layout of the 16x16 MFMA: lane holds column (lane & 15) = row
+          // m, register r holds W row 4*(lane/16) + r
+          const int n = (gi + (f / nkb) * G) * TILE_ROWS + wave * 16 + 4 * g;
 #pragma unroll
-          for (int t = 0; t < MT; ++t)
+          for (int w = 0; w < NW; ++w)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              red[wave - half][((w * NT + s) * MT + t) * 4 + r][lane] = acc[w][s][t][r];
-    }
-    __syncthreads();
-    if (wave < half) {
-#pragma unroll
-      for (int w = 0; w < NW; ++w)
-#pragma unroll
-        for (int s = 0; s < NT; ++s)
-#pragma unroll
-          for (int t = 0; t < MT; ++t)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              acc[w][s][t][r] += red[wave][((w * NT + s) * MT + t) * 4 + r][lane];
-    }
-    __syncthreads();
-  }
-  if (wave != 0) return;
-
-  // C layout of the 16x16 MFMA: lane holds column (lane & 15) = output row
-  // m, register r holds W row 4*(lane/16) + r of the 16-row tile.
-#pragma unroll
-  for (int s = 0; s < NT; ++s)
-#pragma unroll
-    for (int t = 0; t < MT; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = t * 16 + i;
-        const int n = n0 + 16 * s + 4 * g + r;
-        if (m >= a.M || n >= a.N) continue;
-        const float v0 = acc[0][s][t][r];
-        const size_t o = (size_t)m * a.ldo + n;
-        if (EPI == EPI_F32) {
-          a.out_f32[o] = v0;
-        } else if (EPI == EPI_RESID) {
-          a.out_f32[o] += v0;
-        } else if (EPI == EPI_BF16) {
-          a.out_bf16[o] = f2bf(v0);
-        } else {
-          const float v1 = acc[NW - 1][s][t][r];
-          a.out_bf16[o] = f2bf(v0 / (1.f + __expf(-v0)) * v1);
+            for (int t = 0; t < MT; ++t) {
+              const int m = t * 16 + i;
+              if (m < M && n < N) {
+                float* dst = part + (size_t)s * part_split + (size_t)m * ldp + w * N + n;
+                *reinterpret_cast<float4*>(dst) =
+                    make_float4(acc[w][t][0], acc[w][t][1], acc[w][t][2], acc[w][t][3]);
+              }
+              acc[w][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
         }
       }
+    }
+  }
 }
 
-// ring depth: three stages when a stage is at most 64 VGPRs, else two
-template <int MT, int NT, int NW>
-constexpr int ring_depth() { return (16 * NT * NW + 16 * MT) <= 64 ? 3 : 2; }
+template <int MT, int NW, bool TAIL>
+void launch_one(dim3 grid, size_t lds, const GemmArgs& a, hipStream_t st) {
+  constexpr int P = NW == 2 ? 3 : 4;
+  hipLaunchKernelGGL((k_gemm<MT, NW, P, TAIL>), grid, dim3(256), lds, st, a);
+}
 
-template <int MT, int NT>
-void dispatch_epi(int epi, dim3 grid, const GemmArgs& a, hipStream_t st) {
-  constexpr int P1 = ring_depth<MT, NT, 1>();
-  constexpr int P2 = ring_depth<MT, NT, 2>();
-  switch (epi) {
-    case EPI_F32: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_F32, P1>), grid, dim3(512), 0, st, a); break;
-    case EPI_BF16: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_BF16, P1>), grid, dim3(512), 0, st, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_RESID, P1>), grid, dim3(512), 0, st, a); break;
-    default: hipLaunchKernelGGL((k_gemm<MT, NT, EPI_SILU, P2>), grid, dim3(512), 0, st, a); break;
+template <int MT>
+void launch_mt(int nw, bool tail, dim3 grid, size_t lds, const GemmArgs& a, hipStream_t st) {
+  if (nw == 2) {
+    if (tail) launch_one<MT, 2, true>(grid, lds, a, st); else launch_one<MT, 2, false>(grid, lds, a, st);
+  } else {
+    if (tail) launch_one<MT, 1, true>(grid, lds, a, st); else launch_one<MT, 1, false>(grid, lds, a, st);
   }
 }
 
 }  // namespace
 
-void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
-                 const int* seg_rows, int n_seg, const uint16_t* W2, int K, float* out_f32,
-                 uint16_t* out_bf16, int ldo, const GemmScratch& s, hipStream_t st) {
+GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs, int lds_bytes) {
+  GemmPlan p;
+  const int mc = M < 64 ? M : 64;
+  p.MT = mc <= 16 ? 1 : (mc <= 32 ? 2 : 4);
+  // X chunk in LDS: MT*16 rows of Kc bf16 within lds_bytes
+  const int kc_max = (lds_bytes / 2 / (p.MT * 16)) / KB * KB;
+  p.S = (K + kc_max - 1) / kc_max;
+  p.Kc = ((K + p.S - 1) / p.S + KB - 1) / KB * KB;
+  p.S = (K + p.Kc - 1) / p.Kc;
+  // workgroups per chunk: about target_wgs in total, with every workgroup
+  // of a chunk getting the same number of tiles
+  const int n_tiles = (N + TILE_ROWS - 1) / TILE_ROWS;
+  int G = (target_wgs + p.S - 1) / p.S;
+  if (G > n_tiles) G = n_tiles;
+  if (G < 1) G = 1;
+  const int per = (n_tiles + G - 1) / G;
+  p.G = (n_tiles + per - 1) / per;
+  p.nw = nw;
+  return p;
+}
+
+size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs, int lds_bytes) {
+  const GemmPlan p = plan_gemm(M, N, K, nw, target_wgs, lds_bytes);
+  return (size_t)p.S * M * N * nw;
+}
+
+void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
+                 const int* seg_rows, int n_seg, const uint16_t* W2, int K, float* part,
+                 const GemmScratch& sc, hipStream_t st) {
   int N = 0;
   GemmArgs base{};
   for (int q = 0; q < 3; ++q) {
@@ -229,39 +234,28 @@ void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* con
     }
     base.seg_end[q] = N;
   }
-  // wider row tiles for wide matrices (fewer re-reads of X) as long as the
-  // grid still covers every CU
-  const int tiles16 = (N + 15) / 16;
-  int nt = 1;
-  if (tiles16 >= 2 * s.target_wgs) nt = 2;
-  if (M > 32) nt = 1;
-  for (int m0 = 0; m0 < M; m0 += 64) {
-    const int mc = (M - m0) < 64 ? (M - m0) : 64;
-    GemmArgs a = base;
-    a.X = X + (size_t)m0 * ldx;
-    a.ldx = ldx;
-    a.M = mc;
-    a.W2 = W2;
-    a.N = N;
-    a.K = K;
-    a.out_f32 = out_f32 ? out_f32 + (size_t)m0 * ldo : nullptr;
-    a.out_bf16 = out_bf16 ? out_bf16 + (size_t)m0 * ldo : nullptr;
-    a.ldo = ldo;
-    dim3 grid((N + 16 * nt - 1) / (16 * nt));
-    if (mc <= 16) {
-      if (nt == 2) dispatch_epi<1, 2>(epi, grid, a, st); else dispatch_epi<1, 1>(epi, grid, a, st);
-    } else if (mc <= 32) {
-      if (nt == 2) dispatch_epi<2, 2>(epi, grid, a, st); else dispatch_epi<2, 1>(epi, grid, a, st);
-    } else {
-      dispatch_epi<4, 1>(epi, grid, a, st);
-    }
-  }
-}
-
-void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* W,
-                 const uint16_t* W2, int N, int K, float* out_f32, uint16_t* out_bf16,
-                 int ldo, const GemmScratch& s, hipStream_t st) {
-  launch_gemm(epi, X, ldx, M, &W, &N, 1, W2, K, out_f32, out_bf16, ldo, s, st);
+  const int nw = W2 ? 2 : 1;
+  const GemmPlan pl = plan_gemm(M, N, K, nw, sc.target_wgs, sc.lds_bytes);
+  // chunks are whole 128-column blocks except when K itself is not
+  const bool tail = (K % KB) != 0;
+  const size_t lds = (size_t)pl.MT * 16 * pl.Kc * 2;
+  GemmArgs a = base;
+  a.X = X;
+  a.ldx = ldx;
+  a.M = M;
+  a.W2 = W2;
+  a.N = N;
+  a.K = K;
+  a.S = pl.S;
+  a.Kc = pl.Kc;
+  a.G = pl.G;
+  a.ldp = N * nw;
+  a.part_split = (size_t)M * N * nw;
+  a.part = part;
+  dim3 grid(pl.S * pl.G);
+  if (pl.MT == 1) launch_mt<1>(nw, tail, grid, lds, a, st);
+  else if (pl.MT == 2) launch_mt<2>(nw, tail, grid, lds, a, st);
+  else launch_mt<4>(nw, tail, grid, lds, a, st);
 }
 
 }  // namespace msd

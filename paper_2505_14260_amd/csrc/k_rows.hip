@@ -68,41 +68,140 @@ __global__ void k_rope_table(float2* tab, int max_pos, int half, double theta) {
   tab[idx] = make_float2((float)c, (float)s);
 }
 
+// Sum over the K chunks of one partial-product element, in chunk order; the
+// loads are independent so several are in flight at once.
+MSD_DEV float part_sum(const Parts& pt, int row, int col) {
+  const float* p = pt.p + (size_t)row * pt.ld + col;
+  float v = 0.f;
+#pragma unroll 8
+  for (int s = 0; s < pt.S; ++s) v += p[(size_t)s * pt.split];
+  return v;
+}
+
+// 1 / sqrt(mean(x^2) + eps) of a row from its per-block sums of squares
+// (summed in block order); 1 when no sums are given.
+MSD_DEV float row_rstd(const RowNorm& rn, int row) {
+  if (!rn.ssq) return 1.f;
+  const float* p = rn.ssq + (size_t)row * rn.nblk;
+  float t = 0.f;
+  for (int q = 0; q < rn.nblk; ++q) t += p[q];
+  return rsqrtf(t / (float)rn.d + rn.eps);
+}
+
 // Rotate-half RoPE on q and k, write q (bf16), K to its slot and V to the
-// transposed V cache.  qkv: [rows][(H + 2KV) * hd] f32.
-__global__ __launch_bounds__(256) void k_rope_kv(const float* qkv, int H, int KV, int hd,
-                                                 const int* pos, const int* row_seq,
-                                                 const int* row_slot, const float2* tab,
-                                                 uint16_t* q, uint16_t* kc, uint16_t* vc, int S) {
+// transposed V cache.  qkv: summed parts, [rows][(H + 2KV) * hd], computed
+// from the un-normalised input, so every row is first scaled by its 1/rms.
+// One block of hd/2 threads per (row, head); heads H.. are the key heads,
+// H+KV.. the value heads.
+__global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, int KV, int hd,
+                                                const int* pos, const int* row_seq,
+                                                const int* row_slot, const float2* tab,
+                                                uint16_t* q, uint16_t* kc, uint16_t* vc, int S) {
   const int row = blockIdx.x;
+  const int head = blockIdx.y;
   const int half = hd / 2;
-  const int ld = (H + 2 * KV) * hd;
-  const float* src = qkv + (size_t)row * ld;
-  const float2* cs = tab + (size_t)pos[row] * half;
   const int slot = row_slot[row];
   const int b = row_seq[row];
-  for (int idx = threadIdx.x; idx < (H + KV) * half; idx += 256) {
-    const int head = idx / half, i = idx - head * half;
-    const float* x = src + head * hd;
-    const float a = x[i], c = x[i + half];
-    const float2 t = cs[i];
+  if (head >= H && slot < 0) return;
+  const float r = row_rstd(rn, row);
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    const float a = r * part_sum(qkv, row, head * hd + i);
+    const float c = r * part_sum(qkv, row, head * hd + i + half);
+    if (head >= H + KV) {
+      const int g = head - H - KV;
+      uint16_t* vr = vc + (size_t)(b * KV + g) * hd * S + slot;
+      vr[(size_t)i * S] = f2bf(a);
+      vr[(size_t)(i + half) * S] = f2bf(c);
+      continue;
+    }
+    const float2 t = tab[(size_t)pos[row] * half + i];
     const float y0 = a * t.x - c * t.y;
     const float y1 = c * t.x + a * t.y;
     if (head < H) {
       q[(size_t)row * H * hd + head * hd + i] = f2bf(y0);
       q[(size_t)row * H * hd + head * hd + i + half] = f2bf(y1);
-    } else if (slot >= 0) {
-      const int g = head - H;
-      uint16_t* kr = kc + ((size_t)(b * KV + g) * S + slot) * hd;
+    } else {
+      uint16_t* kr = kc + ((size_t)(b * KV + head - H) * S + slot) * hd;
       kr[i] = f2bf(y0);
       kr[i + half] = f2bf(y1);
     }
   }
-  if (slot < 0) return;
-  for (int idx = threadIdx.x; idx < KV * hd; idx += 256) {
-    const int g = idx / hd, e = idx - g * hd;
-    vc[((size_t)(b * KV + g) * hd + e) * S + slot] = f2bf(src[(H + KV) * hd + idx]);
+}
+
+MSD_DEV float block_sum_1024(float v, float* sh) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) t += sh[q];
+  return t;
+}
+
+// x = sum of parts (RN_SET), x + sum (RN_ADD) or x (RN_KEEP); then the
+// RMSNorm of the new x (bf16, gain g) and/or x itself in bf16.  One block of
+// 1024 threads per row.
+__global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, int mode, float* x,
+                                                     const uint16_t* g, float eps, uint16_t* xn,
+                                                     uint16_t* xb) {
+  __shared__ float sh[16];
+  const int row = blockIdx.x;
+  float* xr = x + (size_t)row * d;
+  float ss = 0.f;
+  for (int e = threadIdx.x; e < d; e += 1024) {
+    float v = xr[e];
+    if (mode != RN_KEEP) {
+      const float p = part_sum(pt, row, col0 + e);
+      v = (mode == RN_SET) ? p : v + p;
+      xr[e] = v;
+    }
+    ss += v * v;
+    if (xb) xb[(size_t)row * d + e] = f2bf(v);
   }
+  if (!g) return;
+  ss = block_sum_1024(ss, sh);
+  const float r = rsqrtf(ss / (float)d + eps);
+  for (int e = threadIdx.x; e < d; e += 1024) xn[(size_t)row * d + e] = f2bf(xr[e] * r * bf2f(g[e]));
+}
+
+// Elementwise residual update: x = sum of parts (RN_SET), x + sum (RN_ADD)
+// or x (RN_KEEP); then xg = bf16(x * g) (the next GEMM's input, normalised
+// later by its consumer), xb = bf16(x), and the block's sum of x^2 into
+// ssq[row][block].  Grid (ceil(d/256), rows).
+__global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float* x,
+                                               const uint16_t* g, uint16_t* xg, uint16_t* xb,
+                                               float* ssq) {
+  __shared__ float sh[4];
+  const int row = blockIdx.y;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  float v = 0.f;
+  if (e < d) {
+    v = x[(size_t)row * d + e];
+    if (mode != RN_KEEP) {
+      const float p = part_sum(pt, row, e);
+      v = (mode == RN_SET) ? p : v + p;
+      x[(size_t)row * d + e] = v;
+    }
+    if (xg) xg[(size_t)row * d + e] = f2bf(v * bf2f(g[e]));
+    if (xb) xb[(size_t)row * d + e] = f2bf(v);
+  }
+  if (!ssq) return;
+  const float t = block_sum_256(v * v, sh);
+  if (threadIdx.x == 0) ssq[(size_t)row * gridDim.x + blockIdx.x] = t;
+}
+
+// act = bf16(silu(gate) * up) with gate at columns [0, F), up at [F, 2F),
+// both scaled by the row's 1/rms (the GEMM read the un-normalised input).
+__global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint16_t* act) {
+  const int row = blockIdx.y;
+  const int f = blockIdx.x * 256 + threadIdx.x;
+  if (f >= F) return;
+  const float r = row_rstd(rn, row);
+  const float gt = r * part_sum(pt, row, f);
+  const float up = r * part_sum(pt, row, F + f);
+  act[(size_t)row * F + f] = f2bf(gt / (1.f + __expf(-gt)) * up);
 }
 
 // out[row] = [h_row | e_next] in bf16, the concat fed to the draft's f_down.
@@ -179,22 +278,23 @@ MSD_DEV void insert_sorted(float* lv, int* li, int& n, int k, float val, int id)
   }
 }
 
-__global__ __launch_bounds__(256) void k_topk_slice(const float* logits, int V, int k, int n_slices,
-                                                    float* cand_v, int* cand_i, float2* stats) {
+__global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, int n_slices,
+                                                    float* cand_v, int* cand_i, float2* stats,
+                                                    float* logits_out) {
   __shared__ float sv[256];
   __shared__ int si[256];
   __shared__ float sm[4];
   __shared__ float ssum[4];
   const int row = blockIdx.x / n_slices;
   const int sl = blockIdx.x - row * n_slices;
-  const float* x = logits + (size_t)row * V;
   const int v0 = sl * TOPK_SLICE, v1 = min(V, v0 + TOPK_SLICE);
   float lv[TOPK_MAX];
   int li[TOPK_MAX];
   int n = 0;
   float mloc = -INFINITY, sloc = 0.f;
   for (int v = v0 + threadIdx.x; v < v1; v += 256) {
-    const float val = x[v];
+    const float val = part_sum(logits, row, v);
+    if (logits_out) logits_out[(size_t)row * V + v] = val;
     if (val > mloc) {
       sloc = sloc * __expf(mloc - val) + 1.f;
       mloc = val;
@@ -277,12 +377,31 @@ void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream
                      hd / 2, theta);
 }
 
-void launch_rope_kv(const float* qkv, int rows, int H, int KV, int hd, const int* pos,
+void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, const int* pos,
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
                     uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_rope_kv, dim3(rows), dim3(256), 0, st, qkv, H, KV, hd, pos, row_seq,
-                     row_slot, rope_tab, q, kc, vc, S);
+  hipLaunchKernelGGL(k_rope_kv, dim3(rows, H + 2 * KV), dim3(64), 0, st, qkv, rn, H, KV, hd, pos,
+                     row_seq, row_slot, rope_tab, q, kc, vc, S);
+}
+
+void launch_resid_norm(Parts pt, int col0, int rows, int d, int mode, float* x,
+                       const uint16_t* g, float eps, uint16_t* xn, uint16_t* xb, hipStream_t st) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(k_resid_norm, dim3(rows), dim3(1024), 0, st, pt, col0, d, mode, x, g, eps, xn,
+                     xb);
+}
+
+void launch_silu(Parts pt, RowNorm rn, int rows, int F, uint16_t* act, hipStream_t st) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(k_silu, dim3((F + 255) / 256, rows), dim3(256), 0, st, pt, rn, F, act);
+}
+
+void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t* g, uint16_t* xg,
+                  uint16_t* xb, float* ssq, hipStream_t st) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(k_resid, dim3((d + 255) / 256, rows), dim3(256), 0, st, pt, d, mode, x, g, xg,
+                     xb, ssq);
 }
 
 void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const uint16_t* E,
@@ -298,15 +417,15 @@ size_t topk_scratch_floats(int rows, int V) {
   return (size_t)rows * n_slices * (2 * TOPK_MAX + 2);
 }
 
-void launch_topk(const float* logits, int rows, int V, int k, int* idx, float* val, float* lse,
-                 float* scratch, hipStream_t st) {
+void launch_topk(Parts logits, int rows, int V, int k, int* idx, float* val, float* lse,
+                 float* logits_out, float* scratch, hipStream_t st) {
   if (rows <= 0) return;
   const int n_slices = (V + TOPK_SLICE - 1) / TOPK_SLICE;
   float* cand_v = scratch;
   int* cand_i = reinterpret_cast<int*>(cand_v + (size_t)rows * n_slices * TOPK_MAX);
   float2* stats = reinterpret_cast<float2*>(cand_i + (size_t)rows * n_slices * TOPK_MAX);
   hipLaunchKernelGGL(k_topk_slice, dim3(rows * n_slices), dim3(256), 0, st, logits, V, k, n_slices,
-                     cand_v, cand_i, stats);
+                     cand_v, cand_i, stats, logits_out);
   hipLaunchKernelGGL(k_topk_merge, dim3(rows), dim3(256), 0, st, k, n_slices, cand_v, cand_i,
                      stats, idx, val, lse);
 }

@@ -31,6 +31,11 @@ constexpr int FEAT = MSD_MAX_TREE + 1;  // draft feature slots per sequence
 constexpr int TOPK = 16;
 constexpr int POOL = 1024;              // dynamic-tree candidates per sequence
 constexpr int STAGE_INTS = 1 << 16;
+// GEMM launch shape: about one workgroup per CU streams best (more
+// concurrent row streams per CU lower the achieved HBM bandwidth), with a
+// 32 KB X chunk per workgroup.
+constexpr int GEMM_WGS = 256;
+constexpr int GEMM_LDS = 32768;
 
 // Bump allocator over the workspace (also used to size it).
 struct Carver {
@@ -47,7 +52,7 @@ struct Carver {
 
 struct Plan {
   int rows_max, lrows, ld_qkv;
-  size_t attn_floats;
+  size_t attn_floats, part_floats;
 };
 
 Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
@@ -58,6 +63,16 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
   const int G = m.n_heads / m.n_kv_heads;
   const int qtiles = (MSD_MAX_TREE * G + 31) / 32;
   p.attn_floats = attn_partial_floats(lim.max_batch, m.n_kv_heads, qtiles, 64, m.head_dim);
+  // GEMM partials of one 64-row launch, for the largest weight of the model
+  const int mm = std::min(64, p.rows_max);
+  const int d = m.d_model, F = m.ffn_dim, hh = m.n_heads * m.head_dim;
+  const size_t cand[6] = {gemm_part_floats(mm, p.ld_qkv, d, 1, GEMM_WGS, GEMM_LDS),
+                          gemm_part_floats(mm, d, hh, 1, GEMM_WGS, GEMM_LDS),
+                          gemm_part_floats(mm, F, d, 2, GEMM_WGS, GEMM_LDS),
+                          gemm_part_floats(mm, d, F, 1, GEMM_WGS, GEMM_LDS),
+                          gemm_part_floats(mm, d, 2 * d, 1, GEMM_WGS, GEMM_LDS),
+                          gemm_part_floats(mm, m.vocab, d, 1, GEMM_WGS, GEMM_LDS)};
+  p.part_floats = *std::max_element(cand, cand + 6);
   return p;
 }
 
@@ -74,8 +89,9 @@ struct msd_ctx {
   uint16_t *tk, *tv, *dk, *dv;
   // workspace
   float* x;
-  uint16_t *xn, *q, *ao, *act, *h;
-  float *qkv, *logits;
+  uint16_t *xn, *xb, *fcin, *q, *ao, *act, *h;
+  float* part;
+  float* ssq;
   Rows rows;
   int *nxt, *prefix, *seq_ids;
   int *d_len, *d_root, *pend_n, *pend_next;
@@ -148,13 +164,15 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   msd_ctx tmp;
   msd_ctx* t = c ? c : &tmp;
   t->x = cv.take<float>((size_t)R * d);
-  t->xn = cv.take<uint16_t>((size_t)R * 2 * d);
-  t->qkv = cv.take<float>((size_t)R * p.ld_qkv);
+  t->xn = cv.take<uint16_t>((size_t)R * d);
+  t->xb = cv.take<uint16_t>((size_t)R * d);
+  t->fcin = cv.take<uint16_t>((size_t)R * 2 * d);
+  t->part = cv.take<float>(p.part_floats);
+  t->ssq = cv.take<float>((size_t)R * ((d + 255) / 256));
   t->q = cv.take<uint16_t>((size_t)R * m.n_heads * m.head_dim);
   t->ao = cv.take<uint16_t>((size_t)R * m.n_heads * m.head_dim);
   t->act = cv.take<uint16_t>((size_t)R * m.ffn_dim);
   t->h = cv.take<uint16_t>((size_t)R * d);
-  t->logits = cv.take<float>((size_t)p.lrows * m.vocab);
   t->rows.tok = cv.take<int>(R);
   t->rows.vis = cv.take<int>(R);
   t->rows.pos = cv.take<int>(R);
@@ -250,39 +268,36 @@ int upload(msd_ctx* c, int* dst, const int* src, int n) {
   return upload_many(c, {{dst, src, sizeof(int) * (size_t)n}});
 }
 
-int gemm(msd_ctx* c, int epi, const uint16_t* X, int ldx, int M, const uint16_t* W,
-         const uint16_t* W2, int N, int K, float* of, uint16_t* ob, int ldo) {
-  const bool tr = c->tracing && ((c->trace_kinds >> epi) & 1) && c->trace.size() < c->trace_cap;
-  if (tr) {
-    msd_ctx::TraceRec r{epi, M, N, K, c->ev_pool[2 * c->trace.size()],
-                        c->ev_pool[2 * c->trace.size() + 1]};
-    HIPC(c, hipEventRecord(r.a, c->st));
-    c->trace.push_back(r);
-  }
-  launch_gemm(epi, X, ldx, M, W, W2, N, K, of, ob, ldo, c->gs, c->st);
-  LAUNCHED(c);
-  if (tr) HIPC(c, hipEventRecord(c->trace.back().b, c->st));
-  return MSD_OK;
-}
+// GEMM launch kinds (for the optional trace)
+enum { GK_QKV = 0, GK_O = 1, GK_DOWN = 2, GK_GATEUP = 3, GK_FC = 4, GK_LMHEAD = 5 };
 
-// q, k and v projections as one launch over the row-concatenated weight.
-int gemm_qkv(msd_ctx* c, const LayerW& w, int rows) {
-  const msd_model_desc& m = c->m;
-  const uint16_t* seg[3] = {w.wq, w.wk, w.wv};
-  const int hd = m.head_dim;
-  const int nrow[3] = {m.n_heads * hd, m.n_kv_heads * hd, m.n_kv_heads * hd};
-  const int N = nrow[0] + nrow[1] + nrow[2];
-  const bool tr = c->tracing && ((c->trace_kinds >> EPI_F32) & 1) && c->trace.size() < c->trace_cap;
+// Partial products of rows [0, M) (M <= 64) of X against the row segments;
+// returns the view the consumer sums.
+int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M,
+         std::initializer_list<const uint16_t*> seg, std::initializer_list<int> seg_rows,
+         const uint16_t* W2, int K, Parts* out) {
+  const uint16_t* sp[3] = {nullptr, nullptr, nullptr};
+  int sr[3] = {0, 0, 0};
+  int n = 0, N = 0;
+  for (const uint16_t* p : seg) sp[n++] = p;
+  n = 0;
+  for (int r : seg_rows) {
+    sr[n++] = r;
+    N += r;
+  }
+  const bool tr = c->tracing && ((c->trace_kinds >> kind) & 1) && c->trace.size() < c->trace_cap;
   if (tr) {
-    msd_ctx::TraceRec r{EPI_F32, rows, N, m.d_model, c->ev_pool[2 * c->trace.size()],
+    msd_ctx::TraceRec r{kind, M, N, K, c->ev_pool[2 * c->trace.size()],
                         c->ev_pool[2 * c->trace.size() + 1]};
     HIPC(c, hipEventRecord(r.a, c->st));
     c->trace.push_back(r);
   }
-  launch_gemm(EPI_F32, c->xn, m.d_model, rows, seg, nrow, 3, nullptr, m.d_model, c->qkv, nullptr,
-              c->plan.ld_qkv, c->gs, c->st);
+  launch_gemm(X, ldx, M, sp, sr, n, W2, K, c->part, c->gs, c->st);
   LAUNCHED(c);
   if (tr) HIPC(c, hipEventRecord(c->trace.back().b, c->st));
+  const int nw = W2 ? 2 : 1;
+  const GemmPlan pl = plan_gemm(M, N, K, nw, c->gs.target_wgs, c->gs.lds_bytes);
+  *out = Parts{c->part, pl.S, (size_t)M * N * nw, N * nw};
   return MSD_OK;
 }
 
@@ -292,13 +307,34 @@ int gemm_qkv(msd_ctx* c, const LayerW& w, int rows) {
     if (r_ != MSD_OK) return r_; \
   } while (0)
 
+constexpr int CHUNK = 64;  // rows per GEMM launch
+
+// GEMM input of a normalised layer: xn = bf16(x * g) and the per-row sums of
+// squares; the GEMM's consumer applies 1/rms (RMSNorm factored through the
+// linear map).
+int norm_rows(msd_ctx* c, int rows, const uint16_t* g) {
+  launch_resid(Parts{nullptr, 0, 0, 0}, rows, c->m.d_model, RN_KEEP, c->x, g, c->xn, nullptr,
+               c->ssq, c->st);
+  LAUNCHED(c);
+  return MSD_OK;
+}
+
+RowNorm row_norm(const msd_ctx* c, int m0) {
+  const int nblk = (c->m.d_model + 255) / 256;
+  return RowNorm{c->ssq + (size_t)m0 * nblk, nblk, c->m.d_model, c->m.norm_eps};
+}
+
 // One decoder stack (the target's layers or the draft's single layer) over
-// n_seq * nq rows of c->x described by c->rows; tree_R < 0 selects causal
-// attention, otherwise tree attention over a region of tree_R slots.
-int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int max_ltot) {
+// n_seq * nq rows of c->x described by c->rows; c->xn must hold the first
+// layer's input norm.  tree_R < 0 selects causal attention, otherwise tree
+// attention over a region of tree_R slots.  After the last layer the rows
+// get x += ..., then final_xn = bf16(rmsnorm(x) * final_g) when final_g and
+// final_xb = bf16(x) when final_xb.
+int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int max_ltot,
+                   const uint16_t* final_g, uint16_t* final_xn, uint16_t* final_xb) {
   const msd_model_desc& m = c->m;
   const int rows = n_seq * nq;
-  const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim;
+  const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim, F = m.ffn_dim;
   const int nl = draft ? 1 : m.n_layers;
   const int B = c->lim.max_batch, S = c->lim.max_seq;
   const size_t layer_kv = (size_t)B * KV * S * hd;
@@ -306,12 +342,15 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     const LayerW& w = draft ? c->dlayer : c->layers[l];
     uint16_t* kc = (draft ? c->dk : c->tk) + (size_t)l * layer_kv;
     uint16_t* vc = (draft ? c->dv : c->tv) + (size_t)l * layer_kv;
-    launch_rmsnorm(c->x, w.n1, rows, d, m.norm_eps, c->xn, c->st);
-    LAUNCHED(c);
-    TRY(gemm_qkv(c, w, rows));
-    launch_rope_kv(c->qkv, rows, H, KV, hd, c->rows.pos, c->rows.seq, c->rows.slot, c->rope,
-                   c->q, kc, vc, S, c->st);
-    LAUNCHED(c);
+    Parts pt;
+    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
+      const int mc = std::min(CHUNK, rows - m0);
+      TRY(gemm(c, GK_QKV, c->xn + (size_t)m0 * d, d, mc, {w.wq, w.wk, w.wv},
+               {H * hd, KV * hd, KV * hd}, nullptr, d, &pt));
+      launch_rope_kv(pt, row_norm(c, m0), mc, H, KV, hd, c->rows.pos + m0, c->rows.seq + m0,
+                     c->rows.slot + m0, c->rope, c->q + (size_t)m0 * H * hd, kc, vc, S, c->st);
+      LAUNCHED(c);
+    }
     AttnArgs a{};
     a.q = c->q;
     a.kc = kc;
@@ -338,53 +377,87 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       a.R = tree_R;
       a.qtiles = (nq * G + 31) / 32;
       // key chunks: enough waves to spread the cache over the chip, but at
-      // least 128 keys per wave so the partial results stay small
+      // least 64 keys per wave so the partial results stay small
       const int base_items = n_seq * KV * a.qtiles;
       int chunks = std::max(1, 512 / std::max(1, base_items));
-      while (chunks > 1 && attn_partial_floats(n_seq, KV, a.qtiles, chunks, hd) >
-                               c->plan.attn_floats)
-        --chunks;
       int ck = (max_ltot + chunks - 1) / chunks;
-      ck = std::max(128, (ck + 31) / 32 * 32);
+      ck = std::max(64, (ck + 31) / 32 * 32);
       while (attn_partial_floats(n_seq, KV, a.qtiles, (max_ltot + ck - 1) / ck, hd) >
              c->plan.attn_floats)
-        ck += 128;
+        ck += 64;
       a.chunk_keys = ck;
       a.n_chunks = (max_ltot + ck - 1) / ck;
       launch_tree_attention(a, c->st);
     }
     LAUNCHED(c);
-    TRY(gemm(c, EPI_RESID, c->ao, H * hd, rows, w.wo, nullptr, d, H * hd, c->x, nullptr, d));
-    launch_rmsnorm(c->x, w.n2, rows, d, m.norm_eps, c->xn, c->st);
-    LAUNCHED(c);
-    TRY(gemm(c, EPI_SILU, c->xn, d, rows, w.wg, w.wu, m.ffn_dim, d, nullptr, c->act, m.ffn_dim));
-    TRY(gemm(c, EPI_RESID, c->act, m.ffn_dim, rows, w.wd, nullptr, d, m.ffn_dim, c->x, nullptr,
-             d));
+    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
+      const int mc = std::min(CHUNK, rows - m0);
+      TRY(gemm(c, GK_O, c->ao + (size_t)m0 * H * hd, H * hd, mc, {w.wo}, {d}, nullptr, H * hd, &pt));
+      launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, w.n2, c->xn + (size_t)m0 * d, nullptr,
+                   c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
+      LAUNCHED(c);
+    }
+    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
+      const int mc = std::min(CHUNK, rows - m0);
+      TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * d, d, mc, {w.wg}, {F}, w.wu, d, &pt));
+      launch_silu(pt, row_norm(c, m0), mc, F, c->act + (size_t)m0 * F, c->st);
+      LAUNCHED(c);
+    }
+    const bool last = (l + 1 == nl);
+    const uint16_t* g_next = last ? final_g : c->layers[l + 1].n1;
+    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
+      const int mc = std::min(CHUNK, rows - m0);
+      TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * F, F, mc, {w.wd}, {d}, nullptr, F, &pt));
+      if (last && final_g) {
+        // the final feature h is materialised (LM head input, draft input)
+        launch_resid_norm(pt, 0, mc, d, RN_ADD, c->x + (size_t)m0 * d, final_g, m.norm_eps,
+                          final_xn + (size_t)m0 * d, nullptr, c->st);
+      } else {
+        launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, last ? nullptr : g_next,
+                     last ? nullptr : c->xn + (size_t)m0 * d,
+                     (last && final_xb) ? final_xb + (size_t)m0 * d : nullptr,
+                     last ? nullptr : c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
+      }
+      LAUNCHED(c);
+    }
   }
   return MSD_OK;
 }
 
-// Draft head on rows whose fc input is already in c->xn ([rows][2d]):
-// f = f_down(concat) -> decoder layer -> features in c->x.
+// Draft head on rows whose f_down input is in c->fcin ([rows][2d]):
+// f = f_down(concat), visual rows replaced by their embeddings, then the
+// decoder layer; features in c->x (f32) and c->xb (bf16).
 int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const uint16_t* visual) {
   const int d = c->m.d_model;
   const int rows = n_seq * nq;
-  TRY(gemm(c, EPI_F32, c->xn, 2 * d, rows, c->fc, nullptr, d, 2 * d, c->x, nullptr, d));
+  Parts pt;
+  for (int m0 = 0; m0 < rows; m0 += CHUNK) {
+    const int mc = std::min(CHUNK, rows - m0);
+    TRY(gemm(c, GK_FC, c->fcin + (size_t)m0 * 2 * d, 2 * d, mc, {c->fc}, {d}, nullptr, 2 * d, &pt));
+    launch_resid(pt, mc, d, RN_SET, c->x + (size_t)m0 * d, visual ? nullptr : c->dlayer.n1,
+                 visual ? nullptr : c->xn + (size_t)m0 * d, nullptr,
+                 visual ? nullptr : c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
+    LAUNCHED(c);
+  }
   if (visual) {
     launch_visual_rows(visual, c->rows.vis, rows, d, c->x, c->st);
     LAUNCHED(c);
+    TRY(norm_rows(c, rows, c->dlayer.n1));
   }
-  return forward_layers(c, true, n_seq, nq, tree_R, max_ltot);
+  return forward_layers(c, true, n_seq, nq, tree_R, max_ltot, nullptr, nullptr, c->xb);
 }
 
-// LM head + top-k over rows of c->x (draft features, f32): no final norm.
+// LM head + top-k (and log-sum-exp) over bf16 rows of c->xb: no final norm.
 int draft_head(msd_ctx* c, int rows, int k) {
   const int d = c->m.d_model, V = c->m.vocab;
-  launch_to_bf16(c->x, rows * d, c->xn, c->st);
-  LAUNCHED(c);
-  TRY(gemm(c, EPI_F32, c->xn, d, rows, c->lm_head, nullptr, V, d, c->logits, nullptr, V));
-  launch_topk(c->logits, rows, V, k, c->tk_idx, c->tk_val, c->tk_lse, c->tk_scratch, c->st);
-  LAUNCHED(c);
+  Parts pt;
+  for (int m0 = 0; m0 < rows; m0 += CHUNK) {
+    const int mc = std::min(CHUNK, rows - m0);
+    TRY(gemm(c, GK_LMHEAD, c->xb + (size_t)m0 * d, d, mc, {c->lm_head}, {V}, nullptr, d, &pt));
+    launch_topk(pt, mc, V, k, c->tk_idx + (size_t)m0 * k, c->tk_val + (size_t)m0 * k,
+                c->tk_lse + m0, nullptr, c->tk_scratch, c->st);
+    LAUNCHED(c);
+  }
   return MSD_OK;
 }
 
@@ -522,8 +595,8 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   c->dk = (uint16_t*)bufs->draft_k;
   c->dv = (uint16_t*)bufs->draft_v;
   carve(c, *m, *lim, (char*)bufs->workspace);
-  c->gs.target_wgs = 256;
-  if (const char* e = std::getenv("MSD_GEMM_WGS")) c->gs.target_wgs = std::max(1, atoi(e));
+  c->gs.target_wgs = GEMM_WGS;
+  c->gs.lds_bytes = GEMM_LDS;
   c->L.assign(lim->max_batch, 0);
   c->pend.assign(lim->max_batch, 0);
   c->ready.assign(lim->max_batch, 0);
@@ -620,19 +693,18 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
   // target over the prompt
   launch_embed(c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, c->x, c->st);
   LAUNCHED(c);
-  TRY(forward_layers(c, false, 1, n, -1, n));
-  launch_rmsnorm(c->x, c->final_norm, n, d, m.norm_eps, c->h, c->st);
-  LAUNCHED(c);
-  TRY(gemm(c, EPI_F32, c->h + (size_t)(n - 1) * d, d, 1, c->lm_head, nullptr, m.vocab, d,
-           c->logits, nullptr, m.vocab));
-  launch_topk(c->logits, 1, m.vocab, 1, c->tk_idx, c->tk_val, nullptr, c->tk_scratch, c->st);
+  TRY(norm_rows(c, n, c->layers[0].n1));
+  TRY(forward_layers(c, false, 1, n, -1, n, c->final_norm, c->h, nullptr));
+  Parts pt;
+  TRY(gemm(c, GK_LMHEAD, c->h + (size_t)(n - 1) * d, d, 1, {c->lm_head}, {m.vocab}, nullptr, d, &pt));
+  launch_topk(pt, 1, m.vocab, 1, c->tk_idx, c->tk_val, nullptr, nullptr, c->tk_scratch, c->st);
   LAUNCHED(c);
   launch_set_int(c->d_root, seq, c->tk_idx, 0, c->st);
   launch_set_int(c->nxt, n - 1, c->tk_idx, 0, c->st);
   LAUNCHED(c);
   // draft over the prompt: text rows f_down(Concat(h_i, e_{i+1})), visual rows e_i
   launch_fc_input(c->h, nullptr, c->rows.hrow, c->embed, c->nxt, (const uint16_t*)visual_d, n, d,
-                  c->xn, c->st);
+                  c->fcin, c->st);
   LAUNCHED(c);
   TRY(draft_pass(c, 1, n, -1, n, n_vis ? (const uint16_t*)visual_d : nullptr));
   launch_store_feat(c->x, n, c->rows.dst, d, c->dfeat, c->st);
@@ -704,7 +776,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
                         c->rows, c->prefix, c->st);
     LAUNCHED(c);
     launch_fc_input(c->pend_h, nullptr, c->rows.hrow, c->embed, c->rows.tok, nullptr,
-                    n_seq * r_max, d, c->xn, c->st);
+                    n_seq * r_max, d, c->fcin, c->st);
     LAUNCHED(c);
     TRY(draft_pass(c, n_seq, r_max, -1, max_l, nullptr));
     launch_store_feat(c->x, n_seq * r_max, c->rows.dst, d, c->dfeat, c->st);
@@ -716,6 +788,9 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
   for (int i = 0; i < n_seq; ++i)
     HIPC(c, hipMemcpyAsync(c->x + (size_t)i * d, c->dfeat + (size_t)seqs_h[i] * FEAT * d,
                            sizeof(float) * d, hipMemcpyDeviceToDevice, c->st));
+  launch_resid_norm(Parts{nullptr, 0, 0, 0}, 0, n_seq, d, RN_KEEP, c->x, nullptr, m.norm_eps,
+                    nullptr, c->xb, c->st);
+  LAUNCHED(c);
   if (spec->kind == MSD_TREE_STATIC) {
     TRY(draft_head(c, n_seq, c->round_k[0]));
     launch_tree_init_static(trees_d, n_seq, c->seq_ids, c->d_root, c->sp, T, c->st);
@@ -729,7 +804,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
                          FEAT, c->rows, c->prefix, c->st);
       LAUNCHED(c);
       launch_fc_input(nullptr, c->dfeat, c->rows.hrow, c->embed, c->rows.tok, nullptr, n_seq * nr,
-                      d, c->xn, c->st);
+                      d, c->fcin, c->st);
       LAUNCHED(c);
       const int R = c->round_exp_end[dd];
       TRY(draft_pass(c, n_seq, nr, R, max_l + R, nullptr));
@@ -748,7 +823,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
       launch_dyn_rows(c->pool, n_seq, c->seq_ids, c->d_len, K, dd, FEAT, c->rows, c->prefix, c->st);
       LAUNCHED(c);
       launch_fc_input(nullptr, c->dfeat, c->rows.hrow, c->embed, c->rows.tok, nullptr, n_seq * K,
-                      d, c->xn, c->st);
+                      d, c->fcin, c->st);
       LAUNCHED(c);
       const int R = exp_base;
       TRY(draft_pass(c, n_seq, K, R, max_l + R, nullptr));
@@ -787,13 +862,16 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
   LAUNCHED(c);
   launch_embed(c->embed, c->rows.tok, nullptr, nullptr, rows, d, c->x, c->st);
   LAUNCHED(c);
-  TRY(forward_layers(c, false, n_seq, T, T, max_l + T));
-  launch_rmsnorm(c->x, c->final_norm, rows, d, m.norm_eps, c->h, c->st);
-  LAUNCHED(c);
-  float* lg = logits_d ? logits_d : c->logits;
-  TRY(gemm(c, EPI_F32, c->h, d, rows, c->lm_head, nullptr, V, d, lg, nullptr, V));
-  launch_topk(lg, rows, V, 1, argmax_d, nullptr, nullptr, c->tk_scratch, c->st);
-  LAUNCHED(c);
+  TRY(norm_rows(c, rows, c->layers[0].n1));
+  TRY(forward_layers(c, false, n_seq, T, T, max_l + T, c->final_norm, c->h, nullptr));
+  Parts pt;
+  for (int m0 = 0; m0 < rows; m0 += CHUNK) {
+    const int mc = std::min(CHUNK, rows - m0);
+    TRY(gemm(c, GK_LMHEAD, c->h + (size_t)m0 * d, d, mc, {c->lm_head}, {V}, nullptr, d, &pt));
+    launch_topk(pt, mc, V, 1, argmax_d + m0, nullptr, nullptr,
+                logits_d ? logits_d + (size_t)m0 * V : nullptr, c->tk_scratch, c->st);
+    LAUNCHED(c);
+  }
   c->verified_T = T;
   c->verified_nseq = n_seq;
   return MSD_OK;

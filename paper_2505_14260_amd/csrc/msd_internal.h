@@ -26,33 +26,55 @@ MSD_DEV bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 namespace msd {
 
 // ---------------------------------------------------------------- GEMM ----
-// Y = X W^T for a thin X (M rows) against a weight streamed from HBM.
-enum Epilogue { EPI_F32 = 0, EPI_BF16 = 1, EPI_RESID = 2, EPI_SILU = 3 };
-
+// Partial products of a thin X (M rows) against a weight streamed from HBM:
+// part[s][m][n] = sum over K-chunk s of X[m][k] * W[n][k] (float32).  With a
+// second weight W2 (the SwiGLU pair) its products go to columns [N, 2N).
+// The consumer sums the S chunks in order.
 struct GemmArgs {
   const uint16_t* X;        // [M][ldx] bf16
   int ldx, M;
   const uint16_t* Wseg[3];  // [N][K] bf16 given as up to three row segments
   int seg_end[3];           // cumulative segment heights (multiples of 16)
-  const uint16_t* W2;       // second weight (EPI_SILU: up projection), [N][K]
+  const uint16_t* W2;       // second weight [N][K] or null
   int N, K;
-  float* out_f32;           // EPI_F32 / EPI_RESID
-  uint16_t* out_bf16;       // EPI_BF16 / EPI_SILU
-  int ldo;
+  int S, Kc, G;             // K chunks, chunk length, workgroups per chunk
+  float* part;              // partials of row 0 of this launch
+  size_t part_split;        // floats between consecutive chunks
+  int ldp;                  // floats between consecutive rows (N or 2N)
+};
+
+struct GemmPlan {
+  int MT, S, Kc, G, nw;
 };
 
 struct GemmScratch {
-  int target_wgs;  // workgroups that keep every CU busy (tile-width choice)
+  int target_wgs;  // workgroups per launch
+  int lds_bytes;   // LDS for the staged X chunk of one workgroup
 };
 
-void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* W,
-                 const uint16_t* W2, int N, int K, float* out_f32, uint16_t* out_bf16,
-                 int ldo, const GemmScratch& s, hipStream_t st);
-// Segmented form: the weight is the row concatenation of n_seg (<= 3)
-// matrices Wseg[q] of seg_rows[q] rows each (multiples of 16).
-void launch_gemm(int epi, const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
-                 const int* seg_rows, int n_seg, const uint16_t* W2, int K, float* out_f32,
-                 uint16_t* out_bf16, int ldo, const GemmScratch& s, hipStream_t st);
+GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs, int lds_bytes);
+// floats of partials for M rows (M <= 64 per launch)
+size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs, int lds_bytes);
+// rows M <= 64; the weight is the row concatenation of n_seg (<= 3) matrices
+void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
+                 const int* seg_rows, int n_seg, const uint16_t* W2, int K, float* part,
+                 const GemmScratch& sc, hipStream_t st);
+
+// Partial sums as seen by a consumer: value(m, n) = sum_s p[s*split + m*ld + n].
+struct Parts {
+  const float* p;
+  int S;
+  size_t split;
+  int ld;
+};
+
+// Per-row RMS of the un-normalised GEMM input: ssq[row][0..nblk) are sums of
+// x^2 over blocks of 256 features (ssq == null: no scaling).
+struct RowNorm {
+  const float* ssq;
+  int nblk, d;
+  float eps;
+};
 
 // ----------------------------------------------------------- attention ----
 struct AttnArgs {
@@ -79,8 +101,18 @@ void launch_embed(const uint16_t* E, const int* tokens, const int* vis_idx,
                   const uint16_t* visual, int rows, int d, float* x, hipStream_t st);
 void launch_rmsnorm(const float* x, const uint16_t* g, int rows, int d, float eps,
                     uint16_t* y, hipStream_t st);
+// x = (mode 1) sum of parts, (mode 2) x + sum of parts, (mode 0) x; then
+// xn = bf16(rmsnorm(x) * g) when g, xb = bf16(x) when xb.
+enum { RN_KEEP = 0, RN_SET = 1, RN_ADD = 2 };
+void launch_resid_norm(Parts pt, int col0, int rows, int d, int mode, float* x,
+                       const uint16_t* g, float eps, uint16_t* xn, uint16_t* xb, hipStream_t st);
+void launch_silu(Parts pt, RowNorm rn, int rows, int F, uint16_t* act, hipStream_t st);
+// Elementwise form: x updated as above, xg = bf16(x * g) when xg, xb = bf16(x)
+// when xb, ssq[row][blk] = sum of x^2 over feature block blk (256 wide).
+void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t* g, uint16_t* xg,
+                  uint16_t* xb, float* ssq, hipStream_t st);
 void launch_to_bf16(const float* x, int n, uint16_t* y, hipStream_t st);
-void launch_rope_kv(const float* qkv, int rows, int H, int KV, int hd, const int* pos,
+void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, const int* pos,
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
                     uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st);
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
@@ -91,10 +123,12 @@ void launch_visual_rows(const uint16_t* visual, const int* vis_idx, int rows, in
                         float* x, hipStream_t st);
 
 // -------------------------------------------------------- selection ----
-// scratch: topk_scratch_floats(rows, V) floats (8-byte aligned)
+// scratch: topk_scratch_floats(rows, V) floats (8-byte aligned).  The
+// logits are the summed parts; when logits_out is given they are also
+// written there ([rows][V]).
 size_t topk_scratch_floats(int rows, int V);
-void launch_topk(const float* logits, int rows, int V, int k, int* idx, float* val,
-                 float* lse, float* scratch, hipStream_t st);
+void launch_topk(Parts logits, int rows, int V, int k, int* idx, float* val, float* lse,
+                 float* logits_out, float* scratch, hipStream_t st);
 
 // ---------------------------------------------------- tree / accept ----
 // Row descriptors of one forward step (device arrays, one entry per row).
