@@ -86,11 +86,9 @@ def cpu_baseline(wl, w, dr, budget_s):
     h = rng.standard_normal(dims.d_model)
     st = O.SeqState(kv=kv, dkv=dkv, L=L, root=int(tok[1]),
                     pending=[O.PendingRow(False, h=h, e_next=m.embed(tok[1]))])
-    st.L = L
     arrays = None
     if wl.tree.kind == "static":
         arrays = synth.static_tree_arrays(wl.tree.paths)
-    st.L = L  # pending row sits at position L-1
     emitted, cycles = 0, 0
     t0 = time.perf_counter()
     while True:
@@ -118,10 +116,23 @@ def main():
     ap.add_argument("--workload", default="llava-1.5-7b-shaped")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy a 1 GiB buffer 8 times (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        for _ in range(8):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": n, "launches": 8}))
+        return
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(see DESIGN.md for how the decode path would shard).", file=sys.stderr)
+        print("bench.py measures one GPU: the decode path here runs on a single GPU "
+              "and has no multi-GPU mode.", file=sys.stderr)
         sys.exit(2)
     if int(os.environ.get("RANK", "0")) != 0:
         return
@@ -195,7 +206,9 @@ def main():
     L_mid = (L_start + L_end) // 2
     vb = verify_bytes(dims, L_mid, T)
     v_med = float(np.median(verify_ms))
-    silu = [r for r in recs if r[0] == SILU_KIND]
+    # the verify step's gate/up launches (M = tree nodes > 16 rows: the MT=2
+    # instantiation of the kernel); the draft's launches use M <= 16 rows
+    silu = [r for r in recs if r[0] == SILU_KIND and r[1] > 16]
     silu_ms = float(np.mean([r[4] for r in silu]))
     silu_bytes = float(np.mean([silu_launch_bytes(dims, r[1]) for r in silu]))
     achieved = silu_bytes / (silu_ms * 1e-3) / 1e9
@@ -225,7 +238,7 @@ def main():
             "batch": 1, "draft_fc_init": wl.draft_fc_mode,
         },
         "roofline": {
-            "kernel": "k_gemm<MT=1, SwiGLU> (gate+up projection)",
+            "kernel": "k_gemm<2, 2, 3, false> (verify-step gate+up projection, M=27)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,

@@ -215,12 +215,14 @@ int msd_set_state(msd_ctx* ctx, int seq, int L, const void* h_d, int32_t next_to
 /*
  * Optional timing trace of the weight-streaming GEMM launches (for
  * measurement tools).  msd_trace_enable(ctx, capacity, kinds) starts
- * recording a pair of stream events around each of the next `capacity` GEMM
- * launches whose kind has its bit set in `kinds` (capacity <= 0 stops and
+ * timing the next `capacity` GEMM launches whose kind has its bit set in
+ * `kinds` with events carried by the launch itself (capacity <= 0 stops and
  * clears); msd_trace_read waits for the stream and returns up to max_recs
  * records (return value: count, or < 0 on error).
- * kind: 0 = f32 store, 1 = bf16 store, 2 = residual add, 3 = SwiGLU pair.
- * The weight of a record is n x k bf16 (twice that for kind 3).
+ * kind: 0 = q/k/v projection, 1 = output projection, 2 = down projection,
+ * 3 = gate+up (SwiGLU) pair, 4 = draft f_down, 5 = LM head.
+ * m is the number of input rows; the weight of a record is n x k bf16
+ * (twice that for kind 3).
  */
 typedef struct msd_trace_rec {
   int32_t kind, m, n, k;

@@ -17,6 +17,8 @@
 //    kernel that consumes the product (residual + RMSNorm, RoPE + KV write,
 //    SwiGLU, vocabulary top-k) sums the S partials in chunk order, so the
 //    result is deterministic.
+#include <hip/hip_ext.h>
+
 #include "msd_internal.h"
 
 namespace msd {
@@ -177,18 +179,28 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
+// With timing events the launch carries them in its dispatch packet, so they
+// bracket the kernel's execution only.
 template <int MT, int NW, bool TAIL>
-void launch_one(dim3 grid, size_t lds, const GemmArgs& a, hipStream_t st) {
+void launch_one(dim3 grid, size_t lds, const GemmArgs& a, const GemmScratch& sc,
+                hipStream_t st) {
   constexpr int P = NW == 2 ? 3 : 4;
-  hipLaunchKernelGGL((k_gemm<MT, NW, P, TAIL>), grid, dim3(256), lds, st, a);
+  if (sc.ev_start)
+    hipExtLaunchKernelGGL((k_gemm<MT, NW, P, TAIL>), grid, dim3(256), lds, st, sc.ev_start,
+                          sc.ev_stop, 0, a);
+  else
+    hipLaunchKernelGGL((k_gemm<MT, NW, P, TAIL>), grid, dim3(256), lds, st, a);
 }
 
 template <int MT>
-void launch_mt(int nw, bool tail, dim3 grid, size_t lds, const GemmArgs& a, hipStream_t st) {
+void launch_mt(int nw, bool tail, dim3 grid, size_t lds, const GemmArgs& a,
+               const GemmScratch& sc, hipStream_t st) {
   if (nw == 2) {
-    if (tail) launch_one<MT, 2, true>(grid, lds, a, st); else launch_one<MT, 2, false>(grid, lds, a, st);
+    if (tail) launch_one<MT, 2, true>(grid, lds, a, sc, st);
+    else launch_one<MT, 2, false>(grid, lds, a, sc, st);
   } else {
-    if (tail) launch_one<MT, 1, true>(grid, lds, a, st); else launch_one<MT, 1, false>(grid, lds, a, st);
+    if (tail) launch_one<MT, 1, true>(grid, lds, a, sc, st);
+    else launch_one<MT, 1, false>(grid, lds, a, sc, st);
   }
 }
 
@@ -253,9 +265,9 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
   a.part_split = (size_t)M * N * nw;
   a.part = part;
   dim3 grid(pl.S * pl.G);
-  if (pl.MT == 1) launch_mt<1>(nw, tail, grid, lds, a, st);
-  else if (pl.MT == 2) launch_mt<2>(nw, tail, grid, lds, a, st);
-  else launch_mt<4>(nw, tail, grid, lds, a, st);
+  if (pl.MT == 1) launch_mt<1>(nw, tail, grid, lds, a, sc, st);
+  else if (pl.MT == 2) launch_mt<2>(nw, tail, grid, lds, a, sc, st);
+  else launch_mt<4>(nw, tail, grid, lds, a, sc, st);
 }
 
 }  // namespace msd

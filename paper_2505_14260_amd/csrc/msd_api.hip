@@ -286,15 +286,16 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M,
     N += r;
   }
   const bool tr = c->tracing && ((c->trace_kinds >> kind) & 1) && c->trace.size() < c->trace_cap;
+  GemmScratch gs = c->gs;
   if (tr) {
     msd_ctx::TraceRec r{kind, M, N, K, c->ev_pool[2 * c->trace.size()],
                         c->ev_pool[2 * c->trace.size() + 1]};
-    HIPC(c, hipEventRecord(r.a, c->st));
+    gs.ev_start = r.a;
+    gs.ev_stop = r.b;
     c->trace.push_back(r);
   }
-  launch_gemm(X, ldx, M, sp, sr, n, W2, K, c->part, c->gs, c->st);
+  launch_gemm(X, ldx, M, sp, sr, n, W2, K, c->part, gs, c->st);
   LAUNCHED(c);
-  if (tr) HIPC(c, hipEventRecord(c->trace.back().b, c->st));
   const int nw = W2 ? 2 : 1;
   const GemmPlan pl = plan_gemm(M, N, K, nw, c->gs.target_wgs, c->gs.lds_bytes);
   *out = Parts{c->part, pl.S, (size_t)M * N * nw, N * nw};
@@ -597,6 +598,8 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   carve(c, *m, *lim, (char*)bufs->workspace);
   c->gs.target_wgs = GEMM_WGS;
   c->gs.lds_bytes = GEMM_LDS;
+  c->gs.ev_start = nullptr;
+  c->gs.ev_stop = nullptr;
   c->L.assign(lim->max_batch, 0);
   c->pend.assign(lim->max_batch, 0);
   c->ready.assign(lim->max_batch, 0);

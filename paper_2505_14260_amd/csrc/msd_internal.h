@@ -50,6 +50,7 @@ struct GemmPlan {
 struct GemmScratch {
   int target_wgs;  // workgroups per launch
   int lds_bytes;   // LDS for the staged X chunk of one workgroup
+  hipEvent_t ev_start, ev_stop;  // when set: recorded around the kernel itself
 };
 
 GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs, int lds_bytes);
