@@ -15,6 +15,9 @@
 // B = P^T).  The K rows feeding MFMA row i are key pi(i) (bits 2 and 3 of i
 // swapped), which makes each lane's eight P values of the second product
 // correspond to eight consecutive keys, i.e. one 16-byte load of V^T.
+// Q (float32) and P enter the MFMAs as bf16 hi + lo pairs (x = hi + lo,
+// lo = bf16(x - hi)), so only the bf16 cache rows limit the precision; the
+// output rows are split rows (the O projection's input).
 #include "msd_internal.h"
 
 namespace msd {
@@ -72,7 +75,8 @@ MSD_DEV void load_v(uint4 (&vf)[HD / 32][2], const uint16_t* vbase, int S, int k
 // query columns; vis(key) decides visibility.  The next block's K rows and
 // the current block's V columns are loaded while the scores are computed.
 template <int HD, typename Vis>
-MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qf)[HD / 16],
+MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qh)[HD / 16],
+                          const bf16x8 (&ql)[HD / 16],
                           const uint16_t* kbase, const uint16_t* vbase, int S,
                           int k_begin, int k_end, int k_valid, float scale, Vis vis) {
   const int lane = threadIdx.x & 63;
@@ -85,9 +89,13 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qf)[HD / 16],
     load_v<HD>(vf, vbase, S, kb, k_valid);
     // ---- S^T tile: rows = keys, columns = query rows
     f32x16 s = {};
+    f32x16 s2 = {};
 #pragma unroll
-    for (int c = 0; c < HD / 16; ++c)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), qf[c], s, 0, 0, 0);
+    for (int c = 0; c < HD / 16; ++c) {
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), qh[c], s, 0, 0, 0);
+      s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), ql[c], s2, 0, 0, 0);
+    }
+    s += s2;
     if (kb + 32 < k_end) load_k<HD>(kf, kbase, kb + 32, k_valid);
     float bm = -INFINITY;
 #pragma unroll
@@ -110,14 +118,19 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qf)[HD / 16],
     const float alpha = (st.m == -INFINITY) ? 0.f : __expf(st.m - m_new);
     st.l = st.l * alpha + rs;
     st.m = m_new;
-    uint4 pb[2];
+    uint4 pb[2], pl[2];
 #pragma unroll
     for (int pk = 0; pk < 2; ++pk) {
-      uint32_t w[4];
+      uint32_t w[4], wl[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        w[e] = (uint32_t)f2bf(p[pk * 8 + 2 * e]) | ((uint32_t)f2bf(p[pk * 8 + 2 * e + 1]) << 16);
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = p[pk * 8 + 2 * e], p1 = p[pk * 8 + 2 * e + 1];
+        const uint16_t h0 = f2bf(p0), h1 = f2bf(p1);
+        w[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        wl[e] = (uint32_t)f2bf(p0 - bf2f(h0)) | ((uint32_t)f2bf(p1 - bf2f(h1)) << 16);
+      }
       pb[pk] = make_uint4(w[0], w[1], w[2], w[3]);
+      pl[pk] = make_uint4(wl[0], wl[1], wl[2], wl[3]);
     }
     // ---- O^T += V^T P^T
 #pragma unroll
@@ -125,19 +138,35 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qf)[HD / 16],
 #pragma unroll
       for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
 #pragma unroll
-      for (int pk = 0; pk < 2; ++pk)
+      for (int pk = 0; pk < 2; ++pk) {
         st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[dt][pk]), as_bf16x8(pb[pk]),
                                                            st.o[dt], 0, 0, 0);
+        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[dt][pk]), as_bf16x8(pl[pk]),
+                                                           st.o[dt], 0, 0, 0);
+      }
     }
   }
 }
 
+// The lane's 8-element slices of its query row, split into bf16 hi and lo.
 template <int HD>
-MSD_DEV void load_q(bf16x8 (&qf)[HD / 16], const uint16_t* qrow) {
+MSD_DEV void load_q(bf16x8 (&qh)[HD / 16], bf16x8 (&ql)[HD / 16], const float* qrow) {
   const int h = (threadIdx.x & 63) >> 5;
 #pragma unroll
-  for (int c = 0; c < HD / 16; ++c)
-    qf[c] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + (HD / 2) * h + 8 * c));
+  for (int c = 0; c < HD / 16; ++c) {
+    const float4* src = reinterpret_cast<const float4*>(qrow + (HD / 2) * h + 8 * c);
+    const float4 a = src[0], b = src[1];
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    uint32_t hw[4], lw[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint16_t h0 = f2bf(v[2 * e]), h1 = f2bf(v[2 * e + 1]);
+      hw[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+      lw[e] = (uint32_t)f2bf(v[2 * e] - bf2f(h0)) | ((uint32_t)f2bf(v[2 * e + 1] - bf2f(h1)) << 16);
+    }
+    qh[c] = as_bf16x8(make_uint4(hw[0], hw[1], hw[2], hw[3]));
+    ql[c] = as_bf16x8(make_uint4(lw[0], lw[1], lw[2], lw[3]));
+  }
 }
 
 template <int HD>
@@ -153,7 +182,7 @@ MSD_DEV void init_state(AttnState<HD>& st) {
 // O^T C layout: lane holds query column (lane & 31), register r of dim tile
 // dt holds dim dt*32 + 8*(r/4) + 4*(lane/32) + r%4.
 template <int HD>
-MSD_DEV void store_final(const AttnState<HD>& st, uint16_t* orow, bool valid) {
+MSD_DEV void store_final(const AttnState<HD>& st, uint16_t* orow, int K, bool valid) {
   if (!valid) return;
   const int h = (threadIdx.x & 63) >> 5;
   const float inv = st.l > 0.f ? 1.f / st.l : 0.f;
@@ -161,7 +190,7 @@ MSD_DEV void store_final(const AttnState<HD>& st, uint16_t* orow, bool valid) {
   for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r)
-      orow[dt * 32 + 8 * (r >> 2) + 4 * h + (r & 3)] = f2bf(st.o[dt][r] * inv);
+      put_split(orow, K, dt * 32 + 8 * (r >> 2) + 4 * h + (r & 3), st.o[dt][r] * inv);
 }
 
 template <int HD>
@@ -185,9 +214,9 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
   const int head = g * G + (qr - node * G);
   const bool valid = node < a.nq;
   if (!valid) node = 0;
-  const uint16_t* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)(valid ? head : g * G) * HD;
-  bf16x8 qf[HD / 16];
-  load_q<HD>(qf, qrow);
+  const float* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)(valid ? head : g * G) * HD;
+  bf16x8 qh[HD / 16], ql[HD / 16];
+  load_q<HD>(qh, ql, qrow);
   const uint64_t msk = a.mask[sidx * a.nq + node];
   const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
   const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
@@ -195,11 +224,12 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
   init_state<HD>(st);
   const int k0 = c * a.chunk_keys;
   const int k1 = min(k0 + a.chunk_keys, Ltot);
-  attend_range<HD>(st, qf, kbase, vbase, a.S, k0, k1, Ltot, a.scale, [&](int key) {
+  attend_range<HD>(st, qh, ql, kbase, vbase, a.S, k0, k1, Ltot, a.scale, [&](int key) {
     return key < P || ((msk >> (key - P)) & 1ull);
   });
   if (a.n_chunks == 1) {
-    store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD, valid);
+    store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * 2 * a.H * HD + (size_t)head * HD,
+                    a.H * HD, valid);
     return;
   }
   float* po = a.part_o + (size_t)wid * 32 * HD;
@@ -248,8 +278,8 @@ __global__ __launch_bounds__(HD) void k_tree_combine(AttnArgs a) {
       num += w * oc;
     }
   }
-  a.out[(size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD + dim] =
-      f2bf(den > 0.f ? num / den : 0.f);
+  put_split(a.out + (size_t)(sidx * a.nq + node) * 2 * a.H * HD, a.H * HD, head * HD + dim,
+            den > 0.f ? num / den : 0.f);
 }
 
 template <int HD>
@@ -269,9 +299,9 @@ __global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
   int node = qt * 32 + j;
   const bool valid = node < a.nq;
   if (!valid) node = a.nq - 1;
-  const uint16_t* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD;
-  bf16x8 qf[HD / 16];
-  load_q<HD>(qf, qrow);
+  const float* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD;
+  bf16x8 qh[HD / 16], ql[HD / 16];
+  load_q<HD>(qh, ql, qrow);
   const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
   const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
   AttnState<HD> st;
@@ -279,9 +309,10 @@ __global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
   const int last = min(qt * 32 + 32, a.nq);
   const int k1 = P + last;
   const int my_last = P + node;
-  attend_range<HD>(st, qf, kbase, vbase, a.S, 0, k1, k1, a.scale,
+  attend_range<HD>(st, qh, ql, kbase, vbase, a.S, 0, k1, k1, a.scale,
                    [&](int key) { return key <= my_last; });
-  store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD, valid);
+  store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * 2 * a.H * HD + (size_t)head * HD,
+                  a.H * HD, valid);
 }
 
 }  // namespace

@@ -1,4 +1,5 @@
-// Thin-M bf16 GEMM on gfx950 MFMA: P_s[m][n] = sum_{k in chunk s} X[m][k] * W[n][k].
+// Thin-M GEMM on gfx950 MFMA: P_s[m][n] = sum_{k in chunk s} X[m][k] * W[n][k],
+// W in bfloat16, X as split rows (bf16 hi + lo).
 //
 // The decode path multiplies a few dozen activation rows (tree nodes) by
 // large weight matrices, so the kernel is bound by streaming W from HBM once.
@@ -9,6 +10,12 @@
 //    tiles, each wave owning 16 rows of a tile, with a ring of P register
 //    stages whose prefetch runs across tile boundaries.  No workgroup or wave
 //    ever waits for another one.
+//  - X arrives split by its producer, x = hi + lo with hi = bf16(x) and
+//    lo = bf16(x - hi), so W x = W hi + W lo carries about 16 significant bits
+//    of the activations (one bf16 rounding of every GEMM input, amplified by
+//    a deep stack of layers, is far larger than the error of the weights'
+//    products themselves).  Two MFMAs per step; the kernel stays bound by
+//    the weight stream.
 //  - v_mfma_f32_16x16x32_bf16 with A = W rows (from HBM) and B = X^T (from
 //    LDS).  The K index inside one MFMA may be any permutation shared by A and
 //    B, so a lane loads 32 physically contiguous bf16 of its W row (the four
@@ -52,9 +59,9 @@ MSD_DEV void load_w(WFrag<NW>& f, const uint16_t* const (&wrow)[NW], int k, int 
   }
 }
 
-// LDS X chunk: row m holds the chunk's columns in 16-byte units; unit u of
-// row m is stored at u ^ (m & 15) so that the 16 rows read by one MFMA
-// operand load hit different banks.
+// LDS X chunk: row m holds the chunk's columns in 16-byte units (8 bf16);
+// unit u of row m is stored at u ^ (m & 15) so that the 16 rows read by one
+// MFMA operand load hit different banks.  The lo halves follow the hi halves.
 MSD_DEV int xs_index(int m, int u, int units_per_row) { return m * units_per_row + (u ^ (m & 15)); }
 
 // Row pointers of W (and W2) for 16-row group `row0` of a tile; only
@@ -103,12 +110,19 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   // kend are zero).  Issued before the weight prefetch: loads complete in
   // order, so staging first does not wait for the first weight blocks.
   const int units = nkb * (KB / 8);
+  const int lo_base = MT * 16 * upr;
   for (int e = threadIdx.x; e < MT * 16 * units; e += 256) {
     const int m = e / units, u = e - m * units;
     const int col = k0 + 8 * u;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (m < M && col < kend) v = *reinterpret_cast<const uint4*>(a.X + (size_t)m * a.ldx + col);
-    xs[xs_index(m, u, upr)] = v;
+    uint4 hi = make_uint4(0, 0, 0, 0), lo = hi;
+    if (m < M && col < kend) {
+      const uint16_t* src = a.X + (size_t)m * a.ldx + col;
+      hi = *reinterpret_cast<const uint4*>(src);
+      lo = *reinterpret_cast<const uint4*>(src + K);
+    }
+    const int xi = xs_index(m, u, upr);
+    xs[xi] = hi;
+    xs[lo_base + xi] = lo;
   }
   WFrag<NW> ring[P];
   if (total > 0) {
@@ -139,19 +153,30 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
       const int f = f0 + p;
       if (f < total) {
         const int kb = f % nkb;
-        uint4 xf[MT][4];
+        uint4 xh[MT][4], xl[MT][4];
 #pragma unroll
         for (int t = 0; t < MT; ++t)
 #pragma unroll
-          for (int c = 0; c < 4; ++c) xf[t][c] = xs[xs_index(t * 16 + i, kb * 16 + 4 * g + c, upr)];
+          for (int c = 0; c < 4; ++c) {
+            const int xi = xs_index(t * 16 + i, kb * 16 + 4 * g + c, upr);
+            xh[t][c] = xs[xi];
+            xl[t][c] = xs[lo_base + xi];
+          }
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+        for (int c = 0; c < 4; ++c) {
 #pragma unroll
           for (int w = 0; w < NW; ++w)
 #pragma unroll
             for (int t = 0; t < MT; ++t)
               acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  as_bf16x8(ring[p].w[w][c]), as_bf16x8(xf[t][c]), acc[w][t], 0, 0, 0);
+                  as_bf16x8(ring[p].w[w][c]), as_bf16x8(xh[t][c]), acc[w][t], 0, 0, 0);
+#pragma unroll
+          for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+              acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(ring[p].w[w][c]), as_bf16x8(xl[t][c]), acc[w][t], 0, 0, 0);
+        }
         const int fn = min(f + P, total - 1);
         const uint16_t* wr[NW];
         row_ptrs<NW>(wr, (gi + (fn / nkb) * G) * TILE_ROWS + row_in_tile, N, K, w0, w1, w2, e0, e1,
@@ -210,8 +235,8 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs, int lds_bytes) {
   GemmPlan p;
   const int mc = M < 64 ? M : 64;
   p.MT = mc <= 16 ? 1 : (mc <= 32 ? 2 : 4);
-  // X chunk in LDS: MT*16 rows of Kc bf16 within lds_bytes
-  const int kc_max = (lds_bytes / 2 / (p.MT * 16)) / KB * KB;
+  // X chunk in LDS: MT*16 rows of Kc bf16 pairs (hi, lo) within lds_bytes
+  const int kc_max = (lds_bytes / 4 / (p.MT * 16)) / KB * KB;
   p.S = (K + kc_max - 1) / kc_max;
   p.Kc = ((K + p.S - 1) / p.S + KB - 1) / KB * KB;
   p.S = (K + p.Kc - 1) / p.Kc;
@@ -250,7 +275,7 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
   const GemmPlan pl = plan_gemm(M, N, K, nw, sc.target_wgs, sc.lds_bytes);
   // chunks are whole 128-column blocks except when K itself is not
   const bool tail = (K % KB) != 0;
-  const size_t lds = (size_t)pl.MT * 16 * pl.Kc * 2;
+  const size_t lds = (size_t)pl.MT * 16 * pl.Kc * 4;
   GemmArgs a = base;
   a.X = X;
   a.ldx = ldx;

@@ -39,24 +39,6 @@ __global__ __launch_bounds__(256) void k_visual_rows(const uint16_t* visual, con
   for (int e = threadIdx.x; e < d; e += 256) x[(size_t)row * d + e] = bf2f(visual[(size_t)v * d + e]);
 }
 
-// y = bf16(x / sqrt(mean(x^2) + eps) * g)
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* x, const uint16_t* g, int d,
-                                                 float eps, uint16_t* y) {
-  __shared__ float sh[4];
-  const int row = blockIdx.x;
-  const float* xr = x + (size_t)row * d;
-  float ss = 0.f;
-  for (int e = threadIdx.x; e < d; e += 256) ss += xr[e] * xr[e];
-  ss = block_sum_256(ss, sh);
-  const float r = rsqrtf(ss / (float)d + eps);
-  for (int e = threadIdx.x; e < d; e += 256) y[(size_t)row * d + e] = f2bf(xr[e] * r * bf2f(g[e]));
-}
-
-__global__ void k_to_bf16(const float* x, int n, uint16_t* y) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) y[i] = f2bf(x[i]);
-}
-
 // cos/sin of pos * theta^(-2i/hd), evaluated in float64.
 __global__ void k_rope_table(float2* tab, int max_pos, int half, double theta) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
@@ -88,15 +70,15 @@ MSD_DEV float row_rstd(const RowNorm& rn, int row) {
   return rsqrtf(t / (float)rn.d + rn.eps);
 }
 
-// Rotate-half RoPE on q and k, write q (bf16), K to its slot and V to the
-// transposed V cache.  qkv: summed parts, [rows][(H + 2KV) * hd], computed
+// Rotate-half RoPE on q and k, write q (float32), K to its slot and V to the
+// transposed V cache (bf16).  qkv: summed parts, [rows][(H + 2KV) * hd], computed
 // from the un-normalised input, so every row is first scaled by its 1/rms.
 // One block of hd/2 threads per (row, head); heads H.. are the key heads,
 // H+KV.. the value heads.
 __global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, int KV, int hd,
                                                 const int* pos, const int* row_seq,
                                                 const int* row_slot, const float2* tab,
-                                                uint16_t* q, uint16_t* kc, uint16_t* vc, int S) {
+                                                float* q, uint16_t* kc, uint16_t* vc, int S) {
   const int row = blockIdx.x;
   const int head = blockIdx.y;
   const int half = hd / 2;
@@ -118,8 +100,8 @@ __global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, in
     const float y0 = a * t.x - c * t.y;
     const float y1 = c * t.x + a * t.y;
     if (head < H) {
-      q[(size_t)row * H * hd + head * hd + i] = f2bf(y0);
-      q[(size_t)row * H * hd + head * hd + i + half] = f2bf(y1);
+      q[(size_t)row * H * hd + head * hd + i] = y0;
+      q[(size_t)row * H * hd + head * hd + i + half] = y1;
     } else {
       uint16_t* kr = kc + ((size_t)(b * KV + head - H) * S + slot) * hd;
       kr[i] = f2bf(y0);
@@ -141,8 +123,8 @@ MSD_DEV float block_sum_1024(float v, float* sh) {
 }
 
 // x = sum of parts (RN_SET), x + sum (RN_ADD) or x (RN_KEEP); then the
-// RMSNorm of the new x (bf16, gain g) and/or x itself in bf16.  One block of
-// 1024 threads per row.
+// RMSNorm of the new x (gain g) and/or a copy of x, as split rows.  One
+// block of 1024 threads per row.
 __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, int mode, float* x,
                                                      const uint16_t* g, float eps, uint16_t* xn,
                                                      uint16_t* xb) {
@@ -158,17 +140,18 @@ __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, 
       xr[e] = v;
     }
     ss += v * v;
-    if (xb) xb[(size_t)row * d + e] = f2bf(v);
+    if (xb) put_split(xb + (size_t)row * 2 * d, d, e, v);
   }
   if (!g) return;
   ss = block_sum_1024(ss, sh);
   const float r = rsqrtf(ss / (float)d + eps);
-  for (int e = threadIdx.x; e < d; e += 1024) xn[(size_t)row * d + e] = f2bf(xr[e] * r * bf2f(g[e]));
+  for (int e = threadIdx.x; e < d; e += 1024)
+    put_split(xn + (size_t)row * 2 * d, d, e, xr[e] * r * bf2f(g[e]));
 }
 
 // Elementwise residual update: x = sum of parts (RN_SET), x + sum (RN_ADD)
-// or x (RN_KEEP); then xg = bf16(x * g) (the next GEMM's input, normalised
-// later by its consumer), xb = bf16(x), and the block's sum of x^2 into
+// or x (RN_KEEP); then xg = x * g (the next GEMM's input, normalised later
+// by its consumer) and xb = x as split rows, and the block's sum of x^2 into
 // ssq[row][block].  Grid (ceil(d/256), rows).
 __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float* x,
                                                const uint16_t* g, uint16_t* xg, uint16_t* xb,
@@ -184,16 +167,17 @@ __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float*
       v = (mode == RN_SET) ? p : v + p;
       x[(size_t)row * d + e] = v;
     }
-    if (xg) xg[(size_t)row * d + e] = f2bf(v * bf2f(g[e]));
-    if (xb) xb[(size_t)row * d + e] = f2bf(v);
+    if (xg) put_split(xg + (size_t)row * 2 * d, d, e, v * bf2f(g[e]));
+    if (xb) put_split(xb + (size_t)row * 2 * d, d, e, v);
   }
   if (!ssq) return;
   const float t = block_sum_256(v * v, sh);
   if (threadIdx.x == 0) ssq[(size_t)row * gridDim.x + blockIdx.x] = t;
 }
 
-// act = bf16(silu(gate) * up) with gate at columns [0, F), up at [F, 2F),
-// both scaled by the row's 1/rms (the GEMM read the un-normalised input).
+// act = silu(gate) * up (split rows) with gate at columns [0, F), up at
+// [F, 2F), both scaled by the row's 1/rms (the GEMM read the un-normalised
+// input).
 __global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint16_t* act) {
   const int row = blockIdx.y;
   const int f = blockIdx.x * 256 + threadIdx.x;
@@ -201,12 +185,13 @@ __global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint1
   const float r = row_rstd(rn, row);
   const float gt = r * part_sum(pt, row, f);
   const float up = r * part_sum(pt, row, F + f);
-  act[(size_t)row * F + f] = f2bf(gt / (1.f + __expf(-gt)) * up);
+  put_split(act + (size_t)row * 2 * F, F, f, gt / (1.f + __expf(-gt)) * up);
 }
 
-// out[row] = [h_row | e_next] in bf16, the concat fed to the draft's f_down.
-// h comes from bf16 rows (target features) or f32 rows (draft features);
-// next_tok >= 0 selects E[next_tok], next_tok < 0 selects visual row -1-next_tok.
+// out[row] = [h_row | e_next] as a split row of 2d, the concat fed to the
+// draft's f_down; h rows are target features (split rows, h) or draft
+// features (float32 rows, hf); next_tok >= 0 selects E[next_tok], next_tok < 0
+// selects visual row -1-next_tok.
 __global__ __launch_bounds__(256) void k_fc_input(const uint16_t* h, const float* hf,
                                                   const int* h_row, const uint16_t* E,
                                                   const int* next_tok, const uint16_t* visual,
@@ -215,10 +200,17 @@ __global__ __launch_bounds__(256) void k_fc_input(const uint16_t* h, const float
   const int hr = h_row[row];
   const int nt = next_tok[row];
   const uint16_t* e = (nt >= 0) ? E + (size_t)nt * d : visual + (size_t)(-1 - nt) * d;
-  uint16_t* o = out + (size_t)row * 2 * d;
+  uint16_t* o = out + (size_t)row * 4 * d;
   for (int i = threadIdx.x; i < d; i += 256) {
-    o[i] = h ? h[(size_t)hr * d + i] : f2bf(hf[(size_t)hr * d + i]);
+    if (h) {
+      const uint16_t* hs = h + (size_t)hr * 2 * d;
+      o[i] = hs[i];
+      o[2 * d + i] = hs[d + i];
+    } else {
+      put_split(o, 2 * d, i, hf[(size_t)hr * d + i]);
+    }
     o[d + i] = e[i];
+    o[3 * d + i] = 0;
   }
 }
 
@@ -360,17 +352,6 @@ void launch_visual_rows(const uint16_t* visual, const int* vis_idx, int rows, in
   hipLaunchKernelGGL(k_visual_rows, dim3(rows), dim3(256), 0, st, visual, vis_idx, d, x);
 }
 
-void launch_rmsnorm(const float* x, const uint16_t* g, int rows, int d, float eps, uint16_t* y,
-                    hipStream_t st) {
-  if (rows <= 0) return;
-  hipLaunchKernelGGL(k_rmsnorm, dim3(rows), dim3(256), 0, st, x, g, d, eps, y);
-}
-
-void launch_to_bf16(const float* x, int n, uint16_t* y, hipStream_t st) {
-  if (n <= 0) return;
-  hipLaunchKernelGGL(k_to_bf16, dim3((n + 255) / 256), dim3(256), 0, st, x, n, y);
-}
-
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st) {
   const int n = max_pos * (hd / 2);
   hipLaunchKernelGGL(k_rope_table, dim3((n + 255) / 256), dim3(256), 0, st, tab, max_pos,
@@ -379,7 +360,7 @@ void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream
 
 void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, const int* pos,
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
-                    uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st) {
+                    float* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st) {
   if (rows <= 0) return;
   hipLaunchKernelGGL(k_rope_kv, dim3(rows, H + 2 * KV), dim3(64), 0, st, qkv, rn, H, KV, hd, pos,
                      row_seq, row_slot, rope_tab, q, kc, vc, S);
@@ -405,11 +386,11 @@ void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t*
 }
 
 void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const uint16_t* E,
-                     const int* next_tok, const uint16_t* visual, int rows, int d,
-                     uint16_t* out, hipStream_t st) {
+                     const int* next_tok, const uint16_t* visual, int rows, int d, uint16_t* out,
+                     hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_fc_input, dim3(rows), dim3(256), 0, st, h, hf, h_row, E, next_tok,
-                     visual, d, out);
+  hipLaunchKernelGGL(k_fc_input, dim3(rows), dim3(256), 0, st, h, hf, h_row, E, next_tok, visual,
+                     d, out);
 }
 
 size_t topk_scratch_floats(int rows, int V) {

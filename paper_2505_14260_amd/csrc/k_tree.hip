@@ -339,9 +339,9 @@ __global__ void k_commit(const int* seq_ids, const int* path, const int* n_path,
   const int n = n_path[sidx];
   if (j >= n) return;
   const int u = path[sidx * MSD_MAX_TREE + j];
-  const uint16_t* src = h_tree + (size_t)(sidx * T + u) * d;
-  uint16_t* dst = pend_h + (size_t)(b * pend_stride + j) * d;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) dst[e] = src[e];
+  const uint16_t* src = h_tree + (size_t)(sidx * T + u) * 2 * d;
+  uint16_t* dst = pend_h + (size_t)(b * pend_stride + j) * 2 * d;
+  for (int e = threadIdx.x; e < 2 * d; e += blockDim.x) dst[e] = src[e];
   if (threadIdx.x == 0) {
     pend_next[b * pend_stride + j] = emitted[sidx * MSD_MAX_TREE + j];
     if (j == 0) {
@@ -349,6 +349,13 @@ __global__ void k_commit(const int* seq_ids, const int* path, const int* n_path,
       d_len[b] += n;
       d_root[b] = emitted[sidx * MSD_MAX_TREE + n - 1];
     }
+  }
+}
+
+__global__ void k_import_row(const uint16_t* src, int n, uint16_t* dst) {
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) {
+    dst[e] = src[e];
+    dst[n + e] = 0;
   }
 }
 
@@ -440,6 +447,11 @@ void launch_commit(int n_seq, const int* seq_ids, const int* path, const int* n_
   hipLaunchKernelGGL(k_commit, dim3(n_seq, MSD_MAX_TREE), dim3(256), 0, st, seq_ids, path,
                      n_path, emitted, h_tree, T, d, pend_h, pend_next, pend_n, pend_stride,
                      d_len, d_root);
+}
+
+void launch_import_row(const uint16_t* src, int n, uint16_t* dst, hipStream_t st) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(k_import_row, dim3((n + 255) / 256), dim3(256), 0, st, src, n, dst);
 }
 
 void launch_set_int(int* p, int idx, const int* src, int src_idx, hipStream_t st) {

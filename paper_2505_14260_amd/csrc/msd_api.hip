@@ -33,9 +33,9 @@ constexpr int POOL = 1024;              // dynamic-tree candidates per sequence
 constexpr int STAGE_INTS = 1 << 16;
 // GEMM launch shape: about one workgroup per CU streams best (more
 // concurrent row streams per CU lower the achieved HBM bandwidth), with a
-// 32 KB X chunk per workgroup.
+// 64 KB X chunk (bf16 hi and lo halves) per workgroup.
 constexpr int GEMM_WGS = 256;
-constexpr int GEMM_LDS = 32768;
+constexpr int GEMM_LDS = 65536;
 
 // Bump allocator over the workspace (also used to size it).
 struct Carver {
@@ -89,7 +89,9 @@ struct msd_ctx {
   uint16_t *tk, *tv, *dk, *dv;
   // workspace
   float* x;
-  uint16_t *xn, *xb, *fcin, *q, *ao, *act, *h;
+  // activation rows: split rows (bf16 hi + lo) for every MFMA input, q in f32
+  uint16_t *xn, *xb, *fcin, *ao, *act, *h;
+  float* q;
   float* part;
   float* ssq;
   Rows rows;
@@ -164,15 +166,15 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   msd_ctx tmp;
   msd_ctx* t = c ? c : &tmp;
   t->x = cv.take<float>((size_t)R * d);
-  t->xn = cv.take<uint16_t>((size_t)R * d);
-  t->xb = cv.take<uint16_t>((size_t)R * d);
-  t->fcin = cv.take<uint16_t>((size_t)R * 2 * d);
+  t->xn = cv.take<uint16_t>((size_t)R * 2 * d);
+  t->xb = cv.take<uint16_t>((size_t)R * 2 * d);
+  t->fcin = cv.take<uint16_t>((size_t)R * 4 * d);
   t->part = cv.take<float>(p.part_floats);
   t->ssq = cv.take<float>((size_t)R * ((d + 255) / 256));
-  t->q = cv.take<uint16_t>((size_t)R * m.n_heads * m.head_dim);
-  t->ao = cv.take<uint16_t>((size_t)R * m.n_heads * m.head_dim);
-  t->act = cv.take<uint16_t>((size_t)R * m.ffn_dim);
-  t->h = cv.take<uint16_t>((size_t)R * d);
+  t->q = cv.take<float>((size_t)R * m.n_heads * m.head_dim);
+  t->ao = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
+  t->act = cv.take<uint16_t>((size_t)R * 2 * m.ffn_dim);
+  t->h = cv.take<uint16_t>((size_t)R * 2 * d);
   t->rows.tok = cv.take<int>(R);
   t->rows.vis = cv.take<int>(R);
   t->rows.pos = cv.take<int>(R);
@@ -188,7 +190,7 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->d_root = cv.take<int>(B);
   t->pend_n = cv.take<int>(B);
   t->pend_next = cv.take<int>((size_t)B * PEND);
-  t->pend_h = cv.take<uint16_t>((size_t)B * PEND * d);
+  t->pend_h = cv.take<uint16_t>((size_t)B * PEND * 2 * d);
   t->dfeat = cv.take<float>((size_t)B * FEAT * d);
   t->acc_path = cv.take<int>((size_t)B * MSD_MAX_TREE);
   t->acc_n = cv.take<int>(B);
@@ -271,8 +273,8 @@ int upload(msd_ctx* c, int* dst, const int* src, int n) {
 // GEMM launch kinds (for the optional trace)
 enum { GK_QKV = 0, GK_O = 1, GK_DOWN = 2, GK_GATEUP = 3, GK_FC = 4, GK_LMHEAD = 5 };
 
-// Partial products of rows [0, M) (M <= 64) of X against the row segments;
-// returns the view the consumer sums.
+// Partial products of rows [0, M) (M <= 64) of the split rows X (row stride
+// ldx = 2K) against the row segments; returns the view the consumer sums.
 int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M,
          std::initializer_list<const uint16_t*> seg, std::initializer_list<int> seg_rows,
          const uint16_t* W2, int K, Parts* out) {
@@ -310,8 +312,8 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M,
 
 constexpr int CHUNK = 64;  // rows per GEMM launch
 
-// GEMM input of a normalised layer: xn = bf16(x * g) and the per-row sums of
-// squares; the GEMM's consumer applies 1/rms (RMSNorm factored through the
+// GEMM input of a normalised layer: xn = x * g (split rows) and the per-row
+// sums of squares; the GEMM's consumer applies 1/rms (RMSNorm factored through the
 // linear map).
 int norm_rows(msd_ctx* c, int rows, const uint16_t* g) {
   launch_resid(Parts{nullptr, 0, 0, 0}, rows, c->m.d_model, RN_KEEP, c->x, g, c->xn, nullptr,
@@ -329,8 +331,8 @@ RowNorm row_norm(const msd_ctx* c, int m0) {
 // n_seq * nq rows of c->x described by c->rows; c->xn must hold the first
 // layer's input norm.  tree_R < 0 selects causal attention, otherwise tree
 // attention over a region of tree_R slots.  After the last layer the rows
-// get x += ..., then final_xn = bf16(rmsnorm(x) * final_g) when final_g and
-// final_xb = bf16(x) when final_xb.
+// get x += ..., then final_xn = rmsnorm(x) * final_g when final_g and
+// final_xb = x when final_xb.
 int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int max_ltot,
                    const uint16_t* final_g, uint16_t* final_xn, uint16_t* final_xb) {
   const msd_model_desc& m = c->m;
@@ -346,7 +348,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     Parts pt;
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_QKV, c->xn + (size_t)m0 * d, d, mc, {w.wq, w.wk, w.wv},
+      TRY(gemm(c, GK_QKV, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, {w.wq, w.wk, w.wv},
                {H * hd, KV * hd, KV * hd}, nullptr, d, &pt));
       launch_rope_kv(pt, row_norm(c, m0), mc, H, KV, hd, c->rows.pos + m0, c->rows.seq + m0,
                      c->rows.slot + m0, c->rope, c->q + (size_t)m0 * H * hd, kc, vc, S, c->st);
@@ -393,30 +395,31 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     LAUNCHED(c);
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_O, c->ao + (size_t)m0 * H * hd, H * hd, mc, {w.wo}, {d}, nullptr, H * hd, &pt));
-      launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, w.n2, c->xn + (size_t)m0 * d, nullptr,
+      TRY(gemm(c, GK_O, c->ao + (size_t)m0 * 2 * H * hd, 2 * H * hd, mc, {w.wo}, {d}, nullptr,
+               H * hd, &pt));
+      launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, w.n2, c->xn + (size_t)m0 * 2 * d, nullptr,
                    c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
       LAUNCHED(c);
     }
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * d, d, mc, {w.wg}, {F}, w.wu, d, &pt));
-      launch_silu(pt, row_norm(c, m0), mc, F, c->act + (size_t)m0 * F, c->st);
+      TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, {w.wg}, {F}, w.wu, d, &pt));
+      launch_silu(pt, row_norm(c, m0), mc, F, c->act + (size_t)m0 * 2 * F, c->st);
       LAUNCHED(c);
     }
     const bool last = (l + 1 == nl);
     const uint16_t* g_next = last ? final_g : c->layers[l + 1].n1;
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * F, F, mc, {w.wd}, {d}, nullptr, F, &pt));
+      TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * 2 * F, 2 * F, mc, {w.wd}, {d}, nullptr, F, &pt));
       if (last && final_g) {
         // the final feature h is materialised (LM head input, draft input)
         launch_resid_norm(pt, 0, mc, d, RN_ADD, c->x + (size_t)m0 * d, final_g, m.norm_eps,
-                          final_xn + (size_t)m0 * d, nullptr, c->st);
+                          final_xn + (size_t)m0 * 2 * d, nullptr, c->st);
       } else {
         launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, last ? nullptr : g_next,
-                     last ? nullptr : c->xn + (size_t)m0 * d,
-                     (last && final_xb) ? final_xb + (size_t)m0 * d : nullptr,
+                     last ? nullptr : c->xn + (size_t)m0 * 2 * d,
+                     (last && final_xb) ? final_xb + (size_t)m0 * 2 * d : nullptr,
                      last ? nullptr : c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
       }
       LAUNCHED(c);
@@ -425,18 +428,18 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
   return MSD_OK;
 }
 
-// Draft head on rows whose f_down input is in c->fcin ([rows][2d]):
+// Draft head on rows whose f_down input is in c->fcin (split rows of 2d):
 // f = f_down(concat), visual rows replaced by their embeddings, then the
-// decoder layer; features in c->x (f32) and c->xb (bf16).
+// decoder layer; features in c->x and c->xb.
 int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const uint16_t* visual) {
   const int d = c->m.d_model;
   const int rows = n_seq * nq;
   Parts pt;
   for (int m0 = 0; m0 < rows; m0 += CHUNK) {
     const int mc = std::min(CHUNK, rows - m0);
-    TRY(gemm(c, GK_FC, c->fcin + (size_t)m0 * 2 * d, 2 * d, mc, {c->fc}, {d}, nullptr, 2 * d, &pt));
+    TRY(gemm(c, GK_FC, c->fcin + (size_t)m0 * 4 * d, 4 * d, mc, {c->fc}, {d}, nullptr, 2 * d, &pt));
     launch_resid(pt, mc, d, RN_SET, c->x + (size_t)m0 * d, visual ? nullptr : c->dlayer.n1,
-                 visual ? nullptr : c->xn + (size_t)m0 * d, nullptr,
+                 visual ? nullptr : c->xn + (size_t)m0 * 2 * d, nullptr,
                  visual ? nullptr : c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
     LAUNCHED(c);
   }
@@ -448,13 +451,14 @@ int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const ui
   return forward_layers(c, true, n_seq, nq, tree_R, max_ltot, nullptr, nullptr, c->xb);
 }
 
-// LM head + top-k (and log-sum-exp) over bf16 rows of c->xb: no final norm.
+// LM head + top-k (and log-sum-exp) over the rows of c->xb: no final norm.
 int draft_head(msd_ctx* c, int rows, int k) {
   const int d = c->m.d_model, V = c->m.vocab;
   Parts pt;
   for (int m0 = 0; m0 < rows; m0 += CHUNK) {
     const int mc = std::min(CHUNK, rows - m0);
-    TRY(gemm(c, GK_LMHEAD, c->xb + (size_t)m0 * d, d, mc, {c->lm_head}, {V}, nullptr, d, &pt));
+    TRY(gemm(c, GK_LMHEAD, c->xb + (size_t)m0 * 2 * d, 2 * d, mc, {c->lm_head}, {V}, nullptr, d,
+             &pt));
     launch_topk(pt, mc, V, k, c->tk_idx + (size_t)m0 * k, c->tk_val + (size_t)m0 * k,
                 c->tk_lse + m0, nullptr, c->tk_scratch, c->st);
     LAUNCHED(c);
@@ -699,7 +703,8 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
   TRY(norm_rows(c, n, c->layers[0].n1));
   TRY(forward_layers(c, false, 1, n, -1, n, c->final_norm, c->h, nullptr));
   Parts pt;
-  TRY(gemm(c, GK_LMHEAD, c->h + (size_t)(n - 1) * d, d, 1, {c->lm_head}, {m.vocab}, nullptr, d, &pt));
+  TRY(gemm(c, GK_LMHEAD, c->h + (size_t)(n - 1) * 2 * d, 2 * d, 1, {c->lm_head}, {m.vocab}, nullptr,
+           d, &pt));
   launch_topk(pt, 1, m.vocab, 1, c->tk_idx, c->tk_val, nullptr, nullptr, c->tk_scratch, c->st);
   LAUNCHED(c);
   launch_set_int(c->d_root, seq, c->tk_idx, 0, c->st);
@@ -733,8 +738,9 @@ int msd_set_state(msd_ctx* c, int seq, int L, const void* h_d, int32_t next_toke
   TRY(upload_many(c, {{c->d_len + seq, v, sizeof(int)}, {c->d_root + seq, v + 1, sizeof(int)},
                       {c->pend_n + seq, v + 2, sizeof(int)},
                       {c->pend_next + (size_t)seq * PEND, v + 3, sizeof(int)}}));
-  HIPC(c, hipMemcpyAsync(c->pend_h + (size_t)seq * PEND * c->m.d_model, h_d,
-                         sizeof(uint16_t) * c->m.d_model, hipMemcpyDeviceToDevice, c->st));
+  launch_import_row((const uint16_t*)h_d, c->m.d_model,
+                    c->pend_h + (size_t)seq * PEND * 2 * c->m.d_model, c->st);
+  LAUNCHED(c);
   HIPC(c, hipStreamSynchronize(c->st));
   c->L[seq] = L;
   c->pend[seq] = 1;
@@ -870,7 +876,8 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
   Parts pt;
   for (int m0 = 0; m0 < rows; m0 += CHUNK) {
     const int mc = std::min(CHUNK, rows - m0);
-    TRY(gemm(c, GK_LMHEAD, c->h + (size_t)m0 * d, d, mc, {c->lm_head}, {V}, nullptr, d, &pt));
+    TRY(gemm(c, GK_LMHEAD, c->h + (size_t)m0 * 2 * d, 2 * d, mc, {c->lm_head}, {V}, nullptr, d,
+             &pt));
     launch_topk(pt, mc, V, 1, argmax_d + m0, nullptr, nullptr,
                 logits_d ? logits_d + (size_t)m0 * V : nullptr, c->tk_scratch, c->st);
     LAUNCHED(c);

@@ -23,15 +23,28 @@ MSD_DEV uint16_t f2bf(float f) {
 
 MSD_DEV bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Split activation rows.  A row of K values that feeds an MFMA product is
+// stored as K bfloat16 "hi" values followed by K bfloat16 "lo" values with
+// hi = bf16(x) and lo = bf16(x - hi): hi + lo keeps about 16 significant bits
+// of x in the bytes of one float32, and W x = W hi + W lo runs on bf16 MFMA.
+MSD_DEV void put_split(uint16_t* row, int K, int k, float v) {
+  const uint16_t h = f2bf(v);
+  row[k] = h;
+  row[K + k] = f2bf(v - bf2f(h));
+}
+MSD_DEV float get_split(const uint16_t* row, int K, int k) {
+  return bf2f(row[k]) + bf2f(row[K + k]);
+}
+
 namespace msd {
 
 // ---------------------------------------------------------------- GEMM ----
-// Partial products of a thin X (M rows) against a weight streamed from HBM:
-// part[s][m][n] = sum over K-chunk s of X[m][k] * W[n][k] (float32).  With a
+// Partial products of a thin X (M split rows) against a bf16 weight streamed
+// from HBM: part[s][m][n] = sum over K-chunk s of X[m][k] * W[n][k] (float32).  With a
 // second weight W2 (the SwiGLU pair) its products go to columns [N, 2N).
 // The consumer sums the S chunks in order.
 struct GemmArgs {
-  const uint16_t* X;        // [M][ldx] bf16
+  const uint16_t* X;        // [M][ldx] split rows: hi at [k], lo at [K + k]
   int ldx, M;
   const uint16_t* Wseg[3];  // [N][K] bf16 given as up to three row segments
   int seg_end[3];           // cumulative segment heights (multiples of 16)
@@ -49,7 +62,7 @@ struct GemmPlan {
 
 struct GemmScratch {
   int target_wgs;  // workgroups per launch
-  int lds_bytes;   // LDS for the staged X chunk of one workgroup
+  int lds_bytes;   // LDS for the staged X chunk (bf16 hi + lo) of one workgroup
   hipEvent_t ev_start, ev_stop;  // when set: recorded around the kernel itself
 };
 
@@ -79,7 +92,7 @@ struct RowNorm {
 
 // ----------------------------------------------------------- attention ----
 struct AttnArgs {
-  const uint16_t* q;      // [n_seq*nq][H*hd] bf16, rotated
+  const float* q;         // [n_seq*nq][H*hd] float32, rotated
   const uint16_t* kc;     // layer K cache  [B][KV][S][hd]
   const uint16_t* vc;     // layer V cache  [B][KV][hd][S]
   const int* seq_ids;     // [n_seq] absolute sequence index into the caches
@@ -89,7 +102,7 @@ struct AttnArgs {
   int n_chunks, chunk_keys, qtiles;
   float* part_o;          // [items][64*hd/2*...] partial outputs (tree mode)
   float* part_ml;         // [items][32][2]
-  uint16_t* out;          // [n_seq*nq][H*hd] bf16
+  uint16_t* out;          // [n_seq*nq] split rows of H*hd
   float scale;
 };
 
@@ -100,26 +113,27 @@ size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd);
 // ------------------------------------------------------------ row ops ----
 void launch_embed(const uint16_t* E, const int* tokens, const int* vis_idx,
                   const uint16_t* visual, int rows, int d, float* x, hipStream_t st);
-void launch_rmsnorm(const float* x, const uint16_t* g, int rows, int d, float eps,
-                    uint16_t* y, hipStream_t st);
 // x = (mode 1) sum of parts, (mode 2) x + sum of parts, (mode 0) x; then
-// xn = bf16(rmsnorm(x) * g) when g, xb = bf16(x) when xb.
+// xn = rmsnorm(x) * g when g, xb = x when xb (split rows of d).
 enum { RN_KEEP = 0, RN_SET = 1, RN_ADD = 2 };
 void launch_resid_norm(Parts pt, int col0, int rows, int d, int mode, float* x,
                        const uint16_t* g, float eps, uint16_t* xn, uint16_t* xb, hipStream_t st);
+// act = silu(gate) * up (split rows of F)
 void launch_silu(Parts pt, RowNorm rn, int rows, int F, uint16_t* act, hipStream_t st);
-// Elementwise form: x updated as above, xg = bf16(x * g) when xg, xb = bf16(x)
-// when xb, ssq[row][blk] = sum of x^2 over feature block blk (256 wide).
+// Elementwise form: x updated as above, xg = x * g when xg, xb = x when xb
+// (split rows of d), ssq[row][blk] = sum of x^2 over feature block blk
+// (256 wide).
 void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t* g, uint16_t* xg,
                   uint16_t* xb, float* ssq, hipStream_t st);
-void launch_to_bf16(const float* x, int n, uint16_t* y, hipStream_t st);
 void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, const int* pos,
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
-                    uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st);
+                    float* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st);
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
-void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row,
-                     const uint16_t* E, const int* next_tok, const uint16_t* visual,
-                     int rows, int d, uint16_t* out, hipStream_t st);
+// out[row] = split row of [h | e] (2d values); h rows are split rows of d
+// (target features) when h, else float32 rows of hf (draft features).
+void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const uint16_t* E,
+                     const int* next_tok, const uint16_t* visual, int rows, int d, uint16_t* out,
+                     hipStream_t st);
 void launch_visual_rows(const uint16_t* visual, const int* vis_idx, int rows, int d,
                         float* x, hipStream_t st);
 
@@ -200,6 +214,8 @@ void launch_commit(int n_seq, const int* seq_ids, const int* path, const int* n_
                    const int* emitted, const uint16_t* h_tree, int T, int d, uint16_t* pend_h,
                    int* pend_next, int* pend_n, int pend_stride, int* d_len, int* d_root,
                    hipStream_t st);
+// dst = split row of the bf16 row src[0..n) (lo = 0): an imported feature
+void launch_import_row(const uint16_t* src, int n, uint16_t* dst, hipStream_t st);
 void launch_set_int(int* p, int idx, const int* src, int src_idx, hipStream_t st);
 
 }  // namespace msd

@@ -15,7 +15,8 @@ import synth
 from synth.configs import TINY, TreeShape, chain_paths
 from oracle import model as M
 from oracle import msd as O
-from parity import RTOL, decided, rank_decided, row_close
+from parity import (compare_dynamic_tree, compare_static_tree, decided, oracle_draft_dynamic,
+                    oracle_draft_static, row_close)
 
 pytestmark = pytest.mark.gpu
 
@@ -169,23 +170,6 @@ def test_accept_compact_bit_exact(setup):
             "paper_2505_14260_amd.msd", fromlist=["x"]).msd_seq_len(eng.ctx, 1)
 
 
-def oracle_static_with_logits(m, st, paths):
-    parent, rank, depth = synth.static_tree_arrays(paths)
-    root_feat = O.draft_catch_up(m, st)
-    root_logits = M.linear(root_feat[None, :], m.w["lm_head"])[0]
-    ex = O._DraftExpander(m, st, root_feat)
-    logs = {0: root_logits}
-
-    def expand(nodes, tokens, d):
-        pk = [None if parent[u] == 0 else int(parent[u]) for u in nodes]
-        rows = ex(list(nodes), pk, tokens, d)
-        for u, r in zip(nodes, rows):
-            logs[u] = r
-        return rows
-    tree = O.select_static_tree(parent, rank, depth, st.root, root_logits, expand)
-    return tree, logs, rank
-
-
 @pytest.mark.parametrize("paths", [TINY.tree.paths, tuple(chain_paths(4))], ids=["binary3", "chain4"])
 def test_static_draft_tree_matches_oracle(setup, paths):
     wl, eng, m, prompt = setup
@@ -196,24 +180,8 @@ def test_static_draft_tree_matches_oracle(setup, paths):
     dev = eng.new_trees(1)
     eng.draft_tree([0], spec, dev)
     g = eng.trees_to_host(dev, 1)[0]
-    ref, logs, rank = oracle_static_with_logits(m, st, paths)
-    assert g.n_nodes == ref.n
-    assert list(g.parent[:ref.n]) == list(ref.parent)
-    assert list(g.depth[:ref.n]) == list(ref.depth)
-    assert [int(x) for x in g.anc[:ref.n]] == [int(x) for x in ref.anc]
-    assert g.token[0] == ref.token[0] == first
-    skip = set()
-    checked = 0
-    for c in range(1, ref.n):
-        p = int(ref.parent[c])
-        if p in skip:
-            skip.add(c)
-            continue
-        if g.token[c] != ref.token[c]:
-            assert not rank_decided(logs[p], int(rank[c])), (c, g.token[c], ref.token[c])
-            skip.add(c)
-        else:
-            checked += 1
+    ref, logs, rank = oracle_draft_static(m, st, paths)
+    checked = compare_static_tree(g, ref, logs, rank)
     print(f"draft tree: {checked}/{ref.n - 1} nodes compared equal")
     assert checked >= (ref.n - 1) // 2
 
@@ -242,6 +210,11 @@ def test_dynamic_tree_decode(setup):
     eng.draft_tree([0], spec, dev)
     g = eng.trees_to_host(dev, 1)[0]
     assert g.n_nodes == 13
+    st, _, _, _ = O.prefill(m, *prompt, max_slots=256)
+    _, pool, rows, root_logits = oracle_draft_dynamic(m, st, shape.topk, shape.depth,
+                                                      shape.n_nodes)
+    same, scored = compare_dynamic_tree(g, pool, rows, root_logits, shape.topk, shape.n_nodes)
+    print(f"dynamic draft tree: {same}/{shape.n_nodes} nodes as the oracle's, {scored} scored")
     for c in range(1, 13):
         assert 0 <= g.parent[c] < c
         assert g.depth[c] == g.depth[g.parent[c]] + 1
@@ -273,3 +246,109 @@ def test_errors_and_capacity(setup):
     with pytest.raises(B.MSDError) as e:
         B.msd_accept_compact(eng.ctx, [0], dev.data_ptr(), 15, dev.data_ptr())
     assert e.value.code == B.MSD_ERR_STATE
+
+
+def test_root_only_tree(setup):
+    """T = 1: the verify step degenerates to one plain decode step."""
+    wl, eng, m, prompt = setup
+    print("case: tiny verify with a root-only tree", flush=True)
+    first = eng.prefill(0, *prompt)
+    st, f_ref, _, _ = O.prefill(m, *prompt, max_slots=256)
+    tree = O.Tree(np.array([first], np.int32), np.array([-1], np.int32), np.zeros(1, np.int32),
+                  np.zeros(1))
+    dev = upload_tree(eng, tree)
+    amax, logits = eng.verify([0], dev, 1, want_logits=True)
+    _, lg_ref = O.verify(m, st, tree)
+    ok, err = row_close(logits.cpu().numpy(), lg_ref)
+    assert ok, err
+    em, slots = eng.accept([0], dev, 1, amax, want_slots=True)
+    assert em[0] == [int(amax.cpu().numpy()[0])]
+    assert slots.cpu().numpy()[0] == wl.prompt_len
+    if decided(lg_ref[0]):
+        assert em[0][0] == int(np.argmax(lg_ref[0]))
+
+
+def test_max_tree_dynamic_64_nodes(setup):
+    """The largest tree (64 nodes incl. the root): draft tree against the
+    oracle's selection, verification logits on it, then a short decode."""
+    wl, eng, m, prompt = setup
+    print("case: tiny dynamic tree K=8 D=4 N=63", flush=True)
+    from paper_2505_14260_amd.msd import make_dynamic_spec
+    K, D, N = 8, 4, 63
+    spec = make_dynamic_spec(K, D, N)
+    eng.prefill(0, *prompt)
+    st, _, _, _ = O.prefill(m, *prompt, max_slots=256)
+    dev = eng.new_trees(1)
+    eng.draft_tree([0], spec, dev)
+    g = eng.trees_to_host(dev, 1)[0]
+    assert g.n_nodes == 64
+    _, pool, rows, root_logits = oracle_draft_dynamic(m, st, K, D, N)
+    same, scored = compare_dynamic_tree(g, pool, rows, root_logits, K, N)
+    print(f"64-node tree: {same}/{N} nodes as the oracle's, {scored} scored")
+    from parity import oracle_tree_of
+    tree = oracle_tree_of(g)
+    amax, logits = eng.verify([0], dev, 64, want_logits=True)
+    _, lg_ref = O.verify(m, st, tree)
+    ok, err = row_close(logits.cpu().numpy(), lg_ref)
+    assert ok, err
+    am = amax.cpu().numpy()
+    for i in range(64):
+        if decided(lg_ref[i]):
+            assert am[i] == int(np.argmax(lg_ref[i])), i
+    eng.accept([0], dev, 64, amax)
+    toks, _ = eng.generate(0, prompt, spec, 24)
+    ref, rows_g = O.greedy_generate(m, prompt, 24, return_logits=True)
+    bad = next((i for i in range(24) if toks[i] != ref[i]), None)
+    if bad is not None:
+        assert not decided(rows_g[bad]), bad
+
+
+def test_batch2_ragged_decode(setup):
+    """Two sequences of different prompt lengths decoded together, each
+    against its own plain greedy decode."""
+    wl, eng, m, prompt = setup
+    print("case: tiny batch of 2 ragged prompts, static tree", flush=True)
+    tokens, is_visual, visual = prompt
+    cut = wl.n_visual + 17
+    p1 = (tokens[:cut], is_visual[:cut], visual)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    outs = [[eng.prefill(0, *prompt)], [eng.prefill(1, *p1)]]
+    trees = eng.new_trees(2)
+    n_new = 40
+    while min(len(o) for o in outs) < n_new:
+        eng.draft_tree([0, 1], spec, trees)
+        amax, _ = eng.verify([0, 1], trees, T)
+        em, _ = eng.accept([0, 1], trees, T, amax)
+        for b in range(2):
+            outs[b].extend(int(t) for t in em[b])
+    for b, p in enumerate((prompt, p1)):
+        ref, rows = O.greedy_generate(m, p, n_new, return_logits=True)
+        got = outs[b][:n_new]
+        bad = next((i for i in range(n_new) if got[i] != ref[i]), None)
+        print(f"seq {b}: {bad if bad is not None else n_new}/{n_new} equal")
+        if bad is not None:
+            assert not decided(rows[bad]), (b, bad)
+
+
+def test_capacity_limits(setup):
+    wl, eng, m, prompt = setup
+    from paper_2505_14260_amd import msd as B
+    spec, _ = static_spec(wl.tree.paths)
+    eng.prefill(0, *prompt)
+    h = torch.zeros(wl.dims.d_model, dtype=torch.int16, device="cuda")
+    with pytest.raises(B.MSDError) as e:
+        B.msd_set_state(eng.ctx, 0, 256 - 63, h.data_ptr(), 1)   # L + max_tree > max_seq
+    assert e.value.code == B.MSD_ERR_CAPACITY
+    B.msd_set_state(eng.ctx, 0, 256 - 64, h.data_ptr(), 1)
+    dev = eng.new_trees(1)
+    B.msd_set_state(eng.ctx, 0, 256 - 64, h.data_ptr(), 1)
+    eng.draft_tree([0], spec, dev)
+    amax, _ = eng.verify([0], dev, spec.n_nodes + 1)
+    eng.accept([0], dev, spec.n_nodes + 1, amax)
+    with pytest.raises(B.MSDError) as e:       # the next tree no longer fits
+        for _ in range(64):
+            eng.draft_tree([0], spec, dev)
+            amax, _ = eng.verify([0], dev, spec.n_nodes + 1)
+            eng.accept([0], dev, spec.n_nodes + 1, amax)
+    assert e.value.code == B.MSD_ERR_CAPACITY

@@ -1,0 +1,103 @@
+"""The GPU-versus-oracle tree comparisons themselves, pinned on the CPU: an
+oracle tree dressed as a GPU result passes them, and planted mistakes (a token
+outside the top-K, a wrong score, a wrong parent, a swapped ranked token) fail
+them.  Runs the oracle only; no GPU."""
+import numpy as np
+import pytest
+
+import synth
+from synth.configs import TINY
+from oracle import msd as O
+from parity import (compare_dynamic_tree, compare_static_tree, oracle_draft_dynamic,
+                    oracle_draft_static, rank_decided)
+
+
+def as_ctypes(tree):
+    from paper_2505_14260_amd.msd import Tree
+    t = Tree()
+    t.n_nodes = tree.n
+    anc = tree.anc
+    for i in range(tree.n):
+        t.token[i] = int(tree.token[i])
+        t.parent[i] = int(tree.parent[i])
+        t.depth[i] = int(tree.depth[i])
+        t.score[i] = float(tree.score[i])
+        t.anc[i] = int(anc[i])
+    return t
+
+
+@pytest.fixture(scope="module")
+def tiny_state():
+    wl = TINY
+    w = synth.make_target_weights(wl.dims, wl.seed)
+    dr = synth.make_draft_weights(wl.dims, w, wl.seed, wl.draft_fc_mode)
+    m = O.Models(wl.dims, w, dr)
+    st, first, _, _ = O.prefill(m, *synth.make_prompt(wl), max_slots=256)
+    return m, st
+
+
+def fresh(st):
+    return O.SeqState(kv=st.kv.copy(), dkv=st.dkv.copy(), L=st.L, root=st.root,
+                      pending=list(st.pending))
+
+
+K, D, N = 3, 4, 12
+
+
+def test_dynamic_checker_accepts_the_oracle_tree(tiny_state):
+    m, st = tiny_state
+    tree, pool, rows, root_logits = oracle_draft_dynamic(m, fresh(st), K, D, N)
+    same, scored = compare_dynamic_tree(as_ctypes(tree), pool, rows, root_logits, K, N)
+    assert same == N and scored == N
+
+
+def test_dynamic_checker_rejects_planted_mistakes(tiny_state):
+    m, st = tiny_state
+    tree, pool, rows, root_logits = oracle_draft_dynamic(m, fresh(st), K, D, N)
+    # a leaf whose token is the parent's least likely one
+    leaf = tree.n - 1
+    bad = O.Tree(tree.token.copy(), tree.parent.copy(), tree.depth.copy(), tree.score.copy())
+    p = int(tree.parent[leaf])
+    row = root_logits if p == 0 else None
+    if row is None:
+        keys = {}
+        for i, (pp, t, d, s) in enumerate(pool):
+            keys[i] = (keys[pp] if pp >= 0 else ()) + (t,)
+        path = []
+        u = p
+        while u > 0:
+            path.append(int(tree.token[u]))
+            u = int(tree.parent[u])
+        pk = tuple(reversed(path))
+        pi = next(i for i, k in keys.items() if k == pk)
+        row = rows[pi]
+    bad.token[leaf] = int(np.argmin(row))
+    with pytest.raises(AssertionError):
+        compare_dynamic_tree(as_ctypes(bad), pool, rows, root_logits, K, N)
+    # a score off by far more than the tolerance
+    bad = O.Tree(tree.token.copy(), tree.parent.copy(), tree.depth.copy(), tree.score.copy())
+    bad.score[3] += 5.0
+    with pytest.raises(AssertionError):
+        compare_dynamic_tree(as_ctypes(bad), pool, rows, root_logits, K, N)
+    # a node hung under the wrong parent (breaks the depth invariant)
+    bad = O.Tree(tree.token.copy(), tree.parent.copy(), tree.depth.copy(), tree.score.copy())
+    bad.parent[leaf] = 0
+    with pytest.raises(AssertionError):
+        compare_dynamic_tree(as_ctypes(bad), pool, rows, root_logits, K, N)
+
+
+def test_static_checker(tiny_state):
+    m, st = tiny_state
+    ref, logs, rank = oracle_draft_static(m, fresh(st), TINY.tree.paths)
+    g = as_ctypes(ref)
+    assert compare_static_tree(g, ref, logs, rank) == ref.n - 1
+    # replace a decided node's token by its sibling's: must be reported
+    c = next(c for c in range(1, ref.n) if rank_decided(logs[int(ref.parent[c])], int(rank[c])))
+    g = as_ctypes(ref)
+    g.token[c] = int(np.argsort(-logs[int(ref.parent[c])])[int(rank[c]) + 1])
+    with pytest.raises(AssertionError):
+        compare_static_tree(g, ref, logs, rank)
+    g = as_ctypes(ref)
+    g.parent[ref.n - 1] = 0
+    with pytest.raises(AssertionError):
+        compare_static_tree(g, ref, logs, rank)
