@@ -93,9 +93,13 @@ typedef struct msd_draft_weights {
  *  draft_k / draft_v: the same layouts with one layer.
  *  workspace: scratch, contents undefined between calls except the library's
  *            own per-sequence state that it keeps there.
+ *  packed_weights: msd_create writes a copy of every matrix the decode path
+ *            multiplies by (target q, k, v, o, gate, up, down per layer, the
+ *            draft layer's, f_down and the LM head) in the streaming layout
+ *            of the library's GEMM (64-row x 128-column blocks, zero-padded).
  */
 typedef struct msd_buffers {
-  void *target_k, *target_v, *draft_k, *draft_v, *workspace;
+  void *target_k, *target_v, *draft_k, *draft_v, *workspace, *packed_weights;
 } msd_buffers;
 
 /* Draft-tree shape for one decode cycle.
@@ -133,16 +137,20 @@ typedef struct msd_tree {
 
 typedef struct msd_ctx msd_ctx;
 
-/* Byte sizes of the caller-owned buffers for this shape and these limits. */
+/* Byte sizes of the caller-owned buffers for this shape and these limits
+ * (any output pointer may be NULL). */
 int msd_buffer_sizes(const msd_model_desc* m, const msd_limits* lim,
                      size_t* target_kv_bytes /* each of K and V */,
                      size_t* draft_kv_bytes /* each of K and V */,
-                     size_t* workspace_bytes);
+                     size_t* workspace_bytes, size_t* weight_bytes /* packed_weights */);
 
-/* Creates a context over caller-owned weights and buffers (device pointers
- * must stay valid until msd_destroy).  stream: a hipStream_t (NULL = the
- * null stream).  Initialises the workspace and zeroes the four KV caches
- * (enqueued on the stream, waited for before returning). */
+/* Creates a context over caller-owned weights and buffers.  stream: a
+ * hipStream_t (NULL = the null stream).  Packs the matrices into
+ * bufs->packed_weights, initialises the workspace and zeroes the four KV
+ * caches (enqueued on the stream, waited for before returning).  After it
+ * returns, the library reads the embedding table, the norm gains and the
+ * packed copies only: the row-major matrices may be released; every other
+ * pointer must stay valid until msd_destroy. */
 int msd_create(const msd_model_desc* m, const msd_limits* lim,
                const msd_target_weights* tw, const msd_draft_weights* dw,
                const msd_buffers* bufs, void* stream, msd_ctx** out);

@@ -1,12 +1,14 @@
 // Attention over the KV cache on gfx950 MFMA.
 //
-// Tree mode (verification and draft expansion): every query row sees the
-// whole prefix [0, P) of its sequence and the slots of region [P, P+R) whose
-// bit is set in its 64-bit ancestor mask (tree-structured attention of the
-// draft/verify phases).  Keys are split into chunks; one wave handles one
-// (sequence, kv head, 32-row query tile, key chunk) with an online softmax,
-// and a combine kernel merges the chunks in fixed order.  Query rows of a
-// tile are (node, head-in-group) pairs so a GQA group shares every K/V load.
+// Tree mode (verification, draft expansion and draft catch-up): every query
+// row sees the whole prefix [0, P) of its sequence and the slots of region
+// [P, P+R) whose bit is set in its 64-bit mask (tree-structured attention of
+// the draft/verify phases; a triangular mask gives causal rows).  A
+// workgroup of 4 waves owns one (sequence, kv head, 32-row query tile, key
+// chunk); its waves split the chunk, run an online softmax each, and merge
+// their states through LDS into one partial per workgroup; a combine kernel
+// merges the chunks in fixed order.  Query rows of a tile are (node,
+// head-in-group) pairs so a GQA group shares every K/V load.
 // Causal mode (prompt processing): one wave per (sequence, head, 32
 // consecutive query rows) over all keys up to the diagonal.
 //
@@ -15,9 +17,9 @@
 // B = P^T).  The K rows feeding MFMA row i are key pi(i) (bits 2 and 3 of i
 // swapped), which makes each lane's eight P values of the second product
 // correspond to eight consecutive keys, i.e. one 16-byte load of V^T.
-// Q (float32) and P enter the MFMAs as bf16 hi + lo pairs (x = hi + lo,
-// lo = bf16(x - hi)), so only the bf16 cache rows limit the precision; the
-// output rows are split rows (the O projection's input).
+// Q (split rows from the RoPE kernel) and P enter the MFMAs as bf16 hi + lo
+// pairs, so only the bf16 cache rows limit the precision; the output rows
+// are split rows (the O projection's input).
 #include "msd_internal.h"
 
 namespace msd {
@@ -148,24 +150,14 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qh)[HD / 16],
   }
 }
 
-// The lane's 8-element slices of its query row, split into bf16 hi and lo.
+// The lane's 8-element slices of its query row (hi at q[k], lo at q[lo + k]).
 template <int HD>
-MSD_DEV void load_q(bf16x8 (&qh)[HD / 16], bf16x8 (&ql)[HD / 16], const float* qrow) {
+MSD_DEV void load_q(bf16x8 (&qh)[HD / 16], bf16x8 (&ql)[HD / 16], const uint16_t* qrow, int lo) {
   const int h = (threadIdx.x & 63) >> 5;
 #pragma unroll
   for (int c = 0; c < HD / 16; ++c) {
-    const float4* src = reinterpret_cast<const float4*>(qrow + (HD / 2) * h + 8 * c);
-    const float4 a = src[0], b = src[1];
-    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-    uint32_t hw[4], lw[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint16_t h0 = f2bf(v[2 * e]), h1 = f2bf(v[2 * e + 1]);
-      hw[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-      lw[e] = (uint32_t)f2bf(v[2 * e] - bf2f(h0)) | ((uint32_t)f2bf(v[2 * e + 1] - bf2f(h1)) << 16);
-    }
-    qh[c] = as_bf16x8(make_uint4(hw[0], hw[1], hw[2], hw[3]));
-    ql[c] = as_bf16x8(make_uint4(lw[0], lw[1], lw[2], lw[3]));
+    qh[c] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + (HD / 2) * h + 8 * c));
+    ql[c] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + lo + (HD / 2) * h + 8 * c));
   }
 }
 
@@ -193,13 +185,29 @@ MSD_DEV void store_final(const AttnState<HD>& st, uint16_t* orow, int K, bool va
       put_split(orow, K, dt * 32 + 8 * (r >> 2) + 4 * h + (r & 3), st.o[dt][r] * inv);
 }
 
+// Output element e of a wave's state: register e / 64 of lane e % 64, i.e.
+// query column (e % 64) & 31 and head dim dim_of(e).
+template <int HD>
+MSD_DEV int dim_of(int e) {
+  const int R = e >> 6, L = e & 63;
+  const int dt = R >> 4, r = R & 15;
+  return dt * 32 + 8 * (r >> 2) + 4 * (L >> 5) + (r & 3);
+}
+
+// Query column j of tile qt -> (node, head); node >= nq marks padding.
+MSD_DEV void column_to_row(int qt, int j, int G, int g, int& node, int& head) {
+  const int qr = qt * 32 + j;
+  node = qr / G;
+  head = g * G + (qr - node * G);
+}
+
 template <int HD>
 __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int n_items = a.n_seq * a.KV * a.qtiles * a.n_chunks;
-  if (wid >= n_items) return;
-  int t = wid;
+  constexpr int E = 32 * HD;                 // state elements of one wave
+  __shared__ float so[4 * E];
+  __shared__ float sml[4][32][2];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int t = blockIdx.x;
   const int c = t % a.n_chunks; t /= a.n_chunks;
   const int qt = t % a.qtiles; t /= a.qtiles;
   const int g = t % a.KV;
@@ -208,78 +216,120 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
   const int P = a.prefix[sidx];
   const int Ltot = P + a.R;
   const int G = a.H / a.KV;
-  const int j = lane & 31;
-  const int qr = qt * 32 + j;
-  int node = qr / G;
-  const int head = g * G + (qr - node * G);
+  int node, head;
+  column_to_row(qt, lane & 31, G, g, node, head);
   const bool valid = node < a.nq;
-  if (!valid) node = 0;
-  const float* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)(valid ? head : g * G) * HD;
+  if (!valid) { node = 0; head = g * G; }
+  const int HH = a.H * HD;
   bf16x8 qh[HD / 16], ql[HD / 16];
-  load_q<HD>(qh, ql, qrow);
+  load_q<HD>(qh, ql, a.q + (size_t)(sidx * a.nq + node) * 2 * HH + (size_t)head * HD, HH);
   const uint64_t msk = a.mask[sidx * a.nq + node];
   const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
   const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
   AttnState<HD> st;
   init_state<HD>(st);
-  const int k0 = c * a.chunk_keys;
-  const int k1 = min(k0 + a.chunk_keys, Ltot);
+  const int wk = a.chunk_keys / 4;
+  const int k0 = c * a.chunk_keys + w * wk;
+  const int k1 = min(k0 + wk, Ltot);
   attend_range<HD>(st, qh, ql, kbase, vbase, a.S, k0, k1, Ltot, a.scale, [&](int key) {
     return key < P || ((msk >> (key - P)) & 1ull);
   });
-  if (a.n_chunks == 1) {
-    store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * 2 * a.H * HD + (size_t)head * HD,
-                    a.H * HD, valid);
-    return;
-  }
-  float* po = a.part_o + (size_t)wid * 32 * HD;
+  // merge the 4 waves' states
 #pragma unroll
   for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) po[(dt * 16 + r) * 64 + lane] = st.o[dt][r];
+    for (int r = 0; r < 16; ++r) so[w * E + (dt * 16 + r) * 64 + lane] = st.o[dt][r];
   if (lane < 32) {
-    a.part_ml[(size_t)wid * 64 + 2 * lane] = st.m;
-    a.part_ml[(size_t)wid * 64 + 2 * lane + 1] = st.l;
+    sml[w][lane][0] = st.m;
+    sml[w][lane][1] = st.l;
+  }
+  __syncthreads();
+  const size_t item = blockIdx.x;
+  for (int e = threadIdx.x; e < E; e += 256) {
+    const int j = (e & 63) & 31;
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) M = fmaxf(M, sml[q][j][0]);
+    float o = 0.f, l = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float mq = sml[q][j][0];
+        const float wq = (mq == -INFINITY) ? 0.f : __expf(mq - M);
+        o += wq * so[q * E + e];
+        l += wq * sml[q][j][1];
+      }
+    }
+    if (a.n_chunks == 1) {
+      int nd, hd_;
+      column_to_row(qt, j, G, g, nd, hd_);
+      if (nd < a.nq)
+        put_split(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH, HH, hd_ * HD + dim_of<HD>(e),
+                  l > 0.f ? o / l : 0.f);
+    } else {
+      a.part_o[item * E + e] = o;
+      if (e < 32) {
+        a.part_ml[item * 64 + 2 * e] = M;
+        a.part_ml[item * 64 + 2 * e + 1] = l;
+      }
+    }
   }
 }
 
-// One block per query column of a tile: merges the chunks' partial softmax
-// states in chunk order.
+// Merges the chunks of one (sequence, kv head, query tile) in chunk order;
+// block (tile, dim tile dt) reads the dt slice of every chunk's state
+// (contiguous) and writes those output dims.
 template <int HD>
-__global__ __launch_bounds__(HD) void k_tree_combine(AttnArgs a) {
-  int t = blockIdx.x;
-  const int j = t & 31; t >>= 5;
+__global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
+  constexpr int E = 32 * HD;
+  constexpr int SL = E / (HD / 32);          // elements of one dim tile
+  __shared__ float wgt[64][32];              // chunk weights per column
+  __shared__ float inv_den[32];
+  const int dt = blockIdx.x % (HD / 32);
+  int t = blockIdx.x / (HD / 32);
+  const size_t item0 = (size_t)t * a.n_chunks;
   const int qt = t % a.qtiles; t /= a.qtiles;
   const int g = t % a.KV;
   const int sidx = t / a.KV;
   const int G = a.H / a.KV;
-  const int qr = qt * 32 + j;
-  const int node = qr / G;
-  if (node >= a.nq) return;
-  const int head = g * G + (qr - node * G);
-  const size_t item0 = (size_t)(blockIdx.x >> 5) * a.n_chunks;
-  const int dim = threadIdx.x;
-  const int dt = dim >> 5, dd = dim & 31;
-  const int hh = (dd >> 2) & 1, r = (dd >> 3) * 4 + (dd & 3);
-  const int idx = (dt * 16 + r) * 64 + j + 32 * hh;
-  // chunk order is fixed; the loads of different chunks are independent
-  float M = -INFINITY;
-#pragma unroll 8
-  for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
-  float num = 0.f, den = 0.f;
-  if (M != -INFINITY) {
-#pragma unroll 8
-    for (int c = 0; c < a.n_chunks; ++c) {
+  const int nc = a.n_chunks;
+  if (threadIdx.x < 32) {
+    const int j = threadIdx.x;
+    float M = -INFINITY;
+    for (int c = 0; c < nc; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
+    float den = 0.f;
+    for (int c = 0; c < nc; ++c) {
       const float mc = a.part_ml[(item0 + c) * 64 + 2 * j];
-      const float lc = a.part_ml[(item0 + c) * 64 + 2 * j + 1];
-      const float oc = a.part_o[(item0 + c) * 32 * HD + idx];
-      const float w = (mc == -INFINITY) ? 0.f : __expf(mc - M);
-      den += w * lc;
-      num += w * oc;
+      const float wc = (M == -INFINITY || mc == -INFINITY) ? 0.f : __expf(mc - M);
+      wgt[c][j] = wc;
+      den += wc * a.part_ml[(item0 + c) * 64 + 2 * j + 1];
+    }
+    inv_den[j] = den > 0.f ? 1.f / den : 0.f;
+  }
+  __syncthreads();
+  const int HH = a.H * HD;
+  for (int e0 = threadIdx.x * 4; e0 < SL; e0 += 1024) {
+    const int e = dt * SL + e0;              // element index in the state
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    const int j0 = e & 31;                   // columns of e .. e+3 (consecutive lanes)
+    for (int c = 0; c < nc; ++c) {
+      const float4 v = *reinterpret_cast<const float4*>(a.part_o + (item0 + c) * E + e);
+      acc.x += wgt[c][j0] * v.x;
+      acc.y += wgt[c][j0 + 1] * v.y;
+      acc.z += wgt[c][j0 + 2] * v.z;
+      acc.w += wgt[c][j0 + 3] * v.w;
+    }
+    const float vals[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = j0 + q;
+      int nd, hd_;
+      column_to_row(qt, j, G, g, nd, hd_);
+      if (nd < a.nq)
+        put_split(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH, HH, hd_ * HD + dim_of<HD>(e + q),
+                  vals[q] * inv_den[j]);
     }
   }
-  put_split(a.out + (size_t)(sidx * a.nq + node) * 2 * a.H * HD, a.H * HD, head * HD + dim,
-            den > 0.f ? num / den : 0.f);
 }
 
 template <int HD>
@@ -299,9 +349,9 @@ __global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
   int node = qt * 32 + j;
   const bool valid = node < a.nq;
   if (!valid) node = a.nq - 1;
-  const float* qrow = a.q + (size_t)(sidx * a.nq + node) * a.H * HD + (size_t)head * HD;
+  const int HH = a.H * HD;
   bf16x8 qh[HD / 16], ql[HD / 16];
-  load_q<HD>(qh, ql, qrow);
+  load_q<HD>(qh, ql, a.q + (size_t)(sidx * a.nq + node) * 2 * HH + (size_t)head * HD, HH);
   const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
   const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
   AttnState<HD> st;
@@ -322,18 +372,16 @@ size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd) 
 }
 
 void launch_tree_attention(AttnArgs a, hipStream_t st) {
-  const int items = a.n_seq * a.KV * a.qtiles * a.n_chunks;
-  dim3 grid((items + 3) / 4);
+  const int items = a.n_seq * a.KV * a.qtiles;
+  dim3 grid(items * a.n_chunks);
   if (a.hd == 128) {
     hipLaunchKernelGGL(k_tree_attn<128>, grid, dim3(256), 0, st, a);
     if (a.n_chunks > 1)
-      hipLaunchKernelGGL(k_tree_combine<128>, dim3(a.n_seq * a.KV * a.qtiles * 32), dim3(128), 0,
-                         st, a);
+      hipLaunchKernelGGL(k_tree_combine<128>, dim3(items * 4), dim3(256), 0, st, a);
   } else {
     hipLaunchKernelGGL(k_tree_attn<64>, grid, dim3(256), 0, st, a);
     if (a.n_chunks > 1)
-      hipLaunchKernelGGL(k_tree_combine<64>, dim3(a.n_seq * a.KV * a.qtiles * 32), dim3(64), 0, st,
-                         a);
+      hipLaunchKernelGGL(k_tree_combine<64>, dim3(items * 2), dim3(256), 0, st, a);
   }
 }
 

@@ -70,15 +70,15 @@ MSD_DEV float row_rstd(const RowNorm& rn, int row) {
   return rsqrtf(t / (float)rn.d + rn.eps);
 }
 
-// Rotate-half RoPE on q and k, write q (float32), K to its slot and V to the
-// transposed V cache (bf16).  qkv: summed parts, [rows][(H + 2KV) * hd], computed
+// Rotate-half RoPE on q and k, write q (split rows), K to its slot and V to
+// the transposed V cache (bf16).  qkv: summed parts, [rows][(H + 2KV) * hd], computed
 // from the un-normalised input, so every row is first scaled by its 1/rms.
 // One block of hd/2 threads per (row, head); heads H.. are the key heads,
 // H+KV.. the value heads.
 __global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, int KV, int hd,
                                                 const int* pos, const int* row_seq,
                                                 const int* row_slot, const float2* tab,
-                                                float* q, uint16_t* kc, uint16_t* vc, int S) {
+                                                uint16_t* q, uint16_t* kc, uint16_t* vc, int S) {
   const int row = blockIdx.x;
   const int head = blockIdx.y;
   const int half = hd / 2;
@@ -100,8 +100,9 @@ __global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, in
     const float y0 = a * t.x - c * t.y;
     const float y1 = c * t.x + a * t.y;
     if (head < H) {
-      q[(size_t)row * H * hd + head * hd + i] = y0;
-      q[(size_t)row * H * hd + head * hd + i + half] = y1;
+      uint16_t* qr = q + (size_t)row * 2 * H * hd;
+      put_split(qr, H * hd, head * hd + i, y0);
+      put_split(qr, H * hd, head * hd + i + half, y1);
     } else {
       uint16_t* kr = kc + ((size_t)(b * KV + head - H) * S + slot) * hd;
       kr[i] = f2bf(y0);
@@ -176,22 +177,22 @@ __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float*
 }
 
 // act = silu(gate) * up (split rows) with gate at columns [0, F), up at
-// [F, 2F), both scaled by the row's 1/rms (the GEMM read the un-normalised
-// input).
+// [off2, off2 + F), both scaled by the row's 1/rms (the GEMM read the
+// un-normalised input).
 __global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint16_t* act) {
   const int row = blockIdx.y;
   const int f = blockIdx.x * 256 + threadIdx.x;
   if (f >= F) return;
   const float r = row_rstd(rn, row);
   const float gt = r * part_sum(pt, row, f);
-  const float up = r * part_sum(pt, row, F + f);
+  const float up = r * part_sum(pt, row, pt.off2 + f);
   put_split(act + (size_t)row * 2 * F, F, f, gt / (1.f + __expf(-gt)) * up);
 }
 
 // out[row] = [h_row | e_next] as a split row of 2d, the concat fed to the
 // draft's f_down; h rows are target features (split rows, h) or draft
 // features (float32 rows, hf); next_tok >= 0 selects E[next_tok], next_tok < 0
-// selects visual row -1-next_tok.
+// selects visual row -1-next_tok.  Grid (rows, ceil(d/256)).
 __global__ __launch_bounds__(256) void k_fc_input(const uint16_t* h, const float* hf,
                                                   const int* h_row, const uint16_t* E,
                                                   const int* next_tok, const uint16_t* visual,
@@ -201,7 +202,8 @@ __global__ __launch_bounds__(256) void k_fc_input(const uint16_t* h, const float
   const int nt = next_tok[row];
   const uint16_t* e = (nt >= 0) ? E + (size_t)nt * d : visual + (size_t)(-1 - nt) * d;
   uint16_t* o = out + (size_t)row * 4 * d;
-  for (int i = threadIdx.x; i < d; i += 256) {
+  const int i = blockIdx.y * 256 + threadIdx.x;
+  if (i < d) {
     if (h) {
       const uint16_t* hs = h + (size_t)hr * 2 * d;
       o[i] = hs[i];
@@ -360,7 +362,7 @@ void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream
 
 void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, const int* pos,
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
-                    float* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st) {
+                    uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st) {
   if (rows <= 0) return;
   hipLaunchKernelGGL(k_rope_kv, dim3(rows, H + 2 * KV), dim3(64), 0, st, qkv, rn, H, KV, hd, pos,
                      row_seq, row_slot, rope_tab, q, kc, vc, S);
@@ -389,8 +391,8 @@ void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const
                      const int* next_tok, const uint16_t* visual, int rows, int d, uint16_t* out,
                      hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_fc_input, dim3(rows), dim3(256), 0, st, h, hf, h_row, E, next_tok, visual,
-                     d, out);
+  hipLaunchKernelGGL(k_fc_input, dim3(rows, (d + 255) / 256), dim3(256), 0, st, h, hf, h_row, E,
+                     next_tok, visual, d, out);
 }
 
 size_t topk_scratch_floats(int rows, int V) {

@@ -247,16 +247,18 @@ __global__ void k_catchup_rows(const int* seq_ids, const int* d_len, const int* 
   r.pos[row] = P + jj;
   r.slot[row] = valid ? P + j : -1;
   r.seq[row] = b;
-  r.mask[row] = 0ull;
+  // causal inside the pending region: row j sees pending rows 0..j
+  r.mask[row] = (jj >= 63) ? ~0ull : ((2ull << jj) - 1ull);
   r.dst[row] = (j == rb - 1) ? b * feat_stride : -1;
 }
 
+// Grid (rows, ceil(d/256)).
 __global__ void k_store_feat(const float* x, const int* dst, int d, float* feat) {
   const int row = blockIdx.x;
   const int o = dst[row];
-  if (o < 0) return;
-  for (int e = threadIdx.x; e < d; e += blockDim.x)
-    feat[(size_t)o * d + e] = x[(size_t)row * d + e];
+  const int e = blockIdx.y * 256 + threadIdx.x;
+  if (o < 0 || e >= d) return;
+  feat[(size_t)o * d + e] = x[(size_t)row * d + e];
 }
 
 // Greedy acceptance: node j is accepted iff its parent is and its token is
@@ -423,7 +425,7 @@ void launch_catchup_rows(int n_seq, const int* seq_ids, const int* d_len, const 
 void launch_store_feat(const float* x, int rows, const int* dst, int d, float* feat,
                        hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_store_feat, dim3(rows), dim3(256), 0, st, x, dst, d, feat);
+  hipLaunchKernelGGL(k_store_feat, dim3(rows, (d + 255) / 256), dim3(256), 0, st, x, dst, d, feat);
 }
 
 void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,

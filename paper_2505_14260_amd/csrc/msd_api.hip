@@ -26,16 +26,48 @@ LayerW to_layer(const msd_layer_weights& l) {
           (const uint16_t*)l.w_down, (const uint16_t*)l.attn_norm, (const uint16_t*)l.ffn_norm};
 }
 
+// A layer's GEMM weights in the packed layout (q|k|v fused).
+struct PackedLayer {
+  const uint16_t *qkv, *o, *g, *u, *d;
+};
+
+// Element offsets of every packed weight in the caller's weight arena:
+// per target layer q|k|v, o, gate, up, down; the draft layer; f_down; LM head.
+struct WeightLayout {
+  std::vector<size_t> layer_off;  // n_layers + 1 (draft last), start of each layer
+  size_t qkv, o, g, u, d;         // sizes of one layer's packed matrices
+  size_t fc_off, lm_off, total;
+};
+
+WeightLayout weight_layout(const msd_model_desc& m) {
+  WeightLayout w;
+  const int d = m.d_model, hd = m.head_dim, H = m.n_heads, KV = m.n_kv_heads, F = m.ffn_dim;
+  w.qkv = packed_elems(H * hd, d) + 2 * packed_elems(KV * hd, d);
+  w.o = packed_elems(d, H * hd);
+  w.g = w.u = packed_elems(F, d);
+  w.d = packed_elems(d, F);
+  const size_t per = w.qkv + w.o + w.g + w.u + w.d;
+  size_t off = 0;
+  for (int l = 0; l <= m.n_layers; ++l) {
+    w.layer_off.push_back(off);
+    off += per;
+  }
+  w.fc_off = off;
+  off += packed_elems(d, 2 * d);
+  w.lm_off = off;
+  off += packed_elems(m.vocab, d);
+  w.total = off;
+  return w;
+}
+
 constexpr int PEND = MSD_MAX_TREE;      // pending draft rows per sequence
 constexpr int FEAT = MSD_MAX_TREE + 1;  // draft feature slots per sequence
 constexpr int TOPK = 16;
 constexpr int POOL = 1024;              // dynamic-tree candidates per sequence
 constexpr int STAGE_INTS = 1 << 16;
 // GEMM launch shape: about one workgroup per CU streams best (more
-// concurrent row streams per CU lower the achieved HBM bandwidth), with a
-// 64 KB X chunk (bf16 hi and lo halves) per workgroup.
+// concurrent weight streams per CU lower the achieved HBM bandwidth).
 constexpr int GEMM_WGS = 256;
-constexpr int GEMM_LDS = 65536;
 
 // Bump allocator over the workspace (also used to size it).
 struct Carver {
@@ -66,12 +98,12 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
   // GEMM partials of one 64-row launch, for the largest weight of the model
   const int mm = std::min(64, p.rows_max);
   const int d = m.d_model, F = m.ffn_dim, hh = m.n_heads * m.head_dim;
-  const size_t cand[6] = {gemm_part_floats(mm, p.ld_qkv, d, 1, GEMM_WGS, GEMM_LDS),
-                          gemm_part_floats(mm, d, hh, 1, GEMM_WGS, GEMM_LDS),
-                          gemm_part_floats(mm, F, d, 2, GEMM_WGS, GEMM_LDS),
-                          gemm_part_floats(mm, d, F, 1, GEMM_WGS, GEMM_LDS),
-                          gemm_part_floats(mm, d, 2 * d, 1, GEMM_WGS, GEMM_LDS),
-                          gemm_part_floats(mm, m.vocab, d, 1, GEMM_WGS, GEMM_LDS)};
+  const size_t cand[6] = {gemm_part_floats(mm, p.ld_qkv, d, 1, GEMM_WGS),
+                          gemm_part_floats(mm, d, hh, 1, GEMM_WGS),
+                          gemm_part_floats(mm, F, d, 2, GEMM_WGS),
+                          gemm_part_floats(mm, d, F, 1, GEMM_WGS),
+                          gemm_part_floats(mm, d, 2 * d, 1, GEMM_WGS),
+                          gemm_part_floats(mm, m.vocab, d, 1, GEMM_WGS)};
   p.part_floats = *std::max_element(cand, cand + 6);
   return p;
 }
@@ -85,14 +117,16 @@ struct msd_ctx {
   hipStream_t st;
   std::vector<LayerW> layers;
   LayerW dlayer;
-  const uint16_t *embed, *final_norm, *lm_head, *fc;
+  std::vector<PackedLayer> players;
+  PackedLayer pdlayer;
+  const uint16_t *embed, *final_norm, *lm_p, *fc_p;
   uint16_t *tk, *tv, *dk, *dv;
   // workspace
   float* x;
-  // activation rows: split rows (bf16 hi + lo) for every MFMA input, q in f32
-  uint16_t *xn, *xb, *fcin, *ao, *act, *h;
-  float* q;
+  // activation rows: split rows (bf16 hi + lo) for every MFMA input
+  uint16_t *xn, *xb, *fcin, *q, *ao, *act, *h;
   float* part;
+  float* sink;  // GEMM rows past M
   float* ssq;
   Rows rows;
   int *nxt, *prefix, *seq_ids;
@@ -110,6 +144,7 @@ struct msd_ctx {
   // host
   int* stage;  // pinned staging
   std::vector<int> L, pend, ready;
+  std::vector<int> seq_ids_h;  // what c->seq_ids holds (empty: unknown)
   std::string err;
   // static spec cache
   std::vector<int> sp_parent, sp_rank;
@@ -154,6 +189,12 @@ int fail(msd_ctx* c, int code, const std::string& msg) {
       return fail(c, MSD_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e_)); \
   } while (0)
 
+#define TRY(x)              \
+  do {                      \
+    int r_ = (x);           \
+    if (r_ != MSD_OK) return r_; \
+  } while (0)
+
 size_t kv_bytes(const msd_model_desc& m, const msd_limits& lim, int layers) {
   return (size_t)layers * lim.max_batch * m.n_kv_heads * (size_t)lim.max_seq * m.head_dim * 2;
 }
@@ -170,8 +211,9 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->xb = cv.take<uint16_t>((size_t)R * 2 * d);
   t->fcin = cv.take<uint16_t>((size_t)R * 4 * d);
   t->part = cv.take<float>(p.part_floats);
+  t->sink = cv.take<float>(256);
   t->ssq = cv.take<float>((size_t)R * ((d + 255) / 256));
-  t->q = cv.take<float>((size_t)R * m.n_heads * m.head_dim);
+  t->q = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
   t->ao = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
   t->act = cv.take<uint16_t>((size_t)R * 2 * m.ffn_dim);
   t->h = cv.take<uint16_t>((size_t)R * 2 * d);
@@ -270,23 +312,24 @@ int upload(msd_ctx* c, int* dst, const int* src, int n) {
   return upload_many(c, {{dst, src, sizeof(int) * (size_t)n}});
 }
 
+// The device copy of the call's sequence list; uploaded (which drains the
+// stream) only when it differs from the previous call's.
+int upload_seqs(msd_ctx* c, const int32_t* seqs, int n) {
+  if ((int)c->seq_ids_h.size() == n && std::equal(seqs, seqs + n, c->seq_ids_h.begin()))
+    return MSD_OK;
+  TRY(upload(c, c->seq_ids, seqs, n));
+  c->seq_ids_h.assign(seqs, seqs + n);
+  return MSD_OK;
+}
+
 // GEMM launch kinds (for the optional trace)
 enum { GK_QKV = 0, GK_O = 1, GK_DOWN = 2, GK_GATEUP = 3, GK_FC = 4, GK_LMHEAD = 5 };
 
 // Partial products of rows [0, M) (M <= 64) of the split rows X (row stride
-// ldx = 2K) against the row segments; returns the view the consumer sums.
-int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M,
-         std::initializer_list<const uint16_t*> seg, std::initializer_list<int> seg_rows,
-         const uint16_t* W2, int K, Parts* out) {
-  const uint16_t* sp[3] = {nullptr, nullptr, nullptr};
-  int sr[3] = {0, 0, 0};
-  int n = 0, N = 0;
-  for (const uint16_t* p : seg) sp[n++] = p;
-  n = 0;
-  for (int r : seg_rows) {
-    sr[n++] = r;
-    N += r;
-  }
+// ldx = 2K) against the packed weight W [N][K] (and W2); returns the view the
+// consumer sums.
+int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t* W,
+         const uint16_t* W2, int N, int K, Parts* out) {
   const bool tr = c->tracing && ((c->trace_kinds >> kind) & 1) && c->trace.size() < c->trace_cap;
   GemmScratch gs = c->gs;
   if (tr) {
@@ -296,19 +339,13 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M,
     gs.ev_stop = r.b;
     c->trace.push_back(r);
   }
-  launch_gemm(X, ldx, M, sp, sr, n, W2, K, c->part, gs, c->st);
+  launch_gemm(X, ldx, M, W, W2, N, K, c->part, c->sink, gs, c->st);
   LAUNCHED(c);
-  const int nw = W2 ? 2 : 1;
-  const GemmPlan pl = plan_gemm(M, N, K, nw, c->gs.target_wgs, c->gs.lds_bytes);
-  *out = Parts{c->part, pl.S, (size_t)M * N * nw, N * nw};
+  const GemmPlan pl = plan_gemm(M, N, K, W2 ? 2 : 1, c->gs.target_wgs);
+  *out = Parts{c->part, pl.S, (size_t)M * pl.ldp, pl.ldp, pl.off2};
   return MSD_OK;
 }
 
-#define TRY(x)              \
-  do {                      \
-    int r_ = (x);           \
-    if (r_ != MSD_OK) return r_; \
-  } while (0)
 
 constexpr int CHUNK = 64;  // rows per GEMM launch
 
@@ -316,7 +353,7 @@ constexpr int CHUNK = 64;  // rows per GEMM launch
 // sums of squares; the GEMM's consumer applies 1/rms (RMSNorm factored through the
 // linear map).
 int norm_rows(msd_ctx* c, int rows, const uint16_t* g) {
-  launch_resid(Parts{nullptr, 0, 0, 0}, rows, c->m.d_model, RN_KEEP, c->x, g, c->xn, nullptr,
+  launch_resid(Parts{nullptr, 0, 0, 0, 0}, rows, c->m.d_model, RN_KEEP, c->x, g, c->xn, nullptr,
                c->ssq, c->st);
   LAUNCHED(c);
   return MSD_OK;
@@ -343,15 +380,16 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
   const size_t layer_kv = (size_t)B * KV * S * hd;
   for (int l = 0; l < nl; ++l) {
     const LayerW& w = draft ? c->dlayer : c->layers[l];
+    const PackedLayer& pw = draft ? c->pdlayer : c->players[l];
     uint16_t* kc = (draft ? c->dk : c->tk) + (size_t)l * layer_kv;
     uint16_t* vc = (draft ? c->dv : c->tv) + (size_t)l * layer_kv;
     Parts pt;
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_QKV, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, {w.wq, w.wk, w.wv},
-               {H * hd, KV * hd, KV * hd}, nullptr, d, &pt));
+      TRY(gemm(c, GK_QKV, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, pw.qkv, nullptr, (H + 2 * KV) * hd,
+               d, &pt));
       launch_rope_kv(pt, row_norm(c, m0), mc, H, KV, hd, c->rows.pos + m0, c->rows.seq + m0,
-                     c->rows.slot + m0, c->rope, c->q + (size_t)m0 * H * hd, kc, vc, S, c->st);
+                     c->rows.slot + m0, c->rope, c->q + (size_t)m0 * 2 * H * hd, kc, vc, S, c->st);
       LAUNCHED(c);
     }
     AttnArgs a{};
@@ -379,15 +417,16 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       const int G = H / KV;
       a.R = tree_R;
       a.qtiles = (nq * G + 31) / 32;
-      // key chunks: enough waves to spread the cache over the chip, but at
-      // least 64 keys per wave so the partial results stay small
+      // key chunks (multiples of 128 keys, 32 per wave of a workgroup):
+      // about two workgroups per CU over the whole launch, at most 64 chunks
       const int base_items = n_seq * KV * a.qtiles;
       int chunks = std::max(1, 512 / std::max(1, base_items));
       int ck = (max_ltot + chunks - 1) / chunks;
-      ck = std::max(64, (ck + 31) / 32 * 32);
-      while (attn_partial_floats(n_seq, KV, a.qtiles, (max_ltot + ck - 1) / ck, hd) >
-             c->plan.attn_floats)
-        ck += 64;
+      ck = std::max(128, (ck + 127) / 128 * 128);
+      while ((max_ltot + ck - 1) / ck > 64 ||
+             attn_partial_floats(n_seq, KV, a.qtiles, (max_ltot + ck - 1) / ck, hd) >
+                 c->plan.attn_floats)
+        ck += 128;
       a.chunk_keys = ck;
       a.n_chunks = (max_ltot + ck - 1) / ck;
       launch_tree_attention(a, c->st);
@@ -395,15 +434,15 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     LAUNCHED(c);
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_O, c->ao + (size_t)m0 * 2 * H * hd, 2 * H * hd, mc, {w.wo}, {d}, nullptr,
-               H * hd, &pt));
+      TRY(gemm(c, GK_O, c->ao + (size_t)m0 * 2 * H * hd, 2 * H * hd, mc, pw.o, nullptr, d, H * hd,
+               &pt));
       launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, w.n2, c->xn + (size_t)m0 * 2 * d, nullptr,
                    c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
       LAUNCHED(c);
     }
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, {w.wg}, {F}, w.wu, d, &pt));
+      TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, pw.g, pw.u, F, d, &pt));
       launch_silu(pt, row_norm(c, m0), mc, F, c->act + (size_t)m0 * 2 * F, c->st);
       LAUNCHED(c);
     }
@@ -411,7 +450,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     const uint16_t* g_next = last ? final_g : c->layers[l + 1].n1;
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
       const int mc = std::min(CHUNK, rows - m0);
-      TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * 2 * F, 2 * F, mc, {w.wd}, {d}, nullptr, F, &pt));
+      TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * 2 * F, 2 * F, mc, pw.d, nullptr, d, F, &pt));
       if (last && final_g) {
         // the final feature h is materialised (LM head input, draft input)
         launch_resid_norm(pt, 0, mc, d, RN_ADD, c->x + (size_t)m0 * d, final_g, m.norm_eps,
@@ -437,7 +476,7 @@ int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const ui
   Parts pt;
   for (int m0 = 0; m0 < rows; m0 += CHUNK) {
     const int mc = std::min(CHUNK, rows - m0);
-    TRY(gemm(c, GK_FC, c->fcin + (size_t)m0 * 4 * d, 4 * d, mc, {c->fc}, {d}, nullptr, 2 * d, &pt));
+    TRY(gemm(c, GK_FC, c->fcin + (size_t)m0 * 4 * d, 4 * d, mc, c->fc_p, nullptr, d, 2 * d, &pt));
     launch_resid(pt, mc, d, RN_SET, c->x + (size_t)m0 * d, visual ? nullptr : c->dlayer.n1,
                  visual ? nullptr : c->xn + (size_t)m0 * 2 * d, nullptr,
                  visual ? nullptr : c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
@@ -457,8 +496,7 @@ int draft_head(msd_ctx* c, int rows, int k) {
   Parts pt;
   for (int m0 = 0; m0 < rows; m0 += CHUNK) {
     const int mc = std::min(CHUNK, rows - m0);
-    TRY(gemm(c, GK_LMHEAD, c->xb + (size_t)m0 * 2 * d, 2 * d, mc, {c->lm_head}, {V}, nullptr, d,
-             &pt));
+    TRY(gemm(c, GK_LMHEAD, c->xb + (size_t)m0 * 2 * d, 2 * d, mc, c->lm_p, nullptr, V, d, &pt));
     launch_topk(pt, mc, V, k, c->tk_idx + (size_t)m0 * k, c->tk_val + (size_t)m0 * k,
                 c->tk_lse + m0, nullptr, c->tk_scratch, c->st);
     LAUNCHED(c);
@@ -558,12 +596,13 @@ int prepare_static(msd_ctx* c, const msd_tree_spec* s) {
 extern "C" {
 
 int msd_buffer_sizes(const msd_model_desc* m, const msd_limits* lim, size_t* target_kv_bytes,
-                     size_t* draft_kv_bytes, size_t* workspace_bytes) {
+                     size_t* draft_kv_bytes, size_t* workspace_bytes, size_t* weight_bytes) {
   int r = check_desc(m, lim, nullptr);
   if (r != MSD_OK) return r;
   if (target_kv_bytes) *target_kv_bytes = kv_bytes(*m, *lim, m->n_layers);
   if (draft_kv_bytes) *draft_kv_bytes = kv_bytes(*m, *lim, 1);
   if (workspace_bytes) *workspace_bytes = carve(nullptr, *m, *lim, nullptr);
+  if (weight_bytes) *weight_bytes = weight_layout(*m).total * sizeof(uint16_t);
   return MSD_OK;
 }
 
@@ -576,10 +615,10 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   if (r != MSD_OK) return r;
   if (!tw || !dw || !bufs || !tw->embed || !tw->layers || !tw->final_norm || !tw->lm_head ||
       !dw->fc || !bufs->target_k || !bufs->target_v || !bufs->draft_k || !bufs->draft_v ||
-      !bufs->workspace)
+      !bufs->workspace || !bufs->packed_weights)
     return fail(nullptr, MSD_ERR_INVALID_ARG, "null weight or buffer pointer");
-  for (int l = 0; l < m->n_layers; ++l) {
-    const msd_layer_weights& w = tw->layers[l];
+  for (int l = 0; l <= m->n_layers; ++l) {
+    const msd_layer_weights& w = l < m->n_layers ? tw->layers[l] : dw->layer;
     if (!w.wq || !w.wk || !w.wv || !w.wo || !w.w_gate || !w.w_up || !w.w_down || !w.attn_norm ||
         !w.ffn_norm)
       return fail(nullptr, MSD_ERR_INVALID_ARG, "null layer weight");
@@ -593,15 +632,24 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   c->dlayer = to_layer(dw->layer);
   c->embed = (const uint16_t*)tw->embed;
   c->final_norm = (const uint16_t*)tw->final_norm;
-  c->lm_head = (const uint16_t*)tw->lm_head;
-  c->fc = (const uint16_t*)dw->fc;
+  // packed copies of every GEMM weight in the caller's arena
+  const WeightLayout wl = weight_layout(*m);
+  uint16_t* arena = (uint16_t*)bufs->packed_weights;
+  for (int l = 0; l <= m->n_layers; ++l) {
+    uint16_t* b = arena + wl.layer_off[l];
+    const PackedLayer pl{b, b + wl.qkv, b + wl.qkv + wl.o, b + wl.qkv + wl.o + wl.g,
+                         b + wl.qkv + wl.o + wl.g + wl.u};
+    if (l < m->n_layers) c->players.push_back(pl);
+    else c->pdlayer = pl;
+  }
+  c->fc_p = arena + wl.fc_off;
+  c->lm_p = arena + wl.lm_off;
   c->tk = (uint16_t*)bufs->target_k;
   c->tv = (uint16_t*)bufs->target_v;
   c->dk = (uint16_t*)bufs->draft_k;
   c->dv = (uint16_t*)bufs->draft_v;
   carve(c, *m, *lim, (char*)bufs->workspace);
   c->gs.target_wgs = GEMM_WGS;
-  c->gs.lds_bytes = GEMM_LDS;
   c->gs.ev_start = nullptr;
   c->gs.ev_stop = nullptr;
   c->L.assign(lim->max_batch, 0);
@@ -623,6 +671,24 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     HIPC(c, hipMemsetAsync(c->pend_n, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->d_root, 0, sizeof(int) * lim->max_batch, c->st));
     launch_rope_table(c->rope, lim->max_seq, m->head_dim, (double)m->rope_theta, c->st);
+    LAUNCHED(c);
+    const int d = m->d_model, hd = m->head_dim, H = m->n_heads, KV = m->n_kv_heads;
+    const int F = m->ffn_dim;
+    for (int l = 0; l <= m->n_layers; ++l) {
+      const LayerW& w = l < m->n_layers ? c->layers[l] : c->dlayer;
+      const PackedLayer& p = l < m->n_layers ? c->players[l] : c->pdlayer;
+      uint16_t* qkv = const_cast<uint16_t*>(p.qkv);
+      launch_pack(w.wq, H * hd, d, qkv, c->st);
+      launch_pack(w.wk, KV * hd, d, qkv + packed_elems(H * hd, d), c->st);
+      launch_pack(w.wv, KV * hd, d, qkv + packed_elems(H * hd, d) + packed_elems(KV * hd, d), c->st);
+      launch_pack(w.wo, d, H * hd, const_cast<uint16_t*>(p.o), c->st);
+      launch_pack(w.wg, F, d, const_cast<uint16_t*>(p.g), c->st);
+      launch_pack(w.wu, F, d, const_cast<uint16_t*>(p.u), c->st);
+      launch_pack(w.wd, d, F, const_cast<uint16_t*>(p.d), c->st);
+      LAUNCHED(c);
+    }
+    launch_pack((const uint16_t*)dw->fc, d, 2 * d, const_cast<uint16_t*>(c->fc_p), c->st);
+    launch_pack((const uint16_t*)tw->lm_head, m->vocab, d, const_cast<uint16_t*>(c->lm_p), c->st);
     LAUNCHED(c);
     HIPC(c, hipStreamSynchronize(c->st));
     return MSD_OK;
@@ -697,14 +763,15 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
                       {c->rows.slot, slot, nb}, {c->rows.seq, sq, nb}, {c->rows.hrow, hrow, nb},
                       {c->rows.dst, dst, nb}, {c->nxt, nxt, nb}, {c->prefix, hdr, sizeof(int)},
                       {c->seq_ids, hdr + 1, sizeof(int)}}));
+  c->seq_ids_h.assign(1, seq);
   // target over the prompt
   launch_embed(c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, c->x, c->st);
   LAUNCHED(c);
   TRY(norm_rows(c, n, c->layers[0].n1));
   TRY(forward_layers(c, false, 1, n, -1, n, c->final_norm, c->h, nullptr));
   Parts pt;
-  TRY(gemm(c, GK_LMHEAD, c->h + (size_t)(n - 1) * 2 * d, 2 * d, 1, {c->lm_head}, {m.vocab}, nullptr,
-           d, &pt));
+  TRY(gemm(c, GK_LMHEAD, c->h + (size_t)(n - 1) * 2 * d, 2 * d, 1, c->lm_p, nullptr, m.vocab, d,
+           &pt));
   launch_topk(pt, 1, m.vocab, 1, c->tk_idx, c->tk_val, nullptr, nullptr, c->tk_scratch, c->st);
   LAUNCHED(c);
   launch_set_int(c->d_root, seq, c->tk_idx, 0, c->st);
@@ -778,7 +845,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
     max_l = std::max(max_l, c->L[b]);
     r_max = std::max(r_max, c->pend[b]);
   }
-  TRY(upload(c, c->seq_ids, seqs_h, n_seq));
+  TRY(upload_seqs(c, seqs_h, n_seq));
   // 1. catch-up: pending rows through the draft head
   if (r_max > 0) {
     launch_catchup_rows(n_seq, c->seq_ids, c->d_len, c->pend_n, c->pend_next, r_max, PEND, FEAT,
@@ -787,7 +854,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
     launch_fc_input(c->pend_h, nullptr, c->rows.hrow, c->embed, c->rows.tok, nullptr,
                     n_seq * r_max, d, c->fcin, c->st);
     LAUNCHED(c);
-    TRY(draft_pass(c, n_seq, r_max, -1, max_l, nullptr));
+    TRY(draft_pass(c, n_seq, r_max, r_max, max_l + r_max, nullptr));
     launch_store_feat(c->x, n_seq * r_max, c->rows.dst, d, c->dfeat, c->st);
     LAUNCHED(c);
     for (int i = 0; i < n_seq; ++i) c->pend[seqs_h[i]] = 0;
@@ -797,7 +864,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
   for (int i = 0; i < n_seq; ++i)
     HIPC(c, hipMemcpyAsync(c->x + (size_t)i * d, c->dfeat + (size_t)seqs_h[i] * FEAT * d,
                            sizeof(float) * d, hipMemcpyDeviceToDevice, c->st));
-  launch_resid_norm(Parts{nullptr, 0, 0, 0}, 0, n_seq, d, RN_KEEP, c->x, nullptr, m.norm_eps,
+  launch_resid_norm(Parts{nullptr, 0, 0, 0, 0}, 0, n_seq, d, RN_KEEP, c->x, nullptr, m.norm_eps,
                     nullptr, c->xb, c->st);
   LAUNCHED(c);
   if (spec->kind == MSD_TREE_STATIC) {
@@ -865,7 +932,7 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
     if (c->L[b] + T > c->lim.max_seq) return fail(c, MSD_ERR_CAPACITY, "KV cache full");
     max_l = std::max(max_l, c->L[b]);
   }
-  TRY(upload(c, c->seq_ids, seqs_h, n_seq));
+  TRY(upload_seqs(c, seqs_h, n_seq));
   const int rows = n_seq * T;
   launch_verify_rows(trees_d, n_seq, c->seq_ids, c->d_len, T, V, c->rows, c->prefix, c->st);
   LAUNCHED(c);
@@ -876,8 +943,7 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
   Parts pt;
   for (int m0 = 0; m0 < rows; m0 += CHUNK) {
     const int mc = std::min(CHUNK, rows - m0);
-    TRY(gemm(c, GK_LMHEAD, c->h + (size_t)m0 * 2 * d, 2 * d, mc, {c->lm_head}, {V}, nullptr, d,
-             &pt));
+    TRY(gemm(c, GK_LMHEAD, c->h + (size_t)m0 * 2 * d, 2 * d, mc, c->lm_p, nullptr, V, d, &pt));
     launch_topk(pt, mc, V, 1, argmax_d + m0, nullptr, nullptr,
                 logits_d ? logits_d + (size_t)m0 * V : nullptr, c->tk_scratch, c->st);
     LAUNCHED(c);
@@ -897,7 +963,7 @@ int msd_accept_compact(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_t
   if (n_nodes != c->verified_T || n_seq != c->verified_nseq)
     return fail(c, MSD_ERR_STATE, "accept must follow msd_verify of the same trees");
   const int T = n_nodes, d = c->m.d_model;
-  TRY(upload(c, c->seq_ids, seqs_h, n_seq));
+  TRY(upload_seqs(c, seqs_h, n_seq));
   int* slots = slot_map_d ? slot_map_d : c->acc_slot;
   launch_accept(trees_d, n_seq, c->seq_ids, T, argmax_d, c->acc_path, c->acc_n, c->acc_emit, slots,
                 c->d_len, c->st);

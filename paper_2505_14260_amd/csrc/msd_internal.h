@@ -39,47 +39,49 @@ MSD_DEV float get_split(const uint16_t* row, int K, int k) {
 namespace msd {
 
 // ---------------------------------------------------------------- GEMM ----
-// Partial products of a thin X (M split rows) against a bf16 weight streamed
-// from HBM: part[s][m][n] = sum over K-chunk s of X[m][k] * W[n][k] (float32).  With a
-// second weight W2 (the SwiGLU pair) its products go to columns [N, 2N).
-// The consumer sums the S chunks in order.
+// Partial products of a thin X (M split rows) against a packed bf16 weight
+// streamed from HBM: part[s][m][n] = sum over K-chunk s of X[m][k] * W[n][k]
+// (float32).  With a second weight W2 (the SwiGLU pair) its products go to
+// columns [off2, off2 + N).  The consumer sums the S chunks in order.
 struct GemmArgs {
   const uint16_t* X;        // [M][ldx] split rows: hi at [k], lo at [K + k]
-  int ldx, M;
-  const uint16_t* Wseg[3];  // [N][K] bf16 given as up to three row segments
-  int seg_end[3];           // cumulative segment heights (multiples of 16)
-  const uint16_t* W2;       // second weight [N][K] or null
-  int N, K;
-  int S, Kc, G;             // K chunks, chunk length, workgroups per chunk
+  int ldx, M, K;
+  const uint16_t* W;        // packed (packed_elems(N, K) elements)
+  const uint16_t* W2;       // second packed weight or null
+  int n_tiles, nkt;         // 64-row tiles, 128-column blocks
+  int S, G;                 // K chunks, workgroups per chunk
   float* part;              // partials of row 0 of this launch
-  size_t part_split;        // floats between consecutive chunks
-  int ldp;                  // floats between consecutive rows (N or 2N)
+  size_t part_split;        // floats between consecutive chunks (M * ldp)
+  int ldp, off2;            // floats between rows; column offset of W2's products
+  float* sink;              // 1 KB written by padded rows
 };
 
 struct GemmPlan {
-  int MT, S, Kc, G, nw;
+  int MT, S, G, nw, n_tiles, nkt, ldp, off2;
 };
 
 struct GemmScratch {
-  int target_wgs;  // workgroups per launch
-  int lds_bytes;   // LDS for the staged X chunk (bf16 hi + lo) of one workgroup
+  int target_wgs;                // workgroups per launch
   hipEvent_t ev_start, ev_stop;  // when set: recorded around the kernel itself
 };
 
-GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs, int lds_bytes);
+// Elements of a packed [N][K] weight (64-row tiles x 128-column blocks).
+size_t packed_elems(int N, int K);
+// Packs the row-major bf16 [N][K] src into dst (packed_elems(N, K) elements).
+void launch_pack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t st);
+GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs);
 // floats of partials for M rows (M <= 64 per launch)
-size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs, int lds_bytes);
-// rows M <= 64; the weight is the row concatenation of n_seg (<= 3) matrices
-void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* const* Wseg,
-                 const int* seg_rows, int n_seg, const uint16_t* W2, int K, float* part,
-                 const GemmScratch& sc, hipStream_t st);
+size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs);
+void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2, int N,
+                 int K, float* part, float* sink, const GemmScratch& sc, hipStream_t st);
 
-// Partial sums as seen by a consumer: value(m, n) = sum_s p[s*split + m*ld + n].
+// Partial sums as seen by a consumer: value(m, n) = sum_s p[s*split + m*ld + n];
+// the second weight's products are at column n + off2.
 struct Parts {
   const float* p;
   int S;
   size_t split;
-  int ld;
+  int ld, off2;
 };
 
 // Per-row RMS of the un-normalised GEMM input: ssq[row][0..nblk) are sums of
@@ -92,15 +94,15 @@ struct RowNorm {
 
 // ----------------------------------------------------------- attention ----
 struct AttnArgs {
-  const float* q;         // [n_seq*nq][H*hd] float32, rotated
+  const uint16_t* q;      // [n_seq*nq] split rows of H*hd, rotated
   const uint16_t* kc;     // layer K cache  [B][KV][S][hd]
   const uint16_t* vc;     // layer V cache  [B][KV][hd][S]
   const int* seq_ids;     // [n_seq] absolute sequence index into the caches
   const int* prefix;      // [n_seq] fully visible prefix length
   const uint64_t* mask;   // [n_seq*nq] region masks (tree mode)
   int S, H, KV, hd, nq, n_seq, R;
-  int n_chunks, chunk_keys, qtiles;
-  float* part_o;          // [items][64*hd/2*...] partial outputs (tree mode)
+  int n_chunks, chunk_keys, qtiles;  // chunk_keys: multiple of 128 (tree mode)
+  float* part_o;          // [items][32*hd] partial outputs (tree mode, n_chunks > 1)
   float* part_ml;         // [items][32][2]
   uint16_t* out;          // [n_seq*nq] split rows of H*hd
   float scale;
@@ -127,7 +129,7 @@ void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t*
                   uint16_t* xb, float* ssq, hipStream_t st);
 void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, const int* pos,
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
-                    float* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st);
+                    uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st);
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
 // out[row] = split row of [h | e] (2d values); h rows are split rows of d
 // (target features) when h, else float32 rows of hf (draft features).

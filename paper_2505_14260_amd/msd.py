@@ -45,7 +45,8 @@ class DraftWeights(ctypes.Structure):
 
 
 class Buffers(ctypes.Structure):
-    _fields_ = [(n, c_vp) for n in ("target_k", "target_v", "draft_k", "draft_v", "workspace")]
+    _fields_ = [(n, c_vp) for n in ("target_k", "target_v", "draft_k", "draft_v", "workspace",
+                                    "packed_weights")]
 
 
 class TreeSpec(ctypes.Structure):
@@ -73,7 +74,7 @@ def lib():
             raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2505_14260_amd/build.py")
         L = ctypes.CDLL(LIB_PATH)
         P = ctypes.POINTER
-        L.msd_buffer_sizes.argtypes = [P(ModelDesc), P(Limits), P(c_sz), P(c_sz), P(c_sz)]
+        L.msd_buffer_sizes.argtypes = [P(ModelDesc), P(Limits), P(c_sz), P(c_sz), P(c_sz), P(c_sz)]
         L.msd_create.argtypes = [P(ModelDesc), P(Limits), P(TargetWeights), P(DraftWeights),
                                  P(Buffers), c_vp, P(c_vp)]
         L.msd_destroy.argtypes = [c_vp]
@@ -114,10 +115,10 @@ def _i32(a):
 # --- the C entry points, same names -------------------------------------------------
 
 def msd_buffer_sizes(desc: ModelDesc, lim: Limits):
-    t, d, w = c_sz(), c_sz(), c_sz()
+    t, d, w, p = c_sz(), c_sz(), c_sz(), c_sz()
     _check(None, lib().msd_buffer_sizes(ctypes.byref(desc), ctypes.byref(lim), ctypes.byref(t),
-                                        ctypes.byref(d), ctypes.byref(w)))
-    return t.value, d.value, w.value
+                                        ctypes.byref(d), ctypes.byref(w), ctypes.byref(p)))
+    return t.value, d.value, w.value, p.value
 
 
 def msd_create(desc, lim, tw, dw, bufs, stream):
@@ -227,9 +228,9 @@ class Engine:
         self.tw = TargetWeights(up(target["embed"]), layers, up(target["final_norm"]),
                                 up(target["lm_head"]))
         self.dw = DraftWeights(up(draft["fc"]), self._layer(draft["layer"]))
-        tkv, dkv, ws = msd_buffer_sizes(self.desc, self.lim)
+        tkv, dkv, ws, pw = msd_buffer_sizes(self.desc, self.lim)
         self.bufs_t = [torch.empty(n, dtype=torch.uint8, device=self.dev)
-                       for n in (tkv, tkv, dkv, dkv, ws)]
+                       for n in (tkv, tkv, dkv, dkv, ws, pw)]
         self.bufs = Buffers(*[b.data_ptr() for b in self.bufs_t])
         self.stream = torch.cuda.current_stream(self.dev).cuda_stream
         self.ctx = msd_create(self.desc, self.lim, self.tw, self.dw, self.bufs, self.stream)

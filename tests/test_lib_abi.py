@@ -44,8 +44,15 @@ def test_buffer_sizes_and_errors_without_gpu():
         pytest.skip("libmsd.so not built")
     d = msd.ModelDesc(2, 128, 4, 2, 64, 256, 512, 1e4, 1e-5)
     lim = msd.Limits(1, 256, 16, 64)
-    tkv, dkv, ws = msd.msd_buffer_sizes(d, lim)
+    tkv, dkv, ws, pw = msd.msd_buffer_sizes(d, lim)
     assert tkv == 2 * 1 * 2 * 256 * 64 * 2 and dkv == tkv // 2 and ws > 0
+
+    def packed(n, k):  # 64-row x 128-column bf16 blocks, zero-padded
+        return -(-n // 64) * -(-k // 128) * 64 * 128 * 2
+    dm, hd, H, KV, F, V = 128, 64, 4, 2, 256, 512
+    layer = (packed(H * hd, dm) + 2 * packed(KV * hd, dm) + packed(dm, H * hd)
+             + 2 * packed(F, dm) + packed(dm, F))
+    assert pw == 3 * layer + packed(dm, 2 * dm) + packed(V, dm)
     bad = msd.ModelDesc(2, 128, 4, 3, 64, 256, 512, 1e4, 1e-5)
     with pytest.raises(msd.MSDError) as e:
         msd.msd_buffer_sizes(bad, lim)
