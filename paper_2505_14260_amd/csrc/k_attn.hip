@@ -1,9 +1,10 @@
 // Attention over the KV cache on gfx950 MFMA.
 //
 // Tree mode (verification, draft expansion and draft catch-up): every query
-// row sees the whole prefix [0, P) of its sequence and the slots of region
-// [P, P+R) whose bit is set in its 64-bit mask (tree-structured attention of
-// the draft/verify phases; a triangular mask gives causal rows).  A
+// row sees the whole prefix [0, P) of its sequence and the slots of its
+// region [P, keys) whose bit is set in its 64-bit mask (tree-structured
+// attention of the draft/verify phases; a triangular mask gives causal
+// rows); slots at or past keys are never read.  A
 // workgroup of 4 waves owns one (sequence, kv head, 32-row query tile, key
 // chunk); its waves split the chunk, run an online softmax each, and merge
 // their states through LDS into one partial per workgroup; a combine kernel
@@ -38,44 +39,56 @@ struct AttnState {
 };
 
 // K rows of the 32-key block starting at kb for the S^T product (A operand).
+// Rows past the cache (S slots) read the last slot instead; their scores
+// are replaced by -inf before any use, so whatever those slots hold is never
+// seen and the loads need no branch.
 template <int HD>
-MSD_DEV void load_k(uint4 (&kf)[HD / 16], const uint16_t* kbase, int kb, int k_valid) {
+MSD_DEV void load_k(uint4 (&kf)[HD / 16], const uint16_t* kbase, int kb, int S) {
   const int lane = threadIdx.x & 63;
-  const int krow = kb + perm_key(lane & 31);
-  const bool kval = krow < k_valid;
-  const uint16_t* kp = kbase + (size_t)(kval ? krow : 0) * HD + (HD / 2) * (lane >> 5);
+  const int krow = min(kb + perm_key(lane & 31), S - 1);
+  const uint16_t* kp = kbase + (size_t)krow * HD + (HD / 2) * (lane >> 5);
 #pragma unroll
-  for (int c = 0; c < HD / 16; ++c)
-    kf[c] = kval ? *reinterpret_cast<const uint4*>(kp + 8 * c) : make_uint4(0, 0, 0, 0);
+  for (int c = 0; c < HD / 16; ++c) kf[c] = *reinterpret_cast<const uint4*>(kp + 8 * c);
 }
 
-// V^T columns of the block for the O^T product (A operand), zero past k_valid.
+// V^T columns of the block for the O^T product (A operand): eight
+// consecutive keys per 16-byte load (S is a multiple of 8).  Keys at or past
+// k_valid read as zero: their probabilities are zero, but the slots may hold
+// any bits (never written, or left by the caller), and 0 * NaN would poison
+// the sum.  The clamp keeps the address inside the cache; a clamped load
+// only ever covers keys at or past S >= k_valid, which the mask zeroes.
 template <int HD>
 MSD_DEV void load_v(uint4 (&vf)[HD / 32][2], const uint16_t* vbase, int S, int kb, int k_valid) {
   const int lane = threadIdx.x & 63;
   const int i = lane & 31, h = lane >> 5;
+  int k0[2];
+  uint32_t keep[2][4];  // per 32-bit word: keys 2e (low half) and 2e+1 (high half)
+#pragma unroll
+  for (int pk = 0; pk < 2; ++pk) {
+    const int kk = kb + 16 * pk + 8 * h;
+    const int nv = k_valid - kk;
+    k0[pk] = min(kk, S - 8);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      keep[pk][e] = (2 * e + 1 < nv) ? 0xFFFFFFFFu : ((2 * e < nv) ? 0x0000FFFFu : 0u);
+  }
 #pragma unroll
   for (int dt = 0; dt < HD / 32; ++dt) {
     const uint16_t* vp = vbase + (size_t)(dt * 32 + i) * S;
 #pragma unroll
     for (int pk = 0; pk < 2; ++pk) {
-      const int k0 = kb + 16 * pk + 8 * h;
-      if (k0 + 8 <= k_valid) {
-        vf[dt][pk] = *reinterpret_cast<const uint4*>(vp + k0);
-      } else {
-        uint16_t t[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) t[e] = (k0 + e < k_valid) ? vp[k0 + e] : (uint16_t)0;
-        vf[dt][pk] = make_uint4(t[0] | (t[1] << 16), t[2] | (t[3] << 16), t[4] | (t[5] << 16),
-                                t[6] | (t[7] << 16));
-      }
+      const uint4 r = *reinterpret_cast<const uint4*>(vp + k0[pk]);
+      vf[dt][pk] = make_uint4(r.x & keep[pk][0], r.y & keep[pk][1], r.z & keep[pk][2],
+                              r.w & keep[pk][3]);
     }
   }
 }
 
-// Processes keys [k_begin, k_end) (k_begin multiple of 32) for the wave's 32
-// query columns; vis(key) decides visibility.  The next block's K rows and
-// the current block's V columns are loaded while the scores are computed.
+// Online-softmax accumulation of keys [k_begin, k_end) (k_begin a multiple
+// of 32) for the 32 query columns of the wave; vis(key) says whether the
+// lane's query sees the key.  Keys at or past k_valid (>= k_end) are never
+// taken from the cache.  The next block's K rows and the current block's V
+// columns are loaded while the scores are computed.
 template <int HD, typename Vis>
 MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qh)[HD / 16],
                           const bf16x8 (&ql)[HD / 16],
@@ -85,7 +98,7 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qh)[HD / 16],
   const int h = lane >> 5;
   if (k_begin >= k_end) return;
   uint4 kf[HD / 16];
-  load_k<HD>(kf, kbase, k_begin, k_valid);
+  load_k<HD>(kf, kbase, k_begin, S);
   for (int kb = k_begin; kb < k_end; kb += 32) {
     uint4 vf[HD / 32][2];
     load_v<HD>(vf, vbase, S, kb, k_valid);
@@ -98,7 +111,7 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qh)[HD / 16],
       s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), ql[c], s2, 0, 0, 0);
     }
     s += s2;
-    if (kb + 32 < k_end) load_k<HD>(kf, kbase, kb + 32, k_valid);
+    load_k<HD>(kf, kbase, kb + 32, S);  // the next block (past the end: unused)
     float bm = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -212,9 +225,9 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
   const int qt = t % a.qtiles; t /= a.qtiles;
   const int g = t % a.KV;
   const int sidx = t / a.KV;
-  const int b = a.seq_ids[sidx];
+  const int b = a.seq[sidx];
   const int P = a.prefix[sidx];
-  const int Ltot = P + a.R;
+  const int Ltot = a.keys[sidx];
   const int G = a.H / a.KV;
   int node, head;
   column_to_row(qt, lane & 31, G, g, node, head);
@@ -244,22 +257,33 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
     sml[w][lane][1] = st.l;
   }
   __syncthreads();
-  const size_t item = blockIdx.x;
-  for (int e = threadIdx.x; e < E; e += 256) {
-    const int j = (e & 63) & 31;
+  // per-column merge weights of the 4 waves: wgt[q][j] = exp(m_q - M_j)
+  __shared__ float wgt[4][32];
+  __shared__ float colm[32][2];
+  if (threadIdx.x < 32) {
+    const int j = threadIdx.x;
     float M = -INFINITY;
 #pragma unroll
     for (int q = 0; q < 4; ++q) M = fmaxf(M, sml[q][j][0]);
-    float o = 0.f, l = 0.f;
-    if (M != -INFINITY) {
+    float l = 0.f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float mq = sml[q][j][0];
-        const float wq = (mq == -INFINITY) ? 0.f : __expf(mq - M);
-        o += wq * so[q * E + e];
-        l += wq * sml[q][j][1];
-      }
+    for (int q = 0; q < 4; ++q) {
+      const float mq = sml[q][j][0];
+      const float wq = (M == -INFINITY || mq == -INFINITY) ? 0.f : __expf(mq - M);
+      wgt[q][j] = wq;
+      l += wq * sml[q][j][1];
     }
+    colm[j][0] = M;
+    colm[j][1] = l;
+  }
+  __syncthreads();
+  const size_t item = blockIdx.x;
+  for (int e = threadIdx.x; e < E; e += 256) {
+    const int j = e & 31;
+    float o = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o += wgt[q][j] * so[q * E + e];
+    const float M = colm[j][0], l = colm[j][1];
     if (a.n_chunks == 1) {
       int nd, hd_;
       column_to_row(qt, j, G, g, nd, hd_);
@@ -342,7 +366,7 @@ __global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
   const int qt = t % a.qtiles; t /= a.qtiles;
   const int head = t % a.H;
   const int sidx = t / a.H;
-  const int b = a.seq_ids[sidx];
+  const int b = a.seq[sidx];
   const int P = a.prefix[sidx];
   const int g = head / (a.H / a.KV);
   const int j = lane & 31;

@@ -17,11 +17,11 @@
 // Work split.  K is cut into chunks of NKB blocks; a workgroup (4 waves) owns
 // one chunk and a strided set of tiles, stages its X chunk in LDS once
 // (XOR-swizzled, hi halves then lo halves) and then streams the W blocks of
-// its tiles through a ring of NKB register stages: while it consumes block p
-// of tile j it loads block p of tile j+1.  The loop has no branch on the
-// data path and stores each tile's partial unconditionally (padded rows go
-// to a small sink), which keeps every weight load in flight across tile
-// boundaries.  Partials part[s][m][n] (float32) are summed in chunk order by
+// its tiles through a ring of P register stages: having consumed a block it
+// loads the block P places further in its (tile, block) sequence.  The loop
+// has no branch on the data path and stores each tile's partial
+// unconditionally (padded rows go to a small sink), which keeps every weight
+// load in flight across tile boundaries.  Partials part[s][m][n] (float32) are summed in chunk order by
 // the kernel that consumes the product, so the result is deterministic.
 //
 // X arrives split by its producer, x = hi + lo with hi = bf16(x) and
@@ -39,6 +39,9 @@ namespace {
 constexpr int KB = 128;       // K elements per block
 constexpr int TILE_ROWS = 64;  // 4 waves x 16 rows
 constexpr int BLOCK_ELEMS = TILE_ROWS * KB;
+// 128-column blocks per K chunk.  Longer chunks (fewer partials) run out of
+// registers for the ring and serialize its loads.
+constexpr int NKB_CHUNK = 4;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 MSD_DEV uint4 load_stream(const uint16_t* p) {
@@ -51,8 +54,9 @@ MSD_DEV uint4 load_stream(const uint16_t* p) {
 // MFMA operand load hit different banks.
 MSD_DEV int xs_index(int m, int u, int upr) { return m * upr + (u ^ (m & 15)); }
 
-template <int MT, int NW, int NKB>
+template <int MT, int NW, int NKB, int P>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+  static_assert(NKB % P == 0, "ring slots must divide the chunk");
   extern __shared__ uint4 xs[];
   constexpr int UPR = NKB * KB / 8;  // 16-byte units per LDS row
   constexpr int LO = MT * 16 * UPR;  // offset of the lo halves
@@ -69,6 +73,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const uint16_t* const W = a.W;
   const uint16_t* const W2 = a.W2;
   const size_t lane_off = (size_t)wave * (BLOCK_ELEMS / 4) + lane * 8;
+  const size_t tstride = (size_t)nkt * BLOCK_ELEMS;
   int kbs[NKB];  // the chunk's blocks (the last chunk repeats block nkt-1; X is zero there)
 #pragma unroll
   for (int p = 0; p < NKB; ++p) kbs[p] = min(kb0 + p, nkt - 1);
@@ -91,10 +96,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     xh[q] = ok ? h : make_uint4(0, 0, 0, 0);
     xl[q] = ok ? l : make_uint4(0, 0, 0, 0);
   }
-  uint4 ring[NKB][NW][4];
+  uint4 ring[P][NW][4];
 #pragma unroll
-  for (int p = 0; p < NKB; ++p) {
-    const size_t o = ((size_t)gi * nkt + kbs[p]) * BLOCK_ELEMS + lane_off;
+  for (int p = 0; p < P; ++p) {
+    const size_t o = (size_t)gi * tstride + (size_t)kbs[p] * BLOCK_ELEMS + lane_off;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       ring[p][0][c] = load_stream(W + o + c * 512);
@@ -131,9 +136,15 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const int ldp = a.ldp, off2 = a.off2;
   float* const part = a.part + (size_t)s * a.part_split;
   float* const sink = a.sink + lane * 4;
+  const uint16_t* const dummy = a.dummy;
   for (int j = 0; j < n_my; ++j) {
     const int tile = gi + j * G;
-    const int tn = gi + min(j + 1, n_my - 1) * G;
+    // the ring's refills for the next tile; after the last tile they read a
+    // small zero block instead (cache-resident, not another weight chunk)
+    const bool more = j + 1 < n_my;
+    const uint16_t* const wn = more ? W : dummy;
+    const uint16_t* const wn2 = more ? W2 : dummy;
+    const size_t tn_base = more ? (size_t)(tile + G) * tstride : 0;
     f32x4 acc[NW][MT];
 #pragma unroll
     for (int w = 0; w < NW; ++w)
@@ -157,20 +168,25 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
           for (int t = 0; t < MT; ++t)
             acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                as_bf16x8(ring[p][w][c]), as_bf16x8(fh[t][c]), acc[w][t], 0, 0, 0);
+                as_bf16x8(ring[p % P][w][c]), as_bf16x8(fh[t][c]), acc[w][t], 0, 0, 0);
 #pragma unroll
         for (int w = 0; w < NW; ++w)
 #pragma unroll
           for (int t = 0; t < MT; ++t)
             acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                as_bf16x8(ring[p][w][c]), as_bf16x8(fl[t][c]), acc[w][t], 0, 0, 0);
+                as_bf16x8(ring[p % P][w][c]), as_bf16x8(fl[t][c]), acc[w][t], 0, 0, 0);
       }
-      // refill with block p of the next tile (the last tile reloads itself)
-      const size_t o = ((size_t)tn * nkt + kbs[p]) * BLOCK_ELEMS + lane_off;
+      // refill with the block P ahead: later in this tile, or in the next one
+      const int q = p + P;
+      const uint16_t* const b1 = q < NKB ? W : wn;
+      const uint16_t* const b2 = q < NKB ? W2 : wn2;
+      const size_t o =
+          q < NKB ? (size_t)tile * tstride + (size_t)kbs[q < NKB ? q : 0] * BLOCK_ELEMS
+                  : tn_base + (size_t)(more ? kbs[q < NKB ? 0 : q - NKB] : q - NKB) * BLOCK_ELEMS;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        ring[p][0][c] = load_stream(W + o + c * 512);
-        if (NW == 2) ring[p][NW - 1][c] = load_stream(W2 + o + c * 512);
+        ring[p % P][0][c] = load_stream(b1 + o + lane_off + c * 512);
+        if (NW == 2) ring[p % P][NW - 1][c] = load_stream(b2 + o + lane_off + c * 512);
       }
     }
     // C layout of the 16x16 MFMA: lane holds column (lane & 15) = row m,
@@ -207,18 +223,20 @@ __global__ void k_pack(const uint16_t* src, int N, int K, int nkt, size_t units,
 
 // With timing events the launch carries them in its dispatch packet, so they
 // bracket the kernel's execution only.
-template <int MT, int NW>
+template <int MT, int NW, int NKB>
 void launch_mt(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
-  constexpr int NKB = 4;
+  constexpr int P = 4;
   const size_t lds = (size_t)MT * 16 * NKB * KB * 4;
   if (sc.ev_start)
-    hipExtLaunchKernelGGL((k_gemm<MT, NW, NKB>), grid, dim3(256), lds, st, sc.ev_start, sc.ev_stop,
-                          0, a);
+    hipExtLaunchKernelGGL((k_gemm<MT, NW, NKB, P>), grid, dim3(256), lds, st, sc.ev_start,
+                          sc.ev_stop, 0, a);
   else
-    hipLaunchKernelGGL((k_gemm<MT, NW, NKB>), grid, dim3(256), lds, st, a);
+    hipLaunchKernelGGL((k_gemm<MT, NW, NKB, P>), grid, dim3(256), lds, st, a);
 }
 
 }  // namespace
+
+size_t gemm_dummy_elems() { return (size_t)NKB_CHUNK * BLOCK_ELEMS; }
 
 size_t packed_elems(int N, int K) {
   return (size_t)((N + TILE_ROWS - 1) / TILE_ROWS) * ((K + KB - 1) / KB) * BLOCK_ELEMS;
@@ -236,7 +254,8 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
   const int mc = M < 64 ? M : 64;
   p.MT = mc <= 16 ? 1 : (mc <= 32 ? 2 : 4);
   p.nkt = (K + KB - 1) / KB;
-  p.S = (p.nkt + 3) / 4;  // chunks of 4 blocks
+  p.nkb = NKB_CHUNK;
+  p.S = (p.nkt + p.nkb - 1) / p.nkb;
   p.n_tiles = (N + TILE_ROWS - 1) / TILE_ROWS;
   // workgroups per chunk: about target_wgs in total, every workgroup of a
   // chunk getting the same number of tiles
@@ -257,7 +276,8 @@ size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs) {
 }
 
 void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2, int N,
-                 int K, float* part, float* sink, const GemmScratch& sc, hipStream_t st) {
+                 int K, float* part, float* sink, const uint16_t* dummy, const GemmScratch& sc,
+                 hipStream_t st) {
   const int nw = W2 ? 2 : 1;
   const GemmPlan pl = plan_gemm(M, N, K, nw, sc.target_wgs);
   GemmArgs a{};
@@ -276,15 +296,16 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
   a.ldp = pl.ldp;
   a.off2 = pl.off2;
   a.sink = sink;
+  a.dummy = dummy;
   const dim3 grid(pl.S * pl.G);
   if (nw == 2) {
-    if (pl.MT == 1) launch_mt<1, 2>(grid, a, sc, st);
-    else if (pl.MT == 2) launch_mt<2, 2>(grid, a, sc, st);
-    else launch_mt<4, 2>(grid, a, sc, st);
+    if (pl.MT == 1) launch_mt<1, 2, NKB_CHUNK>(grid, a, sc, st);
+    else if (pl.MT == 2) launch_mt<2, 2, NKB_CHUNK>(grid, a, sc, st);
+    else launch_mt<4, 2, NKB_CHUNK>(grid, a, sc, st);
   } else {
-    if (pl.MT == 1) launch_mt<1, 1>(grid, a, sc, st);
-    else if (pl.MT == 2) launch_mt<2, 1>(grid, a, sc, st);
-    else launch_mt<4, 1>(grid, a, sc, st);
+    if (pl.MT == 1) launch_mt<1, 1, NKB_CHUNK>(grid, a, sc, st);
+    else if (pl.MT == 2) launch_mt<2, 1, NKB_CHUNK>(grid, a, sc, st);
+    else launch_mt<4, 1, NKB_CHUNK>(grid, a, sc, st);
   }
 }
 

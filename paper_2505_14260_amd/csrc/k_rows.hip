@@ -287,12 +287,14 @@ __global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, 
   int n = 0;
   float mloc = -INFINITY, sloc = 0.f;
   for (int v = v0 + threadIdx.x; v < v1; v += 256) {
-    const float val = part_sum(logits, row, v);
-    if (logits_out) logits_out[(size_t)row * V + v] = val;
+    const float raw = part_sum(logits, row, v);
+    if (logits_out) logits_out[(size_t)row * V + v] = raw;
+    // a NaN ranks as -inf, so the selected ids are always vocabulary ids
+    const float val = (raw == raw) ? raw : -INFINITY;
     if (val > mloc) {
       sloc = sloc * __expf(mloc - val) + 1.f;
       mloc = val;
-    } else {
+    } else if (val != -INFINITY) {
       sloc += __expf(val - mloc);
     }
     insert_sorted(lv, li, n, k, val, v);

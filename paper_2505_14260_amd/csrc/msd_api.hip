@@ -60,6 +60,7 @@ WeightLayout weight_layout(const msd_model_desc& m) {
   return w;
 }
 
+constexpr int MSD_MAX_BATCH_ARGS = ATT_MAX_SEQ;
 constexpr int PEND = MSD_MAX_TREE;      // pending draft rows per sequence
 constexpr int FEAT = MSD_MAX_TREE + 1;  // draft feature slots per sequence
 constexpr int TOPK = 16;
@@ -126,7 +127,8 @@ struct msd_ctx {
   // activation rows: split rows (bf16 hi + lo) for every MFMA input
   uint16_t *xn, *xb, *fcin, *q, *ao, *act, *h;
   float* part;
-  float* sink;  // GEMM rows past M
+  float* sink;          // GEMM rows past M
+  uint16_t* gemm_zero;  // zero block the GEMM ring reads after its last tile
   float* ssq;
   Rows rows;
   int *nxt, *prefix, *seq_ids;
@@ -145,6 +147,10 @@ struct msd_ctx {
   int* stage;  // pinned staging
   std::vector<int> L, pend, ready;
   std::vector<int> seq_ids_h;  // what c->seq_ids holds (empty: unknown)
+  // attention bounds of the next passes per call slot: slots below att_pre
+  // are visible to every row, [att_pre, att_keys) through the row masks
+  int att_pre[MSD_MAX_BATCH_ARGS];
+  int att_keys[MSD_MAX_BATCH_ARGS];
   std::string err;
   // static spec cache
   std::vector<int> sp_parent, sp_rank;
@@ -212,6 +218,7 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->fcin = cv.take<uint16_t>((size_t)R * 4 * d);
   t->part = cv.take<float>(p.part_floats);
   t->sink = cv.take<float>(256);
+  t->gemm_zero = cv.take<uint16_t>(gemm_dummy_elems());
   t->ssq = cv.take<float>((size_t)R * ((d + 255) / 256));
   t->q = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
   t->ao = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
@@ -269,7 +276,7 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
 int check_desc(const msd_model_desc* m, const msd_limits* lim, msd_ctx* c) {
   if (!m || !lim) return fail(c, MSD_ERR_INVALID_ARG, "null model or limits");
   if (m->n_layers <= 0 || m->d_model <= 0 || m->n_heads <= 0 || m->n_kv_heads <= 0 ||
-      m->n_heads % m->n_kv_heads || m->ffn_dim <= 0 || m->vocab <= 0)
+      m->n_heads % m->n_kv_heads || m->ffn_dim <= 0 || m->vocab < TOPK)
     return fail(c, MSD_ERR_INVALID_ARG, "bad model shape");
   if (m->head_dim != 128 && m->head_dim != 64)
     return fail(c, MSD_ERR_INVALID_ARG, "head_dim must be 64 or 128");
@@ -339,7 +346,7 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
     gs.ev_stop = r.b;
     c->trace.push_back(r);
   }
-  launch_gemm(X, ldx, M, W, W2, N, K, c->part, c->sink, gs, c->st);
+  launch_gemm(X, ldx, M, W, W2, N, K, c->part, c->sink, c->gemm_zero, gs, c->st);
   LAUNCHED(c);
   const GemmPlan pl = plan_gemm(M, N, K, W2 ? 2 : 1, c->gs.target_wgs);
   *out = Parts{c->part, pl.S, (size_t)M * pl.ldp, pl.ldp, pl.off2};
@@ -396,8 +403,11 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     a.q = c->q;
     a.kc = kc;
     a.vc = vc;
-    a.seq_ids = c->seq_ids;
-    a.prefix = c->prefix;
+    for (int i = 0; i < n_seq; ++i) {
+      a.seq[i] = c->seq_ids_h[i];
+      a.prefix[i] = c->att_pre[i];
+      a.keys[i] = c->att_keys[i];
+    }
     a.mask = c->rows.mask;
     a.S = S;
     a.H = H;
@@ -415,7 +425,6 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       launch_causal_attention(a, c->st);
     } else {
       const int G = H / KV;
-      a.R = tree_R;
       a.qtiles = (nq * G + 31) / 32;
       // key chunks (multiples of 128 keys, 32 per wave of a workgroup):
       // about two workgroups per CU over the whole launch, at most 64 chunks
@@ -670,6 +679,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     HIPC(c, hipMemsetAsync(c->d_len, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->pend_n, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->d_root, 0, sizeof(int) * lim->max_batch, c->st));
+    HIPC(c, hipMemsetAsync(c->gemm_zero, 0, sizeof(uint16_t) * gemm_dummy_elems(), c->st));
     launch_rope_table(c->rope, lim->max_seq, m->head_dim, (double)m->rope_theta, c->st);
     LAUNCHED(c);
     const int d = m->d_model, hd = m->head_dim, H = m->n_heads, KV = m->n_kv_heads;
@@ -764,6 +774,8 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
                       {c->rows.dst, dst, nb}, {c->nxt, nxt, nb}, {c->prefix, hdr, sizeof(int)},
                       {c->seq_ids, hdr + 1, sizeof(int)}}));
   c->seq_ids_h.assign(1, seq);
+  c->att_pre[0] = 0;
+  c->att_keys[0] = n;
   // target over the prompt
   launch_embed(c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, c->x, c->st);
   LAUNCHED(c);
@@ -847,6 +859,11 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
   }
   TRY(upload_seqs(c, seqs_h, n_seq));
   // 1. catch-up: pending rows through the draft head
+  // (a shorter sequence's padding rows write nothing: its region ends at L)
+  for (int i = 0; i < n_seq; ++i) {
+    c->att_pre[i] = c->L[seqs_h[i]] - c->pend[seqs_h[i]];
+    c->att_keys[i] = c->L[seqs_h[i]];
+  }
   if (r_max > 0) {
     launch_catchup_rows(n_seq, c->seq_ids, c->d_len, c->pend_n, c->pend_next, r_max, PEND, FEAT,
                         c->rows, c->prefix, c->st);
@@ -859,6 +876,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
     LAUNCHED(c);
     for (int i = 0; i < n_seq; ++i) c->pend[seqs_h[i]] = 0;
   }
+  for (int i = 0; i < n_seq; ++i) c->att_pre[i] = c->L[seqs_h[i]];
   // 2. draft distribution at the root: the last catch-up feature of each
   //    sequence goes through the LM head
   for (int i = 0; i < n_seq; ++i)
@@ -883,6 +901,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
                       d, c->fcin, c->st);
       LAUNCHED(c);
       const int R = c->round_exp_end[dd];
+      for (int i = 0; i < n_seq; ++i) c->att_keys[i] = c->L[seqs_h[i]] + R;
       TRY(draft_pass(c, n_seq, nr, R, max_l + R, nullptr));
       launch_store_feat(c->x, n_seq * nr, c->rows.dst, d, c->dfeat, c->st);
       LAUNCHED(c);
@@ -902,6 +921,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
                       d, c->fcin, c->st);
       LAUNCHED(c);
       const int R = exp_base;
+      for (int i = 0; i < n_seq; ++i) c->att_keys[i] = c->L[seqs_h[i]] + R;
       TRY(draft_pass(c, n_seq, K, R, max_l + R, nullptr));
       launch_store_feat(c->x, n_seq * K, c->rows.dst, d, c->dfeat, c->st);
       LAUNCHED(c);
@@ -933,6 +953,10 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
     max_l = std::max(max_l, c->L[b]);
   }
   TRY(upload_seqs(c, seqs_h, n_seq));
+  for (int i = 0; i < n_seq; ++i) {
+    c->att_pre[i] = c->L[seqs_h[i]];
+    c->att_keys[i] = c->L[seqs_h[i]] + T;
+  }
   const int rows = n_seq * T;
   launch_verify_rows(trees_d, n_seq, c->seq_ids, c->d_len, T, V, c->rows, c->prefix, c->st);
   LAUNCHED(c);

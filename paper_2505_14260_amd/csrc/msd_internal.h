@@ -54,10 +54,11 @@ struct GemmArgs {
   size_t part_split;        // floats between consecutive chunks (M * ldp)
   int ldp, off2;            // floats between rows; column offset of W2's products
   float* sink;              // 1 KB written by padded rows
+  const uint16_t* dummy;    // gemm_dummy_elems() zeros read by the ring after the last tile
 };
 
 struct GemmPlan {
-  int MT, S, G, nw, n_tiles, nkt, ldp, off2;
+  int MT, nkb, S, G, nw, n_tiles, nkt, ldp, off2;
 };
 
 struct GemmScratch {
@@ -72,8 +73,10 @@ void launch_pack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t s
 GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs);
 // floats of partials for M rows (M <= 64 per launch)
 size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs);
+size_t gemm_dummy_elems();
 void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2, int N,
-                 int K, float* part, float* sink, const GemmScratch& sc, hipStream_t st);
+                 int K, float* part, float* sink, const uint16_t* dummy, const GemmScratch& sc,
+                 hipStream_t st);
 
 // Partial sums as seen by a consumer: value(m, n) = sum_s p[s*split + m*ld + n];
 // the second weight's products are at column n + off2.
@@ -93,14 +96,17 @@ struct RowNorm {
 };
 
 // ----------------------------------------------------------- attention ----
+constexpr int ATT_MAX_SEQ = 8;
 struct AttnArgs {
   const uint16_t* q;      // [n_seq*nq] split rows of H*hd, rotated
   const uint16_t* kc;     // layer K cache  [B][KV][S][hd]
   const uint16_t* vc;     // layer V cache  [B][KV][hd][S]
-  const int* seq_ids;     // [n_seq] absolute sequence index into the caches
-  const int* prefix;      // [n_seq] fully visible prefix length
+  int seq[ATT_MAX_SEQ];   // absolute sequence index into the caches, per call slot
+  int prefix[ATT_MAX_SEQ];  // fully visible prefix length, per call slot
+  int keys[ATT_MAX_SEQ];  // tree mode: slots [prefix, keys) are the masked region;
+                          // no slot at or past keys is read
   const uint64_t* mask;   // [n_seq*nq] region masks (tree mode)
-  int S, H, KV, hd, nq, n_seq, R;
+  int S, H, KV, hd, nq, n_seq;
   int n_chunks, chunk_keys, qtiles;  // chunk_keys: multiple of 128 (tree mode)
   float* part_o;          // [items][32*hd] partial outputs (tree mode, n_chunks > 1)
   float* part_ml;         // [items][32][2]

@@ -331,6 +331,58 @@ def test_batch2_ragged_decode(setup):
             assert not decided(rows[bad]), (b, bad)
 
 
+def test_stale_cache_slots_never_read(setup):
+    """KV slots at or past a sequence's committed length may hold any bits
+    (never written, rejected tree nodes, or whatever the caller left there).
+    Every such slot of both caches is filled with NaN and infinity patterns
+    before each cycle of a ragged batch-of-2 decode; the tokens must still
+    be the plain greedy decode's.  Catch-up padding of the shorter sequence
+    and the last partial key block of every attention pass are covered."""
+    from paper_2505_14260_amd.msd import msd_seq_len
+    wl, eng, m, prompt = setup
+    print("case: tiny batch of 2 with NaN/inf bits past every length", flush=True)
+    tokens, is_visual, visual = prompt
+    cut = wl.n_visual + 9
+    p1 = (tokens[:cut], is_visual[:cut], visual)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    tk, tv, dk, dv = eng.kv_views()
+    bits = (-1, 0x7F80, -128)       # NaN, +inf, -inf as bf16 bit patterns
+
+    def poison(b, t_from, d_from, pat):
+        for a, lo in ((tk, t_from), (dk, d_from)):
+            a[:, b, :, lo:, :] = pat
+        for a, lo in ((tv, t_from), (dv, d_from)):
+            a[:, b, :, :, lo:] = pat
+        torch.cuda.synchronize()        # the library runs on its own stream
+
+    outs = [[eng.prefill(0, *prompt)], [eng.prefill(1, *p1)]]
+    for b in range(2):
+        L = msd_seq_len(eng.ctx, b)
+        poison(b, L, L, bits[b])
+    trees = eng.new_trees(2)
+    n_new = 24
+    cycle = 0
+    while min(len(o) for o in outs) < n_new:
+        eng.draft_tree([0, 1], spec, trees)
+        amax, _ = eng.verify([0, 1], trees, T)
+        em, _ = eng.accept([0, 1], trees, T, amax)
+        cycle += 1
+        for b in range(2):
+            outs[b].extend(int(t) for t in em[b])
+            L = msd_seq_len(eng.ctx, b)
+            # target slots past L and draft slots past the catch-up start
+            poison(b, L, L - len(em[b]), bits[(b + cycle) % 3])
+    torch.cuda.synchronize()
+    for b, p in enumerate((prompt, p1)):
+        ref, rows = O.greedy_generate(m, p, n_new, return_logits=True)
+        got = outs[b][:n_new]
+        bad = next((i for i in range(n_new) if got[i] != ref[i]), None)
+        print(f"seq {b}: {bad if bad is not None else n_new}/{n_new} equal")
+        if bad is not None:
+            assert not decided(rows[bad]), (b, bad)
+
+
 def test_capacity_limits(setup):
     wl, eng, m, prompt = setup
     from paper_2505_14260_amd import msd as B
