@@ -39,9 +39,11 @@ namespace {
 constexpr int KB = 128;       // K elements per block
 constexpr int TILE_ROWS = 64;  // 4 waves x 16 rows
 constexpr int BLOCK_ELEMS = TILE_ROWS * KB;
-// 128-column blocks per K chunk.  Longer chunks (fewer partials) run out of
-// registers for the ring and serialize its loads.
-constexpr int NKB_CHUNK = 4;
+// 128-column blocks per K chunk: 8 for up to 32 rows (X chunk 64 or 128 KB
+// of LDS), 4 for 64 rows.  Longer chunks mean fewer partials to write and
+// re-read; the ring depth stays at RING blocks either way.
+constexpr int RING = 4;
+__host__ __device__ constexpr int chunk_blocks(int MT) { return MT <= 2 ? 8 : 4; }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 MSD_DEV uint4 load_stream(const uint16_t* p) {
@@ -61,7 +63,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int UPR = NKB * KB / 8;  // 16-byte units per LDS row
   constexpr int LO = MT * 16 * UPR;  // offset of the lo halves
   constexpr int NX = MT * 16 * UPR / 256;
-  constexpr int XB = NX < 8 ? NX : 8;  // staging batch (loads in flight)
+  constexpr int XB = NX < 16 ? NX : 16;  // staging batch (loads in flight)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
   const int S = a.S, G = a.G, K = a.K, M = a.M, nkt = a.nkt, n_tiles = a.n_tiles;
@@ -74,9 +76,9 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const uint16_t* const W2 = a.W2;
   const size_t lane_off = (size_t)wave * (BLOCK_ELEMS / 4) + lane * 8;
   const size_t tstride = (size_t)nkt * BLOCK_ELEMS;
-  int kbs[NKB];  // the chunk's blocks (the last chunk repeats block nkt-1; X is zero there)
-#pragma unroll
-  for (int p = 0; p < NKB; ++p) kbs[p] = min(kb0 + p, nkt - 1);
+  // the chunk's blocks; past K (last chunk) the loads read the zero block,
+  // X being zero there too
+  const int nvb = min(NKB, nkt - kb0);
 
   // X[0:MT*16, k0:k0+NKB*128) into LDS; rows past M and columns past K are
   // zero.  The first batch's loads are issued before the weight ring's, so
@@ -96,14 +98,18 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     xh[q] = ok ? h : make_uint4(0, 0, 0, 0);
     xl[q] = ok ? l : make_uint4(0, 0, 0, 0);
   }
+  const uint16_t* const dummy = a.dummy + lane_off;
   uint4 ring[P][NW][4];
 #pragma unroll
   for (int p = 0; p < P; ++p) {
-    const size_t o = (size_t)gi * tstride + (size_t)kbs[p] * BLOCK_ELEMS + lane_off;
+    const size_t o = (size_t)gi * tstride + (size_t)(kb0 + p) * BLOCK_ELEMS + lane_off;
+    const bool in = p < nvb;
+    const uint16_t* const b1 = in ? W + o : dummy;
+    const uint16_t* const b2 = in ? W2 + o : dummy;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      ring[p][0][c] = load_stream(W + o + c * 512);
-      if (NW == 2) ring[p][NW - 1][c] = load_stream(W2 + o + c * 512);
+      ring[p][0][c] = load_stream(b1 + c * 512);
+      if (NW == 2) ring[p][NW - 1][c] = load_stream(b2 + c * 512);
     }
   }
 #pragma unroll
@@ -136,57 +142,62 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const int ldp = a.ldp, off2 = a.off2;
   float* const part = a.part + (size_t)s * a.part_split;
   float* const sink = a.sink + lane * 4;
-  const uint16_t* const dummy = a.dummy;
   for (int j = 0; j < n_my; ++j) {
     const int tile = gi + j * G;
-    // the ring's refills for the next tile; after the last tile they read a
+    // the ring's refills for the next tile; after the last tile they read the
     // small zero block instead (cache-resident, not another weight chunk)
     const bool more = j + 1 < n_my;
-    const uint16_t* const wn = more ? W : dummy;
-    const uint16_t* const wn2 = more ? W2 : dummy;
-    const size_t tn_base = more ? (size_t)(tile + G) * tstride : 0;
+    const size_t t_base = (size_t)tile * tstride + (size_t)kb0 * BLOCK_ELEMS + lane_off;
+    const size_t tn_base = t_base + (size_t)G * tstride;
     f32x4 acc[NW][MT];
 #pragma unroll
     for (int w = 0; w < NW; ++w)
 #pragma unroll
       for (int t = 0; t < MT; ++t) acc[w][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // passes of P blocks over the chunk; ring slot r of pass pp holds block
+    // pp + r and is refilled with the block P places further
+#pragma unroll 1
+    for (int pp = 0; pp < NKB; pp += P) {
 #pragma unroll
-    for (int p = 0; p < NKB; ++p) {
-      uint4 fh[MT][4], fl[MT][4];
+      for (int r = 0; r < P; ++r) {
+        const int p = pp + r;
+        uint4 fh[MT][4], fl[MT][4];
 #pragma unroll
-      for (int t = 0; t < MT; ++t)
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int xi = xs_index(t * 16 + i, p * 16 + 4 * g + c, UPR);
+            fh[t][c] = xs[xi];
+            fl[t][c] = xs[LO + xi];
+          }
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const int xi = xs_index(t * 16 + i, p * 16 + 4 * g + c, UPR);
-          fh[t][c] = xs[xi];
-          fl[t][c] = xs[LO + xi];
+#pragma unroll
+          for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+              acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(ring[r][w][c]), as_bf16x8(fh[t][c]), acc[w][t], 0, 0, 0);
+#pragma unroll
+          for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+              acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(ring[r][w][c]), as_bf16x8(fl[t][c]), acc[w][t], 0, 0, 0);
         }
+        // refill: later in this tile, or in the next one
+        const int q = p + P;
+        const bool next = q >= NKB;
+        const int qb = next ? q - NKB : q;  // block of the chunk
+        const bool in = (!next || more) && qb < nvb;
+        const size_t o = (next ? tn_base : t_base) + (size_t)qb * BLOCK_ELEMS;
+        const uint16_t* const b1 = in ? W + o : dummy;
+        const uint16_t* const b2 = in ? W2 + o : dummy;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-#pragma unroll
-        for (int w = 0; w < NW; ++w)
-#pragma unroll
-          for (int t = 0; t < MT; ++t)
-            acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                as_bf16x8(ring[p % P][w][c]), as_bf16x8(fh[t][c]), acc[w][t], 0, 0, 0);
-#pragma unroll
-        for (int w = 0; w < NW; ++w)
-#pragma unroll
-          for (int t = 0; t < MT; ++t)
-            acc[w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                as_bf16x8(ring[p % P][w][c]), as_bf16x8(fl[t][c]), acc[w][t], 0, 0, 0);
-      }
-      // refill with the block P ahead: later in this tile, or in the next one
-      const int q = p + P;
-      const uint16_t* const b1 = q < NKB ? W : wn;
-      const uint16_t* const b2 = q < NKB ? W2 : wn2;
-      const size_t o =
-          q < NKB ? (size_t)tile * tstride + (size_t)kbs[q < NKB ? q : 0] * BLOCK_ELEMS
-                  : tn_base + (size_t)(more ? kbs[q < NKB ? 0 : q - NKB] : q - NKB) * BLOCK_ELEMS;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        ring[p % P][0][c] = load_stream(b1 + o + lane_off + c * 512);
-        if (NW == 2) ring[p % P][NW - 1][c] = load_stream(b2 + o + lane_off + c * 512);
+        for (int c = 0; c < 4; ++c) {
+          ring[r][0][c] = load_stream(b1 + c * 512);
+          if (NW == 2) ring[r][NW - 1][c] = load_stream(b2 + c * 512);
+        }
       }
     }
     // C layout of the 16x16 MFMA: lane holds column (lane & 15) = row m,
@@ -223,9 +234,10 @@ __global__ void k_pack(const uint16_t* src, int N, int K, int nkt, size_t units,
 
 // With timing events the launch carries them in its dispatch packet, so they
 // bracket the kernel's execution only.
-template <int MT, int NW, int NKB>
+template <int MT, int NW>
 void launch_mt(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
-  constexpr int P = 4;
+  constexpr int P = RING;
+  constexpr int NKB = chunk_blocks(MT);
   const size_t lds = (size_t)MT * 16 * NKB * KB * 4;
   if (sc.ev_start)
     hipExtLaunchKernelGGL((k_gemm<MT, NW, NKB, P>), grid, dim3(256), lds, st, sc.ev_start,
@@ -236,7 +248,7 @@ void launch_mt(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t 
 
 }  // namespace
 
-size_t gemm_dummy_elems() { return (size_t)NKB_CHUNK * BLOCK_ELEMS; }
+size_t gemm_dummy_elems() { return (size_t)BLOCK_ELEMS; }
 
 size_t packed_elems(int N, int K) {
   return (size_t)((N + TILE_ROWS - 1) / TILE_ROWS) * ((K + KB - 1) / KB) * BLOCK_ELEMS;
@@ -254,7 +266,7 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
   const int mc = M < 64 ? M : 64;
   p.MT = mc <= 16 ? 1 : (mc <= 32 ? 2 : 4);
   p.nkt = (K + KB - 1) / KB;
-  p.nkb = NKB_CHUNK;
+  p.nkb = chunk_blocks(p.MT);
   p.S = (p.nkt + p.nkb - 1) / p.nkb;
   p.n_tiles = (N + TILE_ROWS - 1) / TILE_ROWS;
   // workgroups per chunk: about target_wgs in total, every workgroup of a
@@ -299,13 +311,13 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
   a.dummy = dummy;
   const dim3 grid(pl.S * pl.G);
   if (nw == 2) {
-    if (pl.MT == 1) launch_mt<1, 2, NKB_CHUNK>(grid, a, sc, st);
-    else if (pl.MT == 2) launch_mt<2, 2, NKB_CHUNK>(grid, a, sc, st);
-    else launch_mt<4, 2, NKB_CHUNK>(grid, a, sc, st);
+    if (pl.MT == 1) launch_mt<1, 2>(grid, a, sc, st);
+    else if (pl.MT == 2) launch_mt<2, 2>(grid, a, sc, st);
+    else launch_mt<4, 2>(grid, a, sc, st);
   } else {
-    if (pl.MT == 1) launch_mt<1, 1, NKB_CHUNK>(grid, a, sc, st);
-    else if (pl.MT == 2) launch_mt<2, 1, NKB_CHUNK>(grid, a, sc, st);
-    else launch_mt<4, 1, NKB_CHUNK>(grid, a, sc, st);
+    if (pl.MT == 1) launch_mt<1, 1>(grid, a, sc, st);
+    else if (pl.MT == 2) launch_mt<2, 1>(grid, a, sc, st);
+    else launch_mt<4, 1>(grid, a, sc, st);
   }
 }
 
