@@ -52,87 +52,126 @@ MSD_DEV void load_k(uint4 (&kf)[HD / 16], const uint16_t* kbase, int kb, int S) 
 }
 
 // V^T columns of the block for the O^T product (A operand): eight
-// consecutive keys per 16-byte load (S is a multiple of 8).  Keys at or past
-// k_valid read as zero: their probabilities are zero, but the slots may hold
-// any bits (never written, or left by the caller), and 0 * NaN would poison
-// the sum.  The clamp keeps the address inside the cache; a clamped load
-// only ever covers keys at or past S >= k_valid, which the mask zeroes.
+// consecutive keys per 16-byte load (S is a multiple of 8).  The clamp keeps
+// the address inside the cache; a clamped load only ever covers keys at or
+// past S, which mask_v zeroes (S >= k_valid).
 template <int HD>
-MSD_DEV void load_v(uint4 (&vf)[HD / 32][2], const uint16_t* vbase, int S, int kb, int k_valid) {
+MSD_DEV void load_v(uint4 (&vf)[HD / 32][2], const uint16_t* vbase, int S, int kb) {
   const int lane = threadIdx.x & 63;
   const int i = lane & 31, h = lane >> 5;
-  int k0[2];
-  uint32_t keep[2][4];  // per 32-bit word: keys 2e (low half) and 2e+1 (high half)
-#pragma unroll
-  for (int pk = 0; pk < 2; ++pk) {
-    const int kk = kb + 16 * pk + 8 * h;
-    const int nv = k_valid - kk;
-    k0[pk] = min(kk, S - 8);
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      keep[pk][e] = (2 * e + 1 < nv) ? 0xFFFFFFFFu : ((2 * e < nv) ? 0x0000FFFFu : 0u);
-  }
 #pragma unroll
   for (int dt = 0; dt < HD / 32; ++dt) {
     const uint16_t* vp = vbase + (size_t)(dt * 32 + i) * S;
 #pragma unroll
-    for (int pk = 0; pk < 2; ++pk) {
-      const uint4 r = *reinterpret_cast<const uint4*>(vp + k0[pk]);
-      vf[dt][pk] = make_uint4(r.x & keep[pk][0], r.y & keep[pk][1], r.z & keep[pk][2],
-                              r.w & keep[pk][3]);
-    }
+    for (int pk = 0; pk < 2; ++pk)
+      vf[dt][pk] = *reinterpret_cast<const uint4*>(vp + min(kb + 16 * pk + 8 * h, S - 8));
   }
 }
 
+// The loaded V^T columns with keys at or past k_valid set to zero: their
+// probabilities are zero, but the slots may hold any bits (never written, or
+// left by the caller), and 0 * NaN would poison the sum.  Applied at the
+// point of use so that the loads stay in flight until then.
+template <int HD>
+MSD_DEV void mask_v(uint4 (&vm)[HD / 32][2], const uint4 (&vf)[HD / 32][2], int kb, int k_valid) {
+  const int h = (threadIdx.x & 63) >> 5;
+#pragma unroll
+  for (int pk = 0; pk < 2; ++pk) {
+    const int nv = k_valid - (kb + 16 * pk + 8 * h);
+    uint32_t keep[4];  // per 32-bit word: keys 2e (low half) and 2e+1 (high half)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      keep[e] = (2 * e + 1 < nv) ? 0xFFFFFFFFu : ((2 * e < nv) ? 0x0000FFFFu : 0u);
+#pragma unroll
+    for (int dt = 0; dt < HD / 32; ++dt)
+      vm[dt][pk] = make_uint4(vf[dt][pk].x & keep[0], vf[dt][pk].y & keep[1],
+                              vf[dt][pk].z & keep[2], vf[dt][pk].w & keep[3]);
+  }
+}
+
+// Two floats as packed bfloat16, rounded to nearest even (one
+// v_cvt_pk_bf16_f32 on gfx950).
+MSD_DEV uint32_t pack_bf16(float a, float b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)a) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)b) << 16);
+}
+
+// The running maximum that scales a column's exponentials is raised only
+// when a block's maximum exceeds it by more than this (natural-log units),
+// so most blocks skip rescaling the output; the exponentials then stay below
+// e^8, far inside float and bfloat16 range.  Any reference gives the same
+// normalised result.
+constexpr float RESCALE_SLACK = 8.f;
+
 // Online-softmax accumulation of keys [k_begin, k_end) (k_begin a multiple
-// of 32) for the 32 query columns of the wave; vis(key) says whether the
-// lane's query sees the key.  Keys at or past k_valid (>= k_end) are never
-// taken from the cache.  The next block's K rows and the current block's V
-// columns are loaded while the scores are computed.
-template <int HD, typename Vis>
-MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qh)[HD / 16],
-                          const bf16x8 (&ql)[HD / 16],
-                          const uint16_t* kbase, const uint16_t* vbase, int S,
-                          int k_begin, int k_end, int k_valid, float scale, Vis vis) {
+// of 32) for the 32 query columns of the wave; qf(c, lo) returns the lane's
+// bf16 hi (lo = 0) or lo (lo = 1) query fragment of MFMA step c, and
+// vis(key) says whether the lane's query sees the key.  Keys at or past
+// k_valid (>= k_end) are never taken from the cache.  Each block's K rows are
+// reloaded with the next block as soon as the score MFMAs have consumed them,
+// the V columns as soon as the output MFMAs have; the last block reloads
+// itself (a cache hit) so the loop has no branch around its loads.  kf and
+// vf arrive holding the block at k_begin (attend_prefetch), so the caller can
+// issue those loads before its own set-up.
+template <int HD>
+MSD_DEV void attend_prefetch(uint4 (&kf)[HD / 16], uint4 (&vf)[HD / 32][2],
+                             const uint16_t* kbase, const uint16_t* vbase, int S, int k_begin) {
+  load_k<HD>(kf, kbase, k_begin, S);
+  load_v<HD>(vf, vbase, S, k_begin);
+}
+
+template <int HD, typename QF, typename Vis>
+MSD_DEV void attend_range(AttnState<HD>& st, QF qf, uint4 (&kf)[HD / 16],
+                          uint4 (&vf)[HD / 32][2], const uint16_t* kbase,
+                          const uint16_t* vbase, int S, int k_begin, int k_end, int k_valid,
+                          float scale, Vis vis) {
   const int lane = threadIdx.x & 63;
   const int h = lane >> 5;
   if (k_begin >= k_end) return;
-  uint4 kf[HD / 16];
-  load_k<HD>(kf, kbase, k_begin, S);
+  const int k_last = k_begin + ((k_end - 1 - k_begin) & ~31);
+  bool fresh = true;  // the output state is still all zero
   for (int kb = k_begin; kb < k_end; kb += 32) {
-    uint4 vf[HD / 32][2];
-    load_v<HD>(vf, vbase, S, kb, k_valid);
+    const int nb = min(kb + 32, k_last);
     // ---- S^T tile: rows = keys, columns = query rows
     f32x16 s = {};
-    f32x16 s2 = {};
 #pragma unroll
     for (int c = 0; c < HD / 16; ++c) {
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), qh[c], s, 0, 0, 0);
-      s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), ql[c], s2, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), qf(c, 0), s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c]), qf(c, 1), s, 0, 0, 0);
     }
-    s += s2;
-    load_k<HD>(kf, kbase, kb + 32, S);  // the next block (past the end: unused)
+    load_k<HD>(kf, kbase, nb, S);
     float bm = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int key = kb + perm_key(8 * (r >> 2) + 4 * h + (r & 3));
-      const bool ok = key < k_end && vis(key);
+      const bool ok = (key < k_end) & vis(key);
       s[r] = ok ? s[r] * scale : -INFINITY;
       bm = fmaxf(bm, s[r]);
     }
     bm = wave_xor32_max(bm);
-    const float m_new = fmaxf(st.m, bm);
+    const bool raise = bm > st.m + RESCALE_SLACK;  // also when st.m is still -inf
+    if (__any(raise)) {
+      const float m_new = raise ? bm : st.m;
+      if (!fresh) {
+        const float alpha = (st.m == -INFINITY) ? 0.f : __expf(st.m - m_new);
+        st.l *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
+      }
+      st.m = m_new;
+    }
+    fresh = false;
     float p[16];
     float rs = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      p[r] = (m_new == -INFINITY) ? 0.f : __expf(s[r] - m_new);
+      p[r] = (st.m == -INFINITY) ? 0.f : __expf(s[r] - st.m);
       rs += p[r];
     }
-    rs = wave_xor32_sum(rs);
-    const float alpha = (st.m == -INFINITY) ? 0.f : __expf(st.m - m_new);
-    st.l = st.l * alpha + rs;
-    st.m = m_new;
+    st.l += wave_xor32_sum(rs);
+    // P as bf16 hi + lo pairs
     uint4 pb[2], pl[2];
 #pragma unroll
     for (int pk = 0; pk < 2; ++pk) {
@@ -140,23 +179,23 @@ MSD_DEV void attend_range(AttnState<HD>& st, const bf16x8 (&qh)[HD / 16],
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float p0 = p[pk * 8 + 2 * e], p1 = p[pk * 8 + 2 * e + 1];
-        const uint16_t h0 = f2bf(p0), h1 = f2bf(p1);
-        w[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        wl[e] = (uint32_t)f2bf(p0 - bf2f(h0)) | ((uint32_t)f2bf(p1 - bf2f(h1)) << 16);
+        w[e] = pack_bf16(p0, p1);
+        wl[e] = pack_bf16(p0 - __uint_as_float(w[e] << 16), p1 - __uint_as_float(w[e] & 0xFFFF0000u));
       }
       pb[pk] = make_uint4(w[0], w[1], w[2], w[3]);
       pl[pk] = make_uint4(wl[0], wl[1], wl[2], wl[3]);
     }
     // ---- O^T += V^T P^T
+    uint4 vm[HD / 32][2];
+    mask_v<HD>(vm, vf, kb, k_valid);
+    load_v<HD>(vf, vbase, S, nb);
 #pragma unroll
     for (int dt = 0; dt < HD / 32; ++dt) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
-#pragma unroll
       for (int pk = 0; pk < 2; ++pk) {
-        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[dt][pk]), as_bf16x8(pb[pk]),
+        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vm[dt][pk]), as_bf16x8(pb[pk]),
                                                            st.o[dt], 0, 0, 0);
-        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[dt][pk]), as_bf16x8(pl[pk]),
+        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vm[dt][pk]), as_bf16x8(pl[pk]),
                                                            st.o[dt], 0, 0, 0);
       }
     }
@@ -207,6 +246,28 @@ MSD_DEV int dim_of(int e) {
   return dt * 32 + 8 * (r >> 2) + 4 * (L >> 5) + (r & 3);
 }
 
+// Inverse of dim_of: the state element of query column j and head dim d.
+template <int HD>
+MSD_DEV int state_index(int j, int d) {
+  const int dt = d >> 5, w = d & 31;
+  const int r = 4 * (w >> 3) + (w & 3), hh = (w >> 2) & 1;
+  return (dt * 16 + r) * 64 + j + 32 * hh;
+}
+
+// Eight consecutive values of a split row: hi halves at row[0..8), lo halves
+// at row[lo..lo+8), one 16-byte store each (row 16-byte aligned).
+MSD_DEV void store_split8(uint16_t* row, int lo, const float (&v)[8]) {
+  uint32_t hw[4], lw[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    hw[e] = pack_bf16(v[2 * e], v[2 * e + 1]);
+    lw[e] = pack_bf16(v[2 * e] - __uint_as_float(hw[e] << 16),
+                      v[2 * e + 1] - __uint_as_float(hw[e] & 0xFFFF0000u));
+  }
+  *reinterpret_cast<uint4*>(row) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+  *reinterpret_cast<uint4*>(row + lo) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+}
+
 // Query column j of tile qt -> (node, head); node >= nq marks padding.
 MSD_DEV void column_to_row(int qt, int j, int G, int g, int& node, int& head) {
   const int qr = qt * 32 + j;
@@ -214,11 +275,40 @@ MSD_DEV void column_to_row(int qt, int j, int G, int g, int& node, int& head) {
   head = g * G + (qr - node * G);
 }
 
+// Query fragments of the causal kernel, held in registers.
 template <int HD>
-__global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
+struct QRegs {
+  const bf16x8* h;
+  const bf16x8* l;
+  MSD_DEV bf16x8 operator()(int c, int lo) const { return lo ? l[c] : h[c]; }
+};
+
+// Query fragments of the tree kernel, read from the workgroup's LDS copy:
+// column j holds its hi then lo halves in 16-byte units, unit u at
+// j * QU + (u ^ (j & 15)) so that 16 lanes reading the same unit of 16
+// different columns hit different banks.
+template <int HD>
+struct QShared {
+  static constexpr int QU = HD / 4;  // 16-byte units per column
+  const uint4* col;                  // the lane's column
+  int sw;                            // j & 15
+  int h;                             // lane / 32
+  MSD_DEV bf16x8 operator()(int c, int lo) const {
+    const int u = lo * (HD / 8) + (HD / 16) * h + c;
+    return as_bf16x8(col[u ^ sw]);
+  }
+};
+
+template <int HD>
+__global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
+  constexpr int NWV = TREE_WAVES;
   constexpr int E = 32 * HD;                 // state elements of one wave
-  __shared__ float so[4 * E];
-  __shared__ float sml[4][32][2];
+  constexpr int QU = QShared<HD>::QU;
+  __shared__ uint4 sq[32 * QU];
+  __shared__ float so[NWV * E];
+  __shared__ float sml[NWV][32][2];
+  __shared__ float wgt[NWV][32];
+  __shared__ float colm[32][2];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int t = blockIdx.x;
   const int c = t % a.n_chunks; t /= a.n_chunks;
@@ -229,25 +319,37 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
   const int P = a.prefix[sidx];
   const int Ltot = a.keys[sidx];
   const int G = a.H / a.KV;
-  int node, head;
-  column_to_row(qt, lane & 31, G, g, node, head);
-  const bool valid = node < a.nq;
-  if (!valid) { node = 0; head = g * G; }
   const int HH = a.H * HD;
-  bf16x8 qh[HD / 16], ql[HD / 16];
-  load_q<HD>(qh, ql, a.q + (size_t)(sidx * a.nq + node) * 2 * HH + (size_t)head * HD, HH);
-  const uint64_t msk = a.mask[sidx * a.nq + node];
   const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
   const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
-  AttnState<HD> st;
-  init_state<HD>(st);
-  const int wk = a.chunk_keys / 4;
+  const int wk = a.chunk_keys / NWV;
   const int k0 = c * a.chunk_keys + w * wk;
   const int k1 = min(k0 + wk, Ltot);
-  attend_range<HD>(st, qh, ql, kbase, vbase, a.S, k0, k1, Ltot, a.scale, [&](int key) {
-    return key < P || ((msk >> (key - P)) & 1ull);
+  uint4 kf[HD / 16], vf[HD / 32][2];
+  attend_prefetch<HD>(kf, vf, kbase, vbase, a.S, k0);
+  // the tile's 32 query columns (hi and lo halves) into LDS; padding
+  // columns copy node 0 (their results are dropped)
+  for (int u = threadIdx.x; u < 32 * QU; u += 64 * NWV) {
+    const int j = u / QU, v = u - j * QU;
+    int node, head;
+    column_to_row(qt, j, G, g, node, head);
+    if (node >= a.nq) { node = 0; head = g * G; }
+    const int half = v / (HD / 8), k8 = v - half * (HD / 8);
+    sq[j * QU + (v ^ (j & 15))] = *reinterpret_cast<const uint4*>(
+        a.q + (size_t)(sidx * a.nq + node) * 2 * HH + (size_t)half * HH + (size_t)head * HD + 8 * k8);
+  }
+  int node, head;
+  column_to_row(qt, lane & 31, G, g, node, head);
+  if (node >= a.nq) node = 0;
+  const uint64_t msk = a.mask[sidx * a.nq + node];
+  AttnState<HD> st;
+  init_state<HD>(st);
+  __syncthreads();
+  const QShared<HD> qf{sq + (lane & 31) * QU, lane & 15, lane >> 5};
+  attend_range<HD>(st, qf, kf, vf, kbase, vbase, a.S, k0, k1, Ltot, a.scale, [&](int key) {
+    return (key < P) | (((msk >> ((key - P) & 63)) & 1ull) != 0);
   });
-  // merge the 4 waves' states
+  // merge the waves' states
 #pragma unroll
   for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
@@ -257,17 +359,15 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
     sml[w][lane][1] = st.l;
   }
   __syncthreads();
-  // per-column merge weights of the 4 waves: wgt[q][j] = exp(m_q - M_j)
-  __shared__ float wgt[4][32];
-  __shared__ float colm[32][2];
+  // per-column merge weights: wgt[q][j] = exp(m_q - M_j)
   if (threadIdx.x < 32) {
     const int j = threadIdx.x;
     float M = -INFINITY;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) M = fmaxf(M, sml[q][j][0]);
+    for (int q = 0; q < NWV; ++q) M = fmaxf(M, sml[q][j][0]);
     float l = 0.f;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < NWV; ++q) {
       const float mq = sml[q][j][0];
       const float wq = (M == -INFINITY || mq == -INFINITY) ? 0.f : __expf(mq - M);
       wgt[q][j] = wq;
@@ -277,26 +377,46 @@ __global__ __launch_bounds__(256) void k_tree_attn(AttnArgs a) {
     colm[j][1] = l;
   }
   __syncthreads();
-  const size_t item = blockIdx.x;
-  for (int e = threadIdx.x; e < E; e += 256) {
-    const int j = e & 31;
-    float o = 0.f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) o += wgt[q][j] * so[q * E + e];
-    const float M = colm[j][0], l = colm[j][1];
-    if (a.n_chunks == 1) {
+  if (a.n_chunks == 1) {
+    // thread -> (query column j, 8 consecutive dims): one 16-byte store each
+    // for the hi and lo halves of the output row
+    for (int u = threadIdx.x; u < 32 * (HD / 8); u += 64 * NWV) {
+      const int j = u & 31, d0 = 8 * (u >> 5);
       int nd, hd_;
       column_to_row(qt, j, G, g, nd, hd_);
-      if (nd < a.nq)
-        put_split(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH, HH, hd_ * HD + dim_of<HD>(e),
-                  l > 0.f ? o / l : 0.f);
-    } else {
-      a.part_o[item * E + e] = o;
-      if (e < 32) {
-        a.part_ml[item * 64 + 2 * e] = M;
-        a.part_ml[item * 64 + 2 * e + 1] = l;
+      if (nd >= a.nq) continue;
+      const float l = colm[j][1];
+      const float inv = l > 0.f ? 1.f / l : 0.f;
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int e = state_index<HD>(j, d0 + i);
+        float o = 0.f;
+#pragma unroll
+        for (int q = 0; q < NWV; ++q) o += wgt[q][j] * so[q * E + e];
+        v[i] = o * inv;
       }
+      store_split8(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH + (size_t)hd_ * HD + d0, HH, v);
     }
+    return;
+  }
+  const size_t item = blockIdx.x;
+  for (int e = 4 * threadIdx.x; e < E; e += 4 * 64 * NWV) {
+    const int j = e & 31;  // columns j .. j+3 (consecutive lanes of one register)
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int q = 0; q < NWV; ++q) {
+      const float4 x = *reinterpret_cast<const float4*>(so + q * E + e);
+      o.x += wgt[q][j] * x.x;
+      o.y += wgt[q][j + 1] * x.y;
+      o.z += wgt[q][j + 2] * x.z;
+      o.w += wgt[q][j + 3] * x.w;
+    }
+    *reinterpret_cast<float4*>(a.part_o + item * E + e) = o;
+  }
+  if (threadIdx.x < 32) {
+    a.part_ml[item * 64 + 2 * threadIdx.x] = colm[threadIdx.x][0];
+    a.part_ml[item * 64 + 2 * threadIdx.x + 1] = colm[threadIdx.x][1];
   }
 }
 
@@ -307,7 +427,7 @@ template <int HD>
 __global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
   constexpr int E = 32 * HD;
   constexpr int SL = E / (HD / 32);          // elements of one dim tile
-  __shared__ float wgt[64][32];              // chunk weights per column
+  __shared__ float wgt[ATT_MAX_CHUNKS][32];  // chunk weights per column
   __shared__ float inv_den[32];
   const int dt = blockIdx.x % (HD / 32);
   int t = blockIdx.x / (HD / 32);
@@ -383,7 +503,9 @@ __global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
   const int last = min(qt * 32 + 32, a.nq);
   const int k1 = P + last;
   const int my_last = P + node;
-  attend_range<HD>(st, qh, ql, kbase, vbase, a.S, 0, k1, k1, a.scale,
+  uint4 kf[HD / 16], vf[HD / 32][2];
+  attend_prefetch<HD>(kf, vf, kbase, vbase, a.S, 0);
+  attend_range<HD>(st, QRegs<HD>{qh, ql}, kf, vf, kbase, vbase, a.S, 0, k1, k1, a.scale,
                    [&](int key) { return key <= my_last; });
   store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * 2 * a.H * HD + (size_t)head * HD,
                   a.H * HD, valid);
@@ -399,11 +521,11 @@ void launch_tree_attention(AttnArgs a, hipStream_t st) {
   const int items = a.n_seq * a.KV * a.qtiles;
   dim3 grid(items * a.n_chunks);
   if (a.hd == 128) {
-    hipLaunchKernelGGL(k_tree_attn<128>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_tree_attn<128>, grid, dim3(64 * TREE_WAVES), 0, st, a);
     if (a.n_chunks > 1)
       hipLaunchKernelGGL(k_tree_combine<128>, dim3(items * 4), dim3(256), 0, st, a);
   } else {
-    hipLaunchKernelGGL(k_tree_attn<64>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_tree_attn<64>, grid, dim3(64 * TREE_WAVES), 0, st, a);
     if (a.n_chunks > 1)
       hipLaunchKernelGGL(k_tree_combine<64>, dim3(items * 2), dim3(256), 0, st, a);
   }

@@ -95,7 +95,8 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
   p.ld_qkv = (m.n_heads + 2 * m.n_kv_heads) * m.head_dim;
   const int G = m.n_heads / m.n_kv_heads;
   const int qtiles = (MSD_MAX_TREE * G + 31) / 32;
-  p.attn_floats = attn_partial_floats(lim.max_batch, m.n_kv_heads, qtiles, 64, m.head_dim);
+  p.attn_floats =
+      attn_partial_floats(lim.max_batch, m.n_kv_heads, qtiles, ATT_MAX_CHUNKS, m.head_dim);
   // GEMM partials of one 64-row launch, for the largest weight of the model
   const int mm = std::min(64, p.rows_max);
   const int d = m.d_model, F = m.ffn_dim, hh = m.n_heads * m.head_dim;
@@ -426,16 +427,21 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     } else {
       const int G = H / KV;
       a.qtiles = (nq * G + 31) / 32;
-      // key chunks (multiples of 128 keys, 32 per wave of a workgroup):
-      // about two workgroups per CU over the whole launch, at most 64 chunks
+      // key chunks: each of a workgroup's TREE_WAVES waves takes
+      // chunk_keys / TREE_WAVES keys (a multiple of 32); enough chunks for
+      // about 192 workgroups while every wave keeps at least one block (a
+      // wave hides little latency behind its own blocks, so spreading the
+      // keys over more CUs pays until the combine pass dominates)
+      const int span = 32 * TREE_WAVES;
       const int base_items = n_seq * KV * a.qtiles;
-      int chunks = std::max(1, 512 / std::max(1, base_items));
+      const int max_chunks = std::max(1, (max_ltot + span - 1) / span);
+      const int chunks = std::min(max_chunks, std::max(1, (192 + base_items - 1) / base_items));
       int ck = (max_ltot + chunks - 1) / chunks;
-      ck = std::max(128, (ck + 127) / 128 * 128);
-      while ((max_ltot + ck - 1) / ck > 64 ||
+      ck = (ck + span - 1) / span * span;
+      while ((max_ltot + ck - 1) / ck > ATT_MAX_CHUNKS ||
              attn_partial_floats(n_seq, KV, a.qtiles, (max_ltot + ck - 1) / ck, hd) >
                  c->plan.attn_floats)
-        ck += 128;
+        ck += span;
       a.chunk_keys = ck;
       a.n_chunks = (max_ltot + ck - 1) / ck;
       launch_tree_attention(a, c->st);

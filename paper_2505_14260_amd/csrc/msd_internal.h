@@ -97,6 +97,8 @@ struct RowNorm {
 
 // ----------------------------------------------------------- attention ----
 constexpr int ATT_MAX_SEQ = 8;
+constexpr int TREE_WAVES = 8;  // waves per tree-attention workgroup (32 keys each per block)
+constexpr int ATT_MAX_CHUNKS = 64;  // key chunks per (sequence, kv head, query tile)
 struct AttnArgs {
   const uint16_t* q;      // [n_seq*nq] split rows of H*hd, rotated
   const uint16_t* kc;     // layer K cache  [B][KV][S][hd]
