@@ -244,7 +244,7 @@ def main():
             "batch": 1, "draft_fc_init": wl.draft_fc_mode,
         },
         "roofline": {
-            "kernel": "k_gemm<2, 2, 4, 4> (verify-step gate+up projection, M=27)",
+            "kernel": "k_gemm<2, 2, 8, 4> (verify-step gate+up projection, M=27)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
