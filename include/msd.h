@@ -51,7 +51,7 @@ typedef struct msd_model_desc {
   int32_t n_kv_heads;  /* key/value heads (n_heads % n_kv_heads == 0) */
   int32_t head_dim;    /* must be 128 or 64 */
   int32_t ffn_dim;
-  int32_t vocab;       /* at least 16 (the widest top-k) */
+  int32_t vocab;       /* 16 .. 262144 */
   float rope_theta;
   float norm_eps;
 } msd_model_desc;

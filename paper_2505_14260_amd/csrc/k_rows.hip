@@ -219,7 +219,9 @@ __global__ __launch_bounds__(256) void k_fc_input(const uint16_t* h, const float
 // Per-row top-k over the vocabulary (value descending, then id ascending)
 // and the row's logsumexp, in two phases: every (row, slice) block reduces a
 // slice of the vocabulary to its own top-k and (max, sum of exp) pair; one
-// block per row then merges the slices in slice order.
+// block per row then merges the slices (logsumexp in slice order).  The
+// order is total, so the result does not depend on how candidates are
+// partitioned.
 constexpr int TOPK_MAX = 16;
 constexpr int TOPK_SLICE = 2048;
 
@@ -227,77 +229,95 @@ MSD_DEV bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
-// Block-wide selection of the k best (value, id) pairs offered by each
-// thread's sorted local list (lv, li of length n).
-MSD_DEV void block_select(const float* lv, const int* li, int n, int k, float* sv, int* si,
-                          float* out_v, int* out_i) {
-  int head = 0;
-  for (int q = 0; q < k; ++q) {
-    sv[threadIdx.x] = (head < n) ? lv[head] : -INFINITY;
-    si[threadIdx.x] = (head < n) ? li[head] : 0x7FFFFFFF;
-    __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-      if (threadIdx.x < s) {
-        const float vb = sv[threadIdx.x + s];
-        const int ib = si[threadIdx.x + s];
-        if (better(vb, ib, sv[threadIdx.x], si[threadIdx.x])) {
-          sv[threadIdx.x] = vb;
-          si[threadIdx.x] = ib;
-        }
-      }
-      __syncthreads();
-    }
-    const int win = si[0];
-    const float wv = sv[0];
-    __syncthreads();
-    if (head < n && li[head] == win) ++head;
-    if (threadIdx.x == 0) {
-      out_i[q] = win;
-      out_v[q] = wv;
+constexpr int TOPK_PER = TOPK_SLICE / 256;  // logits per thread of a slice block
+constexpr int TOPK_MERGE_PER = 8;           // slice candidates per thread of the merge
+constexpr int NO_ID = 0x7FFFFFFF;           // an absent candidate (ranks after every id)
+
+// The wave's best (value, id) over its lanes' offers.
+MSD_DEV void wave_best(float& v, int& id) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(v, o);
+    const int oi = __shfl_xor(id, o);
+    if (better(ov, oi, v, id)) {
+      v = ov;
+      id = oi;
     }
   }
 }
 
-MSD_DEV void insert_sorted(float* lv, int* li, int& n, int k, float val, int id) {
-  if (n < k || better(val, id, lv[k - 1], li[k - 1])) {
-    int p = (n < k) ? n : k - 1;
-    while (p > 0 && better(val, id, lv[p - 1], li[p - 1])) {
-      lv[p] = lv[p - 1];
-      li[p] = li[p - 1];
-      --p;
+// The k best of the wave's candidates (N per lane, ids unique apart from
+// NO_ID), best first: k rounds of a wave-wide argmax in which the owner of
+// the winner retires it.  Lane 0 writes them to out_v / out_i.
+template <int N>
+MSD_DEV void wave_select(const float (&cv)[N], const int (&ci)[N], int k, float* out_v,
+                         int* out_i) {
+  uint32_t taken = 0;
+  for (int q = 0; q < k; ++q) {
+    float bv = -INFINITY;
+    int bi = NO_ID, bj = -1;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      if (!((taken >> j) & 1u) && better(cv[j], ci[j], bv, bi)) {
+        bv = cv[j];
+        bi = ci[j];
+        bj = j;
+      }
     }
-    lv[p] = val;
-    li[p] = id;
-    if (n < k) ++n;
+    float wv = bv;
+    int wi = bi;
+    wave_best(wv, wi);
+    if (bj >= 0 && bi == wi) taken |= 1u << bj;
+    if ((threadIdx.x & 63) == 0) {
+      out_v[q] = wv;
+      out_i[q] = wi;
+    }
   }
+}
+
+// The k best of the 4 waves' lists (wv/wi[w][0..k)), selected by wave 0.
+MSD_DEV void block_merge(const float (*wv)[TOPK_MAX], const int (*wi)[TOPK_MAX], int k,
+                         float* out_v, int* out_i) {
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  float c[1] = {lane < 4 * k ? wv[lane / k][lane % k] : -INFINITY};
+  int ci[1] = {lane < 4 * k ? wi[lane / k][lane % k] : NO_ID};
+  wave_select<1>(c, ci, k, out_v, out_i);
 }
 
 __global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, int n_slices,
                                                     float* cand_v, int* cand_i, float2* stats,
                                                     float* logits_out) {
-  __shared__ float sv[256];
-  __shared__ int si[256];
+  __shared__ float wv[4][TOPK_MAX];
+  __shared__ int wi[4][TOPK_MAX];
   __shared__ float sm[4];
   __shared__ float ssum[4];
   const int row = blockIdx.x / n_slices;
   const int sl = blockIdx.x - row * n_slices;
-  const int v0 = sl * TOPK_SLICE, v1 = min(V, v0 + TOPK_SLICE);
-  float lv[TOPK_MAX];
-  int li[TOPK_MAX];
-  int n = 0;
+  const int v0 = sl * TOPK_SLICE;
+  float cv[TOPK_PER];
+  int ci[TOPK_PER];
   float mloc = -INFINITY, sloc = 0.f;
-  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
-    const float raw = part_sum(logits, row, v);
-    if (logits_out) logits_out[(size_t)row * V + v] = raw;
-    // a NaN ranks as -inf, so the selected ids are always vocabulary ids
-    const float val = (raw == raw) ? raw : -INFINITY;
-    if (val > mloc) {
-      sloc = sloc * __expf(mloc - val) + 1.f;
-      mloc = val;
-    } else if (val != -INFINITY) {
-      sloc += __expf(val - mloc);
+#pragma unroll
+  for (int e = 0; e < TOPK_PER; ++e) {
+    const int v = v0 + threadIdx.x + 256 * e;
+    float val = -INFINITY;
+    int id = NO_ID;
+    if (v < V) {
+      const float raw = part_sum(logits, row, v);
+      if (logits_out) logits_out[(size_t)row * V + v] = raw;
+      // a NaN ranks as -inf, so the selected ids are always vocabulary ids
+      val = (raw == raw) ? raw : -INFINITY;
+      id = v;
+      if (val > mloc) {
+        sloc = sloc * __expf(mloc - val) + 1.f;
+        mloc = val;
+      } else if (val != -INFINITY) {
+        sloc += __expf(val - mloc);
+      }
     }
-    insert_sorted(lv, li, n, k, val, v);
+    cv[e] = val;
+    ci[e] = id;
   }
   float mm = mloc;
   for (int o = 32; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
@@ -307,29 +327,40 @@ __global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, 
   const float part = (mloc == -INFINITY) ? 0.f : sloc * __expf(mloc - M);
   const float tot = block_sum_256(part, ssum);
   if (threadIdx.x == 0) stats[blockIdx.x] = make_float2(M, tot);
-  block_select(lv, li, n, k, sv, si, cand_v + (size_t)blockIdx.x * k,
-               cand_i + (size_t)blockIdx.x * k);
+  const int w = threadIdx.x >> 6;
+  wave_select<TOPK_PER>(cv, ci, k, wv[w], wi[w]);
+  __syncthreads();
+  block_merge(wv, wi, k, cand_v + (size_t)blockIdx.x * k, cand_i + (size_t)blockIdx.x * k);
 }
 
+// One block per row merges its slices' candidates (n_slices * k of them,
+// at most 256 * TOPK_MERGE_PER) and their logsumexp parts.
 __global__ __launch_bounds__(256) void k_topk_merge(int k, int n_slices, const float* cand_v,
                                                     const int* cand_i, const float2* stats,
                                                     int* out_idx, float* out_val, float* out_lse) {
-  __shared__ float sv[256];
-  __shared__ int si[256];
-  __shared__ float ov[TOPK_MAX];
-  __shared__ int oi[TOPK_MAX];
+  __shared__ float wv[4][TOPK_MAX];
+  __shared__ int wi[4][TOPK_MAX];
+  __shared__ float fv[TOPK_MAX];
+  __shared__ int fi[TOPK_MAX];
   const int row = blockIdx.x;
-  const size_t c0 = (size_t)row * n_slices * k;
-  float lv[TOPK_MAX];
-  int li[TOPK_MAX];
-  int n = 0;
-  for (int c = threadIdx.x; c < n_slices * k; c += 256)
-    insert_sorted(lv, li, n, k, cand_v[c0 + c], cand_i[c0 + c]);
-  block_select(lv, li, n, k, sv, si, ov, oi);
+  const int n = n_slices * k;
+  const size_t c0 = (size_t)row * n;
+  float cv[TOPK_MERGE_PER];
+  int ci[TOPK_MERGE_PER];
+#pragma unroll
+  for (int e = 0; e < TOPK_MERGE_PER; ++e) {
+    const int c = threadIdx.x + 256 * e;
+    cv[e] = c < n ? cand_v[c0 + c] : -INFINITY;
+    ci[e] = c < n ? cand_i[c0 + c] : NO_ID;
+  }
+  const int w = threadIdx.x >> 6;
+  wave_select<TOPK_MERGE_PER>(cv, ci, k, wv[w], wi[w]);
+  __syncthreads();
+  block_merge(wv, wi, k, fv, fi);
   __syncthreads();
   if (threadIdx.x < k) {
-    out_idx[(size_t)row * k + threadIdx.x] = oi[threadIdx.x];
-    if (out_val) out_val[(size_t)row * k + threadIdx.x] = ov[threadIdx.x];
+    out_idx[(size_t)row * k + threadIdx.x] = fi[threadIdx.x];
+    if (out_val) out_val[(size_t)row * k + threadIdx.x] = fv[threadIdx.x];
   }
   if (threadIdx.x == 0 && out_lse) {
     const float2* st = stats + (size_t)row * n_slices;

@@ -64,6 +64,7 @@ constexpr int MSD_MAX_BATCH_ARGS = ATT_MAX_SEQ;
 constexpr int PEND = MSD_MAX_TREE;      // pending draft rows per sequence
 constexpr int FEAT = MSD_MAX_TREE + 1;  // draft feature slots per sequence
 constexpr int TOPK = 16;
+constexpr int MAX_VOCAB = 262144;  // 128 top-k slices of 2048 logits
 constexpr int POOL = 1024;              // dynamic-tree candidates per sequence
 constexpr int STAGE_INTS = 1 << 16;
 // GEMM launch shape: about one workgroup per CU streams best (more
@@ -279,6 +280,7 @@ int check_desc(const msd_model_desc* m, const msd_limits* lim, msd_ctx* c) {
   if (m->n_layers <= 0 || m->d_model <= 0 || m->n_heads <= 0 || m->n_kv_heads <= 0 ||
       m->n_heads % m->n_kv_heads || m->ffn_dim <= 0 || m->vocab < TOPK)
     return fail(c, MSD_ERR_INVALID_ARG, "bad model shape");
+  if (m->vocab > MAX_VOCAB) return fail(c, MSD_ERR_INVALID_ARG, "vocabulary larger than 262144");
   if (m->head_dim != 128 && m->head_dim != 64)
     return fail(c, MSD_ERR_INVALID_ARG, "head_dim must be 64 or 128");
   if (m->d_model % 8 || m->ffn_dim % 8)
