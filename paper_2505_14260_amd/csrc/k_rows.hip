@@ -60,6 +60,33 @@ MSD_DEV float part_sum(const Parts& pt, int row, int col) {
   return v;
 }
 
+// The same for four consecutive elements (col a multiple of 4).
+MSD_DEV float4 part_sum4(const Parts& pt, int row, int col) {
+  const float* p = pt.p + (size_t)row * pt.ld + col;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+  for (int s = 0; s < pt.S; ++s) {
+    const float4 q = *reinterpret_cast<const float4*>(p + (size_t)s * pt.split);
+    v = make_float4(v.x + q.x, v.y + q.y, v.z + q.z, v.w + q.w);
+  }
+  return v;
+}
+
+// Four consecutive values of a split row (hi halves at row[k..], lo halves
+// at row[K + k..]; k a multiple of 4).
+MSD_DEV void put_split4(uint16_t* row, int K, int k, const float (&v)[4]) {
+  uint16_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    h[e] = f2bf(v[e]);
+    l[e] = f2bf(v[e] - bf2f(h[e]));
+  }
+  *reinterpret_cast<uint2*>(row + k) =
+      make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+  *reinterpret_cast<uint2*>(row + K + k) =
+      make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+}
+
 // 1 / sqrt(mean(x^2) + eps) of a row from its per-block sums of squares
 // (summed in block order); 1 when no sums are given.
 MSD_DEV float row_rstd(const RowNorm& rn, int row) {
@@ -154,25 +181,37 @@ __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, 
 // or x (RN_KEEP); then xg = x * g (the next GEMM's input, normalised later
 // by its consumer) and xb = x as split rows, and the block's sum of x^2 into
 // ssq[row][block].  Grid (ceil(d/256), rows).
+// Four consecutive features per thread; a block covers SSQ_BLOCK features of
+// one row and writes their sum of squares.  d is a multiple of 4.
 __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float* x,
                                                const uint16_t* g, uint16_t* xg, uint16_t* xb,
                                                float* ssq) {
   __shared__ float sh[4];
   const int row = blockIdx.y;
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  float v = 0.f;
+  const int e = blockIdx.x * SSQ_BLOCK + 4 * threadIdx.x;
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
   if (e < d) {
-    v = x[(size_t)row * d + e];
+    float* const xr = x + (size_t)row * d + e;
+    float4 x4 = *reinterpret_cast<const float4*>(xr);
     if (mode != RN_KEEP) {
-      const float p = part_sum(pt, row, e);
-      v = (mode == RN_SET) ? p : v + p;
-      x[(size_t)row * d + e] = v;
+      const float4 p = part_sum4(pt, row, e);
+      x4 = (mode == RN_SET) ? p : make_float4(x4.x + p.x, x4.y + p.y, x4.z + p.z, x4.w + p.w);
+      *reinterpret_cast<float4*>(xr) = x4;
     }
-    if (xg) put_split(xg + (size_t)row * 2 * d, d, e, v * bf2f(g[e]));
-    if (xb) put_split(xb + (size_t)row * 2 * d, d, e, v);
+    v[0] = x4.x;
+    v[1] = x4.y;
+    v[2] = x4.z;
+    v[3] = x4.w;
+    if (xg) {
+      const uint2 gb = *reinterpret_cast<const uint2*>(g + e);
+      const float vg[4] = {v[0] * bf2f(gb.x & 0xFFFF), v[1] * bf2f(gb.x >> 16),
+                           v[2] * bf2f(gb.y & 0xFFFF), v[3] * bf2f(gb.y >> 16)};
+      put_split4(xg + (size_t)row * 2 * d, d, e, vg);
+    }
+    if (xb) put_split4(xb + (size_t)row * 2 * d, d, e, v);
   }
   if (!ssq) return;
-  const float t = block_sum_256(v * v, sh);
+  const float t = block_sum_256(v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3], sh);
   if (threadIdx.x == 0) ssq[(size_t)row * gridDim.x + blockIdx.x] = t;
 }
 
@@ -181,12 +220,19 @@ __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float*
 // un-normalised input).
 __global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint16_t* act) {
   const int row = blockIdx.y;
-  const int f = blockIdx.x * 256 + threadIdx.x;
+  const int f = blockIdx.x * 1024 + 4 * threadIdx.x;  // F is a multiple of 4
   if (f >= F) return;
   const float r = row_rstd(rn, row);
-  const float gt = r * part_sum(pt, row, f);
-  const float up = r * part_sum(pt, row, pt.off2 + f);
-  put_split(act + (size_t)row * 2 * F, F, f, gt / (1.f + __expf(-gt)) * up);
+  const float4 gt = part_sum4(pt, row, f);
+  const float4 up = part_sum4(pt, row, pt.off2 + f);
+  const float g4[4] = {gt.x, gt.y, gt.z, gt.w}, u4[4] = {up.x, up.y, up.z, up.w};
+  float o[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float gv = r * g4[e];
+    o[e] = gv / (1.f + __expf(-gv)) * (r * u4[e]);
+  }
+  put_split4(act + (size_t)row * 2 * F, F, f, o);
 }
 
 // out[row] = [h_row | e_next] as a split row of 2d, the concat fed to the
@@ -410,13 +456,13 @@ void launch_resid_norm(Parts pt, int col0, int rows, int d, int mode, float* x,
 
 void launch_silu(Parts pt, RowNorm rn, int rows, int F, uint16_t* act, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_silu, dim3((F + 255) / 256, rows), dim3(256), 0, st, pt, rn, F, act);
+  hipLaunchKernelGGL(k_silu, dim3((F + 1023) / 1024, rows), dim3(256), 0, st, pt, rn, F, act);
 }
 
 void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t* g, uint16_t* xg,
                   uint16_t* xb, float* ssq, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_resid, dim3((d + 255) / 256, rows), dim3(256), 0, st, pt, d, mode, x, g, xg,
+  hipLaunchKernelGGL(k_resid, dim3(ssq_blocks(d), rows), dim3(256), 0, st, pt, d, mode, x, g, xg,
                      xb, ssq);
 }
 

@@ -221,7 +221,7 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->part = cv.take<float>(p.part_floats);
   t->sink = cv.take<float>(256);
   t->gemm_zero = cv.take<uint16_t>(gemm_dummy_elems());
-  t->ssq = cv.take<float>((size_t)R * ((d + 255) / 256));
+  t->ssq = cv.take<float>((size_t)R * ssq_blocks(d));
   t->q = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
   t->ao = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
   t->act = cv.take<uint16_t>((size_t)R * 2 * m.ffn_dim);
@@ -370,7 +370,7 @@ int norm_rows(msd_ctx* c, int rows, const uint16_t* g) {
 }
 
 RowNorm row_norm(const msd_ctx* c, int m0) {
-  const int nblk = (c->m.d_model + 255) / 256;
+  const int nblk = ssq_blocks(c->m.d_model);
   return RowNorm{c->ssq + (size_t)m0 * nblk, nblk, c->m.d_model, c->m.norm_eps};
 }
 
@@ -454,7 +454,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       TRY(gemm(c, GK_O, c->ao + (size_t)m0 * 2 * H * hd, 2 * H * hd, mc, pw.o, nullptr, d, H * hd,
                &pt));
       launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, w.n2, c->xn + (size_t)m0 * 2 * d, nullptr,
-                   c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
+                   c->ssq + (size_t)m0 * ssq_blocks(d), c->st);
       LAUNCHED(c);
     }
     for (int m0 = 0; m0 < rows; m0 += CHUNK) {
@@ -476,7 +476,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
         launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, last ? nullptr : g_next,
                      last ? nullptr : c->xn + (size_t)m0 * 2 * d,
                      (last && final_xb) ? final_xb + (size_t)m0 * 2 * d : nullptr,
-                     last ? nullptr : c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
+                     last ? nullptr : c->ssq + (size_t)m0 * ssq_blocks(d), c->st);
       }
       LAUNCHED(c);
     }
@@ -496,7 +496,7 @@ int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const ui
     TRY(gemm(c, GK_FC, c->fcin + (size_t)m0 * 4 * d, 4 * d, mc, c->fc_p, nullptr, d, 2 * d, &pt));
     launch_resid(pt, mc, d, RN_SET, c->x + (size_t)m0 * d, visual ? nullptr : c->dlayer.n1,
                  visual ? nullptr : c->xn + (size_t)m0 * 2 * d, nullptr,
-                 visual ? nullptr : c->ssq + (size_t)m0 * ((d + 255) / 256), c->st);
+                 visual ? nullptr : c->ssq + (size_t)m0 * ssq_blocks(d), c->st);
     LAUNCHED(c);
   }
   if (visual) {

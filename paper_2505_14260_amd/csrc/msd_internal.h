@@ -87,8 +87,12 @@ struct Parts {
   int ld, off2;
 };
 
+// Per-row sums of squares come in blocks of SSQ_BLOCK features.
+constexpr int SSQ_BLOCK = 1024;
+inline int ssq_blocks(int d) { return (d + SSQ_BLOCK - 1) / SSQ_BLOCK; }
+
 // Per-row RMS of the un-normalised GEMM input: ssq[row][0..nblk) are sums of
-// x^2 over blocks of 256 features (ssq == null: no scaling).
+// x^2 over blocks of SSQ_BLOCK features (ssq == null: no scaling).
 struct RowNorm {
   const float* ssq;
   int nblk, d;
