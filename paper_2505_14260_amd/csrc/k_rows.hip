@@ -185,7 +185,7 @@ __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, 
 // one row and writes their sum of squares.  d is a multiple of 4.
 __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float* x,
                                                const uint16_t* g, uint16_t* xg, uint16_t* xb,
-                                               float* ssq) {
+                                               float* ssq, const int* dst, float* feat) {
   __shared__ float sh[4];
   const int row = blockIdx.y;
   const int e = blockIdx.x * SSQ_BLOCK + 4 * threadIdx.x;
@@ -202,6 +202,10 @@ __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float*
     v[1] = x4.y;
     v[2] = x4.z;
     v[3] = x4.w;
+    if (feat) {
+      const int o = dst[row];
+      if (o >= 0) *reinterpret_cast<float4*>(feat + (size_t)o * d + e) = x4;
+    }
     if (xg) {
       const uint2 gb = *reinterpret_cast<const uint2*>(g + e);
       const float vg[4] = {v[0] * bf2f(gb.x & 0xFFFF), v[1] * bf2f(gb.x >> 16),
@@ -213,6 +217,21 @@ __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float*
   if (!ssq) return;
   const float t = block_sum_256(v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3], sh);
   if (threadIdx.x == 0) ssq[(size_t)row * gridDim.x + blockIdx.x] = t;
+}
+
+// x[i] = the last feature of sequence seq_ids[i] (its feature slot 0), xb
+// the same as a split row; four features per thread.
+__global__ __launch_bounds__(256) void k_root_feat(const int* seq_ids, const float* feat,
+                                                   int feat_stride, int d, float* x,
+                                                   uint16_t* xb) {
+  const int i = blockIdx.y;
+  const int e = blockIdx.x * 1024 + 4 * threadIdx.x;
+  if (e >= d) return;
+  const float4 v =
+      *reinterpret_cast<const float4*>(feat + (size_t)seq_ids[i] * feat_stride * d + e);
+  *reinterpret_cast<float4*>(x + (size_t)i * d + e) = v;
+  const float w[4] = {v.x, v.y, v.z, v.w};
+  put_split4(xb + (size_t)i * 2 * d, d, e, w);
 }
 
 // act = silu(gate) * up (split rows) with gate at columns [0, F), up at
@@ -454,16 +473,23 @@ void launch_resid_norm(Parts pt, int col0, int rows, int d, int mode, float* x,
                      xb);
 }
 
+void launch_root_feat(int n_seq, const int* seq_ids, const float* feat, int feat_stride, int d,
+                      float* x, uint16_t* xb, hipStream_t st) {
+  if (n_seq <= 0) return;
+  hipLaunchKernelGGL(k_root_feat, dim3((d + 1023) / 1024, n_seq), dim3(256), 0, st, seq_ids,
+                     feat, feat_stride, d, x, xb);
+}
+
 void launch_silu(Parts pt, RowNorm rn, int rows, int F, uint16_t* act, hipStream_t st) {
   if (rows <= 0) return;
   hipLaunchKernelGGL(k_silu, dim3((F + 1023) / 1024, rows), dim3(256), 0, st, pt, rn, F, act);
 }
 
 void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t* g, uint16_t* xg,
-                  uint16_t* xb, float* ssq, hipStream_t st) {
+                  uint16_t* xb, float* ssq, hipStream_t st, const int* dst, float* feat) {
   if (rows <= 0) return;
   hipLaunchKernelGGL(k_resid, dim3(ssq_blocks(d), rows), dim3(256), 0, st, pt, d, mode, x, g, xg,
-                     xb, ssq);
+                     xb, ssq, dst, feat);
 }
 
 void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const uint16_t* E,

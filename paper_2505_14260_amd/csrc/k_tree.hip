@@ -29,25 +29,94 @@ __global__ void k_tree_init_static(msd_tree* trees, const int* seq_ids, const in
   if (threadIdx.x == 0) t->n_nodes = T;
 }
 
-__global__ void k_static_rows(const msd_tree* trees, const int* seq_ids, const int* d_len,
-                              StaticSpec sp, int round_off, int n_round, int depth,
-                              int feat_stride, Rows r, int* prefix) {
-  const int sidx = blockIdx.x;
-  const int j = threadIdx.x;
+
+// Round `depth` (>= 1) of a static tree, one block per (row, 256-feature
+// slice).  The row's node takes the rank-th best token of its parent's draft
+// distribution (the previous round's top-k, n_prev rows per sequence).  The
+// slice-0 block writes the row descriptor; the sequence's first row's slice-0
+// block also assigns every node of this depth (leaves included); every block
+// gathers its slice of the f_down input [parent feature | token embedding]
+// as a split row of 2d.
+__global__ __launch_bounds__(256) void k_static_next(msd_tree* trees, const int* seq_ids,
+                                                     const int* d_len, StaticSpec sp, int T,
+                                                     int depth, const int* topk_idx, int k,
+                                                     int n_prev, int round_off, int n_round,
+                                                     int feat_stride, Rows r, int* prefix,
+                                                     const float* feat, const uint16_t* E, int d,
+                                                     uint16_t* out) {
+  const int row = blockIdx.x;
+  const int sidx = row / n_round, j = row - sidx * n_round;
   const int b = seq_ids[sidx];
-  const int L = d_len[b];
-  if (j == 0) prefix[sidx] = L;
-  if (j >= n_round) return;
   const int u = sp.round_nodes[round_off + j];
-  const int row = sidx * n_round + j;
-  r.tok[row] = trees[sidx].token[u];
-  r.vis[row] = -1;
-  r.hrow[row] = b * feat_stride + sp.pslot[u];
-  r.pos[row] = L + depth - 1;
-  r.slot[row] = L + sp.exp_idx[u];
-  r.seq[row] = b;
-  r.mask[row] = sp.exp_mask[u];
-  r.dst[row] = b * feat_stride + 1 + sp.exp_idx[u];
+  const auto token_of = [&](int c) {
+    return topk_idx[(size_t)(sidx * n_prev + sp.round_pos[sp.parent[c]]) * k + sp.rank[c]];
+  };
+  const int tok = token_of(u);
+  if (blockIdx.y == 0) {
+    if (threadIdx.x == 0) {
+      const int L = d_len[b];
+      if (j == 0) prefix[sidx] = L;
+      r.tok[row] = tok;
+      r.vis[row] = -1;
+      r.hrow[row] = b * feat_stride + sp.pslot[u];
+      r.pos[row] = L + depth - 1;
+      r.slot[row] = L + sp.exp_idx[u];
+      r.seq[row] = b;
+      r.mask[row] = sp.exp_mask[u];
+      r.dst[row] = b * feat_stride + 1 + sp.exp_idx[u];
+    }
+    if (j == 0)
+      for (int c = 1 + threadIdx.x; c < T; c += blockDim.x)
+        if (sp.depth[c] == depth) trees[sidx].token[c] = token_of(c);
+  }
+  const int i = blockIdx.y * 256 + threadIdx.x;
+  if (i < d) {
+    uint16_t* const o = out + (size_t)row * 4 * d;
+    put_split(o, 2 * d, i, feat[(size_t)(b * feat_stride + sp.pslot[u]) * d + i]);
+    o[d + i] = E[(size_t)tok * d + i];
+    o[3 * d + i] = 0;
+  }
+}
+
+// Pending draft rows of each sequence, padded to r_max rows per sequence, one
+// block per (row, 256-feature slice): the slice-0 block writes the row
+// descriptor, every block its slice of the f_down input [pending feature |
+// embedding of the next token].  A sequence with no pending row (a padding
+// row only) takes token 0 and a zero feature; its row is never stored.
+__global__ __launch_bounds__(256) void k_catchup_next(const int* seq_ids, const int* d_len,
+                                                      const int* pend_n, const int* pend_next,
+                                                      int r_max, int pend_stride, int feat_stride,
+                                                      Rows r, int* prefix, const uint16_t* pend_h,
+                                                      const uint16_t* E, int d, uint16_t* out) {
+  const int row = blockIdx.x;
+  const int sidx = row / r_max, j = row - sidx * r_max;
+  const int b = seq_ids[sidx];
+  const int rb = pend_n[b];
+  const bool valid = j < rb;
+  const int jj = valid ? j : (rb > 0 ? rb - 1 : 0);
+  const int tok = rb > 0 ? pend_next[b * pend_stride + jj] : 0;
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
+    const int P = d_len[b] - rb;
+    if (j == 0) prefix[sidx] = P;
+    r.tok[row] = tok;
+    r.vis[row] = -1;
+    r.hrow[row] = b * pend_stride + jj;
+    r.pos[row] = P + jj;
+    r.slot[row] = valid ? P + j : -1;
+    r.seq[row] = b;
+    // causal inside the pending region: row j sees pending rows 0..j
+    r.mask[row] = (jj >= 63) ? ~0ull : ((2ull << jj) - 1ull);
+    r.dst[row] = (j == rb - 1) ? b * feat_stride : -1;
+  }
+  const int i = blockIdx.y * 256 + threadIdx.x;
+  if (i < d) {
+    const uint16_t* const hs = pend_h + (size_t)(b * pend_stride + jj) * 2 * d;
+    uint16_t* const o = out + (size_t)row * 4 * d;
+    o[i] = rb > 0 ? hs[i] : (uint16_t)0;
+    o[2 * d + i] = rb > 0 ? hs[d + i] : (uint16_t)0;
+    o[d + i] = E[(size_t)tok * d + i];
+    o[3 * d + i] = 0;
+  }
 }
 
 // Children of the round's nodes: node c with parent p takes the rank[c]-th
@@ -227,39 +296,7 @@ __global__ void k_verify_rows(const msd_tree* trees, const int* seq_ids, const i
   r.mask[row] = t->anc[i];
 }
 
-// Pending draft rows of each sequence, padded to r_max rows per sequence.
-__global__ void k_catchup_rows(const int* seq_ids, const int* d_len, const int* pend_n,
-                               const int* pend_next, int r_max, int pend_stride,
-                               int feat_stride, Rows r, int* prefix) {
-  const int sidx = blockIdx.x;
-  const int j = threadIdx.x;
-  const int b = seq_ids[sidx];
-  const int rb = pend_n[b];
-  const int P = d_len[b] - rb;
-  if (j == 0) prefix[sidx] = P;
-  if (j >= r_max) return;
-  const bool valid = j < rb;
-  const int jj = valid ? j : (rb > 0 ? rb - 1 : 0);
-  const int row = sidx * r_max + j;
-  r.tok[row] = pend_next[b * pend_stride + jj];
-  r.vis[row] = -1;
-  r.hrow[row] = b * pend_stride + jj;
-  r.pos[row] = P + jj;
-  r.slot[row] = valid ? P + j : -1;
-  r.seq[row] = b;
-  // causal inside the pending region: row j sees pending rows 0..j
-  r.mask[row] = (jj >= 63) ? ~0ull : ((2ull << jj) - 1ull);
-  r.dst[row] = (j == rb - 1) ? b * feat_stride : -1;
-}
 
-// Grid (rows, ceil(d/256)).
-__global__ void k_store_feat(const float* x, const int* dst, int d, float* feat) {
-  const int row = blockIdx.x;
-  const int o = dst[row];
-  const int e = blockIdx.y * 256 + threadIdx.x;
-  if (o < 0 || e >= d) return;
-  feat[(size_t)o * d + e] = x[(size_t)row * d + e];
-}
 
 // Greedy acceptance: node j is accepted iff its parent is and its token is
 // the parent's argmax; the deepest accepted node ends the path (unique since
@@ -373,17 +410,32 @@ void launch_tree_init_static(void* trees, int n_seq, const int* seq_ids, const i
                      seq_ids, d_root, sp, T);
 }
 
-void launch_static_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
-                        StaticSpec sp, int round_off, int n_round, int depth, int feat_stride,
-                        Rows r, int* prefix, hipStream_t st) {
-  hipLaunchKernelGGL(k_static_rows, dim3(n_seq), dim3(64), 0, st, (const msd_tree*)trees,
-                     seq_ids, d_len, sp, round_off, n_round, depth, feat_stride, r, prefix);
-}
 
 void launch_static_assign(void* trees, int n_seq, StaticSpec sp, int T, int parent_depth,
                           const int* topk_idx, int k, int n_round, hipStream_t st) {
   hipLaunchKernelGGL(k_static_assign, dim3(n_seq), dim3(64), 0, st, (msd_tree*)trees, sp, T,
                      parent_depth, topk_idx, k, n_round);
+}
+
+void launch_static_next(void* trees, int n_seq, const int* seq_ids, const int* d_len,
+                        StaticSpec sp, int T, int depth, const int* topk_idx, int k, int n_prev,
+                        int round_off, int n_round, int feat_stride, Rows r, int* prefix,
+                        const float* feat, const uint16_t* E, int d, uint16_t* out,
+                        hipStream_t st) {
+  if (n_seq * n_round <= 0) return;
+  hipLaunchKernelGGL(k_static_next, dim3(n_seq * n_round, (d + 255) / 256), dim3(256), 0, st,
+                     (msd_tree*)trees, seq_ids, d_len, sp, T, depth, topk_idx, k, n_prev,
+                     round_off, n_round, feat_stride, r, prefix, feat, E, d, out);
+}
+
+void launch_catchup_next(int n_seq, const int* seq_ids, const int* d_len, const int* pend_n,
+                         const int* pend_next, int r_max, int pend_stride, int feat_stride,
+                         Rows r, int* prefix, const uint16_t* pend_h, const uint16_t* E, int d,
+                         uint16_t* out, hipStream_t st) {
+  if (n_seq * r_max <= 0) return;
+  hipLaunchKernelGGL(k_catchup_next, dim3(n_seq * r_max, (d + 255) / 256), dim3(256), 0, st,
+                     seq_ids, d_len, pend_n, pend_next, r_max, pend_stride, feat_stride, r,
+                     prefix, pend_h, E, d, out);
 }
 
 void launch_dyn_root(DynPool pool, int n_seq, const int* topk_idx, const float* topk_val,
@@ -415,18 +467,7 @@ void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const 
                      seq_ids, d_len, T, vocab, r, prefix);
 }
 
-void launch_catchup_rows(int n_seq, const int* seq_ids, const int* d_len, const int* pend_n,
-                         const int* pend_next, int r_max, int pend_stride, int feat_stride,
-                         Rows r, int* prefix, hipStream_t st) {
-  hipLaunchKernelGGL(k_catchup_rows, dim3(n_seq), dim3(64), 0, st, seq_ids, d_len, pend_n,
-                     pend_next, r_max, pend_stride, feat_stride, r, prefix);
-}
 
-void launch_store_feat(const float* x, int rows, const int* dst, int d, float* feat,
-                       hipStream_t st) {
-  if (rows <= 0) return;
-  hipLaunchKernelGGL(k_store_feat, dim3(rows, (d + 255) / 256), dim3(256), 0, st, x, dst, d, feat);
-}
 
 void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,
                    int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,

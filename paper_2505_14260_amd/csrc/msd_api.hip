@@ -381,7 +381,8 @@ RowNorm row_norm(const msd_ctx* c, int m0) {
 // get x += ..., then final_xn = rmsnorm(x) * final_g when final_g and
 // final_xb = x when final_xb.
 int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int max_ltot,
-                   const uint16_t* final_g, uint16_t* final_xn, uint16_t* final_xb) {
+                   const uint16_t* final_g, uint16_t* final_xn, uint16_t* final_xb,
+                   const int* feat_dst = nullptr, float* feat = nullptr) {
   const msd_model_desc& m = c->m;
   const int rows = n_seq * nq;
   const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim, F = m.ffn_dim;
@@ -476,7 +477,8 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
         launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, last ? nullptr : g_next,
                      last ? nullptr : c->xn + (size_t)m0 * 2 * d,
                      (last && final_xb) ? final_xb + (size_t)m0 * 2 * d : nullptr,
-                     last ? nullptr : c->ssq + (size_t)m0 * ssq_blocks(d), c->st);
+                     last ? nullptr : c->ssq + (size_t)m0 * ssq_blocks(d), c->st,
+                     (last && feat) ? feat_dst + m0 : nullptr, last ? feat : nullptr);
       }
       LAUNCHED(c);
     }
@@ -486,7 +488,8 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
 
 // Draft head on rows whose f_down input is in c->fcin (split rows of 2d):
 // f = f_down(concat), visual rows replaced by their embeddings, then the
-// decoder layer; features in c->x and c->xb.
+// decoder layer; features in c->x and c->xb, and in the feature slots
+// c->rows.dst names (-1: none).
 int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const uint16_t* visual) {
   const int d = c->m.d_model;
   const int rows = n_seq * nq;
@@ -504,7 +507,9 @@ int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const ui
     LAUNCHED(c);
     TRY(norm_rows(c, rows, c->dlayer.n1));
   }
-  return forward_layers(c, true, n_seq, nq, tree_R, max_ltot, nullptr, nullptr, c->xb);
+  // the final features also go to their draft feature slots (rows.dst)
+  return forward_layers(c, true, n_seq, nq, tree_R, max_ltot, nullptr, nullptr, c->xb,
+                        c->rows.dst, c->dfeat);
 }
 
 // LM head + top-k (and log-sum-exp) over the rows of c->xb: no final norm.
@@ -802,8 +807,6 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
                   c->fcin, c->st);
   LAUNCHED(c);
   TRY(draft_pass(c, 1, n, -1, n, n_vis ? (const uint16_t*)visual_d : nullptr));
-  launch_store_feat(c->x, n, c->rows.dst, d, c->dfeat, c->st);
-  LAUNCHED(c);
   int st_len[2] = {n, 0};
   TRY(upload_many(c, {{c->d_len + seq, st_len, sizeof(int)}, {c->pend_n + seq, st_len + 1, sizeof(int)}}));
   int* back = c->stage + STAGE_INTS - 64;
@@ -873,50 +876,42 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
     c->att_keys[i] = c->L[seqs_h[i]];
   }
   if (r_max > 0) {
-    launch_catchup_rows(n_seq, c->seq_ids, c->d_len, c->pend_n, c->pend_next, r_max, PEND, FEAT,
-                        c->rows, c->prefix, c->st);
-    LAUNCHED(c);
-    launch_fc_input(c->pend_h, nullptr, c->rows.hrow, c->embed, c->rows.tok, nullptr,
-                    n_seq * r_max, d, c->fcin, c->st);
+    launch_catchup_next(n_seq, c->seq_ids, c->d_len, c->pend_n, c->pend_next, r_max, PEND, FEAT,
+                        c->rows, c->prefix, c->pend_h, c->embed, d, c->fcin, c->st);
     LAUNCHED(c);
     TRY(draft_pass(c, n_seq, r_max, r_max, max_l + r_max, nullptr));
-    launch_store_feat(c->x, n_seq * r_max, c->rows.dst, d, c->dfeat, c->st);
-    LAUNCHED(c);
     for (int i = 0; i < n_seq; ++i) c->pend[seqs_h[i]] = 0;
   }
   for (int i = 0; i < n_seq; ++i) c->att_pre[i] = c->L[seqs_h[i]];
   // 2. draft distribution at the root: the last catch-up feature of each
   //    sequence goes through the LM head
-  for (int i = 0; i < n_seq; ++i)
-    HIPC(c, hipMemcpyAsync(c->x + (size_t)i * d, c->dfeat + (size_t)seqs_h[i] * FEAT * d,
-                           sizeof(float) * d, hipMemcpyDeviceToDevice, c->st));
-  launch_resid_norm(Parts{nullptr, 0, 0, 0, 0}, 0, n_seq, d, RN_KEEP, c->x, nullptr, m.norm_eps,
-                    nullptr, c->xb, c->st);
+  launch_root_feat(n_seq, c->seq_ids, c->dfeat, FEAT, d, c->x, c->xb, c->st);
   LAUNCHED(c);
   if (spec->kind == MSD_TREE_STATIC) {
     TRY(draft_head(c, n_seq, c->round_k[0]));
     launch_tree_init_static(trees_d, n_seq, c->seq_ids, c->d_root, c->sp, T, c->st);
     LAUNCHED(c);
-    launch_static_assign(trees_d, n_seq, c->sp, T, 0, c->tk_idx, c->round_k[0], 1, c->st);
-    LAUNCHED(c);
+    // round dd expands the depth-dd nodes that have children; its kernel
+    // also assigns all depth-dd tokens from the previous round's top-k
+    int prev_n = 1, prev_k = c->round_k[0], prev_depth = 0;
     for (int dd = 1; dd < D; ++dd) {
       const int nr = c->round_n[dd];
-      if (nr == 0) continue;
-      launch_static_rows(trees_d, n_seq, c->seq_ids, c->d_len, c->sp, c->round_off[dd], nr, dd,
-                         FEAT, c->rows, c->prefix, c->st);
-      LAUNCHED(c);
-      launch_fc_input(nullptr, c->dfeat, c->rows.hrow, c->embed, c->rows.tok, nullptr, n_seq * nr,
-                      d, c->fcin, c->st);
+      if (nr == 0) break;  // no node at this depth has children: none deeper
+      launch_static_next(trees_d, n_seq, c->seq_ids, c->d_len, c->sp, T, dd, c->tk_idx, prev_k,
+                         prev_n, c->round_off[dd], nr, FEAT, c->rows, c->prefix, c->dfeat,
+                         c->embed, d, c->fcin, c->st);
       LAUNCHED(c);
       const int R = c->round_exp_end[dd];
       for (int i = 0; i < n_seq; ++i) c->att_keys[i] = c->L[seqs_h[i]] + R;
       TRY(draft_pass(c, n_seq, nr, R, max_l + R, nullptr));
-      launch_store_feat(c->x, n_seq * nr, c->rows.dst, d, c->dfeat, c->st);
-      LAUNCHED(c);
       TRY(draft_head(c, n_seq * nr, c->round_k[dd]));
-      launch_static_assign(trees_d, n_seq, c->sp, T, dd, c->tk_idx, c->round_k[dd], nr, c->st);
-      LAUNCHED(c);
+      prev_n = nr;
+      prev_k = c->round_k[dd];
+      prev_depth = dd;
     }
+    // the deepest nodes' tokens
+    launch_static_assign(trees_d, n_seq, c->sp, T, prev_depth, c->tk_idx, prev_k, prev_n, c->st);
+    LAUNCHED(c);
   } else {
     TRY(draft_head(c, n_seq, K));
     launch_dyn_root(c->pool, n_seq, c->tk_idx, c->tk_val, c->tk_lse, K, c->st);
@@ -931,8 +926,6 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
       const int R = exp_base;
       for (int i = 0; i < n_seq; ++i) c->att_keys[i] = c->L[seqs_h[i]] + R;
       TRY(draft_pass(c, n_seq, K, R, max_l + R, nullptr));
-      launch_store_feat(c->x, n_seq * K, c->rows.dst, d, c->dfeat, c->st);
-      LAUNCHED(c);
       TRY(draft_head(c, n_seq * K, K));
       launch_dyn_expand(c->pool, n_seq, c->tk_idx, c->tk_val, c->tk_lse, K, n_pool, exp_base, c->st);
       LAUNCHED(c);

@@ -137,8 +137,11 @@ void launch_silu(Parts pt, RowNorm rn, int rows, int F, uint16_t* act, hipStream
 // Elementwise form: x updated as above, xg = x * g when xg, xb = x when xb
 // (split rows of d), ssq[row][blk] = sum of x^2 over feature block blk
 // (256 wide).
+// feat: when given, row r of the new x is also copied to feat row dst[r]
+// (dst[r] < 0: no copy), the draft's feature store.
 void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t* g, uint16_t* xg,
-                  uint16_t* xb, float* ssq, hipStream_t st);
+                  uint16_t* xb, float* ssq, hipStream_t st, const int* dst = nullptr,
+                  float* feat = nullptr);
 void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, const int* pos,
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
                     uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st);
@@ -198,9 +201,22 @@ struct DynPool {
 
 void launch_tree_init_static(void* trees, int n_seq, const int* seq_ids, const int* d_root,
                              StaticSpec sp, int T, hipStream_t st);
-void launch_static_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
-                        StaticSpec sp, int round_off, int n_round, int depth, int feat_stride,
-                        Rows r, int* prefix, hipStream_t st);
+// Round `depth` of a static tree: the depth's tokens from the previous
+// round's top-k, the round's row descriptors and f_down inputs.
+void launch_static_next(void* trees, int n_seq, const int* seq_ids, const int* d_len,
+                        StaticSpec sp, int T, int depth, const int* topk_idx, int k, int n_prev,
+                        int round_off, int n_round, int feat_stride, Rows r, int* prefix,
+                        const float* feat, const uint16_t* E, int d, uint16_t* out,
+                        hipStream_t st);
+// Catch-up rows (pending draft rows) and their f_down inputs.
+void launch_catchup_next(int n_seq, const int* seq_ids, const int* d_len, const int* pend_n,
+                         const int* pend_next, int r_max, int pend_stride, int feat_stride,
+                         Rows r, int* prefix, const uint16_t* pend_h, const uint16_t* E, int d,
+                         uint16_t* out, hipStream_t st);
+// Root rows of a draft tree: x = each sequence's last feature, xb the same
+// as split rows.
+void launch_root_feat(int n_seq, const int* seq_ids, const float* feat, int feat_stride, int d,
+                      float* x, uint16_t* xb, hipStream_t st);
 void launch_static_assign(void* trees, int n_seq, StaticSpec sp, int T, int parent_depth,
                           const int* topk_idx, int k, int n_round, hipStream_t st);
 void launch_dyn_root(DynPool pool, int n_seq, const int* topk_idx, const float* topk_val,
@@ -213,11 +229,6 @@ void launch_dyn_finalize(DynPool pool, void* trees, int n_seq, const int* seq_id
                          const int* d_root, int n_pool, int N, hipStream_t st);
 void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
                         int T, int vocab, Rows r, int* prefix, hipStream_t st);
-void launch_catchup_rows(int n_seq, const int* seq_ids, const int* d_len, const int* pend_n,
-                         const int* pend_next, int r_max, int pend_stride, int feat_stride,
-                         Rows r, int* prefix, hipStream_t st);
-void launch_store_feat(const float* x, int rows, const int* dst, int d, float* feat,
-                       hipStream_t st);
 void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,
                    int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,
                    hipStream_t st);

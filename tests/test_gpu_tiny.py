@@ -331,6 +331,42 @@ def test_batch2_ragged_decode(setup):
             assert not decided(rows[bad]), (b, bad)
 
 
+def test_sequence_joins_running_batch(setup):
+    """A sequence prefilled while another already has pending draft rows: the
+    catch-up batch pads the new sequence (which has none), and both decode as
+    their plain greedy decodes."""
+    wl, eng, m, prompt = setup
+    print("case: tiny batch, second sequence joins after two cycles", flush=True)
+    tokens, is_visual, visual = prompt
+    cut = wl.n_visual + 13
+    p1 = (tokens[:cut], is_visual[:cut], visual)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    outs = [[eng.prefill(0, *prompt)], []]
+    one = eng.new_trees(1)
+    for _ in range(2):
+        eng.draft_tree([0], spec, one)
+        amax, _ = eng.verify([0], one, T)
+        em, _ = eng.accept([0], one, T, amax)
+        outs[0].extend(int(t) for t in em[0])
+    outs[1].append(eng.prefill(1, *p1))
+    trees = eng.new_trees(2)
+    n_new = 24
+    while min(len(o) for o in outs) < n_new:
+        eng.draft_tree([0, 1], spec, trees)
+        amax, _ = eng.verify([0, 1], trees, T)
+        em, _ = eng.accept([0, 1], trees, T, amax)
+        for b in range(2):
+            outs[b].extend(int(t) for t in em[b])
+    for b, p in enumerate((prompt, p1)):
+        ref, rows = O.greedy_generate(m, p, n_new, return_logits=True)
+        got = outs[b][:n_new]
+        bad = next((i for i in range(n_new) if got[i] != ref[i]), None)
+        print(f"seq {b}: {bad if bad is not None else n_new}/{n_new} equal")
+        if bad is not None:
+            assert not decided(rows[bad]), (b, bad)
+
+
 def test_stale_cache_slots_never_read(setup):
     """KV slots at or past a sequence's committed length may hold any bits
     (never written, rejected tree nodes, or whatever the caller left there).
