@@ -16,6 +16,9 @@ order the paper gives them:
             greedy verification / longest accepted path with the bonus token
             (Sec. 3.2 verification, temperature 0), KV compaction, the full
             speculative decode loop and the plain greedy decode it must equal.
+  sampling.py speculative sampling on the tree at temperature > 0 (Sec. 3.2
+            acceptance rule and adjusted distribution) with its counter-based
+            SplitMix64 draws.
   metrics.py the expected-tokens closed form omega(gamma, alpha) and the
             speedup model of Sec. 5.1.3.
 """
