@@ -10,7 +10,8 @@
  *                       (Sec. 3.2, verification phase);
  *   msd_accept_compact  greedy longest-path acceptance plus the bonus token
  *                       (Sec. 3.2 acceptance rule with a one-hot target) and
- *                       in-place compaction of the target KV cache.
+ *                       in-place compaction of the target KV cache;
+ *   msd_accept_sample   the same at temperature > 0 (speculative sampling).
  * msd_prefill processes the interleaved visual + text prompt (Sec. 3.1).
  *
  * Conventions
@@ -19,8 +20,8 @@
  *  - Weights are bfloat16 (raw 16-bit patterns), row-major [out][in], no
  *    biases.  Norm gains are bfloat16 [d].
  *  - All device work is enqueued on the stream given to msd_create, in order.
- *    Only msd_prefill and msd_accept_compact wait for the stream (to return
- *    host outputs).  A context serves one stream and is not thread-safe.
+ *    Only msd_prefill and the two acceptance calls wait for the stream (to
+ *    return host outputs).  A context serves one stream and is not thread-safe.
  *  - Return value: MSD_OK (0) or a negative MSD_ERR_*; msd_last_error()
  *    returns a message for the last failure on that context (or of
  *    msd_create when ctx is NULL).
@@ -206,6 +207,33 @@ int msd_verify(msd_ctx* ctx, int n_seq, const int32_t* seqs_h, const msd_tree* t
 int msd_accept_compact(msd_ctx* ctx, int n_seq, const int32_t* seqs_h,
                        const msd_tree* trees_d, int n_nodes, const int32_t* argmax_d,
                        int32_t* emitted_h, int32_t* n_emitted_h, int32_t* slot_map_d);
+
+/*
+ * Acceptance by speculative sampling at temperature > 0 (Sec. 3.2,
+ * verification phase: acceptance probability min(1, p/q) and the adjusted
+ * distribution norm(max(0, p - q)) after a rejection; the extra draw from p
+ * when every drafted token is accepted).  The tree's children are the
+ * draft's top-ranked tokens, so each child's proposal q is the point mass on
+ * its token: walking down from the root, the children of the current node
+ * are tried in node order, a child with token x being accepted with
+ * probability p(x) / (1 - target mass of the children already rejected
+ * there), where p = softmax(logits / temperature) at the current node; a
+ * rejection removes x from p.  When no child is accepted, the bonus token is
+ * drawn from p without the rejected tokens.  The emitted tokens follow the
+ * target's own sampling distribution.
+ *
+ * logits_d [n_seq][n_nodes][V] float32: the logits msd_verify wrote for these
+ * trees (its logits_d output).  temperature: positive and finite.  Draw j of
+ * sequence slot b in the cycle starting at committed length L (L < 2^24) is
+ * output n = b*2^40 + L*2^8 + j of the SplitMix64 generator (Steele, Lea and
+ * Flood, 2014) started at `seed`, its top 24 bits scaled by 2^-24.
+ * Everything else (outputs, compaction, pending rows, the wait) is as for
+ * msd_accept_compact, which remains the temperature-0 rule.
+ */
+int msd_accept_sample(msd_ctx* ctx, int n_seq, const int32_t* seqs_h,
+                      const msd_tree* trees_d, int n_nodes, const float* logits_d,
+                      float temperature, uint64_t seed, int32_t* emitted_h,
+                      int32_t* n_emitted_h, int32_t* slot_map_d);
 
 /* Committed KV length of a sequence (host-side bookkeeping), or < 0. */
 int msd_seq_len(const msd_ctx* ctx, int seq);

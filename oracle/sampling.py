@@ -64,8 +64,9 @@ def sample_accept(tree, logits, temperature, seed, seq, L):
     logits: [T][V] target logits of the tree's nodes.  Returns
     (path, emitted, decisions): the accepted root-to-node path, the emitted
     tokens (accepted drafted tokens, then the bonus token), and one record per
-    random decision with its distance to the threshold (for gating the
-    comparison with a float32 implementation).
+    random decision: the node it was taken at and its distance to the
+    threshold (relative to the remaining mass for the bonus draw), for gating
+    the comparison with a float32 implementation.
     """
     T = len(tree.token)
     children = [[] for _ in range(T)]
@@ -84,7 +85,7 @@ def sample_accept(tree, logits, temperature, seed, seq, L):
             j += 1
             rem = 1.0 - removed
             ratio = p[x] / rem if rem > 0 else 0.0
-            decisions.append({"kind": "child", "node": u, "r": r, "ratio": ratio,
+            decisions.append({"kind": "child", "at": cur, "child": u, "r": r, "ratio": ratio,
                               "margin": abs(r - ratio)})
             if r < ratio:
                 nxt = u
@@ -111,6 +112,6 @@ def sample_accept(tree, logits, temperature, seed, seq, L):
             masked[rejected] = -np.inf
             y = int(np.argmax(masked))
             margin = 0.0
-        decisions.append({"kind": "bonus", "node": cur, "r": r, "token": y, "margin": margin})
+        decisions.append({"kind": "bonus", "at": cur, "r": r, "token": y, "margin": margin})
         emitted = [int(tree.token[u]) for u in path[1:]] + [y]
         return path, emitted, decisions

@@ -5,7 +5,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["msd_api.hip", "k_gemm.hip", "k_attn.hip", "k_rows.hip", "k_tree.hip"]
+SOURCES = ["msd_api.hip", "k_gemm.hip", "k_attn.hip", "k_rows.hip", "k_tree.hip", "k_sample.hip"]
 LIB = os.path.join(HERE, "libmsd.so")
 ARCH = os.environ.get("MSD_OFFLOAD_ARCH", "gfx950")
 

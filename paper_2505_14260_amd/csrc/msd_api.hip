@@ -613,6 +613,45 @@ int prepare_static(msd_ctx* c, const msd_tree_spec* s) {
   return MSD_OK;
 }
 
+// Checks shared by the two acceptance calls.
+int check_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,
+                 int n_nodes, int32_t* emitted_h, int32_t* n_emitted_h) {
+  TRY(check_seqs(c, n_seq, seqs_h));
+  if (!trees_d || !emitted_h || !n_emitted_h) return fail(c, MSD_ERR_INVALID_ARG, "null argument");
+  if (n_nodes != c->verified_T || n_seq != c->verified_nseq)
+    return fail(c, MSD_ERR_STATE, "accept must follow msd_verify of the same trees");
+  return upload_seqs(c, seqs_h, n_seq);
+}
+
+// After the accepted paths are in acc_path / acc_n / acc_emit: compaction of
+// the target cache, the pending draft rows, and the host copy of the
+// emitted tokens (the one wait of the cycle).
+int finish_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, int T, int32_t* emitted_h,
+                  int32_t* n_emitted_h) {
+  const int d = c->m.d_model;
+  launch_compact(c->tk, c->tv, c->m.n_layers, c->lim.max_batch, c->m.n_kv_heads, c->lim.max_seq,
+                 c->m.head_dim, n_seq, c->seq_ids, c->acc_path, c->acc_n, c->d_len, c->st);
+  LAUNCHED(c);
+  launch_commit(n_seq, c->seq_ids, c->acc_path, c->acc_n, c->acc_emit, c->h, T, d, c->pend_h,
+                c->pend_next, c->pend_n, PEND, c->d_len, c->d_root, c->st);
+  LAUNCHED(c);
+  int* back = c->stage + STAGE_INTS - (MSD_MAX_TREE + 1) * 8 - 64;
+  HIPC(c, hipMemcpyAsync(back, c->acc_emit, sizeof(int) * MSD_MAX_TREE * n_seq,
+                         hipMemcpyDeviceToHost, c->st));
+  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8, c->acc_n, sizeof(int) * n_seq,
+                         hipMemcpyDeviceToHost, c->st));
+  HIPC(c, hipStreamSynchronize(c->st));
+  for (int i = 0; i < n_seq; ++i) {
+    const int n = back[MSD_MAX_TREE * 8 + i];
+    n_emitted_h[i] = n;
+    for (int j = 0; j < MSD_MAX_TREE; ++j) emitted_h[i * MSD_MAX_TREE + j] = back[i * MSD_MAX_TREE + j];
+    c->L[seqs_h[i]] += n;
+    c->pend[seqs_h[i]] = n;
+  }
+  c->verified_T = 0;
+  return MSD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -982,38 +1021,31 @@ int msd_accept_compact(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_t
                        int n_nodes, const int32_t* argmax_d, int32_t* emitted_h,
                        int32_t* n_emitted_h, int32_t* slot_map_d) {
   if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
-  TRY(check_seqs(c, n_seq, seqs_h));
-  if (!trees_d || !argmax_d || !emitted_h || !n_emitted_h)
-    return fail(c, MSD_ERR_INVALID_ARG, "null argument");
-  if (n_nodes != c->verified_T || n_seq != c->verified_nseq)
-    return fail(c, MSD_ERR_STATE, "accept must follow msd_verify of the same trees");
-  const int T = n_nodes, d = c->m.d_model;
-  TRY(upload_seqs(c, seqs_h, n_seq));
+  TRY(check_accept(c, n_seq, seqs_h, trees_d, n_nodes, emitted_h, n_emitted_h));
+  if (!argmax_d) return fail(c, MSD_ERR_INVALID_ARG, "null argument");
   int* slots = slot_map_d ? slot_map_d : c->acc_slot;
-  launch_accept(trees_d, n_seq, c->seq_ids, T, argmax_d, c->acc_path, c->acc_n, c->acc_emit, slots,
-                c->d_len, c->st);
+  launch_accept(trees_d, n_seq, c->seq_ids, n_nodes, argmax_d, c->acc_path, c->acc_n,
+                c->acc_emit, slots, c->d_len, c->st);
   LAUNCHED(c);
-  launch_compact(c->tk, c->tv, c->m.n_layers, c->lim.max_batch, c->m.n_kv_heads, c->lim.max_seq,
-                 c->m.head_dim, n_seq, c->seq_ids, c->acc_path, c->acc_n, c->d_len, c->st);
+  return finish_accept(c, n_seq, seqs_h, n_nodes, emitted_h, n_emitted_h);
+}
+
+int msd_accept_sample(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,
+                      int n_nodes, const float* logits_d, float temperature, uint64_t seed,
+                      int32_t* emitted_h, int32_t* n_emitted_h, int32_t* slot_map_d) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  TRY(check_accept(c, n_seq, seqs_h, trees_d, n_nodes, emitted_h, n_emitted_h));
+  if (!logits_d) return fail(c, MSD_ERR_INVALID_ARG, "null logits");
+  const float inv_t = 1.0f / temperature;
+  if (!(temperature > 0.f) || !std::isfinite(temperature) || !std::isfinite(inv_t))
+    return fail(c, MSD_ERR_INVALID_ARG, "temperature must be positive and finite");
+  for (int i = 0; i < n_seq; ++i)
+    if (c->L[seqs_h[i]] >= (1 << 24)) return fail(c, MSD_ERR_INVALID_ARG, "sequence too long");
+  int* slots = slot_map_d ? slot_map_d : c->acc_slot;
+  launch_accept_sample(trees_d, n_seq, c->seq_ids, n_nodes, logits_d, c->m.vocab, inv_t, seed,
+                       c->acc_path, c->acc_n, c->acc_emit, slots, c->d_len, c->st);
   LAUNCHED(c);
-  launch_commit(n_seq, c->seq_ids, c->acc_path, c->acc_n, c->acc_emit, c->h, T, d, c->pend_h,
-                c->pend_next, c->pend_n, PEND, c->d_len, c->d_root, c->st);
-  LAUNCHED(c);
-  int* back = c->stage + STAGE_INTS - (MSD_MAX_TREE + 1) * 8 - 64;
-  HIPC(c, hipMemcpyAsync(back, c->acc_emit, sizeof(int) * MSD_MAX_TREE * n_seq,
-                         hipMemcpyDeviceToHost, c->st));
-  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8, c->acc_n, sizeof(int) * n_seq,
-                         hipMemcpyDeviceToHost, c->st));
-  HIPC(c, hipStreamSynchronize(c->st));
-  for (int i = 0; i < n_seq; ++i) {
-    const int n = back[MSD_MAX_TREE * 8 + i];
-    n_emitted_h[i] = n;
-    for (int j = 0; j < MSD_MAX_TREE; ++j) emitted_h[i * MSD_MAX_TREE + j] = back[i * MSD_MAX_TREE + j];
-    c->L[seqs_h[i]] += n;
-    c->pend[seqs_h[i]] = n;
-  }
-  c->verified_T = 0;
-  return MSD_OK;
+  return finish_accept(c, n_seq, seqs_h, n_nodes, emitted_h, n_emitted_h);
 }
 
 int msd_trace_enable(msd_ctx* c, int capacity, int kinds) {

@@ -232,6 +232,11 @@ void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const 
 void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,
                    int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,
                    hipStream_t st);
+// Speculative sampling acceptance (k_sample.hip): same outputs as launch_accept.
+void launch_accept_sample(const void* trees, int n_seq, const int* seq_ids, int T,
+                          const float* logits, int V, float inv_t, uint64_t seed, int* path,
+                          int* n_path, int* emitted, int* slot_map, const int* d_len,
+                          hipStream_t st);
 void launch_compact(uint16_t* kc, uint16_t* vc, int n_layers, int B, int KV, int S, int hd,
                     int n_seq, const int* seq_ids, const int* path, const int* n_path,
                     const int* d_len, hipStream_t st);

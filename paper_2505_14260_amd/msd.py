@@ -87,6 +87,9 @@ def lib():
         L.msd_verify.argtypes = [c_vp, ctypes.c_int, P(c_i32), c_vp, ctypes.c_int, c_vp, c_vp]
         L.msd_accept_compact.argtypes = [c_vp, ctypes.c_int, P(c_i32), c_vp, ctypes.c_int, c_vp,
                                          P(c_i32), P(c_i32), c_vp]
+        L.msd_accept_sample.argtypes = [c_vp, ctypes.c_int, P(c_i32), c_vp, ctypes.c_int, c_vp,
+                                        ctypes.c_float, ctypes.c_uint64, P(c_i32), P(c_i32),
+                                        c_vp]
         L.msd_seq_len.argtypes = [c_vp, ctypes.c_int]
         L.msd_set_state.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, c_vp, c_i32]
         L.msd_trace_enable.argtypes = [c_vp, ctypes.c_int, ctypes.c_int]
@@ -163,6 +166,18 @@ def msd_accept_compact(ctx, seqs, trees_ptr, n_nodes, argmax_ptr, slot_map_ptr=N
     n_emit = np.zeros(len(s), dtype=np.int32)
     _check(ctx, lib().msd_accept_compact(
         ctx, len(s), ps, trees_ptr, n_nodes, argmax_ptr,
+        emitted.ctypes.data_as(ctypes.POINTER(c_i32)),
+        n_emit.ctypes.data_as(ctypes.POINTER(c_i32)), slot_map_ptr))
+    return [list(emitted[i, :n_emit[i]]) for i in range(len(s))]
+
+
+def msd_accept_sample(ctx, seqs, trees_ptr, n_nodes, logits_ptr, temperature, seed,
+                      slot_map_ptr=None):
+    s, ps = _i32(seqs)
+    emitted = np.zeros((len(s), MAX_TREE), dtype=np.int32)
+    n_emit = np.zeros(len(s), dtype=np.int32)
+    _check(ctx, lib().msd_accept_sample(
+        ctx, len(s), ps, trees_ptr, n_nodes, logits_ptr, float(temperature), int(seed),
         emitted.ctypes.data_as(ctypes.POINTER(c_i32)),
         n_emit.ctypes.data_as(ctypes.POINTER(c_i32)), slot_map_ptr))
     return [list(emitted[i, :n_emit[i]]) for i in range(len(s))]
@@ -307,8 +322,21 @@ class Engine:
                                 slots.data_ptr() if slots is not None else None)
         return em, slots
 
-    def generate(self, seq, prompt, spec, n_new, record=False):
-        """Speculative greedy decoding of one sequence: n_new tokens."""
+    def accept_sample(self, seqs, trees_t, n_nodes, logits, temperature, seed,
+                      want_slots=False):
+        """Acceptance by speculative sampling; logits: verify's float32 logits."""
+        slots = None
+        if want_slots:
+            slots = self.torch.empty(len(seqs) * MAX_TREE, dtype=self.torch.int32, device=self.dev)
+        em = msd_accept_sample(self.ctx, seqs, trees_t.data_ptr(), n_nodes, logits.data_ptr(),
+                               temperature, seed,
+                               slots.data_ptr() if slots is not None else None)
+        return em, slots
+
+    def generate(self, seq, prompt, spec, n_new, record=False, temperature=0.0, seed=0):
+        """Speculative decoding of one sequence: n_new tokens, greedy at
+        temperature 0, else speculative sampling (the first token, from the
+        prompt, is the greedy one either way)."""
         tokens, is_visual, visual = prompt
         out = [self.prefill(seq, tokens, is_visual, visual)]
         T = spec.n_nodes + 1
@@ -316,8 +344,11 @@ class Engine:
         cycles = []
         while len(out) < n_new:
             self.draft_tree([seq], spec, trees)
-            amax, _ = self.verify([seq], trees, T)
-            em, _ = self.accept([seq], trees, T, amax)
+            amax, logits = self.verify([seq], trees, T, want_logits=temperature > 0)
+            if temperature > 0:
+                em, _ = self.accept_sample([seq], trees, T, logits, temperature, seed)
+            else:
+                em, _ = self.accept([seq], trees, T, amax)
             out.extend(int(t) for t in em[0])
             cycles.append(len(em[0]))
         return out[:n_new], cycles

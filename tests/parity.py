@@ -210,3 +210,23 @@ def oracle_tree_of(g):
     from oracle import msd as O
     tok, par, dep, sc = gpu_tree_arrays(g)
     return O.Tree(token=tok, parent=par, depth=dep, score=sc)
+
+
+# Speculative sampling: a float32 decision may differ from the float64 one
+# only when the oracle's draw lies this close to the threshold.
+SAMPLE_GATE = 1e-4
+
+
+def sampling_agrees(path, emitted, r_path, r_emit, decisions, gate=SAMPLE_GATE):
+    """GPU sampling acceptance against the oracle's on the same logits and
+    draws: identical, or the first difference follows a decision the oracle
+    took within `gate` of its threshold at the last node both paths share."""
+    path, emitted = [int(x) for x in path], [int(x) for x in emitted]
+    if path == list(r_path) and emitted == list(r_emit):
+        return True
+    k = 0
+    while k < min(len(path), len(r_path)) and path[k] == r_path[k]:
+        k += 1
+    node = r_path[k - 1]
+    return any(d["at"] == node and d["margin"] < gate for d in decisions)
+

@@ -35,7 +35,7 @@ from oracle import model as M
 from oracle import msd as O
 from parity import (RTOL, compare_dynamic_tree, compare_static_tree, decided,
                     gpu_tree_arrays, oracle_draft_dynamic, oracle_draft_static,
-                    oracle_tree_of, row_close)
+                    oracle_tree_of, row_close, sampling_agrees)
 
 pytestmark = pytest.mark.gpu
 
@@ -203,6 +203,41 @@ class Case:
             log(f"[{label} seq {b}] accepted path {path}, emitted {emitted}")
         log(f"[{label}] cycle checked in {time.perf_counter() - t0:.1f}s")
 
+    def sample_cycle(self, temperature, seed, label):
+        """One cycle with speculative-sampling acceptance, checked against the
+        oracle's rule on the GPU's own logits and draws (the state is not
+        tracked further)."""
+        from oracle import sampling as S
+        from paper_2505_14260_amd.msd import MAX_TREE, msd_seq_len
+        eng, T = self.eng, self.T
+        n = len(self.states)
+        seqs = list(range(n))
+        trees = eng.new_trees(n)
+        eng.draft_tree(seqs, self.spec, trees)
+        gts = eng.trees_to_host(trees, n)
+        _, logits = eng.verify(seqs, trees, T, want_logits=True)
+        torch.cuda.synchronize()
+        lg = logits.cpu().numpy().reshape(n, T, -1)
+        Ls = [msd_seq_len(eng.ctx, b) for b in seqs]
+        tk, tv, _, _ = eng.kv_views()
+        before_k = [tk[:, b, :, Ls[b]:Ls[b] + T, :].clone() for b in seqs]
+        before_v = [tv[:, b, :, :, Ls[b]:Ls[b] + T].clone() for b in seqs]
+        em, slots = eng.accept_sample(seqs, trees, T, logits, temperature, seed, want_slots=True)
+        torch.cuda.synchronize()
+        sl = slots.cpu().numpy().reshape(n, MAX_TREE)
+        for b in seqs:
+            L, k = Ls[b], len(em[b])
+            path = [int(x) - L for x in sl[b, :k]]
+            r_path, r_emit, dec = S.sample_accept(oracle_tree_of(gts[b]), lg[b], temperature,
+                                                  seed, b, L)
+            assert sampling_agrees(path, em[b], r_path, r_emit, dec), (b, path, r_path)
+            for j, u in enumerate(path):
+                assert torch.equal(tk[:, b, :, L + j, :], before_k[b][:, :, u, :]), (b, j)
+                assert torch.equal(tv[:, b, :, :, L + j], before_v[b][:, :, :, u]), (b, j)
+            assert msd_seq_len(eng.ctx, b) == L + k
+            log(f"[{label} seq {b}] sampled at T={temperature}: path {path}, emitted {em[b]} "
+                f"({'as the oracle' if path == r_path else 'gated'})")
+
 
 @pytest.mark.timeout(240)
 def test_llava7b_two_cycles():
@@ -212,6 +247,7 @@ def test_llava7b_two_cycles():
     try:
         c.cycle([3], "7b c1")
         c.cycle([0], "7b c2")
+        c.sample_cycle(1.0, 2024, "7b c3")
     finally:
         c.close()
 
@@ -243,9 +279,10 @@ def test_qwen7b_gqa_batch4_ragged():
     n = QWEN7B.prompt_len
     lengths = [n, n - 37, n + 5, n - 100]
     log(f"case: full qwen2.5-vl-7b-shaped, batch 4, L={lengths}")
-    c = Case(QWEN7B, lengths, cycles=1)
+    c = Case(QWEN7B, lengths, cycles=2)
     try:
         c.cycle([0, 1, 3, 6], "qwen")
+        c.sample_cycle(0.8, 99, "qwen sampled")
     finally:
         c.close()
 

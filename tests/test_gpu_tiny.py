@@ -16,7 +16,7 @@ from synth.configs import TINY, TreeShape, chain_paths
 from oracle import model as M
 from oracle import msd as O
 from parity import (compare_dynamic_tree, compare_static_tree, decided, oracle_draft_dynamic,
-                    oracle_draft_static, row_close)
+                    oracle_draft_static, row_close, sampling_agrees)
 
 pytestmark = pytest.mark.gpu
 
@@ -365,6 +365,102 @@ def test_sequence_joins_running_batch(setup):
         print(f"seq {b}: {bad if bad is not None else n_new}/{n_new} equal")
         if bad is not None:
             assert not decided(rows[bad]), (b, bad)
+
+
+def oracle_tree_from(g, T):
+    return O.Tree(np.array(g.token[:T], dtype=np.int32), np.array(g.parent[:T], dtype=np.int32),
+                  np.array(g.depth[:T], dtype=np.int32), np.zeros(T))
+
+
+def test_sample_accept_matches_oracle(setup):
+    """Speculative sampling at temperature > 0: path, slots and emitted tokens
+    equal the oracle's on the GPU's own float32 logits and the same draws
+    (a decision may differ only within float32 rounding of its threshold);
+    the accepted rows are compacted like the greedy rule's."""
+    from oracle import sampling as S
+    from paper_2505_14260_amd.msd import MAX_TREE, msd_seq_len
+    wl, eng, m, prompt = setup
+    print("case: tiny sampling acceptance, 10 cycles at temperatures 1.0 / 0.7", flush=True)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    eng.prefill(0, *prompt)
+    trees = eng.new_trees(1)
+    tk, tv, _, _ = eng.kv_views()
+    deep = 0
+    for cyc in range(10):
+        temp = (1.0, 0.7)[cyc % 2]
+        eng.draft_tree([0], spec, trees)
+        amax, logits = eng.verify([0], trees, T, want_logits=True)
+        L = msd_seq_len(eng.ctx, 0)
+        tree = oracle_tree_from(eng.trees_to_host(trees, 1)[0], T)
+        lg = logits.cpu().numpy().reshape(T, -1)
+        before_k = tk[:, 0, :, L:L + T, :].clone()
+        em, slots = eng.accept_sample([0], trees, T, logits, temp, 4242, want_slots=True)
+        torch.cuda.synchronize()
+        sl = slots.cpu().numpy()[:MAX_TREE]
+        n = len(em[0])
+        path = [int(x) - L for x in sl[:n]]
+        assert all(x == -1 for x in sl[n:])
+        r_path, r_emit, dec = S.sample_accept(tree, lg, temp, 4242, 0, L)
+        same = path == r_path and [int(x) for x in em[0]] == r_emit
+        print(f"cycle {cyc} T={temp}: path {path} emitted {list(em[0])} "
+              f"{'equal' if same else 'gated'}")
+        assert sampling_agrees(path, em[0], r_path, r_emit, dec), (cyc, path, r_path, em, r_emit)
+        assert msd_seq_len(eng.ctx, 0) == L + n
+        for j, u in enumerate(path):
+            assert torch.equal(tk[:, 0, :, L + j, :], before_k[:, :, u, :]), (cyc, j)
+        deep += n > 1
+    print(f"{deep}/10 cycles accepted at least one drafted token")
+
+
+def test_sampling_is_lossless_on_gpu(setup):
+    """Over many cycles the first emitted token follows the target
+    distribution at the root: its randomised probability integral transform
+    under that distribution is uniform (Kolmogorov-Smirnov)."""
+    from scipy import stats
+    from oracle import sampling as S
+    from paper_2505_14260_amd.msd import msd_seq_len
+    wl, eng, m, prompt = setup
+    n_cycles = 240
+    print(f"case: tiny sampling distribution, {n_cycles} cycles at temperature 1", flush=True)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    trees = eng.new_trees(1)
+    rng = np.random.default_rng(0)
+    pit, epoch = [], 0
+    eng.prefill(0, *prompt)
+    for _ in range(n_cycles):
+        if msd_seq_len(eng.ctx, 0) + 2 * T > 256:
+            eng.prefill(0, *prompt)
+            epoch += 1  # a fresh seed: the same lengths come round again
+        eng.draft_tree([0], spec, trees)
+        amax, logits = eng.verify([0], trees, T, want_logits=True)
+        p = S.target_probs(logits[0].cpu().numpy(), 1.0)
+        em, _ = eng.accept_sample([0], trees, T, logits, 1.0, 1000 + epoch)
+        y = int(em[0][0])
+        lo = p[:y].sum()
+        pit.append(lo + rng.random() * p[y])
+    res = stats.kstest(pit, "uniform")
+    print(f"KS statistic {res.statistic:.3f}, p-value {res.pvalue:.3g} over {n_cycles} cycles")
+    assert res.pvalue > 1e-3
+
+
+def test_sample_accept_argument_checks(setup):
+    from paper_2505_14260_amd.msd import MSDError
+    wl, eng, m, prompt = setup
+    print("case: tiny sampling acceptance error paths", flush=True)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    eng.prefill(0, *prompt)
+    trees = eng.new_trees(1)
+    eng.draft_tree([0], spec, trees)
+    amax, logits = eng.verify([0], trees, T, want_logits=True)
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        with pytest.raises(MSDError):
+            eng.accept_sample([0], trees, T, logits, bad, 1)
+    eng.accept_sample([0], trees, T, logits, 1.0, 1)
+    with pytest.raises(MSDError):  # a second acceptance of the same verify
+        eng.accept_sample([0], trees, T, logits, 1.0, 1)
 
 
 def test_stale_cache_slots_never_read(setup):
