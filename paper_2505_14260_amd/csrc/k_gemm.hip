@@ -215,6 +215,170 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
+// Many-row GEMM (prompt rows, large batches): a 128 x 128 output tile per
+// workgroup over all of K, both operands staged through LDS.
+//
+// Per 128-column block of K the workgroup holds two packed weight blocks
+// (tiles 2t and 2t+1, 32 KB, in their packed order) and the X block of its
+// 128 rows (hi and lo halves, 64 KB, XOR-swizzled as in k_gemm).  Waves form
+// a 2 x 2 grid of 64 x 64 sub-tiles: wave (wn, wm) multiplies packed block wn
+// with X rows 64 wm .. 64 wm + 63, 4 x 4 MFMA tiles, hi and lo.
+//
+// Global loads run P blocks ahead through a ring of register stages; the
+// ring has no branch on its loads (past the last block a stage reloads the
+// last one, a cache hit), and the barriers order LDS only, so loads stay in
+// flight across them.  Tiles are dealt XCD by XCD (a workgroup runs on XCD
+// blockIdx % 8), the M tiles of one (N tile, K split) consecutively, so a
+// weight tile is fetched once into that XCD's L2 and reused by its M tiles.
+// Narrow outputs split K so that the grid still covers the chip; each split
+// writes its own partial, summed in split order by the consumer.
+struct BigArgs {
+  const uint16_t* X;
+  int ldx, M, K;
+  const uint16_t* W;
+  const uint16_t* dummy;
+  int n_tiles, nkt, n_nt, n_mt, per_xcd;
+  int ks, kbs;         // K splits, 128-column blocks per split
+  float* part;
+  size_t part_split;   // floats between the partials of consecutive K splits
+  int ldp;
+};
+
+constexpr int BIG_N = 128, BIG_M = 128;
+constexpr int BIG_STAGES = 2;
+constexpr int BIG_XU = 2 * KB / 8;                 // 16-byte units per X row (hi + lo)
+constexpr int BIG_W_UNITS = 2 * BLOCK_ELEMS / 8;  // two packed blocks
+constexpr int BIG_X_UNITS = BIG_M * BIG_XU;
+constexpr int BIG_WQ = BIG_W_UNITS / 256, BIG_XQ = BIG_X_UNITS / 256;  // per thread
+constexpr size_t BIG_LDS = (size_t)(BIG_W_UNITS + BIG_X_UNITS) * 16;
+
+// hi units 0..15 and lo units 16..31 of row m, each half swizzled by m & 15
+MSD_DEV int big_xs_index(int m, int u) { return m * BIG_XU + (u & 16) + ((u & 15) ^ (m & 15)); }
+
+// Workgroup barrier that orders LDS accesses only: global loads issued
+// before it stay in flight.
+MSD_DEV void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+MSD_DEV bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// One block of K: the weight units and the X units of this thread.
+// kb counts blocks from the split's first (kbeg).
+MSD_DEV void big_load(const BigArgs& a, int kbeg, int kb, int m0, const uint16_t* w0,
+                      const uint16_t* w1, u32x4 (&wq)[BIG_WQ], u32x4 (&xq)[BIG_XQ]) {
+#pragma unroll
+  for (int q = 0; q < BIG_WQ; ++q) {
+    const int blk = q >= BIG_WQ / 2;
+    const int ue = threadIdx.x + 256 * (q - blk * (BIG_WQ / 2));
+    const uint16_t* src = blk ? w1 + (w1 == a.dummy ? 0 : (size_t)kb * BLOCK_ELEMS)
+                              : w0 + (size_t)kb * BLOCK_ELEMS;
+    wq[q] = *reinterpret_cast<const u32x4*>(src + (size_t)ue * 8);
+  }
+#pragma unroll
+  for (int q = 0; q < BIG_XQ; ++q) {
+    const int e = threadIdx.x + 256 * q;
+    const int m = e / BIG_XU, u = e - m * BIG_XU;
+    const int col = (kbeg + kb) * KB + 8 * (u & 15);
+    const bool ok = m0 + m < a.M && col < a.K;
+    const uint16_t* src = a.X + (ok ? (size_t)(m0 + m) * a.ldx + (u >= 16 ? a.K : 0) + col : 0);
+    const u32x4 v = *reinterpret_cast<const u32x4*>(src);
+    xq[q] = ok ? v : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int P>
+__global__ __launch_bounds__(256) void k_gemm_big(BigArgs a) {
+  extern __shared__ u32x4 lds_big[];
+  u32x4* const ws = lds_big;
+  u32x4* const xs = lds_big + BIG_W_UNITS;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int i = lane & 15, g = lane >> 4;
+  const int flat = (blockIdx.x & 7) * a.per_xcd + (blockIdx.x >> 3);
+  if (flat >= a.n_nt * a.ks * a.n_mt) return;
+  const int mt = flat % a.n_mt, nk = flat / a.n_mt;
+  const int nt = nk / a.ks, ksp = nk - nt * a.ks;
+  const int m0 = mt * BIG_M;
+  // this split's blocks [kbeg, kbeg + nkt) of the weight's a.nkt
+  const int kbeg = ksp * a.kbs;
+  const int nkt = min(a.kbs, a.nkt - kbeg);
+  const bool has2 = 2 * nt + 1 < a.n_tiles;
+  const uint16_t* const w0 = a.W + ((size_t)(2 * nt) * a.nkt + kbeg) * BLOCK_ELEMS;
+  // a missing second tile reads the zero block (one packed block) instead
+  const uint16_t* const w1 =
+      has2 ? a.W + ((size_t)(2 * nt + 1) * a.nkt + kbeg) * BLOCK_ELEMS : a.dummy;
+  float* const part = a.part + (size_t)ksp * a.part_split;
+
+  u32x4 wr[P][BIG_WQ], xr[P][BIG_XQ];
+#pragma unroll
+  for (int p = 0; p < P; ++p) big_load(a, kbeg, min(p, nkt - 1), m0, w0, w1, wr[p], xr[p]);
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[s][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll 1
+  for (int kb0 = 0; kb0 < nkt; kb0 += P) {
+#pragma unroll
+    for (int r = 0; r < P; ++r) {
+      const int kb = kb0 + r;
+      lds_barrier();  // the previous block's MFMAs are done with the LDS
+#pragma unroll
+      for (int q = 0; q < BIG_WQ; ++q) ws[threadIdx.x + 256 * q] = wr[r][q];
+#pragma unroll
+      for (int q = 0; q < BIG_XQ; ++q) {
+        const int e = threadIdx.x + 256 * q;
+        const int m = e / BIG_XU, u = e - m * BIG_XU;
+        xs[big_xs_index(m, u)] = xr[r][q];
+      }
+      lds_barrier();
+      big_load(a, kbeg, min(kb + P, nkt - 1), m0, w0, w1, wr[r], xr[r]);
+      if (kb < nkt) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          u32x4 af[4], bh[4], bl[4];
+#pragma unroll
+          for (int s = 0; s < 4; ++s) af[s] = ws[wn * (BLOCK_ELEMS / 8) + (s * 4 + c) * 64 + lane];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int m = wm * 64 + t * 16 + i;
+            bh[t] = xs[big_xs_index(m, 4 * g + c)];
+            bl[t] = xs[big_xs_index(m, 16 + 4 * g + c)];
+          }
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(af[s]), as_bf16x8(bh[t]), acc[s][t], 0, 0, 0);
+              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(af[s]), as_bf16x8(bl[t]), acc[s][t], 0, 0, 0);
+            }
+        }
+      }
+    }
+  }
+  // lane holds output row m = (lane & 15) of its M group and four consecutive
+  // weight rows 4 * (lane >> 4) + r of its 16-row slab
+  if (wn == 1 && !has2) return;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int m = m0 + wm * 64 + t * 16 + i;
+    if (m >= a.M) continue;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int n = nt * BIG_N + wn * 64 + s * 16 + 4 * g;
+      *reinterpret_cast<float4*>(part + (size_t)m * a.ldp + n) =
+          make_float4(acc[s][t][0], acc[s][t][1], acc[s][t][2], acc[s][t][3]);
+    }
+  }
+}
+
 // One thread per 16-byte unit of the packed layout.
 __global__ void k_pack(const uint16_t* src, int N, int K, int nkt, size_t units, uint16_t* dst) {
   const size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -319,6 +483,42 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
     else if (pl.MT == 2) launch_mt<2, 1>(grid, a, sc, st);
     else launch_mt<4, 1>(grid, a, sc, st);
   }
+}
+
+int launch_gemm_big(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2,
+                    int N, int K, float* part, size_t part_cap, const uint16_t* dummy,
+                    hipStream_t st) {
+  const int nw = W2 ? 2 : 1;
+  BigArgs a{};
+  a.X = X;
+  a.ldx = ldx;
+  a.M = M;
+  a.K = K;
+  a.dummy = dummy;
+  a.n_tiles = (N + TILE_ROWS - 1) / TILE_ROWS;
+  a.nkt = (K + KB - 1) / KB;
+  a.n_nt = (a.n_tiles + 1) / 2;
+  a.n_mt = (M + BIG_M - 1) / BIG_M;
+  a.ldp = a.n_tiles * TILE_ROWS * nw;
+  a.part_split = (size_t)M * a.ldp;
+  // K splits for grids that would leave most CUs idle (single weights only;
+  // the partials of every split must fit the buffer).  With half the CUs
+  // busy or more, the extra partials cost more than the extra workgroups gain.
+  int ks = 1;
+  if (nw == 1)
+    while (ks < 4 && a.n_nt * a.n_mt * ks < 128 && a.nkt >= 8 * (ks + 1) &&
+           (size_t)(ks + 1) * a.part_split <= part_cap)
+      ++ks;
+  a.kbs = (a.nkt + ks - 1) / ks;
+  a.ks = (a.nkt + a.kbs - 1) / a.kbs;
+  a.per_xcd = (a.n_nt * a.ks * a.n_mt + 7) / 8;
+  const dim3 grid(8 * a.per_xcd);
+  for (int w = 0; w < nw; ++w) {
+    a.W = w ? W2 : W;
+    a.part = part + (size_t)w * a.n_tiles * TILE_ROWS;
+    hipLaunchKernelGGL(k_gemm_big<BIG_STAGES>, grid, dim3(256), BIG_LDS, st, a);
+  }
+  return a.ks;
 }
 
 }  // namespace msd

@@ -70,6 +70,14 @@ constexpr int STAGE_INTS = 1 << 16;
 // GEMM launch shape: about one workgroup per CU streams best (more
 // concurrent weight streams per CU lower the achieved HBM bandwidth).
 constexpr int GEMM_WGS = 256;
+constexpr int CHUNK = 64;         // rows per weight-streaming GEMM launch
+constexpr int BIG_CHUNK = 1024;   // rows per many-row GEMM launch
+// Passes over more rows than this use the many-row GEMM (below it, a few
+// weight-streaming launches of CHUNK rows are faster).
+constexpr int BIG_MIN_ROWS = 256;
+
+// Rows per GEMM launch for a pass over `rows` rows.
+int row_chunk(int rows) { return rows > BIG_MIN_ROWS ? BIG_CHUNK : CHUNK; }
 
 // Bump allocator over the workspace (also used to size it).
 struct Carver {
@@ -108,6 +116,14 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
                           gemm_part_floats(mm, d, 2 * d, 1, GEMM_WGS),
                           gemm_part_floats(mm, m.vocab, d, 1, GEMM_WGS)};
   p.part_floats = *std::max_element(cand, cand + 6);
+  // full products of one many-row launch (every GEMM but the LM head, which
+  // always runs in CHUNK-row launches)
+  if (p.rows_max > BIG_MIN_ROWS) {
+    const size_t big = std::min(BIG_CHUNK, p.rows_max);
+    auto ldp = [](int N, int nw) { return (size_t)(N + 63) / 64 * 64 * nw; };
+    const size_t w = std::max({ldp(p.ld_qkv, 1), ldp(d, 1), ldp(F, 2)});
+    p.part_floats = std::max(p.part_floats, big * w);
+  }
   return p;
 }
 
@@ -340,6 +356,16 @@ enum { GK_QKV = 0, GK_O = 1, GK_DOWN = 2, GK_GATEUP = 3, GK_FC = 4, GK_LMHEAD = 
 // consumer sums.
 int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t* W,
          const uint16_t* W2, int N, int K, Parts* out) {
+  if (M > CHUNK) {
+    if (kind == GK_LMHEAD || M > BIG_CHUNK)
+      return fail(c, MSD_ERR_INVALID_ARG, "internal: GEMM launch with too many rows");
+    const int S = launch_gemm_big(X, ldx, M, W, W2, N, K, c->part, c->plan.part_floats,
+                                  c->gemm_zero, c->st);
+    LAUNCHED(c);
+    const int nt = (N + 63) / 64, nw = W2 ? 2 : 1;
+    *out = Parts{c->part, S, (size_t)M * nt * 64 * nw, nt * 64 * nw, nt * 64};
+    return MSD_OK;
+  }
   const bool tr = c->tracing && ((c->trace_kinds >> kind) & 1) && c->trace.size() < c->trace_cap;
   GemmScratch gs = c->gs;
   if (tr) {
@@ -356,8 +382,6 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
   return MSD_OK;
 }
 
-
-constexpr int CHUNK = 64;  // rows per GEMM launch
 
 // GEMM input of a normalised layer: xn = x * g (split rows) and the per-row
 // sums of squares; the GEMM's consumer applies 1/rms (RMSNorm factored through the
@@ -387,6 +411,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
   const int rows = n_seq * nq;
   const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim, F = m.ffn_dim;
   const int nl = draft ? 1 : m.n_layers;
+  const int ch = row_chunk(rows);
   const int B = c->lim.max_batch, S = c->lim.max_seq;
   const size_t layer_kv = (size_t)B * KV * S * hd;
   for (int l = 0; l < nl; ++l) {
@@ -395,8 +420,8 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     uint16_t* kc = (draft ? c->dk : c->tk) + (size_t)l * layer_kv;
     uint16_t* vc = (draft ? c->dv : c->tv) + (size_t)l * layer_kv;
     Parts pt;
-    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
-      const int mc = std::min(CHUNK, rows - m0);
+    for (int m0 = 0; m0 < rows; m0 += ch) {
+      const int mc = std::min(ch, rows - m0);
       TRY(gemm(c, GK_QKV, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, pw.qkv, nullptr, (H + 2 * KV) * hd,
                d, &pt));
       launch_rope_kv(pt, row_norm(c, m0), mc, H, KV, hd, c->rows.pos + m0, c->rows.seq + m0,
@@ -450,24 +475,24 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       launch_tree_attention(a, c->st);
     }
     LAUNCHED(c);
-    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
-      const int mc = std::min(CHUNK, rows - m0);
+    for (int m0 = 0; m0 < rows; m0 += ch) {
+      const int mc = std::min(ch, rows - m0);
       TRY(gemm(c, GK_O, c->ao + (size_t)m0 * 2 * H * hd, 2 * H * hd, mc, pw.o, nullptr, d, H * hd,
                &pt));
       launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, w.n2, c->xn + (size_t)m0 * 2 * d, nullptr,
                    c->ssq + (size_t)m0 * ssq_blocks(d), c->st);
       LAUNCHED(c);
     }
-    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
-      const int mc = std::min(CHUNK, rows - m0);
+    for (int m0 = 0; m0 < rows; m0 += ch) {
+      const int mc = std::min(ch, rows - m0);
       TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, pw.g, pw.u, F, d, &pt));
       launch_silu(pt, row_norm(c, m0), mc, F, c->act + (size_t)m0 * 2 * F, c->st);
       LAUNCHED(c);
     }
     const bool last = (l + 1 == nl);
     const uint16_t* g_next = last ? final_g : c->layers[l + 1].n1;
-    for (int m0 = 0; m0 < rows; m0 += CHUNK) {
-      const int mc = std::min(CHUNK, rows - m0);
+    for (int m0 = 0; m0 < rows; m0 += ch) {
+      const int mc = std::min(ch, rows - m0);
       TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * 2 * F, 2 * F, mc, pw.d, nullptr, d, F, &pt));
       if (last && final_g) {
         // the final feature h is materialised (LM head input, draft input)
@@ -493,9 +518,10 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
 int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const uint16_t* visual) {
   const int d = c->m.d_model;
   const int rows = n_seq * nq;
+  const int ch = row_chunk(rows);
   Parts pt;
-  for (int m0 = 0; m0 < rows; m0 += CHUNK) {
-    const int mc = std::min(CHUNK, rows - m0);
+  for (int m0 = 0; m0 < rows; m0 += ch) {
+    const int mc = std::min(ch, rows - m0);
     TRY(gemm(c, GK_FC, c->fcin + (size_t)m0 * 4 * d, 4 * d, mc, c->fc_p, nullptr, d, 2 * d, &pt));
     launch_resid(pt, mc, d, RN_SET, c->x + (size_t)m0 * d, visual ? nullptr : c->dlayer.n1,
                  visual ? nullptr : c->xn + (size_t)m0 * 2 * d, nullptr,

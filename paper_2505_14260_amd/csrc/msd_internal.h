@@ -73,6 +73,12 @@ void launch_pack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t s
 GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs);
 // floats of partials for M rows (M <= 64 per launch)
 size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs);
+// Many-row GEMM: products of rows [0, M) into part [S][M][ldp] (same ldp and
+// W2 column offset as the thin plan; S K splits, part_cap floats available);
+// returns S.
+int launch_gemm_big(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2,
+                    int N, int K, float* part, size_t part_cap, const uint16_t* dummy,
+                    hipStream_t st);
 size_t gemm_dummy_elems();
 void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2, int N,
                  int K, float* part, float* sink, const uint16_t* dummy, const GemmScratch& sc,

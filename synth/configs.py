@@ -127,4 +127,14 @@ MINI_GQA = Workload(
     new_tokens=24, seed=1010,
 )
 
-WORKLOADS = {w.name: w for w in (TINY, LLAVA7B, LLAVA13B, LLAVA7B_LONG, QWEN7B, MINI_GQA)}
+# Wider small model with a 320-row prompt for the many-row GEMM: an odd
+# number of 64-row FFN tiles, a partial last 128-column block and K splits.
+WIDE = Workload(
+    name="wide-gqa-2L-d1024",
+    dims=ModelDims(2, 1024, 8, 2, 128, 2880, 4096, 1e4, 1e-5),
+    n_visual=256, n_text=64, visual_scale=1.0 / 32,
+    tree=TreeShape("static", 3, tuple(full_tree_paths(3, 2))),
+    new_tokens=16, seed=1011,
+)
+
+WORKLOADS = {w.name: w for w in (TINY, LLAVA7B, LLAVA13B, LLAVA7B_LONG, QWEN7B, MINI_GQA, WIDE)}

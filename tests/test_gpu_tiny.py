@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import synth
-from synth.configs import TINY, TreeShape, chain_paths
+from synth.configs import TINY, WIDE, TreeShape, chain_paths
 from oracle import model as M
 from oracle import msd as O
 from parity import (compare_dynamic_tree, compare_static_tree, decided, oracle_draft_dynamic,
@@ -87,6 +87,45 @@ def test_prefill_kv_and_first_token(setup):
     kg = bits_to_f64(dk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
     ok, err = row_close(kg, st.dkv.k[0, :n].reshape(n, -1))
     assert ok, ("draft K", err)
+
+
+def test_prefill_many_rows_wide():
+    """A 320-row prompt through the many-row GEMM path (K splits, an odd FFN
+    tile count, a partial last K block): every layer's K/V, the first token
+    and the draft cache against the oracle."""
+    from paper_2505_14260_amd.msd import Engine
+    wl = WIDE
+    dims = wl.dims
+    print(f"case: prefill {wl.name} n={wl.prompt_len}", flush=True)
+    w = synth.make_target_weights(dims, wl.seed)
+    dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
+    prompt = synth.make_prompt(wl)
+    m = O.Models(dims, w, dr)
+    eng = Engine(dims, w, dr, max_batch=1, max_seq=512, max_tree=64, max_prompt=wl.prompt_len)
+    try:
+        first = eng.prefill(0, *prompt)
+        st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=512)
+        if decided(logits[-1]):
+            assert first == f_ref
+        n = wl.prompt_len
+        tk, tv, dk, dv = eng.kv_views()
+        torch.cuda.synchronize()
+        worst = 0.0
+        for l in range(dims.n_layers):
+            kg = bits_to_f64(tk[l, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+            vg = bits_to_f64(tv[l, 0, :, :, :n].permute(2, 0, 1).reshape(n, -1))
+            ok, err = row_close(kg, st.kv.k[l, :n].reshape(n, -1))
+            assert ok, (l, "K", err)
+            ok2, err2 = row_close(vg, st.kv.v[l, :n].reshape(n, -1))
+            assert ok2, (l, "V", err2)
+            worst = max(worst, err, err2)
+        O.draft_catch_up(m, st)
+        kg = bits_to_f64(dk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        ok, err = row_close(kg, st.dkv.k[0, :n].reshape(n, -1))
+        assert ok, ("draft K", err)
+        print(f"target K/V max rel err {worst:.2e}, draft K {err:.2e}")
+    finally:
+        eng.close()
 
 
 def test_verify_logits_on_fixed_tree(setup):
