@@ -215,14 +215,16 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
-// Many-row GEMM (prompt rows, large batches): a 128 x 128 output tile per
-// workgroup over all of K, both operands staged through LDS.
+// Many-row GEMM (prompt rows, large batches): a (64 NB) x 128 output tile
+// per workgroup over all of K, both operands staged through LDS.
 //
-// Per 128-column block of K the workgroup holds two packed weight blocks
-// (tiles 2t and 2t+1, 32 KB, in their packed order) and the X block of its
-// 128 rows (hi and lo halves, 64 KB, XOR-swizzled as in k_gemm).  Waves form
-// a 2 x 2 grid of 64 x 64 sub-tiles: wave (wn, wm) multiplies packed block wn
-// with X rows 64 wm .. 64 wm + 63, 4 x 4 MFMA tiles, hi and lo.
+// Per 128-column block of K the workgroup holds NB packed weight blocks
+// (tiles NB t .. NB t + NB - 1, 16 KB each, in their packed order) and the X
+// block of its 128 rows (hi and lo halves, 64 KB, XOR-swizzled as in
+// k_gemm).  Waves form a 2 x 2 grid: wave (wn, wm) multiplies packed blocks
+// NB/2 wn .. NB/2 wn + NB/2 - 1 with X rows 64 wm .. 64 wm + 63, in 16 x 16
+// MFMA tiles, hi and lo.  Wider tiles reuse each X fragment read from LDS
+// for more MFMAs.
 //
 // Global loads run P blocks ahead through a ring of register stages; the
 // ring has no branch on its loads (past the last block a stage reloads the
@@ -244,13 +246,19 @@ struct BigArgs {
   int ldp;
 };
 
-constexpr int BIG_N = 128, BIG_M = 128;
-constexpr int BIG_STAGES = 2;
-constexpr int BIG_XU = 2 * KB / 8;                 // 16-byte units per X row (hi + lo)
-constexpr int BIG_W_UNITS = 2 * BLOCK_ELEMS / 8;  // two packed blocks
+constexpr int BIG_M = 128;
+// Launched configurations: four packed blocks per N tile with one register
+// stage (the registers of a second stage would spill) from 512 rows on; two
+// blocks with two stages below, where the wider tiles leave too few
+// workgroups for the chip.
+constexpr int BIG_WIDE_ROWS = 512;
+constexpr int BIG_XU = 2 * KB / 8;                  // 16-byte units per X row (hi + lo)
 constexpr int BIG_X_UNITS = BIG_M * BIG_XU;
-constexpr int BIG_WQ = BIG_W_UNITS / 256, BIG_XQ = BIG_X_UNITS / 256;  // per thread
-constexpr size_t BIG_LDS = (size_t)(BIG_W_UNITS + BIG_X_UNITS) * 16;
+constexpr int BIG_XQ = BIG_X_UNITS / 256;           // X units per thread
+__host__ __device__ constexpr int big_w_units(int NB) { return NB * BLOCK_ELEMS / 8; }
+__host__ __device__ constexpr size_t big_lds(int NB) {
+  return (size_t)(big_w_units(NB) + BIG_X_UNITS) * 16;
+}
 
 // hi units 0..15 and lo units 16..31 of row m, each half swizzled by m & 15
 MSD_DEV int big_xs_index(int m, int u) { return m * BIG_XU + (u & 16) + ((u & 15) ^ (m & 15)); }
@@ -265,16 +273,19 @@ MSD_DEV void lds_barrier() {
 
 MSD_DEV bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// One block of K: the weight units and the X units of this thread.
-// kb counts blocks from the split's first (kbeg).
-MSD_DEV void big_load(const BigArgs& a, int kbeg, int kb, int m0, const uint16_t* w0,
-                      const uint16_t* w1, u32x4 (&wq)[BIG_WQ], u32x4 (&xq)[BIG_XQ]) {
+// One block of K (kb counts from the split's first block kbeg): the weight
+// units and the X units of this thread.  wt[j] is packed tile j of the
+// workgroup's N tile at block kbeg (the zero block for tiles past N, which
+// then takes no block offset).
+template <int NB>
+MSD_DEV void big_load(const BigArgs& a, int kbeg, int kb, int m0,
+                      const uint16_t* const (&wt)[NB], u32x4 (&wq)[NB * 4],
+                      u32x4 (&xq)[BIG_XQ]) {
 #pragma unroll
-  for (int q = 0; q < BIG_WQ; ++q) {
-    const int blk = q >= BIG_WQ / 2;
-    const int ue = threadIdx.x + 256 * (q - blk * (BIG_WQ / 2));
-    const uint16_t* src = blk ? w1 + (w1 == a.dummy ? 0 : (size_t)kb * BLOCK_ELEMS)
-                              : w0 + (size_t)kb * BLOCK_ELEMS;
+  for (int q = 0; q < NB * 4; ++q) {
+    const int j = q / 4;  // packed block of this unit
+    const int ue = threadIdx.x + 256 * (q % 4);
+    const uint16_t* src = wt[j] + (wt[j] == a.dummy ? 0 : (size_t)kb * BLOCK_ELEMS);
     wq[q] = *reinterpret_cast<const u32x4*>(src + (size_t)ue * 8);
   }
 #pragma unroll
@@ -289,11 +300,15 @@ MSD_DEV void big_load(const BigArgs& a, int kbeg, int kb, int m0, const uint16_t
   }
 }
 
-template <int P>
+template <int NB, int P>
 __global__ __launch_bounds__(256) void k_gemm_big(BigArgs a) {
+  static_assert(NB == 2 || NB == 4, "two or four packed blocks per N tile");
+  constexpr int WB = NB / 2;      // packed blocks per wave
+  constexpr int SL = 4 * WB;      // 16-row weight slabs per wave
+  constexpr int WU = big_w_units(NB);
   extern __shared__ u32x4 lds_big[];
   u32x4* const ws = lds_big;
-  u32x4* const xs = lds_big + BIG_W_UNITS;
+  u32x4* const xs = lds_big + WU;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wn = wave & 1, wm = wave >> 1;
   const int i = lane & 15, g = lane >> 4;
@@ -305,20 +320,21 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigArgs a) {
   // this split's blocks [kbeg, kbeg + nkt) of the weight's a.nkt
   const int kbeg = ksp * a.kbs;
   const int nkt = min(a.kbs, a.nkt - kbeg);
-  const bool has2 = 2 * nt + 1 < a.n_tiles;
-  const uint16_t* const w0 = a.W + ((size_t)(2 * nt) * a.nkt + kbeg) * BLOCK_ELEMS;
-  // a missing second tile reads the zero block (one packed block) instead
-  const uint16_t* const w1 =
-      has2 ? a.W + ((size_t)(2 * nt + 1) * a.nkt + kbeg) * BLOCK_ELEMS : a.dummy;
+  const uint16_t* wt[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int tile = NB * nt + j;
+    wt[j] = tile < a.n_tiles ? a.W + ((size_t)tile * a.nkt + kbeg) * BLOCK_ELEMS : a.dummy;
+  }
   float* const part = a.part + (size_t)ksp * a.part_split;
 
-  u32x4 wr[P][BIG_WQ], xr[P][BIG_XQ];
+  u32x4 wr[P][NB * 4], xr[P][BIG_XQ];
 #pragma unroll
-  for (int p = 0; p < P; ++p) big_load(a, kbeg, min(p, nkt - 1), m0, w0, w1, wr[p], xr[p]);
+  for (int p = 0; p < P; ++p) big_load<NB>(a, kbeg, min(p, nkt - 1), m0, wt, wr[p], xr[p]);
 
-  f32x4 acc[4][4];
+  f32x4 acc[SL][4];
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
+  for (int s = 0; s < SL; ++s)
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[s][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -329,7 +345,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigArgs a) {
       const int kb = kb0 + r;
       lds_barrier();  // the previous block's MFMAs are done with the LDS
 #pragma unroll
-      for (int q = 0; q < BIG_WQ; ++q) ws[threadIdx.x + 256 * q] = wr[r][q];
+      for (int q = 0; q < NB * 4; ++q) ws[(q / 4) * 1024 + threadIdx.x + 256 * (q % 4)] = wr[r][q];
 #pragma unroll
       for (int q = 0; q < BIG_XQ; ++q) {
         const int e = threadIdx.x + 256 * q;
@@ -337,13 +353,11 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigArgs a) {
         xs[big_xs_index(m, u)] = xr[r][q];
       }
       lds_barrier();
-      big_load(a, kbeg, min(kb + P, nkt - 1), m0, w0, w1, wr[r], xr[r]);
+      big_load<NB>(a, kbeg, min(kb + P, nkt - 1), m0, wt, wr[r], xr[r]);
       if (kb < nkt) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          u32x4 af[4], bh[4], bl[4];
-#pragma unroll
-          for (int s = 0; s < 4; ++s) af[s] = ws[wn * (BLOCK_ELEMS / 8) + (s * 4 + c) * 64 + lane];
+          u32x4 bh[4], bl[4];
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
             const int m = wm * 64 + t * 16 + i;
@@ -351,28 +365,33 @@ __global__ __launch_bounds__(256) void k_gemm_big(BigArgs a) {
             bl[t] = xs[big_xs_index(m, 16 + 4 * g + c)];
           }
 #pragma unroll
-          for (int s = 0; s < 4; ++s)
+          for (int s = 0; s < SL; ++s) {
+            // slab s: packed block WB wn + s / 4, wave-slab s % 4
+            const u32x4 af = ws[(WB * wn + s / 4) * 1024 + ((s % 4) * 4 + c) * 64 + lane];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  as_bf16x8(af[s]), as_bf16x8(bh[t]), acc[s][t], 0, 0, 0);
-              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  as_bf16x8(af[s]), as_bf16x8(bl[t]), acc[s][t], 0, 0, 0);
+              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(af), as_bf16x8(bh[t]),
+                                                                   acc[s][t], 0, 0, 0);
+              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(af), as_bf16x8(bl[t]),
+                                                                   acc[s][t], 0, 0, 0);
             }
+          }
         }
       }
     }
   }
   // lane holds output row m = (lane & 15) of its M group and four consecutive
-  // weight rows 4 * (lane >> 4) + r of its 16-row slab
-  if (wn == 1 && !has2) return;
+  // weight rows 4 * (lane >> 4) + r of its 16-row slab; slabs of tiles past
+  // N are not stored
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int m = m0 + wm * 64 + t * 16 + i;
     if (m >= a.M) continue;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int n = nt * BIG_N + wn * 64 + s * 16 + 4 * g;
+    for (int s = 0; s < SL; ++s) {
+      const int tile = NB * nt + WB * wn + s / 4;
+      if (tile >= a.n_tiles) continue;
+      const int n = tile * TILE_ROWS + (s % 4) * 16 + 4 * g;
       *reinterpret_cast<float4*>(part + (size_t)m * a.ldp + n) =
           make_float4(acc[s][t][0], acc[s][t][1], acc[s][t][2], acc[s][t][3]);
     }
@@ -497,7 +516,9 @@ int launch_gemm_big(const uint16_t* X, int ldx, int M, const uint16_t* W, const 
   a.dummy = dummy;
   a.n_tiles = (N + TILE_ROWS - 1) / TILE_ROWS;
   a.nkt = (K + KB - 1) / KB;
-  a.n_nt = (a.n_tiles + 1) / 2;
+  const bool wide = M >= BIG_WIDE_ROWS;
+  const int NB = wide ? 4 : 2;
+  a.n_nt = (a.n_tiles + NB - 1) / NB;
   a.n_mt = (M + BIG_M - 1) / BIG_M;
   a.ldp = a.n_tiles * TILE_ROWS * nw;
   a.part_split = (size_t)M * a.ldp;
@@ -516,7 +537,10 @@ int launch_gemm_big(const uint16_t* X, int ldx, int M, const uint16_t* W, const 
   for (int w = 0; w < nw; ++w) {
     a.W = w ? W2 : W;
     a.part = part + (size_t)w * a.n_tiles * TILE_ROWS;
-    hipLaunchKernelGGL(k_gemm_big<BIG_STAGES>, grid, dim3(256), BIG_LDS, st, a);
+    if (wide)
+      hipLaunchKernelGGL((k_gemm_big<4, 1>), grid, dim3(256), big_lds(4), st, a);
+    else
+      hipLaunchKernelGGL((k_gemm_big<2, 2>), grid, dim3(256), big_lds(2), st, a);
   }
   return a.ks;
 }

@@ -89,22 +89,25 @@ def test_prefill_kv_and_first_token(setup):
     assert ok, ("draft K", err)
 
 
-def test_prefill_many_rows_wide():
-    """A 320-row prompt through the many-row GEMM path (K splits, an odd FFN
-    tile count, a partial last K block): every layer's K/V, the first token
-    and the draft cache against the oracle."""
+@pytest.mark.parametrize("n_visual", [256, 480])
+def test_prefill_many_rows_wide(n_visual):
+    """A 320- or 544-row prompt through the many-row GEMM path (both tile
+    widths, K splits, an odd FFN tile count, a partial last K block, tiles
+    past N): every layer's K/V, the first token and the draft cache against
+    the oracle."""
+    import dataclasses
     from paper_2505_14260_amd.msd import Engine
-    wl = WIDE
+    wl = dataclasses.replace(WIDE, n_visual=n_visual)
     dims = wl.dims
     print(f"case: prefill {wl.name} n={wl.prompt_len}", flush=True)
     w = synth.make_target_weights(dims, wl.seed)
     dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
     prompt = synth.make_prompt(wl)
     m = O.Models(dims, w, dr)
-    eng = Engine(dims, w, dr, max_batch=1, max_seq=512, max_tree=64, max_prompt=wl.prompt_len)
+    eng = Engine(dims, w, dr, max_batch=1, max_seq=1024, max_tree=64, max_prompt=wl.prompt_len)
     try:
         first = eng.prefill(0, *prompt)
-        st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=512)
+        st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=1024)
         if decided(logits[-1]):
             assert first == f_ref
         n = wl.prompt_len
