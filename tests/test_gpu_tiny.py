@@ -89,12 +89,12 @@ def test_prefill_kv_and_first_token(setup):
     assert ok, ("draft K", err)
 
 
-@pytest.mark.parametrize("n_visual", [256, 480])
+@pytest.mark.parametrize("n_visual", [256, 480, 1036])
 def test_prefill_many_rows_wide(n_visual):
-    """A 320- or 544-row prompt through the many-row GEMM path (both tile
-    widths, K splits, an odd FFN tile count, a partial last K block, tiles
-    past N): every layer's K/V, the first token and the draft cache against
-    the oracle."""
+    """320-, 544- and 1100-row prompts through the many-row GEMM path (both
+    tile widths, K splits, an odd FFN tile count, a partial last K block,
+    tiles past N; 1100 rows = one 1024-row launch plus a 76-row one): every
+    layer's K/V, the first token and the draft cache against the oracle."""
     import dataclasses
     from paper_2505_14260_amd.msd import Engine
     wl = dataclasses.replace(WIDE, n_visual=n_visual)
@@ -104,10 +104,11 @@ def test_prefill_many_rows_wide(n_visual):
     dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
     prompt = synth.make_prompt(wl)
     m = O.Models(dims, w, dr)
-    eng = Engine(dims, w, dr, max_batch=1, max_seq=1024, max_tree=64, max_prompt=wl.prompt_len)
+    max_seq = (wl.prompt_len + 64 + 255) // 256 * 256
+    eng = Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64, max_prompt=wl.prompt_len)
     try:
         first = eng.prefill(0, *prompt)
-        st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=1024)
+        st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=max_seq)
         if decided(logits[-1]):
             assert first == f_ref
         n = wl.prompt_len
