@@ -7,6 +7,9 @@ speedup_ratio: normal-decoding time over speculative-decoding time for N
 output tokens including the prompt-processing time, with per-token target
 time T_p, draft time T_q per drafted token and verification time T_v.
 tau: mean tokens emitted per draft-verify cycle.
+n_alpha: acceptance rate of the n-th drafted token of chain drafts (one token
+per draft forward, Sec. 5.1.3): of the cycles whose first n-1 drafted tokens
+were accepted, so that the n-th was judged, the fraction that accepted it.
 """
 
 
@@ -24,3 +27,15 @@ def speedup_ratio(N, T_p, T_q, T_v, gamma, alpha, T_prompt):
 def tau(emitted_per_cycle):
     n = len(emitted_per_cycle)
     return sum(emitted_per_cycle) / n if n else 0.0
+
+
+def n_alpha(accepted_per_cycle, gamma):
+    """[n-alpha for n = 1..gamma] from the number of accepted drafted tokens
+    of each chain cycle (None where no cycle reached position n)."""
+    out = []
+    for n in range(1, gamma + 1):
+        judged = sum(1 for a in accepted_per_cycle if a >= n - 1)
+        accepted = sum(1 for a in accepted_per_cycle if a >= n)
+        out.append(accepted / judged if judged else None)
+    return out
+

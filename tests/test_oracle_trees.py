@@ -238,3 +238,23 @@ def test_speedup_ratio_limits():
     assert np.isclose(metrics.speedup_ratio(100, 1.0, 0.0, 1.0, 4, 0.0, 0.0), 1.0)
     # perfect acceptance, free drafting, verify == one step -> gamma + 1
     assert np.isclose(metrics.speedup_ratio(100, 1.0, 0.0, 1.0, 4, 1.0, 0.0), 5.0)
+
+
+def test_n_alpha_counts_and_iid_limit():
+    # hand count: cycles accepting 0, 1, 3, 3 of a 3-token chain
+    assert metrics.n_alpha([0, 1, 3, 3], 3) == [3 / 4, 2 / 3, 2 / 2]
+    assert metrics.n_alpha([0, 0], 2) == [0.0, None]
+    # independent acceptance with probability alpha at every position: each
+    # n-alpha estimates alpha, and the mean emitted tokens is omega
+    rng = np.random.default_rng(5)
+    alpha, gamma = 0.6, 5
+    acc = []
+    for _ in range(40000):
+        a = 0
+        while a < gamma and rng.random() < alpha:
+            a += 1
+        acc.append(a)
+    for v in metrics.n_alpha(acc, gamma):
+        assert abs(v - alpha) < 0.02
+    assert abs(np.mean(acc) + 1 - metrics.omega(gamma, alpha)) < 0.02
+
