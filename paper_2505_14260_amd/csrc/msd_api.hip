@@ -457,13 +457,13 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       a.qtiles = (nq * G + 31) / 32;
       // key chunks: each of a workgroup's TREE_WAVES waves takes
       // chunk_keys / TREE_WAVES keys (a multiple of 32); enough chunks for
-      // about 192 workgroups while every wave keeps at least one block (a
-      // wave hides little latency behind its own blocks, so spreading the
+      // about one workgroup per CU while every wave keeps at least one block
+      // (a wave hides little latency behind its own blocks, so spreading the
       // keys over more CUs pays until the combine pass dominates)
       const int span = 32 * TREE_WAVES;
       const int base_items = n_seq * KV * a.qtiles;
       const int max_chunks = std::max(1, (max_ltot + span - 1) / span);
-      const int chunks = std::min(max_chunks, std::max(1, (192 + base_items - 1) / base_items));
+      const int chunks = std::min(max_chunks, std::max(1, (256 + base_items - 1) / base_items));
       int ck = (max_ltot + chunks - 1) / chunks;
       ck = (ck + span - 1) / span * span;
       while ((max_ltot + ck - 1) / ck > ATT_MAX_CHUNKS ||
