@@ -132,6 +132,51 @@ def test_prefill_many_rows_wide(n_visual):
         eng.close()
 
 
+def test_bitwise_deterministic(setup):
+    """Two identical runs give bitwise-equal caches, trees and logits (every
+    reduction has a fixed order; a race would show here)."""
+    import dataclasses
+    from paper_2505_14260_amd.msd import Engine
+    wl, eng, m, prompt = setup
+    print("case: determinism, tiny cycle twice and a 544-row wide prefill twice", flush=True)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    n = wl.prompt_len
+    tk, tv, dk, dv = eng.kv_views()
+    trees = eng.new_trees(1)
+    runs = []
+    for _ in range(2):
+        eng.prefill(0, *prompt)
+        eng.draft_tree([0], spec, trees)
+        amax, logits = eng.verify([0], trees, T, want_logits=True)
+        torch.cuda.synchronize()
+        runs.append([tk[:, 0, :, :n + T].clone(), tv[:, 0, :, :, :n + T].clone(),
+                     dk[:, 0, :, :n].clone(), dv[:, 0, :, :, :n].clone(), trees.clone(),
+                     amax.clone(), logits.clone()])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+    wide = dataclasses.replace(WIDE, n_visual=480)
+    w = synth.make_target_weights(wide.dims, wide.seed)
+    dr = synth.make_draft_weights(wide.dims, w, wide.seed, wide.draft_fc_mode)
+    wp = synth.make_prompt(wide)
+    e2 = Engine(wide.dims, w, dr, max_batch=1, max_seq=1024, max_tree=64,
+                max_prompt=wide.prompt_len)
+    try:
+        kvs = []
+        for _ in range(2):
+            first = e2.prefill(0, *wp)
+            k2, v2, d2, _ = e2.kv_views()
+            torch.cuda.synchronize()
+            kvs.append((first, k2[:, 0, :, :wide.prompt_len].clone(),
+                        v2[:, 0, :, :, :wide.prompt_len].clone(),
+                        d2[:, 0, :, :wide.prompt_len].clone()))
+        assert kvs[0][0] == kvs[1][0]
+        for a, b in zip(kvs[0][1:], kvs[1][1:]):
+            assert torch.equal(a, b)
+    finally:
+        e2.close()
+
+
 def test_verify_logits_on_fixed_tree(setup):
     wl, eng, m, prompt = setup
     print("case: verify tiny fixed tree", flush=True)
