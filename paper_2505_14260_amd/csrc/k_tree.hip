@@ -222,58 +222,101 @@ __global__ void k_dyn_expand(DynPool pool, const int* topk_idx, const float* top
 
 // Final tree: best N of the pool (score desc, creation asc), laid out by
 // (depth, creation) with the root as node 0.
-__global__ void k_dyn_finalize(DynPool pool, msd_tree* trees, const int* seq_ids,
-                               const int* d_root, int n_pool, int N) {
-  __shared__ int node_of[1024];
+// The tree of one sequence from its candidate pool: the N best candidates
+// (score descending, then creation order) in canonical order (depth, then
+// creation order).  A bitonic sort of the (score, index) keys in LDS puts
+// the N best first; the kept candidates are then ordered by counting over
+// at most MSD_MAX_TREE entries, and each node builds its ancestor mask by
+// walking up its parent chain in LDS.
+constexpr int FIN_THREADS = 1024;  // >= the pool capacity (a power of two)
+
+__global__ __launch_bounds__(FIN_THREADS) void k_dyn_finalize(DynPool pool, msd_tree* trees,
+                                                              const int* seq_ids,
+                                                              const int* d_root, int n_pool,
+                                                              int N) {
+  __shared__ float ks[FIN_THREADS];
+  __shared__ int ki[FIN_THREADS];
+  __shared__ int node_of[FIN_THREADS];
+  __shared__ int kept[MSD_MAX_TREE], kdep[MSD_MAX_TREE];
   __shared__ int keep[MSD_MAX_TREE];
+  __shared__ int par[MSD_MAX_TREE];
   const int sidx = blockIdx.x;
   const size_t base = (size_t)sidx * pool.cap;
-  for (int i = threadIdx.x; i < n_pool; i += blockDim.x) {
-    const float si = pool.score[base + i];
-    int rank = 0;
-    for (int q = 0; q < n_pool; ++q) rank += better_score(pool.score[base + q], q, si, i) ? 1 : 0;
-    node_of[i] = (rank < N) ? 1 : 0;
+  const int i = threadIdx.x;
+  // past the pool: -inf keys with indices after every candidate
+  ks[i] = i < n_pool ? pool.score[base + i] : -INFINITY;
+  ki[i] = i;
+  node_of[i] = 0;
+  __syncthreads();
+  // best first: "less" is better_score
+  for (int k = 2; k <= FIN_THREADS; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const int l = i ^ j;
+      if (l > i) {
+        const float si = ks[i], sl = ks[l];
+        const int ii = ki[i], il = ki[l];
+        const bool up = (i & k) == 0;
+        if (up ? better_score(sl, il, si, ii) : better_score(si, ii, sl, il)) {
+          ks[i] = sl;
+          ks[l] = si;
+          ki[i] = il;
+          ki[l] = ii;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (i < N) {
+    kept[i] = ki[i];
+    kdep[i] = pool.depth[base + ki[i]];
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < n_pool; i += blockDim.x) {
-    if (!node_of[i]) continue;
-    const int di = pool.depth[base + i];
+  // canonical position of kept candidate i among the N kept
+  if (i < N) {
+    const int c = kept[i], dc = kdep[i];
     int pos = 0;
-    for (int q = 0; q < n_pool; ++q)
-      if (node_of[q] && (pool.depth[base + q] < di || (pool.depth[base + q] == di && q < i)))
-        ++pos;
-    keep[pos] = i;
+    for (int q = 0; q < N; ++q)
+      pos += (int)(kdep[q] < dc) | ((int)(kdep[q] == dc) & (int)(kept[q] < c));
+    keep[pos] = c;
   }
   __syncthreads();
-  for (int n = threadIdx.x; n < N; n += blockDim.x) node_of[keep[n]] = 2 + n;
+  if (i < N) node_of[keep[i]] = 2 + i;
   __syncthreads();
   msd_tree* t = trees + sidx;
-  if (threadIdx.x == 0) {
-    t->n_nodes = N + 1;
-    t->token[0] = d_root[seq_ids[sidx]];
-    t->parent[0] = -1;
-    t->depth[0] = 0;
-    t->score[0] = 0.f;
-    t->anc[0] = 1ull;
-    for (int n = 1; n <= N; ++n) {
-      const int i = keep[n - 1];
-      const int p = pool.parent[base + i];
+  if (i < MSD_MAX_TREE) {
+    int tok = 0, pn = -1, d = 0;
+    float s = 0.f;
+    if (i == 0) {
+      tok = d_root[seq_ids[sidx]];
+    } else if (i <= N) {
+      const int c = keep[i - 1];
+      const int p = pool.parent[base + c];
       // a kept node's parent is always kept (scores never increase along a
-      // path); the guard only keeps a malformed pool inside the tree arrays
-      const int pn = (p < 0 || node_of[p] < 2) ? 0 : node_of[p] - 1;
-      t->token[n] = pool.tok[base + i];
-      t->parent[n] = pn;
-      t->depth[n] = pool.depth[base + i];
-      t->score[n] = pool.score[base + i];
-      t->anc[n] = t->anc[pn] | (1ull << n);
+      // path) and comes earlier; the guard only keeps a malformed pool
+      // inside the tree arrays
+      pn = (p < 0 || p >= n_pool || node_of[p] < 2) ? 0 : node_of[p] - 1;
+      tok = pool.tok[base + c];
+      d = pool.depth[base + c];
+      s = pool.score[base + c];
     }
-    for (int n = N + 1; n < MSD_MAX_TREE; ++n) {
-      t->token[n] = 0;
-      t->parent[n] = -1;
-      t->depth[n] = 0;
-      t->score[n] = 0.f;
-      t->anc[n] = 0ull;
+    par[i] = pn;
+    t->token[i] = tok;
+    t->parent[i] = pn;
+    t->depth[i] = d;
+    t->score[i] = s;
+  }
+  if (i == 0) t->n_nodes = N + 1;
+  __syncthreads();
+  if (i < MSD_MAX_TREE) {
+    uint64_t m = 0ull;
+    if (i <= N) {
+      int u = i;
+      for (int step = 0; step < MSD_MAX_TREE && u >= 0; ++step) {
+        m |= 1ull << u;
+        u = (u == 0 || par[u] >= u) ? -1 : par[u];
+      }
     }
+    t->anc[i] = m;
   }
 }
 
@@ -457,8 +500,8 @@ void launch_dyn_expand(DynPool pool, int n_seq, const int* topk_idx, const float
 
 void launch_dyn_finalize(DynPool pool, void* trees, int n_seq, const int* seq_ids,
                          const int* d_root, int n_pool, int N, hipStream_t st) {
-  hipLaunchKernelGGL(k_dyn_finalize, dim3(n_seq), dim3(256), 0, st, pool, (msd_tree*)trees,
-                     seq_ids, d_root, n_pool, N);
+  hipLaunchKernelGGL(k_dyn_finalize, dim3(n_seq), dim3(FIN_THREADS), 0, st, pool,
+                     (msd_tree*)trees, seq_ids, d_root, n_pool, N);
 }
 
 void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
