@@ -398,6 +398,20 @@ __global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, 
   block_merge(wv, wi, k, cand_v + (size_t)blockIdx.x * k, cand_i + (size_t)blockIdx.x * k);
 }
 
+// (m, t) <- the merge of two (max, sum of exp(x - max)) pairs.
+MSD_DEV void lse_merge(float& m, float& t, float m2, float t2) {
+  if (m2 == -INFINITY) return;
+  if (m == -INFINITY) {
+    m = m2;
+    t = t2;
+  } else if (m2 > m) {
+    t = t * __expf(m - m2) + t2;
+    m = m2;
+  } else {
+    t += t2 * __expf(m2 - m);
+  }
+}
+
 // One block per row merges its slices' candidates (n_slices * k of them,
 // at most 256 * TOPK_MERGE_PER) and their logsumexp parts.
 __global__ __launch_bounds__(256) void k_topk_merge(int k, int n_slices, const float* cand_v,
@@ -427,14 +441,24 @@ __global__ __launch_bounds__(256) void k_topk_merge(int k, int n_slices, const f
     out_idx[(size_t)row * k + threadIdx.x] = fi[threadIdx.x];
     if (out_val) out_val[(size_t)row * k + threadIdx.x] = fv[threadIdx.x];
   }
-  if (threadIdx.x == 0 && out_lse) {
+  if (out_lse) {
+    // logsumexp over the slices' (max, sum of exp) pairs: every thread merges
+    // its slices, then the waves and the block merge in a fixed order
     const float2* st = stats + (size_t)row * n_slices;
-    float M = -INFINITY;
-    for (int q = 0; q < n_slices; ++q) M = fmaxf(M, st[q].x);
-    float tot = 0.f;
-    for (int q = 0; q < n_slices; ++q)
-      tot += (st[q].x == -INFINITY) ? 0.f : st[q].y * __expf(st[q].x - M);
-    out_lse[row] = M + __logf(tot);
+    float m = -INFINITY, t = 0.f;
+    for (int q = threadIdx.x; q < n_slices; q += 256) lse_merge(m, t, st[q].x, st[q].y);
+    for (int o = 32; o > 0; o >>= 1) lse_merge(m, t, __shfl_xor(m, o), __shfl_xor(t, o));
+    __shared__ float lm[4], lt[4];
+    if ((threadIdx.x & 63) == 0) {
+      lm[threadIdx.x >> 6] = m;
+      lt[threadIdx.x >> 6] = t;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float M = -INFINITY, T = 0.f;
+      for (int w = 0; w < 4; ++w) lse_merge(M, T, lm[w], lt[w]);
+      out_lse[row] = M + __logf(T);
+    }
   }
 }
 
