@@ -437,16 +437,37 @@ __global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
   const int sidx = t / a.KV;
   const int G = a.H / a.KV;
   const int nc = a.n_chunks;
+  // chunks in groups of 8 with every load of a group in flight (indices past
+  // the last chunk reload it and are not used); sums stay in chunk order
+  constexpr int CG = 8;
   if (threadIdx.x < 32) {
     const int j = threadIdx.x;
     float M = -INFINITY;
-    for (int c = 0; c < nc; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
+    for (int c0 = 0; c0 < nc; c0 += CG) {
+      float2 ml[CG];
+#pragma unroll
+      for (int q = 0; q < CG; ++q)
+        ml[q] = *reinterpret_cast<const float2*>(a.part_ml + (item0 + min(c0 + q, nc - 1)) * 64 +
+                                                 2 * j);
+#pragma unroll
+      for (int q = 0; q < CG; ++q)
+        if (c0 + q < nc) M = fmaxf(M, ml[q].x);
+    }
     float den = 0.f;
-    for (int c = 0; c < nc; ++c) {
-      const float mc = a.part_ml[(item0 + c) * 64 + 2 * j];
-      const float wc = (M == -INFINITY || mc == -INFINITY) ? 0.f : __expf(mc - M);
-      wgt[c][j] = wc;
-      den += wc * a.part_ml[(item0 + c) * 64 + 2 * j + 1];
+    for (int c0 = 0; c0 < nc; c0 += CG) {
+      float2 ml[CG];
+#pragma unroll
+      for (int q = 0; q < CG; ++q)
+        ml[q] = *reinterpret_cast<const float2*>(a.part_ml + (item0 + min(c0 + q, nc - 1)) * 64 +
+                                                 2 * j);
+#pragma unroll
+      for (int q = 0; q < CG; ++q) {
+        if (c0 + q >= nc) continue;
+        const float mc = ml[q].x;
+        const float wc = (M == -INFINITY || mc == -INFINITY) ? 0.f : __expf(mc - M);
+        wgt[c0 + q][j] = wc;
+        den += wc * ml[q].y;
+      }
     }
     inv_den[j] = den > 0.f ? 1.f / den : 0.f;
   }
@@ -456,12 +477,20 @@ __global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
     const int e = dt * SL + e0;              // element index in the state
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     const int j0 = e & 31;                   // columns of e .. e+3 (consecutive lanes)
-    for (int c = 0; c < nc; ++c) {
-      const float4 v = *reinterpret_cast<const float4*>(a.part_o + (item0 + c) * E + e);
-      acc.x += wgt[c][j0] * v.x;
-      acc.y += wgt[c][j0 + 1] * v.y;
-      acc.z += wgt[c][j0 + 2] * v.z;
-      acc.w += wgt[c][j0 + 3] * v.w;
+    for (int c0 = 0; c0 < nc; c0 += CG) {
+      float4 v[CG];
+#pragma unroll
+      for (int q = 0; q < CG; ++q)
+        v[q] = *reinterpret_cast<const float4*>(a.part_o + (item0 + min(c0 + q, nc - 1)) * E + e);
+#pragma unroll
+      for (int q = 0; q < CG; ++q) {
+        if (c0 + q >= nc) continue;
+        const int c = c0 + q;
+        acc.x += wgt[c][j0] * v[q].x;
+        acc.y += wgt[c][j0 + 1] * v[q].y;
+        acc.z += wgt[c][j0 + 2] * v[q].z;
+        acc.w += wgt[c][j0 + 3] * v[q].w;
+      }
     }
     const float vals[4] = {acc.x, acc.y, acc.z, acc.w};
 #pragma unroll

@@ -50,26 +50,89 @@ __global__ void k_rope_table(float2* tab, int max_pos, int half, double theta) {
   tab[idx] = make_float2((float)c, (float)s);
 }
 
-// Sum over the K chunks of one partial-product element, in chunk order; the
-// loads are independent so several are in flight at once.
+// Sum over the K chunks of one partial-product element, in chunk order.
+// The chunks are loaded in groups of PART_GROUP, all loads of a group in
+// flight at once (indices past the last chunk reload the last one and are
+// not added): a loop over a runtime count would otherwise wait for each load
+// of its remainder before issuing the next.
+constexpr int PART_GROUP = 8;
+
+// Sums over the K chunks of N elements of one row (N columns; every load of a
+// chunk group, for all N, in flight at once), in chunk order per element.
+// The first group is outside the loop: at a loop head the compiler waits for
+// every load in flight, including the caller's.  Entries past the last chunk
+// are masked to +0 bitwise rather than skipped: a branch per entry would also
+// make the compiler wait at each branch.
+MSD_DEV float keep_if(float v, uint32_t m) { return __uint_as_float(__float_as_uint(v) & m); }
+template <int N>
+MSD_DEV void part_sums_group(const Parts& pt, const float* p, int s0, const int (&col)[N],
+                             float (&out)[N]) {
+  float q[N][PART_GROUP];
+#pragma unroll
+  for (int n = 0; n < N; ++n)
+#pragma unroll
+    for (int j = 0; j < PART_GROUP; ++j)
+      q[n][j] = p[col[n] + (size_t)min(s0 + j, pt.S - 1) * pt.split];
+#pragma unroll
+  for (int j = 0; j < PART_GROUP; ++j) {
+    const uint32_t m = s0 + j < pt.S ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+    for (int n = 0; n < N; ++n) out[n] += keep_if(q[n][j], m);
+  }
+}
+
+template <int N>
+MSD_DEV void part_sums(const Parts& pt, int row, const int (&col)[N], float (&out)[N]) {
+  const float* p = pt.p + (size_t)row * pt.ld;
+#pragma unroll
+  for (int n = 0; n < N; ++n) out[n] = 0.f;
+  part_sums_group<N>(pt, p, 0, col, out);
+  for (int s0 = PART_GROUP; s0 < pt.S; s0 += PART_GROUP) part_sums_group<N>(pt, p, s0, col, out);
+}
+
+template <int N>
+MSD_DEV void part_sums4_group(const Parts& pt, const float* p, int s0, const int (&col)[N],
+                              float4 (&out)[N]) {
+  float4 q[N][PART_GROUP];
+#pragma unroll
+  for (int n = 0; n < N; ++n)
+#pragma unroll
+    for (int j = 0; j < PART_GROUP; ++j)
+      q[n][j] = *reinterpret_cast<const float4*>(p + col[n] +
+                                                 (size_t)min(s0 + j, pt.S - 1) * pt.split);
+#pragma unroll
+  for (int j = 0; j < PART_GROUP; ++j) {
+    const uint32_t m = s0 + j < pt.S ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+    for (int n = 0; n < N; ++n)
+      out[n] = make_float4(out[n].x + keep_if(q[n][j].x, m), out[n].y + keep_if(q[n][j].y, m),
+                           out[n].z + keep_if(q[n][j].z, m), out[n].w + keep_if(q[n][j].w, m));
+  }
+}
+
+template <int N>
+MSD_DEV void part_sums4(const Parts& pt, int row, const int (&col)[N], float4 (&out)[N]) {
+  const float* p = pt.p + (size_t)row * pt.ld;
+#pragma unroll
+  for (int n = 0; n < N; ++n) out[n] = make_float4(0.f, 0.f, 0.f, 0.f);
+  part_sums4_group<N>(pt, p, 0, col, out);
+  for (int s0 = PART_GROUP; s0 < pt.S; s0 += PART_GROUP)
+    part_sums4_group<N>(pt, p, s0, col, out);
+}
+
 MSD_DEV float part_sum(const Parts& pt, int row, int col) {
-  const float* p = pt.p + (size_t)row * pt.ld + col;
-  float v = 0.f;
-#pragma unroll 8
-  for (int s = 0; s < pt.S; ++s) v += p[(size_t)s * pt.split];
-  return v;
+  const int c[1] = {col};
+  float o[1];
+  part_sums<1>(pt, row, c, o);
+  return o[0];
 }
 
 // The same for four consecutive elements (col a multiple of 4).
 MSD_DEV float4 part_sum4(const Parts& pt, int row, int col) {
-  const float* p = pt.p + (size_t)row * pt.ld + col;
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 8
-  for (int s = 0; s < pt.S; ++s) {
-    const float4 q = *reinterpret_cast<const float4*>(p + (size_t)s * pt.split);
-    v = make_float4(v.x + q.x, v.y + q.y, v.z + q.z, v.w + q.w);
-  }
-  return v;
+  const int c[1] = {col};
+  float4 o[1];
+  part_sums4<1>(pt, row, c, o);
+  return o[0];
 }
 
 // Four consecutive values of a split row (hi halves at row[k..], lo halves
@@ -88,13 +151,30 @@ MSD_DEV void put_split4(uint16_t* row, int K, int k, const float (&v)[4]) {
 }
 
 // 1 / sqrt(mean(x^2) + eps) of a row from its per-block sums of squares
-// (summed in block order); 1 when no sums are given.
-MSD_DEV float row_rstd(const RowNorm& rn, int row) {
-  if (!rn.ssq) return 1.f;
+// (summed in block order); 1 when no sums are given.  ssq_begin issues the
+// loads of the first PART_GROUP sums, so that the caller can issue its own
+// loads before ssq_end waits for them.
+MSD_DEV void ssq_begin(const RowNorm& rn, int row, float (&v)[PART_GROUP]) {
+  if (!rn.ssq) return;
   const float* p = rn.ssq + (size_t)row * rn.nblk;
+#pragma unroll
+  for (int j = 0; j < PART_GROUP; ++j) v[j] = p[min(j, rn.nblk - 1)];
+}
+
+MSD_DEV float ssq_end(const RowNorm& rn, int row, const float (&v)[PART_GROUP]) {
+  if (!rn.ssq) return 1.f;
   float t = 0.f;
-  for (int q = 0; q < rn.nblk; ++q) t += p[q];
+#pragma unroll
+  for (int j = 0; j < PART_GROUP; ++j) t += keep_if(v[j], j < rn.nblk ? 0xFFFFFFFFu : 0u);
+  const float* p = rn.ssq + (size_t)row * rn.nblk;
+  for (int q = PART_GROUP; q < rn.nblk; ++q) t += p[q];
   return rsqrtf(t / (float)rn.d + rn.eps);
+}
+
+MSD_DEV float row_rstd(const RowNorm& rn, int row) {
+  float v[PART_GROUP];
+  ssq_begin(rn, row, v);
+  return ssq_end(rn, row, v);
 }
 
 // Rotate-half RoPE on q and k, write q (split rows), K to its slot and V to
@@ -112,10 +192,18 @@ __global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, in
   const int slot = row_slot[row];
   const int b = row_seq[row];
   if (head >= H && slot < 0) return;
-  const float r = row_rstd(rn, row);
+  float sq[PART_GROUP];
+  ssq_begin(rn, row, sq);
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
-    const float a = r * part_sum(qkv, row, head * hd + i);
-    const float c = r * part_sum(qkv, row, head * hd + i + half);
+    // every load (sums of squares, table row, partials) issued before the
+    // first use
+    const float2 t = tab[(size_t)pos[row] * half + i];
+    const int cols[2] = {head * hd + i, head * hd + i + half};
+    float ac[2];
+    part_sums<2>(qkv, row, cols, ac);
+    const float r = ssq_end(rn, row, sq);
+    const float a = r * ac[0];
+    const float c = r * ac[1];
     if (head >= H + KV) {
       const int g = head - H - KV;
       uint16_t* vr = vc + (size_t)(b * KV + g) * hd * S + slot;
@@ -123,7 +211,6 @@ __global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, in
       vr[(size_t)(i + half) * S] = f2bf(c);
       continue;
     }
-    const float2 t = tab[(size_t)pos[row] * half + i];
     const float y0 = a * t.x - c * t.y;
     const float y1 = c * t.x + a * t.y;
     if (head < H) {
@@ -241,9 +328,13 @@ __global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint1
   const int row = blockIdx.y;
   const int f = blockIdx.x * 1024 + 4 * threadIdx.x;  // F is a multiple of 4
   if (f >= F) return;
-  const float r = row_rstd(rn, row);
-  const float4 gt = part_sum4(pt, row, f);
-  const float4 up = part_sum4(pt, row, pt.off2 + f);
+  float sq[PART_GROUP];
+  ssq_begin(rn, row, sq);
+  const int cols[2] = {f, pt.off2 + f};
+  float4 gu[2];
+  part_sums4<2>(pt, row, cols, gu);
+  const float r = ssq_end(rn, row, sq);
+  const float4 gt = gu[0], up = gu[1];
   const float g4[4] = {gt.x, gt.y, gt.z, gt.w}, u4[4] = {up.x, up.y, up.z, up.w};
   float o[4];
 #pragma unroll
@@ -363,13 +454,18 @@ __global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, 
   float cv[TOPK_PER];
   int ci[TOPK_PER];
   float mloc = -INFINITY, sloc = 0.f;
+  int cols[TOPK_PER];
+#pragma unroll
+  for (int e = 0; e < TOPK_PER; ++e) cols[e] = min(v0 + threadIdx.x + 256 * e, V - 1);
+  float raws[TOPK_PER];
+  part_sums<TOPK_PER>(logits, row, cols, raws);
 #pragma unroll
   for (int e = 0; e < TOPK_PER; ++e) {
     const int v = v0 + threadIdx.x + 256 * e;
     float val = -INFINITY;
     int id = NO_ID;
     if (v < V) {
-      const float raw = part_sum(logits, row, v);
+      const float raw = raws[e];
       if (logits_out) logits_out[(size_t)row * V + v] = raw;
       // a NaN ranks as -inf, so the selected ids are always vocabulary ids
       val = (raw == raw) ? raw : -INFINITY;
