@@ -47,7 +47,7 @@ enum {
 /* Llama-style decoder shape (the target; the draft layer uses the same). */
 typedef struct msd_model_desc {
   int32_t n_layers;
-  int32_t d_model;
+  int32_t d_model;     /* multiple of 8, at most 8192 */
   int32_t n_heads;     /* query heads */
   int32_t n_kv_heads;  /* key/value heads (n_heads % n_kv_heads == 0) */
   int32_t head_dim;    /* must be 128 or 64 */

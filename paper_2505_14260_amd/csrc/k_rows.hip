@@ -26,7 +26,22 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, const int* tok
   const uint16_t* src = (v >= 0) ? visual + (size_t)v * d : E + (size_t)tokens[row] * d;
   // token ids were validated on the host or clamped by the row builder
   float* dst = x + (size_t)row * d;
-  for (int e = threadIdx.x; e < d; e += 256) dst[e] = bf2f(src[e]);
+  // 8-element units, every load issued before the first store (d <= 8192)
+  uint4 bits[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int u = threadIdx.x + 256 * k;
+    bits[k] = 8 * u < d ? *reinterpret_cast<const uint4*>(src + 8 * u) : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int u = threadIdx.x + 256 * k;
+    if (8 * u >= d) continue;
+    const uint32_t w[4] = {bits[k].x, bits[k].y, bits[k].z, bits[k].w};
+    float4* o = reinterpret_cast<float4*>(dst + 8 * u);
+    o[0] = make_float4(bf2f(w[0] & 0xFFFF), bf2f(w[0] >> 16), bf2f(w[1] & 0xFFFF), bf2f(w[1] >> 16));
+    o[1] = make_float4(bf2f(w[2] & 0xFFFF), bf2f(w[2] >> 16), bf2f(w[3] & 0xFFFF), bf2f(w[3] >> 16));
+  }
 }
 
 // Overwrites the visual rows of x with their embeddings (draft input rule for
@@ -246,22 +261,46 @@ __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, 
   __shared__ float sh[16];
   const int row = blockIdx.x;
   float* xr = x + (size_t)row * d;
+  // four consecutive features per thread and unit, at most two units per
+  // thread (d <= 8192); loads issued before their first use, values kept in
+  // registers for the normalisation
+  constexpr int U = 2;
+  float4 v[U], p[U];
+  int cols[U];
+#pragma unroll
+  for (int k = 0; k < U; ++k) {
+    const int e = 4 * (threadIdx.x + 1024 * k);
+    cols[k] = col0 + min(e, d - 4);
+    v[k] = e < d ? *reinterpret_cast<const float4*>(xr + e) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (mode != RN_KEEP) part_sums4<U>(pt, row, cols, p);
   float ss = 0.f;
-  for (int e = threadIdx.x; e < d; e += 1024) {
-    float v = xr[e];
+#pragma unroll
+  for (int k = 0; k < U; ++k) {
+    const int e = 4 * (threadIdx.x + 1024 * k);
+    if (e >= d) continue;
     if (mode != RN_KEEP) {
-      const float p = part_sum(pt, row, col0 + e);
-      v = (mode == RN_SET) ? p : v + p;
-      xr[e] = v;
+      v[k] = (mode == RN_SET) ? p[k]
+                              : make_float4(v[k].x + p[k].x, v[k].y + p[k].y, v[k].z + p[k].z,
+                                            v[k].w + p[k].w);
+      *reinterpret_cast<float4*>(xr + e) = v[k];
     }
-    ss += v * v;
-    if (xb) put_split(xb + (size_t)row * 2 * d, d, e, v);
+    ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
+    const float vals[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+    if (xb) put_split4(xb + (size_t)row * 2 * d, d, e, vals);
   }
   if (!g) return;
   ss = block_sum_1024(ss, sh);
   const float r = rsqrtf(ss / (float)d + eps);
-  for (int e = threadIdx.x; e < d; e += 1024)
-    put_split(xn + (size_t)row * 2 * d, d, e, xr[e] * r * bf2f(g[e]));
+#pragma unroll
+  for (int k = 0; k < U; ++k) {
+    const int e = 4 * (threadIdx.x + 1024 * k);
+    if (e >= d) continue;
+    const uint2 gg = *reinterpret_cast<const uint2*>(g + e);
+    const float o[4] = {v[k].x * r * bf2f(gg.x & 0xFFFF), v[k].y * r * bf2f(gg.x >> 16),
+                        v[k].z * r * bf2f(gg.y & 0xFFFF), v[k].w * r * bf2f(gg.y >> 16)};
+    put_split4(xn + (size_t)row * 2 * d, d, e, o);
+  }
 }
 
 // Elementwise residual update: x = sum of parts (RN_SET), x + sum (RN_ADD)

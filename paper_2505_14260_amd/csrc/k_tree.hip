@@ -343,36 +343,56 @@ __global__ void k_verify_rows(const msd_tree* trees, const int* seq_ids, const i
 
 // Greedy acceptance: node j is accepted iff its parent is and its token is
 // the parent's argmax; the deepest accepted node ends the path (unique since
-// siblings carry distinct tokens).
-__global__ void k_accept(const msd_tree* trees, const int* seq_ids, int T, const int* amax,
-                         int* path, int* n_path, int* emitted, int* slot_map, const int* d_len) {
-  const int sidx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (sidx >= gridDim.x * blockDim.x) return;
+// siblings carry distinct tokens).  One wave per sequence: the tree and the
+// argmax row are staged in LDS by one lane per node, lane 0 takes the
+// decisions in node order, and the lanes write the outputs.
+__global__ __launch_bounds__(MSD_MAX_TREE) void k_accept(const msd_tree* trees,
+                                                         const int* seq_ids, int T,
+                                                         const int* amax, int* path,
+                                                         int* n_path, int* emitted,
+                                                         int* slot_map, const int* d_len) {
+  __shared__ int par[MSD_MAX_TREE], tok[MSD_MAX_TREE], dep[MSD_MAX_TREE], am[MSD_MAX_TREE];
+  __shared__ int pth[MSD_MAX_TREE];
+  __shared__ int n_sh;
+  const int sidx = blockIdx.x;
+  const int j = threadIdx.x;
   const msd_tree* t = trees + sidx;
-  const int* am = amax + (size_t)sidx * T;
-  uint64_t ok = 1ull;
-  int best = 0;
-  for (int j = 1; j < T; ++j) {
-    const int p = t->parent[j];
-    if (p < 0 || p >= j) continue;  // malformed: parents must precede children
-    if (((ok >> p) & 1ull) && t->token[j] == am[p]) {
-      ok |= 1ull << j;
-      if (t->depth[j] > t->depth[best]) best = j;
+  if (j < T) {
+    par[j] = t->parent[j];
+    tok[j] = t->token[j];
+    dep[j] = t->depth[j];
+    am[j] = amax[(size_t)sidx * T + j];
+  }
+  __syncthreads();
+  if (j == 0) {
+    uint64_t ok = 1ull;
+    int best = 0;
+    for (int u = 1; u < T; ++u) {
+      const int p = par[u];
+      if (p < 0 || p >= u) continue;  // malformed: parents must precede children
+      if (((ok >> p) & 1ull) && tok[u] == am[p]) {
+        ok |= 1ull << u;
+        if (dep[u] > dep[best]) best = u;
+      }
     }
+    // the path root .. best: its length first, then written from the end
+    int n = 0;
+    for (int u = best; u >= 0 && n < MSD_MAX_TREE; u = (par[u] < u) ? par[u] : -1) ++n;
+    int u = best;
+    for (int q = n - 1; q >= 0; --q) {
+      pth[q] = u;
+      u = (par[u] < u) ? par[u] : -1;
+    }
+    n_sh = n;
   }
-  int tmp[MSD_MAX_TREE];
-  int n = 0;
-  for (int u = best; u >= 0 && n < MSD_MAX_TREE; u = (t->parent[u] < u) ? t->parent[u] : -1)
-    tmp[n++] = u;
+  __syncthreads();
+  const int n = n_sh;
   const int L = d_len[seq_ids[sidx]];
-  for (int j = 0; j < MSD_MAX_TREE; ++j) {
-    const int u = (j < n) ? tmp[n - 1 - j] : -1;
-    path[sidx * MSD_MAX_TREE + j] = u;
-    slot_map[sidx * MSD_MAX_TREE + j] = (j < n) ? L + u : -1;
-    emitted[sidx * MSD_MAX_TREE + j] =
-        (j + 1 < n) ? t->token[tmp[n - 2 - j]] : ((j + 1 == n) ? am[best] : -1);
-  }
-  n_path[sidx] = n;
+  const int u = (j < n) ? pth[j] : -1;
+  path[sidx * MSD_MAX_TREE + j] = u;
+  slot_map[sidx * MSD_MAX_TREE + j] = (j < n) ? L + u : -1;
+  emitted[sidx * MSD_MAX_TREE + j] = (j + 1 < n) ? tok[pth[j + 1]] : ((j + 1 == n) ? am[pth[n - 1]] : -1);
+  if (j == 0) n_path[sidx] = n;
 }
 
 // In place: K rows L + path[j] -> L + j and the matching V^T columns, for
@@ -421,9 +441,21 @@ __global__ void k_commit(const int* seq_ids, const int* path, const int* n_path,
   const int n = n_path[sidx];
   if (j >= n) return;
   const int u = path[sidx * MSD_MAX_TREE + j];
-  const uint16_t* src = h_tree + (size_t)(sidx * T + u) * 2 * d;
-  uint16_t* dst = pend_h + (size_t)(b * pend_stride + j) * 2 * d;
-  for (int e = threadIdx.x; e < 2 * d; e += blockDim.x) dst[e] = src[e];
+  const uint4* src = reinterpret_cast<const uint4*>(h_tree + (size_t)(sidx * T + u) * 2 * d);
+  uint4* dst = reinterpret_cast<uint4*>(pend_h + (size_t)(b * pend_stride + j) * 2 * d);
+  // the split row (2d bf16, d <= 8192) in 16-byte units, every load issued
+  // before the first store
+  uint4 v[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int q = threadIdx.x + 256 * k;
+    v[k] = 8 * q < 2 * d ? src[q] : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int q = threadIdx.x + 256 * k;
+    if (8 * q < 2 * d) dst[q] = v[k];
+  }
   if (threadIdx.x == 0) {
     pend_next[b * pend_stride + j] = emitted[sidx * MSD_MAX_TREE + j];
     if (j == 0) {
@@ -515,8 +547,8 @@ void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const 
 void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,
                    int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,
                    hipStream_t st) {
-  hipLaunchKernelGGL(k_accept, dim3(n_seq), dim3(1), 0, st, (const msd_tree*)trees, seq_ids, T,
-                     amax, path, n_path, emitted, slot_map, d_len);
+  hipLaunchKernelGGL(k_accept, dim3(n_seq), dim3(MSD_MAX_TREE), 0, st, (const msd_tree*)trees,
+                     seq_ids, T, amax, path, n_path, emitted, slot_map, d_len);
 }
 
 void launch_compact(uint16_t* kc, uint16_t* vc, int n_layers, int B, int KV, int S, int hd,

@@ -301,6 +301,7 @@ int check_desc(const msd_model_desc* m, const msd_limits* lim, msd_ctx* c) {
     return fail(c, MSD_ERR_INVALID_ARG, "head_dim must be 64 or 128");
   if (m->d_model % 8 || m->ffn_dim % 8)
     return fail(c, MSD_ERR_INVALID_ARG, "d_model and ffn_dim must be multiples of 8");
+  if (m->d_model > MAX_D_MODEL) return fail(c, MSD_ERR_INVALID_ARG, "d_model larger than 8192");
   if (m->n_heads / m->n_kv_heads > 16)
     return fail(c, MSD_ERR_INVALID_ARG, "query group larger than 16");
   if (lim->max_batch <= 0 || lim->max_batch > 8 || lim->max_tree <= 0 ||

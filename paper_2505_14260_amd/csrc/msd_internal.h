@@ -94,6 +94,8 @@ struct Parts {
 };
 
 // Per-row sums of squares come in blocks of SSQ_BLOCK features.
+// Row width limit of the whole-row kernels (four 16-byte units per thread).
+constexpr int MAX_D_MODEL = 8192;
 constexpr int SSQ_BLOCK = 1024;
 inline int ssq_blocks(int d) { return (d + SSQ_BLOCK - 1) / SSQ_BLOCK; }
 
