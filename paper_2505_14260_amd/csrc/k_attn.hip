@@ -328,16 +328,26 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
   uint4 kf[HD / 16], vf[HD / 32][2];
   attend_prefetch<HD>(kf, vf, kbase, vbase, a.S, k0);
   // the tile's 32 query columns (hi and lo halves) into LDS; padding
-  // columns copy node 0 (their results are dropped)
-  for (int u = threadIdx.x; u < 32 * QU; u += 64 * NWV) {
+  // columns copy node 0 (their results are dropped).  Every thread's loads
+  // are issued before its first LDS store.
+  constexpr int QN = 32 * QU / (64 * NWV);  // 16-byte units per thread
+  static_assert(QN * 64 * NWV == 32 * QU, "query units must divide over the threads");
+  uint4 qv[QN];
+  int qi[QN];
+#pragma unroll
+  for (int r = 0; r < QN; ++r) {
+    const int u = threadIdx.x + r * 64 * NWV;
     const int j = u / QU, v = u - j * QU;
     int node, head;
     column_to_row(qt, j, G, g, node, head);
     if (node >= a.nq) { node = 0; head = g * G; }
     const int half = v / (HD / 8), k8 = v - half * (HD / 8);
-    sq[j * QU + (v ^ (j & 15))] = *reinterpret_cast<const uint4*>(
+    qi[r] = j * QU + (v ^ (j & 15));
+    qv[r] = *reinterpret_cast<const uint4*>(
         a.q + (size_t)(sidx * a.nq + node) * 2 * HH + (size_t)half * HH + (size_t)head * HD + 8 * k8);
   }
+#pragma unroll
+  for (int r = 0; r < QN; ++r) sq[qi[r]] = qv[r];
   int node, head;
   column_to_row(qt, lane & 31, G, g, node, head);
   if (node >= a.nq) node = 0;
