@@ -432,11 +432,18 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
 
 // Merges the chunks of one (sequence, kv head, query tile) in chunk order;
 // block (tile, dim tile dt) reads the dt slice of every chunk's state
-// (contiguous) and writes those output dims.
+// (contiguous), one float4 per thread, and writes those output dims.
+// Chunks go in groups of CG with every load of a group in flight (indices
+// past the last chunk reload it and are not used).  The first group of
+// state loads is issued before the merge weights are known, and the weights
+// come from one read of the chunks' (max, sum) pairs, so a merge with at
+// most CG chunks waits for memory once.
 template <int HD>
 __global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
   constexpr int E = 32 * HD;
   constexpr int SL = E / (HD / 32);          // elements of one dim tile
+  static_assert(SL == 4 * 256, "one float4 of the dim tile per thread");
+  constexpr int CG = 8;
   __shared__ float wgt[ATT_MAX_CHUNKS][32];  // chunk weights per column
   __shared__ float inv_den[32];
   const int dt = blockIdx.x % (HD / 32);
@@ -447,71 +454,67 @@ __global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
   const int sidx = t / a.KV;
   const int G = a.H / a.KV;
   const int nc = a.n_chunks;
-  // chunks in groups of 8 with every load of a group in flight (indices past
-  // the last chunk reload it and are not used); sums stay in chunk order
-  constexpr int CG = 8;
+  const int e = dt * SL + 4 * threadIdx.x;  // element index in the state
+  const int j0 = e & 31;                    // columns of e .. e+3 (consecutive lanes)
+  float4 v[CG];
+#pragma unroll
+  for (int q = 0; q < CG; ++q)
+    v[q] = *reinterpret_cast<const float4*>(a.part_o + (item0 + min(q, nc - 1)) * E + e);
   if (threadIdx.x < 32) {
     const int j = threadIdx.x;
+    float2 ml[CG];
+#pragma unroll
+    for (int q = 0; q < CG; ++q)
+      ml[q] = *reinterpret_cast<const float2*>(a.part_ml + (item0 + min(q, nc - 1)) * 64 + 2 * j);
     float M = -INFINITY;
-    for (int c0 = 0; c0 < nc; c0 += CG) {
-      float2 ml[CG];
 #pragma unroll
-      for (int q = 0; q < CG; ++q)
-        ml[q] = *reinterpret_cast<const float2*>(a.part_ml + (item0 + min(c0 + q, nc - 1)) * 64 +
-                                                 2 * j);
-#pragma unroll
-      for (int q = 0; q < CG; ++q)
-        if (c0 + q < nc) M = fmaxf(M, ml[q].x);
-    }
+    for (int q = 0; q < CG; ++q)
+      if (q < nc) M = fmaxf(M, ml[q].x);
+    for (int c = CG; c < nc; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
     float den = 0.f;
-    for (int c0 = 0; c0 < nc; c0 += CG) {
-      float2 ml[CG];
 #pragma unroll
-      for (int q = 0; q < CG; ++q)
-        ml[q] = *reinterpret_cast<const float2*>(a.part_ml + (item0 + min(c0 + q, nc - 1)) * 64 +
-                                                 2 * j);
-#pragma unroll
-      for (int q = 0; q < CG; ++q) {
-        if (c0 + q >= nc) continue;
-        const float mc = ml[q].x;
-        const float wc = (M == -INFINITY || mc == -INFINITY) ? 0.f : __expf(mc - M);
-        wgt[c0 + q][j] = wc;
-        den += wc * ml[q].y;
-      }
+    for (int q = 0; q < CG; ++q) {
+      if (q >= nc) continue;
+      const float wc = (M == -INFINITY || ml[q].x == -INFINITY) ? 0.f : __expf(ml[q].x - M);
+      wgt[q][j] = wc;
+      den += wc * ml[q].y;
+    }
+    for (int c = CG; c < nc; ++c) {
+      const float2 mc = *reinterpret_cast<const float2*>(a.part_ml + (item0 + c) * 64 + 2 * j);
+      const float wc = (M == -INFINITY || mc.x == -INFINITY) ? 0.f : __expf(mc.x - M);
+      wgt[c][j] = wc;
+      den += wc * mc.y;
     }
     inv_den[j] = den > 0.f ? 1.f / den : 0.f;
   }
   __syncthreads();
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = 0;;) {
+#pragma unroll
+    for (int q = 0; q < CG; ++q) {
+      if (c0 + q >= nc) continue;
+      const int c = c0 + q;
+      acc.x += wgt[c][j0] * v[q].x;
+      acc.y += wgt[c][j0 + 1] * v[q].y;
+      acc.z += wgt[c][j0 + 2] * v[q].z;
+      acc.w += wgt[c][j0 + 3] * v[q].w;
+    }
+    c0 += CG;
+    if (c0 >= nc) break;
+#pragma unroll
+    for (int q = 0; q < CG; ++q)
+      v[q] = *reinterpret_cast<const float4*>(a.part_o + (item0 + min(c0 + q, nc - 1)) * E + e);
+  }
   const int HH = a.H * HD;
-  for (int e0 = threadIdx.x * 4; e0 < SL; e0 += 1024) {
-    const int e = dt * SL + e0;              // element index in the state
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    const int j0 = e & 31;                   // columns of e .. e+3 (consecutive lanes)
-    for (int c0 = 0; c0 < nc; c0 += CG) {
-      float4 v[CG];
+  const float vals[4] = {acc.x, acc.y, acc.z, acc.w};
 #pragma unroll
-      for (int q = 0; q < CG; ++q)
-        v[q] = *reinterpret_cast<const float4*>(a.part_o + (item0 + min(c0 + q, nc - 1)) * E + e);
-#pragma unroll
-      for (int q = 0; q < CG; ++q) {
-        if (c0 + q >= nc) continue;
-        const int c = c0 + q;
-        acc.x += wgt[c][j0] * v[q].x;
-        acc.y += wgt[c][j0 + 1] * v[q].y;
-        acc.z += wgt[c][j0 + 2] * v[q].z;
-        acc.w += wgt[c][j0 + 3] * v[q].w;
-      }
-    }
-    const float vals[4] = {acc.x, acc.y, acc.z, acc.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = j0 + q;
-      int nd, hd_;
-      column_to_row(qt, j, G, g, nd, hd_);
-      if (nd < a.nq)
-        put_split(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH, HH, hd_ * HD + dim_of<HD>(e + q),
-                  vals[q] * inv_den[j]);
-    }
+  for (int q = 0; q < 4; ++q) {
+    const int j = j0 + q;
+    int nd, hd_;
+    column_to_row(qt, j, G, g, nd, hd_);
+    if (nd < a.nq)
+      put_split(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH, HH, hd_ * HD + dim_of<HD>(e + q),
+                vals[q] * inv_den[j]);
   }
 }
 

@@ -195,48 +195,51 @@ MSD_DEV float row_rstd(const RowNorm& rn, int row) {
 // Rotate-half RoPE on q and k, write q (split rows), K to its slot and V to
 // the transposed V cache (bf16).  qkv: summed parts, [rows][(H + 2KV) * hd], computed
 // from the un-normalised input, so every row is first scaled by its 1/rms.
-// One block of hd/2 threads per (row, head); heads H.. are the key heads,
-// H+KV.. the value heads.
-__global__ __launch_bounds__(64) void k_rope_kv(Parts qkv, RowNorm rn, int H, int KV, int hd,
-                                                const int* pos, const int* row_seq,
-                                                const int* row_slot, const float2* tab,
-                                                uint16_t* q, uint16_t* kc, uint16_t* vc, int S) {
+// Heads H.. are the key heads, H+KV.. the value heads.  One thread per
+// (row, head, rotation pair i): a block of ROPE_THREADS threads covers
+// ROPE_THREADS / (hd/2) heads of one row (hd/2 divides ROPE_THREADS).
+constexpr int ROPE_THREADS = 256;
+__global__ __launch_bounds__(ROPE_THREADS) void k_rope_kv(Parts qkv, RowNorm rn, int H, int KV,
+                                                          int hd, const int* pos,
+                                                          const int* row_seq,
+                                                          const int* row_slot, const float2* tab,
+                                                          uint16_t* q, uint16_t* kc,
+                                                          uint16_t* vc, int S) {
   const int row = blockIdx.x;
-  const int head = blockIdx.y;
   const int half = hd / 2;
+  const int head = blockIdx.y * (ROPE_THREADS / half) + threadIdx.x / half;
+  const int i = threadIdx.x % half;
   const int slot = row_slot[row];
   const int b = row_seq[row];
-  if (head >= H && slot < 0) return;
+  if (head >= H + 2 * KV || (head >= H && slot < 0)) return;
+  // every load (sums of squares, table row, partials) issued before the
+  // first use
   float sq[PART_GROUP];
   ssq_begin(rn, row, sq);
-  for (int i = threadIdx.x; i < half; i += blockDim.x) {
-    // every load (sums of squares, table row, partials) issued before the
-    // first use
-    const float2 t = tab[(size_t)pos[row] * half + i];
-    const int cols[2] = {head * hd + i, head * hd + i + half};
-    float ac[2];
-    part_sums<2>(qkv, row, cols, ac);
-    const float r = ssq_end(rn, row, sq);
-    const float a = r * ac[0];
-    const float c = r * ac[1];
-    if (head >= H + KV) {
-      const int g = head - H - KV;
-      uint16_t* vr = vc + (size_t)(b * KV + g) * hd * S + slot;
-      vr[(size_t)i * S] = f2bf(a);
-      vr[(size_t)(i + half) * S] = f2bf(c);
-      continue;
-    }
-    const float y0 = a * t.x - c * t.y;
-    const float y1 = c * t.x + a * t.y;
-    if (head < H) {
-      uint16_t* qr = q + (size_t)row * 2 * H * hd;
-      put_split(qr, H * hd, head * hd + i, y0);
-      put_split(qr, H * hd, head * hd + i + half, y1);
-    } else {
-      uint16_t* kr = kc + ((size_t)(b * KV + head - H) * S + slot) * hd;
-      kr[i] = f2bf(y0);
-      kr[i + half] = f2bf(y1);
-    }
+  const float2 t = tab[(size_t)pos[row] * half + i];
+  const int cols[2] = {head * hd + i, head * hd + i + half};
+  float ac[2];
+  part_sums<2>(qkv, row, cols, ac);
+  const float r = ssq_end(rn, row, sq);
+  const float a = r * ac[0];
+  const float c = r * ac[1];
+  if (head >= H + KV) {
+    const int g = head - H - KV;
+    uint16_t* vr = vc + (size_t)(b * KV + g) * hd * S + slot;
+    vr[(size_t)i * S] = f2bf(a);
+    vr[(size_t)(i + half) * S] = f2bf(c);
+    return;
+  }
+  const float y0 = a * t.x - c * t.y;
+  const float y1 = c * t.x + a * t.y;
+  if (head < H) {
+    uint16_t* qr = q + (size_t)row * 2 * H * hd;
+    put_split(qr, H * hd, head * hd + i, y0);
+    put_split(qr, H * hd, head * hd + i + half, y1);
+  } else {
+    uint16_t* kr = kc + ((size_t)(b * KV + head - H) * S + slot) * hd;
+    kr[i] = f2bf(y0);
+    kr[i + half] = f2bf(y1);
   }
 }
 
@@ -621,7 +624,9 @@ void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, cons
                     const int* row_seq, const int* row_slot, const float2* rope_tab,
                     uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_rope_kv, dim3(rows, H + 2 * KV), dim3(64), 0, st, qkv, rn, H, KV, hd, pos,
+  const int per_block = ROPE_THREADS / (hd / 2);
+  hipLaunchKernelGGL(k_rope_kv, dim3(rows, (H + 2 * KV + per_block - 1) / per_block),
+                     dim3(ROPE_THREADS), 0, st, qkv, rn, H, KV, hd, pos,
                      row_seq, row_slot, rope_tab, q, kc, vc, S);
 }
 
