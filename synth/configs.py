@@ -137,4 +137,15 @@ WIDE = Workload(
     new_tokens=16, seed=1011,
 )
 
-WORKLOADS = {w.name: w for w in (TINY, LLAVA7B, LLAVA13B, LLAVA7B_LONG, QWEN7B, MINI_GQA, WIDE)}
+# The widest model the library accepts (d_model 8192, 8-way GQA), one layer,
+# with a small FFN and vocabulary so that the oracle stays quick.
+MAXW = Workload(
+    name="max-width-1L-d8192",
+    dims=ModelDims(1, 8192, 64, 8, 128, 2048, 4096, 1e4, 1e-5),
+    n_visual=40, n_text=24, visual_scale=1.0 / 64,
+    tree=TreeShape("static", 3, tuple(full_tree_paths(3, 2))),
+    new_tokens=12, seed=1012,
+)
+
+WORKLOADS = {w.name: w for w in (TINY, LLAVA7B, LLAVA13B, LLAVA7B_LONG, QWEN7B, MINI_GQA, WIDE,
+                                 MAXW)}

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import synth
-from synth.configs import TINY, WIDE, TreeShape, chain_paths
+from synth.configs import MAXW, TINY, WIDE, TreeShape, chain_paths
 from oracle import model as M
 from oracle import msd as O
 from parity import (compare_dynamic_tree, compare_static_tree, decided, oracle_draft_dynamic,
@@ -128,6 +128,68 @@ def test_prefill_many_rows_wide(n_visual):
         ok, err = row_close(kg, st.dkv.k[0, :n].reshape(n, -1))
         assert ok, ("draft K", err)
         print(f"target K/V max rel err {worst:.2e}, draft K {err:.2e}")
+    finally:
+        eng.close()
+
+
+def test_max_width_model():
+    """d_model 8192, the library's limit (whole-row kernels at two 16-byte
+    units per thread), with 8-way GQA: the prompt forward's K/V, first token
+    and draft cache, verification logits on a fixed tree, and a short
+    speculative decode against the plain greedy one."""
+    from paper_2505_14260_amd.msd import Engine
+    wl = MAXW
+    dims = wl.dims
+    print(f"case: {wl.name} prefill, verify and decode", flush=True)
+    w = synth.make_target_weights(dims, wl.seed)
+    dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
+    prompt = synth.make_prompt(wl)
+    m = O.Models(dims, w, dr)
+    n = wl.prompt_len
+    max_seq = 256
+    eng = Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64, max_prompt=n)
+    try:
+        first = eng.prefill(0, *prompt)
+        st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=max_seq)
+        if decided(logits[-1]):
+            assert first == f_ref
+        tk, tv, dk, dv = eng.kv_views()
+        torch.cuda.synchronize()
+        kg = bits_to_f64(tk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        vg = bits_to_f64(tv[0, 0, :, :, :n].permute(2, 0, 1).reshape(n, -1))
+        ok, ek = row_close(kg, st.kv.k[0, :n].reshape(n, -1))
+        ok2, ev = row_close(vg, st.kv.v[0, :n].reshape(n, -1))
+        assert ok and ok2, (ek, ev)
+        O.draft_catch_up(m, st)
+        dkg = bits_to_f64(dk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        ok3, ed = row_close(dkg, st.dkv.k[0, :n].reshape(n, -1))
+        assert ok3, ed
+        parent, rank, depth = synth.static_tree_arrays(wl.tree.paths)
+        toks = synth.ids(len(parent), wl.seed, synth.TID_TEST, dims.vocab)
+        toks[0] = first
+        tree = O.Tree(toks.astype(np.int32), parent, depth, np.zeros(len(parent)))
+        dev = upload_tree(eng, tree)
+        amax, lg = eng.verify([0], dev, tree.n, want_logits=True)
+        _, lg_ref = O.verify(m, st, tree)
+        ok4, el = row_close(lg.cpu().numpy(), lg_ref)
+        assert ok4, el
+        am = amax.cpu().numpy()
+        for i in range(tree.n):
+            if decided(lg_ref[i]):
+                assert am[i] == int(np.argmax(lg_ref[i])), i
+        print(f"K/V max rel err {max(ek, ev):.2e}, draft K {ed:.2e}, logits {el:.2e}")
+    finally:
+        eng.close()
+    eng = Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64, max_prompt=n)
+    try:
+        spec, _ = static_spec(wl.tree.paths)
+        out, cycles = eng.generate(0, prompt, spec, wl.new_tokens)
+        ref, rows = O.greedy_generate(m, prompt, wl.new_tokens, return_logits=True)
+        bad = next((i for i in range(len(ref)) if out[i] != ref[i]), None)
+        print(f"decode: {bad if bad is not None else len(ref)}/{len(ref)} tokens equal, "
+              f"tau={np.mean(cycles):.2f}")
+        if bad is not None:
+            assert not decided(rows[bad]), (bad, out[bad], ref[bad])
     finally:
         eng.close()
 
