@@ -420,6 +420,66 @@ def test_errors_and_capacity(setup):
     assert e.value.code == B.MSD_ERR_STATE
 
 
+def test_empty_and_malformed_calls(setup):
+    """Empty inputs and malformed argument lists are rejected on the host
+    with MSD_ERR_INVALID_ARG before any kernel runs, and the context keeps
+    working afterwards (a root-only verify against the oracle)."""
+    wl, _, m, prompt = setup
+    from paper_2505_14260_amd import msd as B
+    print("case: tiny empty and malformed calls", flush=True)
+    eng = B.Engine(wl.dims, m.w, m.draft, max_batch=2, max_seq=256, max_tree=64, max_prompt=128)
+    try:
+        _empty_and_malformed(wl, eng, m, prompt, B)
+    finally:
+        eng.close()
+
+
+def _empty_and_malformed(wl, eng, m, prompt, B):
+    first = eng.prefill(0, *prompt)
+    empty = np.zeros(0, np.int32)
+    with pytest.raises(B.MSDError) as e:                       # empty prompt
+        eng.prefill(1, empty, np.zeros(0, np.uint8), None)
+    assert e.value.code == B.MSD_ERR_INVALID_ARG
+    tokens, is_visual, _ = prompt
+    bad = tokens.copy()
+    bad[-1] = wl.dims.vocab                                     # token id out of range
+    with pytest.raises(B.MSDError) as e:
+        eng.prefill(1, bad, is_visual, None)
+    assert e.value.code == B.MSD_ERR_INVALID_ARG
+    with pytest.raises(B.MSDError) as e:                       # visual rows without embeddings
+        eng.prefill(1, tokens, is_visual, None)
+    assert e.value.code == B.MSD_ERR_INVALID_ARG
+    spec, _ = static_spec(wl.tree.paths)
+    dev = eng.new_trees(2)
+    amax = torch.zeros(2 * 64, dtype=torch.int32, device="cuda")
+    for seqs in ([], [0, 0], [5], [-1]):                        # empty, duplicate, out of range
+        with pytest.raises(B.MSDError) as e:
+            B.msd_draft_tree(eng.ctx, seqs, spec, dev.data_ptr())
+        assert e.value.code == B.MSD_ERR_INVALID_ARG, seqs
+        with pytest.raises(B.MSDError) as e:
+            B.msd_verify(eng.ctx, seqs, dev.data_ptr(), 4, amax.data_ptr())
+        assert e.value.code == B.MSD_ERR_INVALID_ARG, seqs
+    with pytest.raises(B.MSDError) as e:                       # sequence without a prompt
+        B.msd_verify(eng.ctx, [1], dev.data_ptr(), 4, amax.data_ptr())
+    assert e.value.code == B.MSD_ERR_STATE
+    for T in (0, 65):                                           # tree sizes outside [1, 64]
+        with pytest.raises(B.MSDError) as e:
+            B.msd_verify(eng.ctx, [0], dev.data_ptr(), T, amax.data_ptr())
+        assert e.value.code == B.MSD_ERR_INVALID_ARG, T
+    with pytest.raises(B.MSDError) as e:                       # a static tree of no nodes
+        B.msd_draft_tree(eng.ctx, [0], B.make_static_spec(np.zeros(0, np.int32),
+                                                          np.zeros(0, np.int32)), dev.data_ptr())
+    assert e.value.code == B.MSD_ERR_INVALID_ARG
+    st, _, _, _ = O.prefill(m, *prompt, max_slots=256)
+    tree = O.Tree(np.array([first], np.int32), np.array([-1], np.int32), np.zeros(1, np.int32),
+                  np.zeros(1))
+    one = upload_tree(eng, tree)
+    am, lg = eng.verify([0], one, 1, want_logits=True)
+    _, lg_ref = O.verify(m, st, tree)
+    ok, err = row_close(lg.cpu().numpy(), lg_ref)
+    assert ok, err
+
+
 def test_root_only_tree(setup):
     """T = 1: the verify step degenerates to one plain decode step."""
     wl, eng, m, prompt = setup
