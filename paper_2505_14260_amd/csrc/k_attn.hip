@@ -310,11 +310,18 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
   __shared__ float wgt[NWV][32];
   __shared__ float colm[32][2];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int t = blockIdx.x;
-  const int c = t % a.n_chunks; t /= a.n_chunks;
-  const int qt = t % a.qtiles; t /= a.qtiles;
-  const int g = t % a.KV;
-  const int sidx = t / a.KV;
+  // Workgroup -> unit u = (sequence, kv head, key chunk) and query tile qt.
+  // The query tiles of one unit read the same K/V blocks, so they get
+  // blockIdx values 8 apart (workgroup i runs on XCD i mod 8) in
+  // consecutive dispatch slots: the first tile's loads bring the blocks
+  // into that XCD's L2 for the others.  Grid: 8 * qtiles * ceil(units / 8).
+  const int slot = blockIdx.x >> 3;
+  const int qt = slot % a.qtiles;
+  const int u = (slot / a.qtiles) * 8 + (blockIdx.x & 7);
+  if (u >= a.n_seq * a.KV * a.n_chunks) return;
+  const int c = u % a.n_chunks;
+  const int g = (u / a.n_chunks) % a.KV;
+  const int sidx = u / a.n_chunks / a.KV;
   const int b = a.seq[sidx];
   const int P = a.prefix[sidx];
   const int Ltot = a.keys[sidx];
@@ -410,7 +417,7 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
     }
     return;
   }
-  const size_t item = blockIdx.x;
+  const size_t item = (((size_t)sidx * a.KV + g) * a.qtiles + qt) * a.n_chunks + c;
   for (int e = 4 * threadIdx.x; e < E; e += 4 * 64 * NWV) {
     const int j = e & 31;  // columns j .. j+3 (consecutive lanes of one register)
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -561,7 +568,8 @@ size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd) 
 
 void launch_tree_attention(AttnArgs a, hipStream_t st) {
   const int items = a.n_seq * a.KV * a.qtiles;
-  dim3 grid(items * a.n_chunks);
+  const int units = a.n_seq * a.KV * a.n_chunks;
+  dim3 grid(8 * a.qtiles * ((units + 7) / 8));
   if (a.hd == 128) {
     hipLaunchKernelGGL(k_tree_attn<128>, grid, dim3(64 * TREE_WAVES), 0, st, a);
     if (a.n_chunks > 1)
