@@ -27,7 +27,10 @@ sys.path.insert(0, ROOT)
 
 METRIC = "verify-step ms + decoded tokens/sec, bs=1, 7B-shaped; % HBM roofline"
 HBM_PEAK_GBS = 8000.0
-PAPER_TAU = 4.63  # MSD, LLaVA-1.5-7B, temperature 0, Hallusion (results table)
+# The paper's results table, MSD rows, Hallusion column, temperature 0:
+# average acceptance length of LLaVA-1.5-7B and the speedup ratios.
+PAPER_TAU = 4.63
+PAPER_SR = {"LLaVA-1.5-7B": 2.29, "LLaVA-1.5-13B": 2.46}
 SILU_KIND = 3
 
 
@@ -300,7 +303,7 @@ def main():
                      "over the measured cycle time, times tokens per cycle; prompt time "
                      "excluded",
             "paper_context": {
-                "LLaVA-1.5-7B": 2.29, "LLaVA-1.5-13B": 2.46,
+                **PAPER_SR,
                 "note": "the paper's speedup ratios at temperature 0 on Hallusion, with "
                         "trained weights and prompt time included; its inference GPU is "
                         "not stated (draft training on four RTX 4090s). Context only",
