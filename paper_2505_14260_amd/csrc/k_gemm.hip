@@ -44,6 +44,7 @@ constexpr int BLOCK_ELEMS = TILE_ROWS * KB;
 // re-read; the ring depth stays at RING blocks either way.
 constexpr int RING = 4;
 __host__ __device__ constexpr int chunk_blocks(int MT) { return MT <= 2 ? 8 : 4; }
+constexpr int PAIR_MAX_TILES = 4;  // tiles per workgroup of the two-chunk kernel
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 MSD_DEV uint4 load_stream(const uint16_t* p) {
@@ -215,6 +216,185 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
+// Units [256 q0, 256 (q0 + XB)) of the X chunk starting at block kb0 (rows
+// past M and columns past K are zero): load_x issues the loads, store_x
+// writes them to LDS (XOR-swizzled, hi then lo halves).
+template <int MT, int NKB, int XB>
+MSD_DEV void load_x(uint4 (&xh)[XB], uint4 (&xl)[XB], const uint16_t* X, int ldx, int M, int K,
+                    int kb0, int q0) {
+  constexpr int UPR = NKB * KB / 8;
+  const int k0 = kb0 * KB;
+#pragma unroll
+  for (int q = 0; q < XB; ++q) {
+    const int e = threadIdx.x + 256 * (q0 + q);
+    const int m = e / UPR, u = e - m * UPR;
+    const int col = k0 + 8 * u;
+    const bool ok = m < M && col < K;
+    const uint16_t* src = X + (ok ? (size_t)m * ldx + col : 0);
+    const uint4 h = *reinterpret_cast<const uint4*>(src);
+    const uint4 l = *reinterpret_cast<const uint4*>(src + (ok ? K : 0));
+    xh[q] = ok ? h : make_uint4(0, 0, 0, 0);
+    xl[q] = ok ? l : make_uint4(0, 0, 0, 0);
+  }
+}
+
+template <int MT, int NKB, int XB>
+MSD_DEV void store_x(uint4* xs, const uint4 (&xh)[XB], const uint4 (&xl)[XB], int q0) {
+  constexpr int UPR = NKB * KB / 8;
+  constexpr int LO = MT * 16 * UPR;
+#pragma unroll
+  for (int q = 0; q < XB; ++q) {
+    const int e = threadIdx.x + 256 * (q0 + q);
+    const int m = e / UPR, u = e - m * UPR;
+    const int xi = xs_index(m, u, UPR);
+    xs[xi] = xh[q];
+    xs[LO + xi] = xl[q];
+  }
+}
+
+// Workgroup barrier that orders LDS accesses only: global loads issued
+// before it stay in flight.
+MSD_DEV void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// The same product with two K chunks per workgroup, for 64-row passes, whose
+// X chunk fills LDS at 4 blocks: each workgroup covers chunks 2s and 2s+1
+// of NT tiles, so it writes one partial per tile for the pair, half the
+// partials (and half the consumer's reads) of one chunk per workgroup.  The
+// weight ring runs through the sequence (chunk 0: tiles 0..NT-1, blocks of
+// each; then chunk 1 likewise) without a branch on its loads; every tile
+// keeps its accumulators across both chunks.  Between the chunks the
+// workgroup restages X in LDS; waiting for those loads also waits for the
+// ring's, once per workgroup.  Slots for tiles past the workgroup's last and
+// blocks past K read the zero block.
+template <int MT, int NW, int NKB, int P, int NT>
+__global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
+  static_assert(NKB % P == 0, "ring slots must divide the chunk");
+  extern __shared__ uint4 xs[];
+  constexpr int UPR = NKB * KB / 8;
+  constexpr int LO = MT * 16 * UPR;
+  constexpr int SEQ = 2 * NT * NKB;  // blocks of the workgroup's sequence
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane & 15, g = lane >> 4;
+  const int S = a.S, G = a.G, M = a.M, nkt = a.nkt, n_tiles = a.n_tiles;
+  const int s = blockIdx.x % S, gi = blockIdx.x / S;
+  const int n_my = gi < n_tiles ? min(NT, (n_tiles - gi + G - 1) / G) : 0;
+  if (n_my == 0) return;
+  const int kb0 = 2 * s * NKB;
+  const uint16_t* const W = a.W;
+  const uint16_t* const W2 = a.W2;
+  const size_t lane_off = (size_t)wave * (BLOCK_ELEMS / 4) + lane * 8;
+  const uint16_t* const dummy = a.dummy + lane_off;
+  // element offset of sequence block q, or -1 for the zero block
+  auto block_off = [&](int q) -> long long {
+    const int h = q / (NT * NKB), j = (q / NKB) % NT, p = q % NKB;
+    const int kb = kb0 + h * NKB + p;
+    if (q >= SEQ || j >= n_my || kb >= nkt) return -1;
+    return ((long long)(gi + j * G) * nkt + kb) * BLOCK_ELEMS + (long long)lane_off;
+  };
+  constexpr int NX = MT * 16 * UPR / 256;  // X units per thread
+  static_assert(NX == 16, "X staging assumes 16 units per thread");
+  // the first chunk's X loads go out before the ring's, so that its LDS
+  // writes wait for them alone
+  uint4 xh[NX], xl[NX];
+  load_x<MT, NKB, NX>(xh, xl, a.X, a.ldx, M, a.K, kb0, 0);
+  uint4 ring[P][NW][4];
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const long long o = block_off(p);
+    const uint16_t* const b1 = o >= 0 ? W + o : dummy;
+    const uint16_t* const b2 = o >= 0 ? W2 + o : dummy;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      ring[p][0][c] = load_stream(b1 + c * 512);
+      if (NW == 2) ring[p][NW - 1][c] = load_stream(b2 + c * 512);
+    }
+  }
+  store_x<MT, NKB, NX>(xs, xh, xl, 0);
+  __syncthreads();
+  f32x4 acc[NT][NW][MT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+      for (int t = 0; t < MT; ++t) acc[j][w][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h == 1) {
+      // the second X chunk: its loads go out before the barrier (every wave
+      // done with the first chunk), its LDS writes after
+      constexpr int XB = NX / 2;
+#pragma unroll
+      for (int q0 = 0; q0 < NX; q0 += XB) {
+        uint4 yh[XB], yl[XB];
+        load_x<MT, NKB, XB>(yh, yl, a.X, a.ldx, M, a.K, kb0 + NKB, q0);
+        if (q0 == 0) lds_barrier();
+        store_x<MT, NKB, XB>(xs, yh, yl, q0);
+      }
+      lds_barrier();
+    }
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int p = 0; p < NKB; ++p) {
+        const int q = (h * NT + j) * NKB + p;
+        const int r = q % P;
+        uint4 fh[MT][4], fl[MT][4];
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int xi = xs_index(t * 16 + i, p * 16 + 4 * g + c, UPR);
+            fh[t][c] = xs[xi];
+            fl[t][c] = xs[LO + xi];
+          }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+#pragma unroll
+          for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+              acc[j][w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(ring[r][w][c]), as_bf16x8(fh[t][c]), acc[j][w][t], 0, 0, 0);
+#pragma unroll
+          for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+              acc[j][w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  as_bf16x8(ring[r][w][c]), as_bf16x8(fl[t][c]), acc[j][w][t], 0, 0, 0);
+        }
+        const long long o = block_off(q + P);
+        const uint16_t* const b1 = o >= 0 ? W + o : dummy;
+        const uint16_t* const b2 = o >= 0 ? W2 + o : dummy;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          ring[r][0][c] = load_stream(b1 + c * 512);
+          if (NW == 2) ring[r][NW - 1][c] = load_stream(b2 + c * 512);
+        }
+      }
+  }
+  const int ldp = a.ldp, off2 = a.off2;
+  float* const part = a.part + (size_t)s * a.part_split;
+  float* const sink = a.sink + lane * 4;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int n = (gi + j * G) * TILE_ROWS + wave * 16 + 4 * g;
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        const int m = t * 16 + i;
+        float* dst = (m < M && j < n_my) ? part + (size_t)m * ldp + w * off2 + n : sink;
+        *reinterpret_cast<float4*>(dst) =
+            make_float4(acc[j][w][t][0], acc[j][w][t][1], acc[j][w][t][2], acc[j][w][t][3]);
+      }
+  }
+}
+
 // Many-row GEMM (prompt rows, large batches): a (64 NB) x 128 output tile
 // per workgroup over all of K, both operands staged through LDS.
 //
@@ -263,13 +443,6 @@ __host__ __device__ constexpr size_t big_lds(int NB) {
 // hi units 0..15 and lo units 16..31 of row m, each half swizzled by m & 15
 MSD_DEV int big_xs_index(int m, int u) { return m * BIG_XU + (u & 16) + ((u & 15) ^ (m & 15)); }
 
-// Workgroup barrier that orders LDS accesses only: global loads issued
-// before it stay in flight.
-MSD_DEV void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 MSD_DEV bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -429,6 +602,26 @@ void launch_mt(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t 
     hipLaunchKernelGGL((k_gemm<MT, NW, NKB, P>), grid, dim3(256), lds, st, a);
 }
 
+template <int NW, int NT>
+void launch_pair(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
+  constexpr int MT = 4, P = RING;
+  constexpr int NKB = chunk_blocks(MT);
+  const size_t lds = (size_t)MT * 16 * NKB * KB * 4;
+  if (sc.ev_start)
+    hipExtLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT>), grid, dim3(256), lds, st, sc.ev_start,
+                          sc.ev_stop, 0, a);
+  else
+    hipLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT>), grid, dim3(256), lds, st, a);
+}
+
+template <int NW>
+void launch_pair_nt(int nt, dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
+  if (nt == 1) launch_pair<NW, 1>(grid, a, sc, st);
+  else if (nt == 2) launch_pair<NW, 2>(grid, a, sc, st);
+  else if (nt == 3) launch_pair<NW, 3>(grid, a, sc, st);
+  else launch_pair<NW, 4>(grid, a, sc, st);
+}
+
 }  // namespace
 
 size_t gemm_dummy_elems() { return (size_t)BLOCK_ELEMS; }
@@ -459,6 +652,24 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
   if (G < 1) G = 1;
   const int per = (p.n_tiles + G - 1) / G;
   p.G = (p.n_tiles + per - 1) / per;
+  p.pair = 0;
+  p.per = per;
+  // 64-row passes: two K chunks per workgroup when that keeps at least
+  // three quarters of the target workgroups with at most PAIR_MAX_TILES
+  // tiles each (the tiles' accumulators live in registers)
+  if (p.MT == 4) {
+    const int S2 = (p.S + 1) / 2;
+    int G2 = (target_wgs + S2 - 1) / S2;
+    if (G2 > p.n_tiles) G2 = p.n_tiles;
+    const int per2 = (p.n_tiles + G2 - 1) / G2;
+    G2 = (p.n_tiles + per2 - 1) / per2;
+    if (per2 <= PAIR_MAX_TILES && 4 * S2 * G2 >= 3 * target_wgs) {
+      p.pair = 1;
+      p.S = S2;
+      p.G = G2;
+      p.per = per2;
+    }
+  }
   p.nw = nw;
   p.ldp = p.n_tiles * TILE_ROWS * nw;
   p.off2 = p.n_tiles * TILE_ROWS;
@@ -493,6 +704,11 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
   a.sink = sink;
   a.dummy = dummy;
   const dim3 grid(pl.S * pl.G);
+  if (pl.pair) {
+    if (nw == 2) launch_pair_nt<2>(pl.per, grid, a, sc, st);
+    else launch_pair_nt<1>(pl.per, grid, a, sc, st);
+    return;
+  }
   if (nw == 2) {
     if (pl.MT == 1) launch_mt<1, 2>(grid, a, sc, st);
     else if (pl.MT == 2) launch_mt<2, 2>(grid, a, sc, st);

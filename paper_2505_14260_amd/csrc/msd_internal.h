@@ -59,6 +59,8 @@ struct GemmArgs {
 
 struct GemmPlan {
   int MT, nkb, S, G, nw, n_tiles, nkt, ldp, off2;
+  int pair;  // two K chunks per workgroup (S counts chunk pairs)
+  int per;   // tiles per workgroup
 };
 
 struct GemmScratch {
