@@ -44,7 +44,7 @@ constexpr int BLOCK_ELEMS = TILE_ROWS * KB;
 // re-read; the ring depth stays at RING blocks either way.
 constexpr int RING = 4;
 __host__ __device__ constexpr int chunk_blocks(int MT) { return MT <= 2 ? 8 : 4; }
-constexpr int PAIR_MAX_TILES = 4;  // tiles per workgroup of the two-chunk kernel
+constexpr int PAIR_MAX_TILES = 5;  // tiles per workgroup of the two-chunk kernel
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 MSD_DEV uint4 load_stream(const uint16_t* p) {
@@ -619,7 +619,8 @@ void launch_pair_nt(int nt, dim3 grid, const GemmArgs& a, const GemmScratch& sc,
   if (nt == 1) launch_pair<NW, 1>(grid, a, sc, st);
   else if (nt == 2) launch_pair<NW, 2>(grid, a, sc, st);
   else if (nt == 3) launch_pair<NW, 3>(grid, a, sc, st);
-  else launch_pair<NW, 4>(grid, a, sc, st);
+  else if (nt == 4) launch_pair<NW, 4>(grid, a, sc, st);
+  else launch_pair<NW, 5>(grid, a, sc, st);
 }
 
 }  // namespace
