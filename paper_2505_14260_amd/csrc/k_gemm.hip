@@ -651,8 +651,15 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
   int G = (target_wgs + p.S - 1) / p.S;
   if (G > p.n_tiles) G = p.n_tiles;
   if (G < 1) G = 1;
-  const int per = (p.n_tiles + G - 1) / G;
-  p.G = (p.n_tiles + per - 1) / per;
+  int per = (p.n_tiles + G - 1) / G;
+  G = (p.n_tiles + per - 1) / per;
+  // one workgroup per CU: a few workgroups past the target would run as a
+  // second wave, so take more tiles per workgroup instead
+  while (p.S * G > target_wgs && G > 1) {
+    ++per;
+    G = (p.n_tiles + per - 1) / per;
+  }
+  p.G = G;
   p.pair = 0;
   p.per = per;
   // 64-row passes: two K chunks per workgroup when that keeps at least
@@ -662,8 +669,12 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
     const int S2 = (p.S + 1) / 2;
     int G2 = (target_wgs + S2 - 1) / S2;
     if (G2 > p.n_tiles) G2 = p.n_tiles;
-    const int per2 = (p.n_tiles + G2 - 1) / G2;
+    int per2 = (p.n_tiles + G2 - 1) / G2;
     G2 = (p.n_tiles + per2 - 1) / per2;
+    while (S2 * G2 > target_wgs && G2 > 1) {
+      ++per2;
+      G2 = (p.n_tiles + per2 - 1) / per2;
+    }
     if (per2 <= PAIR_MAX_TILES && 4 * S2 * G2 >= 3 * target_wgs) {
       p.pair = 1;
       p.S = S2;
