@@ -260,8 +260,9 @@ MSD_DEV void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// The same product with two K chunks per workgroup, for 64-row passes, whose
-// X chunk fills LDS at 4 blocks: each workgroup covers chunks 2s and 2s+1
+// The same product with two K chunks per workgroup, for 64-row passes (whose
+// X chunk fills LDS at 4 blocks) and the widest 32-row ones: each workgroup
+// covers chunks 2s and 2s+1
 // of NT tiles, so it writes one partial per tile for the pair, half the
 // partials (and half the consumer's reads) of one chunk per workgroup.  The
 // weight ring runs through the sequence (chunk 0: tiles 0..NT-1, blocks of
@@ -602,9 +603,9 @@ void launch_mt(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t 
     hipLaunchKernelGGL((k_gemm<MT, NW, NKB, P>), grid, dim3(256), lds, st, a);
 }
 
-template <int NW, int NT>
+template <int MT, int NW, int NT>
 void launch_pair(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
-  constexpr int MT = 4, P = RING;
+  constexpr int P = RING;
   constexpr int NKB = chunk_blocks(MT);
   const size_t lds = (size_t)MT * 16 * NKB * KB * 4;
   if (sc.ev_start)
@@ -614,13 +615,13 @@ void launch_pair(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_
     hipLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT>), grid, dim3(256), lds, st, a);
 }
 
-template <int NW>
+template <int MT, int NW>
 void launch_pair_nt(int nt, dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
-  if (nt == 1) launch_pair<NW, 1>(grid, a, sc, st);
-  else if (nt == 2) launch_pair<NW, 2>(grid, a, sc, st);
-  else if (nt == 3) launch_pair<NW, 3>(grid, a, sc, st);
-  else if (nt == 4) launch_pair<NW, 4>(grid, a, sc, st);
-  else launch_pair<NW, 5>(grid, a, sc, st);
+  if (nt == 1) launch_pair<MT, NW, 1>(grid, a, sc, st);
+  else if (nt == 2) launch_pair<MT, NW, 2>(grid, a, sc, st);
+  else if (nt == 3) launch_pair<MT, NW, 3>(grid, a, sc, st);
+  else if (nt == 4) launch_pair<MT, NW, 4>(grid, a, sc, st);
+  else launch_pair<MT, NW, 5>(grid, a, sc, st);
 }
 
 }  // namespace
@@ -662,10 +663,13 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
   p.G = G;
   p.pair = 0;
   p.per = per;
-  // 64-row passes: two K chunks per workgroup when that keeps at least
-  // three quarters of the target workgroups with at most PAIR_MAX_TILES
-  // tiles each (the tiles' accumulators live in registers)
-  if (p.MT == 4) {
+  // Two K chunks per workgroup (the tiles' accumulators live in registers,
+  // at most PAIR_MAX_TILES of them).  64-row passes: when at least three
+  // quarters of the target workgroups stay busy.  32-row passes, whose
+  // partials are half as many per weight byte: only when the workgroup count
+  // stays within 5% and each workgroup has four tiles or more to amortise
+  // the mid-stream restage of X (the wide LM heads).
+  if ((p.MT == 4 || (p.MT == 2 && nw == 1)) && p.S >= 2) {
     const int S2 = (p.S + 1) / 2;
     int G2 = (target_wgs + S2 - 1) / S2;
     if (G2 > p.n_tiles) G2 = p.n_tiles;
@@ -675,7 +679,9 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
       ++per2;
       G2 = (p.n_tiles + per2 - 1) / per2;
     }
-    if (per2 <= PAIR_MAX_TILES && 4 * S2 * G2 >= 3 * target_wgs) {
+    const bool busy = p.MT == 4 ? 4 * S2 * G2 >= 3 * target_wgs
+                                : (per2 >= 4 && 20 * S2 * G2 >= 19 * p.S * p.G);
+    if (per2 <= PAIR_MAX_TILES && busy) {
       p.pair = 1;
       p.S = S2;
       p.G = G2;
@@ -717,8 +723,10 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
   a.dummy = dummy;
   const dim3 grid(pl.S * pl.G);
   if (pl.pair) {
-    if (nw == 2) launch_pair_nt<2>(pl.per, grid, a, sc, st);
-    else launch_pair_nt<1>(pl.per, grid, a, sc, st);
+    // 32-row passes pair only single weights (the LM heads)
+    if (pl.MT == 2) launch_pair_nt<2, 1>(pl.per, grid, a, sc, st);
+    else if (nw == 2) launch_pair_nt<4, 2>(pl.per, grid, a, sc, st);
+    else launch_pair_nt<4, 1>(pl.per, grid, a, sc, st);
     return;
   }
   if (nw == 2) {
