@@ -235,10 +235,12 @@ class _DraftExpander:
         self.m, self.st = m, st
         self.feat = {None: root_feat}
         self.slot, self.mask = {}, {}
+        self.path = {None: ()}   # token path from the root, for inspection only
 
     def __call__(self, keys, parent_keys, tokens, depth):
         m, st = self.m, self.st
-        for k, pk in zip(keys, parent_keys):
+        for k, pk, t in zip(keys, parent_keys, tokens):
+            self.path[k] = self.path[pk] + (int(t),)
             self.slot[k] = len(self.slot)
             a = np.uint64(1 << self.slot[k])
             if pk is not None:
@@ -257,8 +259,14 @@ class _DraftExpander:
         return M.linear(out, m.w["lm_head"])
 
 
-def draft_tree(m: Models, st: SeqState, shape, static_arrays=None):
-    """Catch-up on the pending rows, then the draft tree for this cycle."""
+def draft_tree(m: Models, st: SeqState, shape, static_arrays=None, trace=None):
+    """Catch-up on the pending rows, then the draft tree for this cycle.
+
+    trace: optional dict that receives, for inspection, the committed length
+    L, the root feature (the catch-up's last predicted feature) and the
+    predicted feature of every expanded node keyed by its token path from the
+    root (a tuple of drafted tokens).
+    """
     root_feat = draft_catch_up(m, st)
     root_logits = M.linear(root_feat[None, :], m.w["lm_head"])[0]
     ex = _DraftExpander(m, st, root_feat)
@@ -268,12 +276,17 @@ def draft_tree(m: Models, st: SeqState, shape, static_arrays=None):
         def expand(nodes, tokens, d):
             pk = [None if parent[u] == 0 else int(parent[u]) for u in nodes]
             return ex(list(nodes), pk, tokens, d)
-        return select_static_tree(parent, rank, depth, st.root, root_logits, expand)
-
-    def expand_dyn(ids, parents, tokens, d):
-        return ex(list(ids), [None if p < 0 else p for p in parents], tokens, d)
-    tree, _ = select_dynamic_tree(shape.topk, shape.depth, shape.n_nodes, st.root,
-                                  root_logits, expand_dyn)
+        tree = select_static_tree(parent, rank, depth, st.root, root_logits, expand)
+    else:
+        def expand_dyn(ids, parents, tokens, d):
+            return ex(list(ids), [None if p < 0 else p for p in parents], tokens, d)
+        tree, _ = select_dynamic_tree(shape.topk, shape.depth, shape.n_nodes, st.root,
+                                      root_logits, expand_dyn)
+    if trace is not None:
+        trace["L"] = st.L
+        trace["root_feat"] = root_feat
+        trace["root_logits"] = root_logits
+        trace["feat"] = {ex.path[k]: ex.feat[k] for k in ex.feat if k is not None}
     return tree
 
 

@@ -23,6 +23,7 @@ from oracle import model as M  # noqa: E402
 from oracle import msd as O  # noqa: E402
 from oracle import sampling as S  # noqa: E402
 
+import test_oracle_draft_pins as PD  # noqa: E402
 import test_oracle_invariants as PI  # noqa: E402
 import test_oracle_primitives as PP  # noqa: E402
 import test_oracle_sampling as PS  # noqa: E402
@@ -30,10 +31,11 @@ import test_oracle_trees as PT  # noqa: E402
 
 
 def mutant(fn, old, new):
-    """fn with the text `old` of its source replaced by `new` (exactly once)."""
+    """fn (a function or class) with the text `old` of its source replaced by
+    `new` (exactly once)."""
     src = textwrap.dedent(inspect.getsource(fn))
     assert src.count(old) == 1, f"mutation site not found in {fn.__name__}: {old!r}"
-    ns = dict(fn.__globals__)
+    ns = dict(sys.modules[fn.__module__].__dict__)
     exec(compile(src.replace(old, new), f"<mutant of {fn.__name__}>", "exec"), ns)
     return ns[fn.__name__]
 
@@ -173,6 +175,17 @@ def greedy_pins():
             for s in range(20)]
 
 
+def draft_branch_pins():
+    return [lambda k=k: PD.test_draft_nodes_equal_sequential_branch_decode(PI.TINY, k)
+            for k in ("static", "dynamic")]
+
+
+def beam_pins():
+    return [lambda s=s: PD.test_dynamic_tree_matches_brute_force_beam(8, 3, 3, 5, s)
+            for s in range(3)] + [lambda: PD.test_dynamic_tree_matches_brute_force_beam(
+                12, 3, 3, 9, 0)]
+
+
 SOURCE_CASES = [
     # acceptance compares with the node's own argmax instead of its parent's
     ("accept_own_argmax", O, "greedy_accept",
@@ -214,6 +227,31 @@ SOURCE_CASES = [
     ("omega_off_by_one", MET, "omega",
      "alpha ** (gamma + 1)", "alpha ** gamma",
      lambda: [lambda: PT.test_omega_matches_monte_carlo(4, 0.8)]),
+    # a drafted node of depth d sits at position L + d instead of L + d - 1
+    ("draft_node_position", O, "_DraftExpander",
+     "np.full(len(keys), st.L + depth - 1, dtype=np.int32)",
+     "np.full(len(keys), st.L + depth, dtype=np.int32)",
+     draft_branch_pins),
+    # a drafted node attends to the committed cache and itself, not its ancestors
+    ("draft_node_without_ancestors", O, "_DraftExpander",
+     "a |= self.mask[pk]", "pass",
+     draft_branch_pins),
+    # the draft catch-up rows are rotated one position too far
+    ("catch_up_positions_shifted", O, "draft_catch_up",
+     "np.arange(L0, L0 + r, dtype=np.int32)", "np.arange(L0 + 1, L0 + r + 1, dtype=np.int32)",
+     lambda: [lambda: PD.test_draft_cache_equals_one_causal_draft_forward(PI.TINY, "static")]),
+    # log-softmax without the log-sum-exp term
+    ("log_softmax_without_lse", O, "log_softmax",
+     "return logits - (m + np.log(np.sum(np.exp(logits - m))))", "return logits - m",
+     lambda: [lambda: PD.test_log_softmax_matches_scipy(1.0)] + beam_pins()),
+    # the dynamic frontier keeps the first K candidates by creation order
+    ("frontier_by_creation_order", O, "select_dynamic_tree",
+     "frontier = [new[i] for i in topk_desc(sc, K)]", "frontier = new[:K]",
+     beam_pins),
+    # within a depth, the kept nodes are ordered by score instead of creation
+    ("final_order_by_score", O, "select_dynamic_tree",
+     "key=lambda i: (pool[i][2], i))", "key=lambda i: (pool[i][2], -pool[i][3]))",
+     beam_pins),
 ]
 
 
