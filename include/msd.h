@@ -139,11 +139,15 @@ typedef struct msd_tree {
 typedef struct msd_ctx msd_ctx;
 
 /* Byte sizes of the caller-owned buffers for this shape and these limits
- * (any output pointer may be NULL). */
+ * (any output pointer may be NULL).  Errors: MSD_ERR_INVALID_ARG for a shape
+ * or limit outside the documented ranges. */
 int msd_buffer_sizes(const msd_model_desc* m, const msd_limits* lim,
                      size_t* target_kv_bytes /* each of K and V */,
                      size_t* draft_kv_bytes /* each of K and V */,
                      size_t* workspace_bytes, size_t* weight_bytes /* packed_weights */);
+
+/* The workspace size alone (the workspace_bytes of msd_buffer_sizes). */
+int msd_workspace_size(const msd_model_desc* m, const msd_limits* lim, size_t* bytes);
 
 /* Creates a context over caller-owned weights and buffers.  stream: a
  * hipStream_t (NULL = the null stream).  Packs the matrices into
@@ -155,7 +159,11 @@ int msd_buffer_sizes(const msd_model_desc* m, const msd_limits* lim,
 int msd_create(const msd_model_desc* m, const msd_limits* lim,
                const msd_target_weights* tw, const msd_draft_weights* dw,
                const msd_buffers* bufs, void* stream, msd_ctx** out);
-void msd_destroy(msd_ctx* ctx);
+/* Waits for the context's stream and frees the host-side context (NULL: no
+ * effect).  The caller's device buffers are untouched.  Returns MSD_ERR_HIP
+ * if that wait or the release of the pinned staging buffer failed (the
+ * context is freed either way; msd_last_error(NULL) has the message). */
+int msd_destroy(msd_ctx* ctx);
 const char* msd_last_error(const msd_ctx* ctx);
 
 /*
@@ -182,13 +190,22 @@ int msd_draft_tree(msd_ctx* ctx, int n_seq, const int32_t* seqs_h,
                    const msd_tree_spec* spec, msd_tree* trees_d);
 
 /*
- * Verification: the target runs over the n_nodes tree tokens of each
- * sequence (node i at position L + depth[i], cache slot L + i) with the
- * ancestor mask, L being the sequence's committed length.  Writes the greedy
- * token of every node to argmax_d [n_seq][n_nodes] (lowest id on ties) and,
- * when logits_d is not NULL, the logits to logits_d [n_seq][n_nodes][V]
- * float32.  The tree rows' KV stay in slots [L, L+n_nodes) until
- * msd_accept_compact.
+ * Verification (Sec. 3.2, verification phase): the target runs over the
+ * n_nodes tree tokens of each sequence (node i at position L + depth[i],
+ * cache slot L + i) with the ancestor mask, L being the sequence's committed
+ * length.  Writes the greedy token of every node to argmax_d
+ * [n_seq][n_nodes] (lowest id on ties) and, when logits_d is not NULL, the
+ * logits to logits_d [n_seq][n_nodes][V] float32.  The tree rows' KV stay in
+ * slots [L, L+n_nodes) until msd_accept_compact.
+ * Trees are read on the device, so their check travels with the stream: a
+ * tree whose n_nodes differs, whose parent does not precede its child, whose
+ * depth or ancestor mask disagrees with its parents, whose token id is out of
+ * range or which repeats a token among siblings is computed with clamped ids
+ * (no access leaves its buffers), and the acceptance call that follows
+ * returns MSD_ERR_INVALID_ARG and accepts nothing for any sequence of it.
+ * Errors here: MSD_ERR_INVALID_ARG (null pointer, n_nodes outside
+ * [1, max_tree], bad sequence list), MSD_ERR_STATE (sequence without a
+ * prompt), MSD_ERR_CAPACITY (L + n_nodes > max_seq).
  */
 int msd_verify(msd_ctx* ctx, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,
                int n_nodes, int32_t* argmax_d, float* logits_d);
@@ -203,6 +220,12 @@ int msd_verify(msd_ctx* ctx, int n_seq, const int32_t* seqs_h, const msd_tree* t
  * features become the next pending draft rows and L grows by len(path).
  * emitted_h [n_seq][MSD_MAX_TREE] and n_emitted_h [n_seq] are host outputs;
  * waits for the stream.
+ * Errors: MSD_ERR_STATE unless the call follows msd_verify of the same
+ * sequence list (same order) and n_nodes, with no msd_prefill,
+ * msd_draft_tree, msd_set_state or other acceptance in between;
+ * MSD_ERR_INVALID_ARG for a malformed tree found by that verify (then
+ * nothing is accepted: caches, lengths and pending rows are unchanged and
+ * n_emitted_h is all zero).
  */
 int msd_accept_compact(msd_ctx* ctx, int n_seq, const int32_t* seqs_h,
                        const msd_tree* trees_d, int n_nodes, const int32_t* argmax_d,

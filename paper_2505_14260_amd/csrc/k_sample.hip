@@ -88,7 +88,8 @@ MSD_DEV bool is_rejected(int v, const int* rej, int n_rej) {
 
 __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sample(
     const msd_tree* trees, const int* seq_ids, int T, const float* logits, int V, float inv_t,
-    uint64_t seed, int* path, int* n_path, int* emitted, int* slot_map, const int* d_len) {
+    uint64_t seed, int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,
+    const int* tree_err, int n_seq) {
   __shared__ float sh_m[SAMPLE_WAVES], sh_s[SAMPLE_WAVES], sh_w[SAMPLE_WAVES];
   __shared__ int sh_path[MSD_MAX_TREE], sh_rej[MSD_MAX_TREE];
   __shared__ int sh_y;
@@ -99,6 +100,15 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sample(
   const int b = seq_ids[sidx];
   const int L = d_len[b];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (any_tree_err(tree_err, n_seq)) {  // a flagged call accepts nothing
+    for (int j = threadIdx.x; j < MSD_MAX_TREE; j += SAMPLE_THREADS) {
+      path[sidx * MSD_MAX_TREE + j] = -1;
+      slot_map[sidx * MSD_MAX_TREE + j] = -1;
+      emitted[sidx * MSD_MAX_TREE + j] = -1;
+    }
+    if (threadIdx.x == 0) n_path[sidx] = 0;
+    return;
+  }
   if (threadIdx.x == 0) sh_path[0] = 0;
   int cur = 0, n = 1, jd = 0, n_rej = 0;
   const float* lg = logits;
@@ -223,10 +233,10 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sample(
 void launch_accept_sample(const void* trees, int n_seq, const int* seq_ids, int T,
                           const float* logits, int V, float inv_t, uint64_t seed, int* path,
                           int* n_path, int* emitted, int* slot_map, const int* d_len,
-                          hipStream_t st) {
+                          const int* tree_err, hipStream_t st) {
   hipLaunchKernelGGL(k_accept_sample, dim3(n_seq), dim3(SAMPLE_THREADS), 0, st,
                      (const msd_tree*)trees, seq_ids, T, logits, V, inv_t, seed, path, n_path,
-                     emitted, slot_map, d_len);
+                     emitted, slot_map, d_len, tree_err, n_seq);
 }
 
 }  // namespace msd

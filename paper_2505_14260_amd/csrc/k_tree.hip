@@ -320,15 +320,50 @@ __global__ __launch_bounds__(FIN_THREADS) void k_dyn_finalize(DynPool pool, msd_
   }
 }
 
-__global__ void k_verify_rows(const msd_tree* trees, const int* seq_ids, const int* d_len,
-                              int T, int vocab, Rows r, int* prefix) {
+// Verify-row descriptors of one sequence's tree (one 64-thread block per
+// sequence), and the tree check: tree_err[sidx] = 1 unless the tree has T
+// nodes, ids in [0, vocab), a root (parent -1, depth 0, anc = bit 0) and, for
+// every other node, a parent that precedes it, depth = parent's depth + 1,
+// anc = parent's anc | own bit, and a token that no earlier sibling carries.
+// The acceptance kernels take no decision on a call with a flagged tree.
+__global__ __launch_bounds__(MSD_MAX_TREE) void k_verify_rows(
+    const msd_tree* trees, const int* seq_ids, const int* d_len, int T, int vocab, Rows r,
+    int* prefix, int* tree_err) {
+  __shared__ int sp[MSD_MAX_TREE], sd[MSD_MAX_TREE], stk[MSD_MAX_TREE];
+  __shared__ uint64_t sa[MSD_MAX_TREE];
+  __shared__ int bad;
   const int sidx = blockIdx.x;
   const int i = threadIdx.x;
   const int b = seq_ids[sidx];
   const int L = d_len[b];
-  if (i == 0) prefix[sidx] = L;
-  if (i >= T) return;
   const msd_tree* t = trees + sidx;
+  if (i == 0) {
+    prefix[sidx] = L;
+    bad = t->n_nodes != T;
+  }
+  if (i < T) {
+    sp[i] = t->parent[i];
+    sd[i] = t->depth[i];
+    stk[i] = t->token[i];
+    sa[i] = t->anc[i];
+  }
+  __syncthreads();
+  if (i < T) {
+    bool e = stk[i] < 0 || stk[i] >= vocab;
+    const int p = sp[i];
+    if (i == 0) {
+      e |= p != -1 || sd[0] != 0 || sa[0] != 1ull;
+    } else if (p < 0 || p >= i) {
+      e = true;
+    } else {
+      e |= sd[i] != sd[p] + 1 || sa[i] != (sa[p] | (1ull << i));
+      for (int j = 1; j < i; ++j) e |= sp[j] == p && stk[j] == stk[i];
+    }
+    if (e) atomicOr(&bad, 1);
+  }
+  __syncthreads();
+  if (i == 0) tree_err[sidx] = bad;
+  if (i >= T) return;
   const int row = sidx * T + i;
   // caller-supplied trees: keep ids and positions inside their tables
   r.tok[row] = min(max(t->token[i], 0), vocab - 1);
@@ -346,17 +381,27 @@ __global__ void k_verify_rows(const msd_tree* trees, const int* seq_ids, const i
 // siblings carry distinct tokens).  One wave per sequence: the tree and the
 // argmax row are staged in LDS by one lane per node, lane 0 takes the
 // decisions in node order, and the lanes write the outputs.
+// A call whose verify flagged any tree (tree_err) accepts nothing: every
+// sequence gets an empty path, so compaction and commit leave it unchanged.
 __global__ __launch_bounds__(MSD_MAX_TREE) void k_accept(const msd_tree* trees,
                                                          const int* seq_ids, int T,
                                                          const int* amax, int* path,
                                                          int* n_path, int* emitted,
-                                                         int* slot_map, const int* d_len) {
+                                                         int* slot_map, const int* d_len,
+                                                         const int* tree_err, int n_seq) {
   __shared__ int par[MSD_MAX_TREE], tok[MSD_MAX_TREE], dep[MSD_MAX_TREE], am[MSD_MAX_TREE];
   __shared__ int pth[MSD_MAX_TREE];
   __shared__ int n_sh;
   const int sidx = blockIdx.x;
   const int j = threadIdx.x;
   const msd_tree* t = trees + sidx;
+  if (any_tree_err(tree_err, n_seq)) {
+    path[sidx * MSD_MAX_TREE + j] = -1;
+    slot_map[sidx * MSD_MAX_TREE + j] = -1;
+    emitted[sidx * MSD_MAX_TREE + j] = -1;
+    if (j == 0) n_path[sidx] = 0;
+    return;
+  }
   if (j < T) {
     par[j] = t->parent[j];
     tok[j] = t->token[j];
@@ -537,18 +582,18 @@ void launch_dyn_finalize(DynPool pool, void* trees, int n_seq, const int* seq_id
 }
 
 void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
-                        int T, int vocab, Rows r, int* prefix, hipStream_t st) {
-  hipLaunchKernelGGL(k_verify_rows, dim3(n_seq), dim3(64), 0, st, (const msd_tree*)trees,
-                     seq_ids, d_len, T, vocab, r, prefix);
+                        int T, int vocab, Rows r, int* prefix, int* tree_err, hipStream_t st) {
+  hipLaunchKernelGGL(k_verify_rows, dim3(n_seq), dim3(MSD_MAX_TREE), 0, st,
+                     (const msd_tree*)trees, seq_ids, d_len, T, vocab, r, prefix, tree_err);
 }
 
 
 
 void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,
                    int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,
-                   hipStream_t st) {
+                   const int* tree_err, hipStream_t st) {
   hipLaunchKernelGGL(k_accept, dim3(n_seq), dim3(MSD_MAX_TREE), 0, st, (const msd_tree*)trees,
-                     seq_ids, T, amax, path, n_path, emitted, slot_map, d_len);
+                     seq_ids, T, amax, path, n_path, emitted, slot_map, d_len, tree_err, n_seq);
 }
 
 void launch_compact(uint16_t* kc, uint16_t* vc, int n_layers, int B, int KV, int S, int hd,

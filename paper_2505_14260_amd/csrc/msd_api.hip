@@ -154,6 +154,7 @@ struct msd_ctx {
   uint16_t* pend_h;
   float* dfeat;
   int *acc_path, *acc_n, *acc_emit, *acc_slot, *feat_idx;
+  int* tree_err;  // per call slot: the last verify found the tree malformed
   int* tk_idx;
   float *tk_val, *tk_lse;
   StaticSpec sp;
@@ -174,7 +175,9 @@ struct msd_ctx {
   std::vector<int> sp_parent, sp_rank;
   std::vector<int> round_off, round_n, round_k, round_exp_end;
   int sp_T = 0, sp_D = 0;
-  int verified_T = 0, verified_nseq = 0;
+  // the last msd_verify not yet followed by an acceptance (verified_T == 0: none)
+  int verified_T = 0;
+  std::vector<int> verified_seqs;
   // optional per-GEMM event trace (msd_trace_enable)
   struct TraceRec {
     int epi, M, N, K;
@@ -264,6 +267,7 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->acc_emit = cv.take<int>((size_t)B * MSD_MAX_TREE);
   t->acc_slot = cv.take<int>((size_t)B * MSD_MAX_TREE);
   t->feat_idx = cv.take<int>(B);
+  t->tree_err = cv.take<int>(B);
   t->tk_idx = cv.take<int>((size_t)p.lrows * TOPK);
   t->tk_val = cv.take<float>((size_t)p.lrows * TOPK);
   t->tk_lse = cv.take<float>(p.lrows);
@@ -645,8 +649,9 @@ int check_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* t
                  int n_nodes, int32_t* emitted_h, int32_t* n_emitted_h) {
   TRY(check_seqs(c, n_seq, seqs_h));
   if (!trees_d || !emitted_h || !n_emitted_h) return fail(c, MSD_ERR_INVALID_ARG, "null argument");
-  if (n_nodes != c->verified_T || n_seq != c->verified_nseq)
-    return fail(c, MSD_ERR_STATE, "accept must follow msd_verify of the same trees");
+  if (c->verified_T == 0 || n_nodes != c->verified_T ||
+      !std::equal(seqs_h, seqs_h + n_seq, c->verified_seqs.begin(), c->verified_seqs.end()))
+    return fail(c, MSD_ERR_STATE, "accept must follow msd_verify of the same sequences and trees");
   return upload_seqs(c, seqs_h, n_seq);
 }
 
@@ -662,12 +667,24 @@ int finish_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, int T, int32_t* 
   launch_commit(n_seq, c->seq_ids, c->acc_path, c->acc_n, c->acc_emit, c->h, T, d, c->pend_h,
                 c->pend_next, c->pend_n, PEND, c->d_len, c->d_root, c->st);
   LAUNCHED(c);
-  int* back = c->stage + STAGE_INTS - (MSD_MAX_TREE + 1) * 8 - 64;
+  int* back = c->stage + STAGE_INTS - (MSD_MAX_TREE + 2) * 8 - 64;
   HIPC(c, hipMemcpyAsync(back, c->acc_emit, sizeof(int) * MSD_MAX_TREE * n_seq,
                          hipMemcpyDeviceToHost, c->st));
   HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8, c->acc_n, sizeof(int) * n_seq,
                          hipMemcpyDeviceToHost, c->st));
+  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8 + 8, c->tree_err, sizeof(int) * n_seq,
+                         hipMemcpyDeviceToHost, c->st));
   HIPC(c, hipStreamSynchronize(c->st));
+  c->verified_T = 0;
+  for (int i = 0; i < n_seq; ++i)
+    if (back[MSD_MAX_TREE * 8 + 8 + i]) {
+      // the kernels accepted nothing for any sequence of the call
+      for (int k = 0; k < n_seq; ++k) n_emitted_h[k] = 0;
+      return fail(c, MSD_ERR_INVALID_ARG,
+                  "malformed tree for call slot " + std::to_string(i) +
+                      " (parent order, depth, ancestor mask, token id or duplicate sibling); "
+                      "nothing was accepted");
+    }
   for (int i = 0; i < n_seq; ++i) {
     const int n = back[MSD_MAX_TREE * 8 + i];
     n_emitted_h[i] = n;
@@ -675,7 +692,6 @@ int finish_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, int T, int32_t* 
     c->L[seqs_h[i]] += n;
     c->pend[seqs_h[i]] = n;
   }
-  c->verified_T = 0;
   return MSD_OK;
 }
 
@@ -692,6 +708,11 @@ int msd_buffer_sizes(const msd_model_desc* m, const msd_limits* lim, size_t* tar
   if (workspace_bytes) *workspace_bytes = carve(nullptr, *m, *lim, nullptr);
   if (weight_bytes) *weight_bytes = weight_layout(*m).total * sizeof(uint16_t);
   return MSD_OK;
+}
+
+int msd_workspace_size(const msd_model_desc* m, const msd_limits* lim, size_t* bytes) {
+  if (!bytes) return fail(nullptr, MSD_ERR_INVALID_ARG, "null output pointer");
+  return msd_buffer_sizes(m, lim, nullptr, nullptr, bytes, nullptr);
 }
 
 int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_weights* tw,
@@ -758,6 +779,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     HIPC(c, hipMemsetAsync(c->d_len, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->pend_n, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->d_root, 0, sizeof(int) * lim->max_batch, c->st));
+    HIPC(c, hipMemsetAsync(c->tree_err, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->gemm_zero, 0, sizeof(uint16_t) * gemm_dummy_elems(), c->st));
     launch_rope_table(c->rope, lim->max_seq, m->head_dim, (double)m->rope_theta, c->st);
     LAUNCHED(c);
@@ -793,12 +815,17 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   return MSD_OK;
 }
 
-void msd_destroy(msd_ctx* c) {
-  if (!c) return;
-  (void)hipStreamSynchronize(c->st);
+int msd_destroy(msd_ctx* c) {
+  if (!c) return MSD_OK;
+  const hipError_t e1 = hipStreamSynchronize(c->st);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
-  (void)hipHostFree(c->stage);
+  const hipError_t e2 = hipHostFree(c->stage);
   delete c;
+  if (e1 != hipSuccess || e2 != hipSuccess) {
+    g_err = std::string("msd_destroy: ") + hipGetErrorString(e1 != hipSuccess ? e1 : e2);
+    return MSD_ERR_HIP;
+  }
+  return MSD_OK;
 }
 
 const char* msd_last_error(const msd_ctx* c) { return c ? c->err.c_str() : g_err.c_str(); }
@@ -818,6 +845,7 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
   if (n + c->lim.max_tree > c->lim.max_seq)
     return fail(c, MSD_ERR_CAPACITY, "prompt does not fit the KV cache");
   if (is_visual_h[n - 1]) return fail(c, MSD_ERR_INVALID_ARG, "prompt must end in a text token");
+  c->verified_T = 0;  // a prompt invalidates a pending verify (it rewrites the features)
   int n_vis = 0;
   for (int i = 0; i < n; ++i) {
     if (!is_visual_h[i] && (tokens_h[i] < 0 || tokens_h[i] >= m.vocab))
@@ -890,6 +918,7 @@ int msd_set_state(msd_ctx* c, int seq, int L, const void* h_d, int32_t next_toke
   if (seq < 0 || seq >= c->lim.max_batch || !h_d) return fail(c, MSD_ERR_INVALID_ARG, "bad argument");
   if (L < 1 || L + c->lim.max_tree > c->lim.max_seq) return fail(c, MSD_ERR_CAPACITY, "length does not fit");
   if (next_token < 0 || next_token >= c->m.vocab) return fail(c, MSD_ERR_INVALID_ARG, "token out of range");
+  c->verified_T = 0;
   int v[4] = {L, next_token, 1, next_token};
   TRY(upload_many(c, {{c->d_len + seq, v, sizeof(int)}, {c->d_root + seq, v + 1, sizeof(int)},
                       {c->pend_n + seq, v + 2, sizeof(int)},
@@ -909,6 +938,7 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
   if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
   TRY(check_seqs(c, n_seq, seqs_h));
   if (!spec || !trees_d) return fail(c, MSD_ERR_INVALID_ARG, "null spec or tree buffer");
+  c->verified_T = 0;
   const msd_model_desc& m = c->m;
   const int d = m.d_model;
   int T = 0, D = 0, K = 0;
@@ -1025,7 +1055,9 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
     c->att_keys[i] = c->L[seqs_h[i]] + T;
   }
   const int rows = n_seq * T;
-  launch_verify_rows(trees_d, n_seq, c->seq_ids, c->d_len, T, V, c->rows, c->prefix, c->st);
+  c->verified_T = 0;
+  launch_verify_rows(trees_d, n_seq, c->seq_ids, c->d_len, T, V, c->rows, c->prefix,
+                     c->tree_err, c->st);
   LAUNCHED(c);
   launch_embed(c->embed, c->rows.tok, nullptr, nullptr, rows, d, c->x, c->st);
   LAUNCHED(c);
@@ -1040,7 +1072,7 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
     LAUNCHED(c);
   }
   c->verified_T = T;
-  c->verified_nseq = n_seq;
+  c->verified_seqs.assign(seqs_h, seqs_h + n_seq);
   return MSD_OK;
 }
 
@@ -1052,7 +1084,7 @@ int msd_accept_compact(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_t
   if (!argmax_d) return fail(c, MSD_ERR_INVALID_ARG, "null argument");
   int* slots = slot_map_d ? slot_map_d : c->acc_slot;
   launch_accept(trees_d, n_seq, c->seq_ids, n_nodes, argmax_d, c->acc_path, c->acc_n,
-                c->acc_emit, slots, c->d_len, c->st);
+                c->acc_emit, slots, c->d_len, c->tree_err, c->st);
   LAUNCHED(c);
   return finish_accept(c, n_seq, seqs_h, n_nodes, emitted_h, n_emitted_h);
 }
@@ -1070,7 +1102,8 @@ int msd_accept_sample(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tr
     if (c->L[seqs_h[i]] >= (1 << 24)) return fail(c, MSD_ERR_INVALID_ARG, "sequence too long");
   int* slots = slot_map_d ? slot_map_d : c->acc_slot;
   launch_accept_sample(trees_d, n_seq, c->seq_ids, n_nodes, logits_d, c->m.vocab, inv_t, seed,
-                       c->acc_path, c->acc_n, c->acc_emit, slots, c->d_len, c->st);
+                       c->acc_path, c->acc_n, c->acc_emit, slots, c->d_len, c->tree_err,
+                       c->st);
   LAUNCHED(c);
   return finish_accept(c, n_seq, seqs_h, n_nodes, emitted_h, n_emitted_h);
 }

@@ -36,6 +36,13 @@ MSD_DEV float get_split(const uint16_t* row, int K, int k) {
   return bf2f(row[k]) + bf2f(row[K + k]);
 }
 
+// True when the verify of this call flagged any of its n_seq trees.
+MSD_DEV bool any_tree_err(const int* tree_err, int n_seq) {
+  int e = 0;
+  for (int i = 0; i < n_seq; ++i) e |= tree_err[i];
+  return e != 0;
+}
+
 namespace msd {
 
 // ---------------------------------------------------------------- GEMM ----
@@ -237,16 +244,18 @@ void launch_dyn_expand(DynPool pool, int n_seq, const int* topk_idx, const float
                        const float* lse, int K, int n_pool, int exp_base, hipStream_t st);
 void launch_dyn_finalize(DynPool pool, void* trees, int n_seq, const int* seq_ids,
                          const int* d_root, int n_pool, int N, hipStream_t st);
+// Verify rows of each tree; tree_err[sidx] = 1 when the tree is malformed.
 void launch_verify_rows(const void* trees, int n_seq, const int* seq_ids, const int* d_len,
-                        int T, int vocab, Rows r, int* prefix, hipStream_t st);
+                        int T, int vocab, Rows r, int* prefix, int* tree_err, hipStream_t st);
+// Greedy acceptance; when any tree_err[0..n_seq) is set, every path is empty.
 void launch_accept(const void* trees, int n_seq, const int* seq_ids, int T, const int* amax,
                    int* path, int* n_path, int* emitted, int* slot_map, const int* d_len,
-                   hipStream_t st);
+                   const int* tree_err, hipStream_t st);
 // Speculative sampling acceptance (k_sample.hip): same outputs as launch_accept.
 void launch_accept_sample(const void* trees, int n_seq, const int* seq_ids, int T,
                           const float* logits, int V, float inv_t, uint64_t seed, int* path,
                           int* n_path, int* emitted, int* slot_map, const int* d_len,
-                          hipStream_t st);
+                          const int* tree_err, hipStream_t st);
 void launch_compact(uint16_t* kc, uint16_t* vc, int n_layers, int B, int KV, int S, int hd,
                     int n_seq, const int* seq_ids, const int* path, const int* n_path,
                     const int* d_len, hipStream_t st);

@@ -77,8 +77,8 @@ def lib():
         L.msd_buffer_sizes.argtypes = [P(ModelDesc), P(Limits), P(c_sz), P(c_sz), P(c_sz), P(c_sz)]
         L.msd_create.argtypes = [P(ModelDesc), P(Limits), P(TargetWeights), P(DraftWeights),
                                  P(Buffers), c_vp, P(c_vp)]
+        L.msd_workspace_size.argtypes = [P(ModelDesc), P(Limits), P(c_sz)]
         L.msd_destroy.argtypes = [c_vp]
-        L.msd_destroy.restype = None
         L.msd_last_error.argtypes = [c_vp]
         L.msd_last_error.restype = ctypes.c_char_p
         L.msd_prefill.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, P(c_i32), P(ctypes.c_uint8),
@@ -131,8 +131,14 @@ def msd_create(desc, lim, tw, dw, bufs, stream):
     return out.value
 
 
+def msd_workspace_size(desc: ModelDesc, lim: Limits):
+    w = c_sz()
+    _check(None, lib().msd_workspace_size(ctypes.byref(desc), ctypes.byref(lim), ctypes.byref(w)))
+    return w.value
+
+
 def msd_destroy(ctx):
-    lib().msd_destroy(ctx)
+    _check(None, lib().msd_destroy(ctx))
 
 
 def msd_last_error(ctx):

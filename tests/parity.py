@@ -25,6 +25,14 @@ def decided(row, rtol=RTOL):
     return (s[0] - s[1]) > rtol * np.abs(row).max()
 
 
+def argmax_ok(g, row, rtol=RTOL):
+    """The GPU's greedy token g is valid for an oracle logits row: it is the
+    oracle's argmax, or (at an undecided row) its oracle logit lies within the
+    tolerance band below the row's maximum."""
+    row = np.asarray(row, dtype=np.float64)
+    return bool(0 <= int(g) < len(row) and row[int(g)] >= row.max() - rtol * np.abs(row).max())
+
+
 def rank_decided(row, r, rtol=RTOL):
     """True when the r-th and (r+1)-th best values are separated (top-k boundary)."""
     s = np.sort(np.asarray(row, dtype=np.float64))[::-1]
@@ -81,13 +89,47 @@ def compare_static_tree(g, ref, logs, rank, rtol=RTOL):
             continue
         if g.token[c] != ref.token[c]:
             assert not rank_decided(logs[p], int(rank[c]), rtol), (c, g.token[c], ref.token[c])
+            # a gated node: the GPU's token must itself sit in the near-tie
+            # band around the oracle's value at that rank
+            row = np.asarray(logs[p], dtype=np.float64)
+            s = np.sort(row)[::-1]
+            gt = int(g.token[c])
+            assert 0 <= gt < len(row)
+            assert abs(row[gt] - s[int(rank[c])]) <= 2 * rtol * np.abs(row).max(), \
+                (c, gt, row[gt], s[int(rank[c])])
             skip.add(c)
         else:
             checked += 1
     return checked
 
 
-def compare_dynamic_tree(g, pool, rows, root_logits, K, N, rtol=RTOL):
+def dynamic_tree_gated(pool, rows, root_logits, K, N, rtol=RTOL):
+    """True when any decision that shapes the oracle's dynamic tree lies
+    within the tolerance: adjacent log-probabilities among the top K + 1 of
+    an expanded row (membership and creation order), the K-th/(K+1)-th score
+    of a depth's candidates (the frontier), or the N-th/(N+1)-th score of the
+    pool (the kept nodes)."""
+    def gaps(vals, k):
+        s = np.sort(np.asarray(vals, dtype=np.float64))[::-1][:k + 1]
+        return np.diff(-s)
+
+    for r in [root_logits] + list(rows.values()):
+        if (gaps(log_softmax(r), K) <= 2 * rtol * np.abs(r).max()).any():
+            return True
+    # cumulative tolerance along a path: one per-step tolerance per depth
+    steps = [2 * rtol * np.abs(r).max() for r in [root_logits] + list(rows.values())]
+    tol = max(steps) * max(p[2] for p in pool)
+    scores = np.array([p[3] for p in pool])
+    depths = np.array([p[2] for p in pool])
+    for d in np.unique(depths):
+        sd = np.sort(scores[depths == d])[::-1]
+        if len(sd) > K and sd[K - 1] - sd[K] <= 2 * tol:
+            return True
+    sp = np.sort(scores)[::-1]
+    return len(sp) > N and sp[N - 1] - sp[N] <= 2 * tol
+
+
+def compare_dynamic_tree(g, pool, rows, root_logits, K, N, rtol=RTOL, ref=None):
     """Dynamic tree against the oracle's pool (select_dynamic_tree's output).
 
     Several trees are correct when draft scores tie within the tolerance, so:
@@ -98,8 +140,10 @@ def compare_dynamic_tree(g, pool, rows, root_logits, K, N, rtol=RTOL):
     within that tolerance of the decision that excluded it (its parent's
     top-K boundary, the frontier boundary at its parent's depth, or the
     top-N boundary of the pool), and so must every oracle node the GPU did
-    not select.  Returns (nodes equal to the oracle's tree, nodes compared
-    by score)."""
+    not select.  When `ref` (the oracle's tree) is given and no decision of
+    the oracle lies within the tolerance, the token, parent, depth and
+    ancestor arrays must equal the oracle's bit for bit.  Returns (nodes
+    equal to the oracle's tree, nodes compared by score)."""
     check_tree_invariants(g)
     assert g.n_nodes == N + 1
     tok, par, dep, sc = gpu_tree_arrays(g)
@@ -133,6 +177,28 @@ def compare_dynamic_tree(g, pool, rows, root_logits, K, N, rtol=RTOL):
     for c in range(1, g.n_nodes):
         k = (gkeys[par[c] - 1] if par[c] > 0 else ()) + (int(tok[c]),)
         gkeys.append(k)
+    if ref is not None:
+        # Bit-exact tree indices unless a near tie decided them: either no
+        # decision of the oracle is near a tie, or the GPU kept the oracle's
+        # nodes and no two kept siblings have log-probabilities within the
+        # tolerance (their creation order, hence the node order, is decided).
+        order_gated = False
+        for k in ref_keys:
+            i = index[k]
+            p = pool[i][0]
+            for k2 in ref_keys:
+                i2 = index[k2]
+                if i2 != i and pool[i2][0] == p and \
+                        abs(lq[p][k[-1]] - lq[p][k2[-1]]) <= rtol_row[p]:
+                    order_gated = True
+        exact = not dynamic_tree_gated(pool, rows, root_logits, K, N, rtol) or \
+            (set(gkeys) == ref_keys and not order_gated)
+        if exact:
+            assert list(tok) == [int(x) for x in ref.token], "tokens differ with no near tie"
+            assert list(par) == [int(x) for x in ref.parent]
+            assert list(dep) == [int(x) for x in ref.depth]
+            assert [int(x) for x in g.anc[:g.n_nodes]] == [int(x) for x in ref.anc]
+            compare_dynamic_tree.exact += 1
     same, scored = 0, 0
     for c, k in enumerate(gkeys, start=1):
         if k in ref_keys:
@@ -164,6 +230,9 @@ def compare_dynamic_tree(g, pool, rows, root_logits, K, N, rtol=RTOL):
             near |= scores[p] <= f_k1 + 2 * tol_of[p] + rtol_row[p]
         assert near, ("oracle node missing on the GPU without a near tie", k)
     return same, scored
+
+
+compare_dynamic_tree.exact = 0  # trees compared bit for bit (no gate fired)
 
 
 def oracle_draft_static(m, st, paths):

@@ -33,7 +33,7 @@ import synth
 from synth.configs import LLAVA7B, LLAVA13B, LLAVA7B_LONG, QWEN7B
 from oracle import model as M
 from oracle import msd as O
-from parity import (RTOL, compare_dynamic_tree, compare_static_tree, decided,
+from parity import (RTOL, argmax_ok, compare_dynamic_tree, compare_static_tree, decided,
                     gpu_tree_arrays, oracle_draft_dynamic, oracle_draft_static,
                     oracle_tree_of, row_close, sampling_agrees)
 
@@ -137,9 +137,10 @@ class Case:
             else:
                 K, N = wl.tree.topk, wl.tree.n_nodes
                 ref, pool, rows, root_logits = oracle_draft_dynamic(m, st, K, wl.tree.depth, N)
-                same, scored = compare_dynamic_tree(g, pool, rows, root_logits, K, N)
+                same, scored = compare_dynamic_tree(g, pool, rows, root_logits, K, N, ref=ref)
                 log(f"[{label} seq {b}] dynamic draft tree: {same}/{N} nodes as the oracle's, "
-                    f"{scored} scores compared")
+                    f"{scored} scores compared, {compare_dynamic_tree.exact} trees compared "
+                    f"bit for bit so far")
         amax, logits = eng.verify(seqs, trees, T, want_logits=True)
         torch.cuda.synchronize()
         lg = logits.cpu().numpy().reshape(n, T, -1)
@@ -152,9 +153,8 @@ class Case:
             ok, err = row_close(lg[b], lg_ref)
             n_dec = 0
             for i in range(T):
-                if decided(lg_ref[i]):
-                    assert am[b, i] == int(np.argmax(lg_ref[i])), (b, i)
-                    n_dec += 1
+                assert argmax_ok(am[b, i], lg_ref[i]), (b, i)
+                n_dec += decided(lg_ref[i])
             L = st.L
             kerr = 0.0
             for l in range(self.dims.n_layers):
@@ -165,7 +165,8 @@ class Case:
                 assert okk and okv, (b, l, ek, ev)
                 kerr = max(kerr, ek, ev)
             log(f"[{label} seq {b}] verify L={L}: logits max rel err {err:.2e}, "
-                f"{n_dec}/{T} argmax decided and equal, tree K/V max rel err {kerr:.2e}")
+                f"{n_dec}/{T} argmax decided and equal (the rest in the near-tie band), "
+                f"tree K/V max rel err {kerr:.2e}")
             assert ok, err
             refs.append((tree, h_ref))
         # acceptance along a chosen chain of first children, forced through argmax

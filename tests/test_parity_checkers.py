@@ -101,3 +101,44 @@ def test_static_checker(tiny_state):
     g.parent[ref.n - 1] = 0
     with pytest.raises(AssertionError):
         compare_static_tree(g, ref, logs, rank)
+
+
+def test_dynamic_checker_exact_mode(tiny_state):
+    """With the oracle's tree given, a GPU tree holding the same nodes in a
+    different order (two leaf siblings swapped) is reported unless their
+    log-probabilities lie within the tolerance."""
+    m, st = tiny_state
+    K, D, N = 2, 2, 3   # a tiny-model tree with no near tie among its decisions
+    tree, pool, rows, root_logits = oracle_draft_dynamic(m, fresh(st), K, D, N)
+    compare_dynamic_tree.exact = 0
+    compare_dynamic_tree(as_ctypes(tree), pool, rows, root_logits, K, N, ref=tree)
+    assert compare_dynamic_tree.exact == 1
+    pairs = [(a, b) for a in range(1, tree.n) for b in range(a + 1, tree.n)
+             if tree.parent[a] == tree.parent[b]]
+    assert pairs
+    a, b = pairs[0]
+    # the same nodes with siblings a and b (and their subtrees) in swapped order
+    perm = np.arange(tree.n)
+    perm[a], perm[b] = b, a
+    bad = O.Tree(tree.token.copy(), tree.parent.copy(), tree.depth.copy(), tree.score.copy())
+    for i in range(tree.n):
+        j = perm[i]
+        bad.token[j], bad.depth[j], bad.score[j] = tree.token[i], tree.depth[i], tree.score[i]
+        bad.parent[j] = perm[tree.parent[i]] if tree.parent[i] >= 0 else -1
+    row = root_logits if tree.parent[a] == 0 else None
+    if row is None:
+        # the parent's draft row: the pool entry with the parent's token path
+        keys = {}
+        for i, (pp, t, d, s) in enumerate(pool):
+            keys[i] = (keys[pp] if pp >= 0 else ()) + (t,)
+        path, u = [], int(tree.parent[a])
+        while u > 0:
+            path.append(int(tree.token[u]))
+            u = int(tree.parent[u])
+        pk = tuple(reversed(path))
+        row = rows[next(i for i, k in keys.items() if k == pk)]
+    from parity import RTOL, log_softmax
+    lq = log_softmax(row)
+    assert abs(lq[tree.token[a]] - lq[tree.token[b]]) > 2 * RTOL * np.abs(row).max()
+    with pytest.raises(AssertionError):
+        compare_dynamic_tree(as_ctypes(bad), pool, rows, root_logits, K, N, ref=tree)
