@@ -211,6 +211,24 @@ int msd_verify(msd_ctx* ctx, int n_seq, const int32_t* seqs_h, const msd_tree* t
                int n_nodes, int32_t* argmax_d, float* logits_d);
 
 /*
+ * msd_verify for callers that cannot allocate device memory or must not make
+ * the library use its workspace for per-call scratch (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).  Same
+ * arguments, results and errors as msd_verify, and the same kernels; the
+ * call's scratch (GEMM split-K partials, attention partials, top-k scratch)
+ * lives in a static device array of MSD_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends.  Nothing is
+ * allocated.  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (other contexts or streams) race and must be ordered by
+ * the caller.  MSD_ERR_INVALID_ARG when n_seq * n_nodes > 256 or when the
+ * call's scratch exceeds MSD_NOALLOC_SCRATCH_BYTES (the message gives the
+ * size needed).
+ */
+#define MSD_NOALLOC_SCRATCH_BYTES (64u << 20)
+int msd_verify_noalloc(msd_ctx* ctx, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,
+                       int n_nodes, int32_t* argmax_d, float* logits_d);
+
+/*
  * Acceptance and compaction: for each sequence, the deepest node whose every
  * token on the root path equals its parent's argmax is accepted; emitted
  * tokens are the accepted drafted tokens followed by the bonus token (the

@@ -6,6 +6,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <initializer_list>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -13,6 +14,35 @@
 #include "msd_internal.h"
 
 using namespace msd;
+
+// Scratch of msd_verify_noalloc: GEMM split-K partials, attention partials
+// and top-k scratch of one verify call.  One copy per GPU, held until the
+// process ends.  Host code never uses this name as an address: it takes the
+// device address from hipGetSymbolAddress (noalloc_scratch below).
+static __device__ __align__(256) float scratch[MSD_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES];  // device address of `scratch` per device
+
+// The device address of this device's `scratch` (resolved once per device,
+// with that device current), or an error.
+hipError_t noalloc_scratch(int dev, void** out) {
+  if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
 
 namespace {
 
@@ -162,6 +192,8 @@ struct msd_ctx {
   GemmScratch gs;
   float *att_po, *att_ml, *tk_scratch;
   float2* rope;
+  int device;            // the GPU current at msd_create
+  float* noalloc_base;   // that GPU's copy of `scratch`
   // host
   int* stage;  // pinned staging
   std::vector<int> L, pend, ready;
@@ -355,7 +387,6 @@ int upload_seqs(msd_ctx* c, const int32_t* seqs, int n) {
 
 // GEMM launch kinds (for the optional trace)
 enum { GK_QKV = 0, GK_O = 1, GK_DOWN = 2, GK_GATEUP = 3, GK_FC = 4, GK_LMHEAD = 5 };
-
 // Partial products of rows [0, M) (M <= 64) of the split rows X (row stride
 // ldx = 2K) against the packed weight W [N][K] (and W2); returns the view the
 // consumer sums.
@@ -387,6 +418,38 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
   return MSD_OK;
 }
 
+
+// Key chunks of a tree-attention pass: each of a workgroup's TREE_WAVES
+// waves takes chunk_keys / TREE_WAVES keys (a multiple of 32); enough chunks
+// for about one workgroup per CU while every wave keeps at least one block
+// (a wave hides little latency behind its own blocks, so spreading the keys
+// over more CUs pays until the combine pass dominates), within the partial
+// buffer of cap floats.
+struct TreeChunks {
+  int qtiles, chunk_keys, n_chunks;
+  size_t part_floats;
+};
+TreeChunks plan_tree_chunks(const msd_model_desc& m, int n_seq, int nq, int max_ltot,
+                            size_t cap) {
+  TreeChunks t;
+  const int KV = m.n_kv_heads, G = m.n_heads / m.n_kv_heads;
+  t.qtiles = (nq * G + 31) / 32;
+  const int span = 32 * TREE_WAVES;
+  const int base_items = n_seq * KV * t.qtiles;
+  const int max_chunks = std::max(1, (max_ltot + span - 1) / span);
+  const int chunks = std::min(max_chunks, std::max(1, (256 + base_items - 1) / base_items));
+  int ck = (max_ltot + chunks - 1) / chunks;
+  ck = (ck + span - 1) / span * span;
+  while ((max_ltot + ck - 1) / ck > ATT_MAX_CHUNKS ||
+         attn_partial_floats(n_seq, KV, t.qtiles, (max_ltot + ck - 1) / ck, m.head_dim) > cap)
+    ck += span;
+  t.chunk_keys = ck;
+  t.n_chunks = (max_ltot + ck - 1) / ck;
+  t.part_floats = t.n_chunks > 1
+                      ? attn_partial_floats(n_seq, KV, t.qtiles, t.n_chunks, m.head_dim)
+                      : 0;
+  return t;
+}
 
 // GEMM input of a normalised layer: xn = x * g (split rows) and the per-row
 // sums of squares; the GEMM's consumer applies 1/rms (RMSNorm factored through the
@@ -458,25 +521,10 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       a.n_chunks = 1;
       launch_causal_attention(a, c->st);
     } else {
-      const int G = H / KV;
-      a.qtiles = (nq * G + 31) / 32;
-      // key chunks: each of a workgroup's TREE_WAVES waves takes
-      // chunk_keys / TREE_WAVES keys (a multiple of 32); enough chunks for
-      // about one workgroup per CU while every wave keeps at least one block
-      // (a wave hides little latency behind its own blocks, so spreading the
-      // keys over more CUs pays until the combine pass dominates)
-      const int span = 32 * TREE_WAVES;
-      const int base_items = n_seq * KV * a.qtiles;
-      const int max_chunks = std::max(1, (max_ltot + span - 1) / span);
-      const int chunks = std::min(max_chunks, std::max(1, (256 + base_items - 1) / base_items));
-      int ck = (max_ltot + chunks - 1) / chunks;
-      ck = (ck + span - 1) / span * span;
-      while ((max_ltot + ck - 1) / ck > ATT_MAX_CHUNKS ||
-             attn_partial_floats(n_seq, KV, a.qtiles, (max_ltot + ck - 1) / ck, hd) >
-                 c->plan.attn_floats)
-        ck += span;
-      a.chunk_keys = ck;
-      a.n_chunks = (max_ltot + ck - 1) / ck;
+      const TreeChunks tc = plan_tree_chunks(m, n_seq, nq, max_ltot, c->plan.attn_floats);
+      a.qtiles = tc.qtiles;
+      a.chunk_keys = tc.chunk_keys;
+      a.n_chunks = tc.n_chunks;
       launch_tree_attention(a, c->st);
     }
     LAUNCHED(c);
@@ -758,6 +806,17 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   c->dk = (uint16_t*)bufs->draft_k;
   c->dv = (uint16_t*)bufs->draft_v;
   carve(c, *m, *lim, (char*)bufs->workspace);
+  {
+    hipError_t e = hipGetDevice(&c->device);
+    void* sp = nullptr;
+    if (e == hipSuccess) e = noalloc_scratch(c->device, &sp);
+    if (e != hipSuccess) {
+      delete c;
+      return fail(nullptr, MSD_ERR_HIP,
+                  std::string("resolving the no-allocation scratch: ") + hipGetErrorString(e));
+    }
+    c->noalloc_base = static_cast<float*>(sp);
+  }
   c->gs.target_wgs = GEMM_WGS;
   c->gs.ev_start = nullptr;
   c->gs.ev_stop = nullptr;
@@ -1034,21 +1093,32 @@ int msd_draft_tree(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree_
   return MSD_OK;
 }
 
-int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d, int n_nodes,
-               int32_t* argmax_d, float* logits_d) {
-  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+}  // extern "C"
+
+namespace {
+
+// Argument checks of a verify call; *max_l receives the longest committed
+// length among the call's sequences.
+int check_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d, int T,
+                 const int32_t* argmax_d, int* max_l) {
   TRY(check_seqs(c, n_seq, seqs_h));
-  const int T = n_nodes;
   if (!trees_d || !argmax_d || T < 1 || T > c->lim.max_tree)
     return fail(c, MSD_ERR_INVALID_ARG, "bad tree");
-  const msd_model_desc& m = c->m;
-  const int d = m.d_model, V = m.vocab;
-  int max_l = 0;
+  *max_l = 0;
   for (int i = 0; i < n_seq; ++i) {
     const int b = seqs_h[i];
     if (c->L[b] + T > c->lim.max_seq) return fail(c, MSD_ERR_CAPACITY, "KV cache full");
-    max_l = std::max(max_l, c->L[b]);
+    *max_l = std::max(*max_l, c->L[b]);
   }
+  return MSD_OK;
+}
+
+// The verification itself (checked arguments): the target over every tree's
+// nodes, then the LM head with argmax (and the logits when asked).
+int verify_impl(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d, int T,
+                int max_l, int32_t* argmax_d, float* logits_d) {
+  const msd_model_desc& m = c->m;
+  const int d = m.d_model, V = m.vocab;
   TRY(upload_seqs(c, seqs_h, n_seq));
   for (int i = 0; i < n_seq; ++i) {
     c->att_pre[i] = c->L[seqs_h[i]];
@@ -1074,6 +1144,86 @@ int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* tre
   c->verified_T = T;
   c->verified_seqs.assign(seqs_h, seqs_h + n_seq);
   return MSD_OK;
+}
+
+// Floats of GEMM partials a verify of `rows` tree rows writes (the largest
+// of its launches: q/k/v, output, gate+up, down and LM head, for each chunk
+// size of CHUNK-row launches).
+size_t verify_part_floats(const msd_model_desc& m, int rows) {
+  const int d = m.d_model, F = m.ffn_dim, hh = m.n_heads * m.head_dim;
+  const int qkv = (m.n_heads + 2 * m.n_kv_heads) * m.head_dim;
+  size_t need = 0;
+  for (int mc : {std::min(CHUNK, rows), rows % CHUNK}) {
+    if (mc <= 0) continue;
+    for (size_t f : {gemm_part_floats(mc, qkv, d, 1, GEMM_WGS),
+                     gemm_part_floats(mc, d, hh, 1, GEMM_WGS),
+                     gemm_part_floats(mc, F, d, 2, GEMM_WGS),
+                     gemm_part_floats(mc, d, F, 1, GEMM_WGS),
+                     gemm_part_floats(mc, m.vocab, d, 1, GEMM_WGS)})
+      need = std::max(need, f);
+  }
+  return need;
+}
+
+}  // namespace
+
+extern "C" {
+
+int msd_verify(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d, int n_nodes,
+               int32_t* argmax_d, float* logits_d) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  int max_l = 0;
+  TRY(check_verify(c, n_seq, seqs_h, trees_d, n_nodes, argmax_d, &max_l));
+  return verify_impl(c, n_seq, seqs_h, trees_d, n_nodes, max_l, argmax_d, logits_d);
+}
+
+int msd_verify_noalloc(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,
+                       int n_nodes, int32_t* argmax_d, float* logits_d) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  int max_l = 0;
+  TRY(check_verify(c, n_seq, seqs_h, trees_d, n_nodes, argmax_d, &max_l));
+  const msd_model_desc& m = c->m;
+  const int rows = n_seq * n_nodes;
+  if (rows > BIG_MIN_ROWS)
+    return fail(c, MSD_ERR_INVALID_ARG,
+                "msd_verify_noalloc takes at most " + std::to_string(BIG_MIN_ROWS) +
+                    " tree rows per call (n_seq * n_nodes)");
+  // the same attention chunking as msd_verify, so both compute identically
+  const TreeChunks tc = plan_tree_chunks(m, n_seq, n_nodes, max_l + n_nodes,
+                                         c->plan.attn_floats);
+  const size_t part = verify_part_floats(m, rows);
+  const size_t att_o = tc.part_floats;
+  const size_t att_ml = att_o / m.head_dim * 2 + 64;
+  const size_t tk = topk_scratch_floats(std::min(CHUNK, rows), m.vocab);
+  auto up = [](size_t f) { return (f + 63) / 64 * 64; };  // 256-byte steps
+  const size_t need = up(part) + up(att_o) + up(att_ml) + up(tk);
+  if (need * sizeof(float) > MSD_NOALLOC_SCRATCH_BYTES)
+    return fail(c, MSD_ERR_INVALID_ARG,
+                "this verify needs " + std::to_string(need * sizeof(float)) +
+                    " bytes of scratch; msd_verify_noalloc holds " +
+                    std::to_string((size_t)MSD_NOALLOC_SCRATCH_BYTES));
+  // swap the workspace scratch for the static one for this call
+  struct Swap {
+    msd_ctx* c;
+    float *part, *att_po, *att_ml, *tk;
+    size_t part_floats, attn_floats;
+    ~Swap() {
+      c->part = part;
+      c->att_po = att_po;
+      c->att_ml = att_ml;
+      c->tk_scratch = tk;
+      c->plan.part_floats = part_floats;
+      c->plan.attn_floats = attn_floats;
+    }
+  } keep{c, c->part, c->att_po, c->att_ml, c->tk_scratch, c->plan.part_floats,
+         c->plan.attn_floats};
+  float* base = c->noalloc_base;
+  c->part = base;
+  c->plan.part_floats = part;
+  c->att_po = base + up(part);
+  c->att_ml = c->att_po + up(att_o);
+  c->tk_scratch = c->att_ml + up(att_ml);
+  return verify_impl(c, n_seq, seqs_h, trees_d, n_nodes, max_l, argmax_d, logits_d);
 }
 
 int msd_accept_compact(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tree* trees_d,

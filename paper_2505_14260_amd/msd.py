@@ -85,6 +85,7 @@ def lib():
                                   c_vp, P(c_i32)]
         L.msd_draft_tree.argtypes = [c_vp, ctypes.c_int, P(c_i32), P(TreeSpec), c_vp]
         L.msd_verify.argtypes = [c_vp, ctypes.c_int, P(c_i32), c_vp, ctypes.c_int, c_vp, c_vp]
+        L.msd_verify_noalloc.argtypes = L.msd_verify.argtypes
         L.msd_accept_compact.argtypes = [c_vp, ctypes.c_int, P(c_i32), c_vp, ctypes.c_int, c_vp,
                                          P(c_i32), P(c_i32), c_vp]
         L.msd_accept_sample.argtypes = [c_vp, ctypes.c_int, P(c_i32), c_vp, ctypes.c_int, c_vp,
@@ -164,6 +165,12 @@ def msd_draft_tree(ctx, seqs, spec: TreeSpec, trees_ptr):
 def msd_verify(ctx, seqs, trees_ptr, n_nodes, argmax_ptr, logits_ptr=None):
     s, ps = _i32(seqs)
     _check(ctx, lib().msd_verify(ctx, len(s), ps, trees_ptr, n_nodes, argmax_ptr, logits_ptr))
+
+
+def msd_verify_noalloc(ctx, seqs, trees_ptr, n_nodes, argmax_ptr, logits_ptr=None):
+    s, ps = _i32(seqs)
+    _check(ctx, lib().msd_verify_noalloc(ctx, len(s), ps, trees_ptr, n_nodes, argmax_ptr,
+                                         logits_ptr))
 
 
 def msd_accept_compact(ctx, seqs, trees_ptr, n_nodes, argmax_ptr, slot_map_ptr=None):
