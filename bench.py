@@ -8,10 +8,18 @@ verification over a KV cache whose prefix holds the 576-row visual prompt plus
 64 text tokens, greedy acceptance and KV compaction.  All inputs are seeded
 synthetic tensors resident in HBM before timing starts.
 
-Prints one JSON line: value = decoded tokens/s over the timed cycles, plus the
-verify-step latency, the roofline of the dominant kernel (the gate/up GEMM,
-timed with events on the library's stream) and the CPU oracle timed on the
+Prints one JSON line: value = decoded tokens/s over the timed cycles; the
+roofline of the verify step (its algorithmic weight + KV bytes over its
+latency, events on the library's stream), per-kernel rows of the verify
+(launches timed by events carried in their own dispatch packets), a verify
+sample at the end-of-generation cache length, and the CPU oracle timed on the
 host's cores on a bounded sample of the same workload.
+
+Measurement modes (no JSON bench line): --verify-only N runs N verify calls
+on a fixed tree from an imported cache state (clean dispatch sets for
+hardware-counter runs); --stream-ceiling times plain HBM streaming (a read
+reduction and a copy of large buffers); --copy-calibration copies a 1 GiB
+buffer 8 times (the reference for the traffic counters).
 """
 import argparse
 import hashlib
@@ -31,7 +39,6 @@ HBM_PEAK_GBS = 8000.0
 # average acceptance length of LLaVA-1.5-7B and the speedup ratios.
 PAPER_TAU = 4.63
 PAPER_SR = {"LLaVA-1.5-7B": 2.29, "LLaVA-1.5-13B": 2.46}
-SILU_KIND = 3
 
 
 def weight_bytes(dims):
@@ -47,24 +54,45 @@ def verify_bytes(dims, L, T, B=1):
     return weight_bytes(dims) + kv + B * T * dims.d_model * 2
 
 
-def silu_launch_bytes(dims, m):
-    """Algorithmic bytes of one gate/up launch: both weights, the input rows
-    and the bf16 output rows."""
-    d, F = dims.d_model, dims.ffn_dim
-    return 2 * F * d * 2 + m * d * 2 + m * F * 2
+KIND_NAMES = {0: "q/k/v projection", 1: "output projection", 2: "down projection",
+              3: "gate+up projection (SwiGLU pair)", 5: "LM head", 6: "tree attention + combine"}
+ATTN_KIND = 6
 
 
-def traffic_from_profile(kernel_src):
-    """HBM bytes per gate/up launch from the committed rocprofv3 counter
-    summary, or None when the kernel source changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "k_gemm_silu_llava7b_traffic.json")
+def launch_bytes(dims, kind, m, n, k):
+    """Algorithmic bytes of one traced launch: for a GEMM the bf16 weight (both
+    matrices for the gate+up pair), the input rows and the bf16 output rows;
+    for a tree-attention pass the K and V rows of every key slot it reads (n
+    slots: prefix + tree) plus the query and output rows."""
+    if kind == ATTN_KIND:
+        kv = n * 2 * dims.n_kv_heads * dims.head_dim * 2
+        return kv + 2 * m * dims.n_heads * dims.head_dim * 2
+    nw = 2 if kind == 3 else 1
+    return nw * n * k * 2 + m * k * 2 + m * n * 2
+
+
+def sources_sha256():
+    """One hash over the library's kernel and API sources."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2505_14260_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode())
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
+def traffic_from_profile(workload):
+    """HBM bytes per verify call from the committed rocprofv3 counter summary
+    of --verify-only runs, or None when the library's sources changed since
+    the counters were taken (or none were taken for this workload)."""
+    path = os.path.join(ROOT, "profiles", f"msd_verify_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    sha = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
-    if rec.get("k_gemm_sha256") != sha:
+    if rec.get("sources_sha256") != sources_sha256():
         return None
-    return rec.get("bytes_per_launch")
+    return rec.get("bytes_per_verify")
 
 
 def cpu_baseline(wl, w, dr, budget_s):
@@ -107,9 +135,114 @@ def cpu_baseline(wl, w, dr, budget_s):
             break
     threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
     return {"value": emitted / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "precision": "float64 (the oracle's arithmetic, stricter than the float32 of the "
+                         "baseline plan)",
             "sample": f"{cycles} MSD cycle(s) of the same workload (draft tree + tree verify "
                       f"at L={L} + accept) from a seeded synthetic cache state; "
                       f"{el:.1f} s, {el / cycles * 1e3:.0f} ms/cycle"}
+
+
+def stream_ceiling():
+    """Plain HBM streaming on this GPU, timed with events (8 repetitions each):
+    the library's streaming read (the weight stream's access pattern) over
+    4 GiB on 256 and 512 workgroups, torch's bf16 sum over 4 GiB and a 1 GiB
+    copy (read + write)."""
+    import torch
+    from paper_2505_14260_amd import msd as B
+    x = torch.zeros(2 << 30, dtype=torch.bfloat16, device="cuda")
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    sink = torch.zeros(1 << 16, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    nb = x.numel() * 2
+    out = {}
+    for name, fn, nbytes in (
+            ("stream_read_4GiB_256wg",
+             lambda: B.msd_stream_read(x.data_ptr(), nb, 256, sink.data_ptr(), st), nb),
+            ("stream_read_4GiB_512wg",
+             lambda: B.msd_stream_read(x.data_ptr(), nb, 512, sink.data_ptr(), st), nb),
+            ("torch_sum_4GiB", lambda: x.sum(), nb),
+            ("copy_1GiB", lambda: dst.copy_(src), 2 * src.numel())):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(8):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        t = float(np.median(ms))
+        out[name] = {"bytes": nbytes, "ms_median": round(t, 4),
+                     "GBs": round(nbytes / (t * 1e-3) / 1e9, 1)}
+    print(json.dumps({"stream_ceiling": out}), flush=True)
+
+
+def host_tree(B, wl, first_token=1):
+    """A well-formed tree of the workload's static shape (tokens 1..T) as
+    msd_tree bytes, for measurement runs that skip the draft."""
+    import synth
+    parent, rank, depth = synth.static_tree_arrays(wl.tree.paths)
+    T = len(parent)
+    t = B.Tree()
+    t.n_nodes = T
+    anc = [0] * T
+    for i in range(T):
+        anc[i] = (anc[parent[i]] if parent[i] >= 0 else 0) | (1 << i)
+        t.token[i], t.parent[i], t.depth[i], t.anc[i] = first_token + i, int(parent[i]), \
+            int(depth[i]), anc[i]
+    return bytes(t), T
+
+
+def verify_only(args, wl, w, dr):
+    """N verify calls on a fixed static tree from an imported cache state
+    (no prompt, no draft): the dispatches after set-up belong to the verifies."""
+    import torch
+    from paper_2505_14260_amd import msd as B
+    dims = wl.dims
+    if wl.tree.kind != "static":
+        raise SystemExit("--verify-only uses the workload's static tree shape")
+    L = wl.prompt_len
+    max_seq = (L + 64 + 255) // 256 * 256
+    eng = B.Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64, max_prompt=L)
+    h = torch.zeros(dims.d_model, dtype=torch.int16, device="cuda")
+    B.msd_set_state(eng.ctx, 0, L, h.data_ptr(), 1)
+    raw, T = host_tree(B, wl)
+    trees = eng.new_trees(1)
+    trees.copy_(torch.frombuffer(bytearray(raw), dtype=torch.uint8))
+    am = torch.empty(T, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    for _ in range(args.verify_only):
+        B.msd_verify(eng.ctx, [0], trees.data_ptr(), T, am.data_ptr())
+    torch.cuda.synchronize()
+    print(json.dumps({"verify_only": args.verify_only, "L": L, "tree_nodes": T,
+                      "algorithmic_bytes_per_verify": verify_bytes(dims, L, T)}), flush=True)
+    eng.close()
+
+
+def kernel_rows(dims, recs, T, n_cycles, verify_ms):
+    """Per-kernel rows of the verify step from traced launches with T rows."""
+    rows = []
+    for kind in (0, 1, 3, 2, ATTN_KIND, 5):
+        rr = [r for r in recs if r[0] == kind and r[1] == T]
+        if not rr:
+            continue
+        us = float(np.mean([r[4] for r in rr])) * 1e3
+        nb = float(np.mean([launch_bytes(dims, kind, r[1], r[2], r[3]) for r in rr]))
+        per_verify = len(rr) / n_cycles
+        rows.append({"kernel": KIND_NAMES[kind], "launches_per_verify": round(per_verify, 2),
+                     "avg_us": round(us, 2), "bytes_per_launch": int(nb),
+                     "GBs": round(nb / (us * 1e-6) / 1e9, 1),
+                     "frac_of_hbm_peak": round(nb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "share_of_verify": round(per_verify * us * 1e-3 / verify_ms, 4)})
+    rest = 1.0 - sum(r["share_of_verify"] for r in rows)
+    rows.append({"kernel": "everything else (RoPE/KV write, residual+norm, SwiGLU, embedding, "
+                           "top-k, row set-up)",
+                 "us_per_verify": round(rest * verify_ms * 1e3, 1),
+                 "share_of_verify": round(rest, 4)})
+    return rows
 
 
 def main():
@@ -122,7 +255,17 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 1 GiB buffer 8 times (HBM counter calibration)")
+    ap.add_argument("--stream-ceiling", action="store_true",
+                    help="only time plain HBM streaming (read reduction, copy)")
+    ap.add_argument("--verify-only", type=int, default=0, metavar="N",
+                    help="only run N verify calls on a fixed tree (counter runs)")
+    ap.add_argument("--late-L", type=int, default=1152,
+                    help="cache length of the end-of-generation verify sample")
     args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the decode path here runs on a single GPU "
+              "and has no multi-GPU mode.", file=sys.stderr)
+        sys.exit(2)
     if args.copy_calibration:
         import torch
         n = 1 << 30
@@ -134,10 +277,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_per_launch": n, "launches": 8}))
         return
-    if args.gpus != 1:
-        print("bench.py measures one GPU: the decode path here runs on a single GPU "
-              "and has no multi-GPU mode.", file=sys.stderr)
-        sys.exit(2)
+    if args.stream_ceiling:
+        stream_ceiling()
+        return
     if int(os.environ.get("RANK", "0")) != 0:
         return
 
@@ -154,8 +296,12 @@ def main():
     prompt = synth.make_prompt(wl)
     print(f"[bench] weights generated in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr,
           flush=True)
+    if args.verify_only:
+        verify_only(args, wl, w, dr)
+        return
     T = wl.tree.n_draft + 1
     max_seq = wl.prompt_len + (args.steps + args.warmup + 18) * (wl.tree.depth + 1) + 2 * T + 32
+    max_seq = max(max_seq, args.late_L + 64 + T)
     max_seq = (max_seq + 255) // 256 * 256
     eng = B.Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64,
                    max_prompt=wl.prompt_len)
@@ -202,15 +348,22 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     L_end = B.msd_seq_len(eng.ctx, 0)
-    # the dominant kernel's launches, timed by events carried in their own
+    draft_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    verify_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    accept_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    v_med = float(np.median(verify_ms))
+    # the verify step's launches, timed by events carried in their own
     # dispatch packets, over further cycles outside the timed region
     n_tr = max(4, min(16, args.steps))
-    B.msd_trace_enable(eng.ctx, 64 * n_tr, 1 << SILU_KIND)
+    kinds = sum(1 << k for k in (0, 1, 2, 3, 5, ATTN_KIND))
+    B.msd_trace_enable(eng.ctx, 400 * n_tr, kinds)
     for _ in range(n_tr):
         cycle()
     torch.cuda.synchronize()
-    recs = B.msd_trace_read(eng.ctx, 64 * n_tr)
+    recs = B.msd_trace_read(eng.ctx, 400 * n_tr)
     B.msd_trace_enable(eng.ctx, 0)
+    krows = kernel_rows(dims, recs, T, n_tr, v_med)
+    dominant = max(krows[:-1], key=lambda r: r["share_of_verify"])
     # plain autoregressive decode steps, for the speedup context: verify and
     # accept of a root-only tree are one target forward over the next token,
     # its argmax and the host read of the emitted token
@@ -232,22 +385,29 @@ def main():
         ar_ms.append(e0.elapsed_time(e1))
         last[0] = int(em1[0][-1])
     ar_step = float(np.median(ar_ms))
-    draft_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    verify_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
-    accept_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    # the end-of-generation cache length: the committed length is imported
+    # (its slots hold whatever the cache holds; the timing does not depend on
+    # the values) and the last drafted tree is verified there
+    h0 = torch.zeros(dims.d_model, dtype=torch.int16, device="cuda")
+    B.msd_set_state(eng.ctx, 0, args.late_L, h0.data_ptr(), last[0])
+    late = []
+    am = torch.empty(T, dtype=torch.int32, device="cuda")
+    for i in range(20):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        B.msd_verify(eng.ctx, [0], trees.data_ptr(), T, am.data_ptr())
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if i >= 4:
+            late.append(e0.elapsed_time(e1))
+    late_ms = float(np.median(late))
+    late_b = verify_bytes(dims, args.late_L, T)
     tokens = int(np.sum(emitted))
     value = tokens / wall
     L_mid = (L_start + L_end) // 2
     vb = verify_bytes(dims, L_mid, T)
-    v_med = float(np.median(verify_ms))
-    # the verify step's gate/up launches (M = tree nodes > 16 rows: the MT=2
-    # instantiation of the kernel); the draft's launches use M <= 16 rows
-    silu = [r for r in recs if r[0] == SILU_KIND and r[1] > 16]
-    silu_ms = float(np.mean([r[4] for r in silu]))
-    silu_bytes = float(np.mean([silu_launch_bytes(dims, r[1]) for r in silu]))
-    achieved = silu_bytes / (silu_ms * 1e-3) / 1e9
-    traffic = traffic_from_profile(os.path.join(ROOT, "paper_2505_14260_amd", "csrc",
-                                                "k_gemm.hip"))
+    achieved = vb / (v_med * 1e-3) / 1e9
+    traffic = traffic_from_profile(wl.name)
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -272,16 +432,19 @@ def main():
             "batch": 1, "draft_fc_init": wl.draft_fc_mode,
         },
         "roofline": {
-            "kernel": "k_gemm<2, 2, 8, 4> (verify-step gate+up projection, M=27)",
+            "kernel": "msd_verify: the whole verification step (embedding, 32 layers of q/k/v, "
+                      "RoPE + KV write, tree attention, output, gate+up, down, final norm, "
+                      "LM head + argmax)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "launches": len(silu),
-            "avg_launch_ms": round(silu_ms, 5),
-            "algorithmic_bytes_per_launch": int(silu_bytes),
+            "launches": args.steps,
+            "avg_launch_ms": round(v_med, 5),
+            "algorithmic_bytes_per_launch": int(vb),
+            "dominant_kernel": dominant["kernel"],
         },
         "verify": {
             "ms_median": round(v_med, 4),
@@ -289,8 +452,13 @@ def main():
             "ms_p90": round(float(np.percentile(verify_ms, 90)), 4),
             "L_start": L_start, "L_end": L_end, "tree_nodes": T,
             "algorithmic_bytes": int(vb),
-            "achieved_GBs": round(vb / (v_med * 1e-3) / 1e9, 1),
-            "frac_of_hbm_peak": round(vb / (v_med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "achieved_GBs": round(achieved, 1),
+            "frac_of_hbm_peak": round(achieved / HBM_PEAK_GBS, 4),
+            "kernels": krows,
+            "late": {"L": args.late_L, "ms_median": round(late_ms, 4),
+                     "algorithmic_bytes": int(late_b),
+                     "frac_of_hbm_peak": round(late_b / (late_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                               4)},
         },
         "draft_ms_median": round(float(np.median(draft_ms)), 4),
         "accept_ms_median": round(float(np.median(accept_ms)), 4),

@@ -290,17 +290,30 @@ int msd_seq_len(const msd_ctx* ctx, int seq);
 int msd_set_state(msd_ctx* ctx, int seq, int L, const void* h_d, int32_t next_token);
 
 /*
- * Optional timing trace of the weight-streaming GEMM launches (for
- * measurement tools).  msd_trace_enable(ctx, capacity, kinds) starts
- * timing the next `capacity` GEMM launches whose kind has its bit set in
- * `kinds` with events carried by the launch itself (capacity <= 0 stops and
- * clears); msd_trace_read waits for the stream and returns up to max_recs
- * records (return value: count, or < 0 on error).
+ * Optional timing trace of the weight-streaming GEMM launches and the
+ * tree-attention passes (for measurement tools).  msd_trace_enable(ctx,
+ * capacity, kinds) starts timing the next `capacity` launches whose kind has
+ * its bit set in `kinds`, with events carried by the launches themselves
+ * (capacity <= 0 stops and clears); msd_trace_read waits for the stream and
+ * returns up to max_recs records (return value: count, or < 0 on error).
  * kind: 0 = q/k/v projection, 1 = output projection, 2 = down projection,
- * 3 = gate+up (SwiGLU) pair, 4 = draft f_down, 5 = LM head.
- * m is the number of input rows; the weight of a record is n x k bf16
- * (twice that for kind 3).
+ * 3 = gate+up (SwiGLU) pair, 4 = draft f_down, 5 = LM head (for these m is
+ * the number of input rows and the weight is n x k bf16, twice that for
+ * kind 3); 6 = a tree-attention pass with its chunk combine (m = query rows,
+ * n = key slots of the longest sequence including the tree, k = key chunks).
  */
+/*
+ * Diagnostic for measurement tools: one kernel that reads `bytes` of the
+ * device buffer buf_d (16-byte aligned, zero-filled, bytes a multiple of
+ * 64 KiB) with the access pattern of the library's weight stream (every wave
+ * load 1 KB contiguous, nontemporal), spread over `workgroups` workgroups; it
+ * computes nothing the decode uses.  sink_d: `workgroups` 32-bit words the
+ * kernel may write.  Enqueued on `stream` (a hipStream_t); no context needed.
+ * This is the achievable streaming rate the GEMMs are compared against.
+ */
+int msd_stream_read(const void* buf_d, size_t bytes, int workgroups, void* sink_d,
+                    void* stream);
+
 typedef struct msd_trace_rec {
   int32_t kind, m, n, k;
   float ms;

@@ -21,6 +21,8 @@
 // Q (split rows from the RoPE kernel) and P enter the MFMAs as bf16 hi + lo
 // pairs, so only the bf16 cache rows limit the precision; the output rows
 // are split rows (the O projection's input).
+#include <hip/hip_ext.h>
+
 #include "msd_internal.h"
 
 namespace msd {
@@ -566,19 +568,28 @@ size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd) 
   return (size_t)n_seq * KV * qtiles * n_chunks * 32 * hd;
 }
 
-void launch_tree_attention(AttnArgs a, hipStream_t st) {
+template <int HD>
+void launch_tree_hd(const AttnArgs& a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   const int items = a.n_seq * a.KV * a.qtiles;
   const int units = a.n_seq * a.KV * a.n_chunks;
-  dim3 grid(8 * a.qtiles * ((units + 7) / 8));
-  if (a.hd == 128) {
-    hipLaunchKernelGGL(k_tree_attn<128>, grid, dim3(64 * TREE_WAVES), 0, st, a);
-    if (a.n_chunks > 1)
-      hipLaunchKernelGGL(k_tree_combine<128>, dim3(items * 4), dim3(256), 0, st, a);
+  const dim3 grid(8 * a.qtiles * ((units + 7) / 8));
+  const bool comb = a.n_chunks > 1;
+  if (ev0) {
+    // events carried by the launches themselves bracket the kernels only
+    hipExtLaunchKernelGGL(k_tree_attn<HD>, grid, dim3(64 * TREE_WAVES), 0, st, ev0,
+                          comb ? nullptr : ev1, 0, a);
+    if (comb)
+      hipExtLaunchKernelGGL(k_tree_combine<HD>, dim3(items * (HD / 32)), dim3(256), 0, st,
+                            nullptr, ev1, 0, a);
   } else {
-    hipLaunchKernelGGL(k_tree_attn<64>, grid, dim3(64 * TREE_WAVES), 0, st, a);
-    if (a.n_chunks > 1)
-      hipLaunchKernelGGL(k_tree_combine<64>, dim3(items * 2), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_tree_attn<HD>, grid, dim3(64 * TREE_WAVES), 0, st, a);
+    if (comb) hipLaunchKernelGGL(k_tree_combine<HD>, dim3(items * (HD / 32)), dim3(256), 0, st, a);
   }
+}
+
+void launch_tree_attention(AttnArgs a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  if (a.hd == 128) launch_tree_hd<128>(a, st, ev0, ev1);
+  else launch_tree_hd<64>(a, st, ev0, ev1);
 }
 
 void launch_causal_attention(AttnArgs a, hipStream_t st) {

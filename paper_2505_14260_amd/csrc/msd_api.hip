@@ -387,6 +387,20 @@ int upload_seqs(msd_ctx* c, const int32_t* seqs, int n) {
 
 // GEMM launch kinds (for the optional trace)
 enum { GK_QKV = 0, GK_O = 1, GK_DOWN = 2, GK_GATEUP = 3, GK_FC = 4, GK_LMHEAD = 5 };
+constexpr int TK_ATTN = 6;  // trace kind of a tree-attention pass (+ its combine)
+
+// A traced launch of `kind` takes the next pair of the context's events
+// (both null when not traced).
+void trace_events(msd_ctx* c, int kind, int M, int N, int K, hipEvent_t* e0, hipEvent_t* e1) {
+  *e0 = *e1 = nullptr;
+  if (!c->tracing || !((c->trace_kinds >> kind) & 1) || c->trace.size() >= c->trace_cap) return;
+  msd_ctx::TraceRec r{kind, M, N, K, c->ev_pool[2 * c->trace.size()],
+                      c->ev_pool[2 * c->trace.size() + 1]};
+  *e0 = r.a;
+  *e1 = r.b;
+  c->trace.push_back(r);
+}
+
 // Partial products of rows [0, M) (M <= 64) of the split rows X (row stride
 // ldx = 2K) against the packed weight W [N][K] (and W2); returns the view the
 // consumer sums.
@@ -402,15 +416,8 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
     *out = Parts{c->part, S, (size_t)M * nt * 64 * nw, nt * 64 * nw, nt * 64};
     return MSD_OK;
   }
-  const bool tr = c->tracing && ((c->trace_kinds >> kind) & 1) && c->trace.size() < c->trace_cap;
   GemmScratch gs = c->gs;
-  if (tr) {
-    msd_ctx::TraceRec r{kind, M, N, K, c->ev_pool[2 * c->trace.size()],
-                        c->ev_pool[2 * c->trace.size() + 1]};
-    gs.ev_start = r.a;
-    gs.ev_stop = r.b;
-    c->trace.push_back(r);
-  }
+  trace_events(c, kind, M, N, K, &gs.ev_start, &gs.ev_stop);
   launch_gemm(X, ldx, M, W, W2, N, K, c->part, c->sink, c->gemm_zero, gs, c->st);
   LAUNCHED(c);
   const GemmPlan pl = plan_gemm(M, N, K, W2 ? 2 : 1, c->gs.target_wgs);
@@ -525,7 +532,9 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
       a.qtiles = tc.qtiles;
       a.chunk_keys = tc.chunk_keys;
       a.n_chunks = tc.n_chunks;
-      launch_tree_attention(a, c->st);
+      hipEvent_t e0, e1;
+      trace_events(c, TK_ATTN, rows, max_ltot, tc.n_chunks, &e0, &e1);
+      launch_tree_attention(a, c->st, e0, e1);
     }
     LAUNCHED(c);
     for (int m0 = 0; m0 < rows; m0 += ch) {
@@ -1256,6 +1265,19 @@ int msd_accept_sample(msd_ctx* c, int n_seq, const int32_t* seqs_h, const msd_tr
                        c->st);
   LAUNCHED(c);
   return finish_accept(c, n_seq, seqs_h, n_nodes, emitted_h, n_emitted_h);
+}
+
+int msd_stream_read(const void* buf_d, size_t bytes, int workgroups, void* sink_d,
+                    void* stream) {
+  const size_t span = stream_span_bytes();
+  if (!buf_d || !sink_d || workgroups <= 0 || workgroups > 65536 || bytes < span ||
+      bytes % span || ((uintptr_t)buf_d & 15))
+    return fail(nullptr, MSD_ERR_INVALID_ARG, "msd_stream_read: bad arguments");
+  launch_stream_read(static_cast<const uint16_t*>(buf_d), bytes / span, workgroups,
+                     static_cast<unsigned*>(sink_d), (hipStream_t)stream);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(nullptr, MSD_ERR_HIP, hipGetErrorString(e));
+  return MSD_OK;
 }
 
 int msd_trace_enable(msd_ctx* c, int capacity, int kinds) {

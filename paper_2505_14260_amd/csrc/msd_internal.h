@@ -89,6 +89,12 @@ int launch_gemm_big(const uint16_t* X, int ldx, int M, const uint16_t* W, const 
                     int N, int K, float* part, size_t part_cap, const uint16_t* dummy,
                     hipStream_t st);
 size_t gemm_dummy_elems();
+// Diagnostic: reads spans * stream_span_bytes() bytes of buf with the weight
+// stream's access pattern on wgs workgroups (sink: wgs words, never written
+// for zero-filled buffers).
+size_t stream_span_bytes();
+void launch_stream_read(const uint16_t* buf, size_t spans, int wgs, unsigned* sink,
+                        hipStream_t st);
 void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2, int N,
                  int K, float* part, float* sink, const uint16_t* dummy, const GemmScratch& sc,
                  hipStream_t st);
@@ -137,7 +143,10 @@ struct AttnArgs {
   float scale;
 };
 
-void launch_tree_attention(AttnArgs a, hipStream_t st);
+// ev0/ev1 (optional): events recorded by the launches themselves, before
+// the attention kernel and after the last kernel of the pass.
+void launch_tree_attention(AttnArgs a, hipStream_t st, hipEvent_t ev0 = nullptr,
+                           hipEvent_t ev1 = nullptr);
 void launch_causal_attention(AttnArgs a, hipStream_t st);
 size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd);
 

@@ -93,6 +93,7 @@ def lib():
                                         c_vp]
         L.msd_seq_len.argtypes = [c_vp, ctypes.c_int]
         L.msd_set_state.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, c_vp, c_i32]
+        L.msd_stream_read.argtypes = [c_vp, c_sz, ctypes.c_int, c_vp, c_vp]
         L.msd_trace_enable.argtypes = [c_vp, ctypes.c_int, ctypes.c_int]
         L.msd_trace_read.argtypes = [c_vp, ctypes.c_int, P(TraceRec)]
         _lib = L
@@ -202,6 +203,10 @@ def msd_seq_len(ctx, seq):
 
 def msd_set_state(ctx, seq, L, h_ptr, next_token):
     _check(ctx, lib().msd_set_state(ctx, seq, L, h_ptr, next_token))
+
+
+def msd_stream_read(buf_ptr, nbytes, workgroups, sink_ptr, stream):
+    _check(None, lib().msd_stream_read(buf_ptr, nbytes, workgroups, sink_ptr, stream))
 
 
 def msd_trace_enable(ctx, capacity, kinds=0xF):
