@@ -301,29 +301,112 @@ struct QShared {
   }
 };
 
-template <int HD>
-__global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
-  constexpr int NWV = TREE_WAVES;
+// Merges the key chunks of one item (sequence, kv head, query tile): run by
+// the workgroup that finishes the item's last chunk.  A chunk's partial is
+// stored by units of (query column j, 8 consecutive head dims d0..d0+7) at
+// ((d0 / 8) * 32 + j) * 8; a thread owns such units: it loads every chunk's
+// slices first, then the (max, sum) pairs, so the merge waits for memory
+// once, and writes each unit as one 16-byte hi and one 16-byte lo store.
+// Chunks merge in chunk order, so the result does not depend on which
+// workgroup merges.
+template <int HD, int NWV>
+MSD_DEV void combine_chunks(const AttnArgs& a, size_t item0, int nc, int qt, int g, int sidx,
+                            float (*wgt)[32], float* inv_den) {
+  constexpr int E = 32 * HD;
+  constexpr int NT = 64 * NWV;
+  constexpr int UN = 32 * HD / 8;           // (column, 8 dims) units
+  constexpr int IT = (UN + NT - 1) / NT;    // units per thread
+  const int G = a.H / a.KV;
+  float4 v[IT][ATT_MAX_CHUNKS][2];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int u = min((int)threadIdx.x + NT * it, UN - 1);
+#pragma unroll
+    for (int q = 0; q < ATT_MAX_CHUNKS; ++q) {
+      const float* src = a.part_o + (item0 + min(q, nc - 1)) * E + 8 * u;
+      v[it][q][0] = *reinterpret_cast<const float4*>(src);
+      v[it][q][1] = *reinterpret_cast<const float4*>(src + 4);
+    }
+  }
+  if (threadIdx.x < 32) {
+    const int j = threadIdx.x;
+    float2 ml[ATT_MAX_CHUNKS];
+#pragma unroll
+    for (int q = 0; q < ATT_MAX_CHUNKS; ++q)
+      ml[q] = *reinterpret_cast<const float2*>(a.part_ml + (item0 + min(q, nc - 1)) * 64 + 2 * j);
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < ATT_MAX_CHUNKS; ++q)
+      if (q < nc) M = fmaxf(M, ml[q].x);
+    float den = 0.f;
+#pragma unroll
+    for (int q = 0; q < ATT_MAX_CHUNKS; ++q) {
+      const float wc = (q >= nc || M == -INFINITY || ml[q].x == -INFINITY) ? 0.f
+                                                                            : __expf(ml[q].x - M);
+      wgt[q][j] = wc;
+      den += wc * ml[q].y;
+    }
+    inv_den[j] = den > 0.f ? 1.f / den : 0.f;
+  }
+  lds_barrier();
+  const int HH = a.H * HD;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int u = threadIdx.x + NT * it;
+    if (u >= UN) break;
+    const int j = u & 31, d0 = 8 * (u >> 5);
+    int nd, hd_;
+    column_to_row(qt, j, G, g, nd, hd_);
+    if (nd >= a.nq) continue;
+    float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < ATT_MAX_CHUNKS; ++q) {
+      const float wq = wgt[q][j];
+      o[0] += wq * v[it][q][0].x;
+      o[1] += wq * v[it][q][0].y;
+      o[2] += wq * v[it][q][0].z;
+      o[3] += wq * v[it][q][0].w;
+      o[4] += wq * v[it][q][1].x;
+      o[5] += wq * v[it][q][1].y;
+      o[6] += wq * v[it][q][1].z;
+      o[7] += wq * v[it][q][1].w;
+    }
+    const float inv = inv_den[j];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] *= inv;
+    store_split8(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH + (size_t)hd_ * HD + d0, HH, o);
+  }
+}
+
+// Two waves per SIMD (two 4-wave workgroups per CU): the registers stay
+// within 256 per lane.
+template <int HD, int NWV>
+__global__ __launch_bounds__(64 * NWV, 2) void k_tree_attn(AttnArgs a) {
   constexpr int E = 32 * HD;                 // state elements of one wave
   constexpr int QU = QShared<HD>::QU;
-  __shared__ uint4 sq[32 * QU];
+  constexpr int NT = 64 * NWV;
+  // the query tile lives in the merge buffer's space until the key loop ends
   __shared__ float so[NWV * E];
+  static_assert(32 * QU * 4 <= NWV * E, "query tile must fit the merge buffer");
+  uint4* const sq = reinterpret_cast<uint4*>(so);
   __shared__ float sml[NWV][32][2];
-  __shared__ float wgt[NWV][32];
+  __shared__ float wgt[ATT_MAX_CHUNKS > NWV ? ATT_MAX_CHUNKS : NWV][32];
   __shared__ float colm[32][2];
+  __shared__ int last;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  // Workgroup -> unit u = (sequence, kv head, key chunk) and query tile qt.
-  // The query tiles of one unit read the same K/V blocks, so they get
-  // blockIdx values 8 apart (workgroup i runs on XCD i mod 8) in
-  // consecutive dispatch slots: the first tile's loads bring the blocks
-  // into that XCD's L2 for the others.  Grid: 8 * qtiles * ceil(units / 8).
+  // Workgroup -> (sequence, kv head) pair, key chunk c and query tile qt.
+  // Every workgroup of one pair runs on one XCD (workgroup i runs on XCD
+  // i mod 8): the chunks of an item meet in that XCD's L2 for the merge,
+  // and the query tiles of one chunk (consecutive slots) read the same K/V
+  // blocks, fetched from HBM once.  Grid: 8 * ceil(pairs / 8) * chunks * qtiles.
+  const int per_pair = a.qtiles * a.n_chunks;
   const int slot = blockIdx.x >> 3;
-  const int qt = slot % a.qtiles;
-  const int u = (slot / a.qtiles) * 8 + (blockIdx.x & 7);
-  if (u >= a.n_seq * a.KV * a.n_chunks) return;
-  const int c = u % a.n_chunks;
-  const int g = (u / a.n_chunks) % a.KV;
-  const int sidx = u / a.n_chunks / a.KV;
+  const int pp = slot / per_pair, rem = slot - pp * per_pair;
+  const int pair = pp * 8 + (blockIdx.x & 7);
+  if (pair >= a.n_seq * a.KV) return;
+  const int c = rem / a.qtiles, qt = rem - c * a.qtiles;
+  const int g = pair % a.KV;
+  const int sidx = pair / a.KV;
   const int b = a.seq[sidx];
   const int P = a.prefix[sidx];
   const int Ltot = a.keys[sidx];
@@ -334,18 +417,17 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
   const int wk = a.chunk_keys / NWV;
   const int k0 = c * a.chunk_keys + w * wk;
   const int k1 = min(k0 + wk, Ltot);
-  uint4 kf[HD / 16], vf[HD / 32][2];
-  attend_prefetch<HD>(kf, vf, kbase, vbase, a.S, k0);
   // the tile's 32 query columns (hi and lo halves) into LDS; padding
-  // columns copy node 0 (their results are dropped).  Every thread's loads
-  // are issued before its first LDS store.
-  constexpr int QN = 32 * QU / (64 * NWV);  // 16-byte units per thread
-  static_assert(QN * 64 * NWV == 32 * QU, "query units must divide over the threads");
+  // columns copy node 0 (their results are dropped).  The query loads go out
+  // first, then the first key block's, so that the query staging waits for
+  // the query loads only.
+  constexpr int QN = 32 * QU / NT;  // 16-byte units per thread
+  static_assert(QN * NT == 32 * QU, "query units must divide over the threads");
   uint4 qv[QN];
   int qi[QN];
 #pragma unroll
   for (int r = 0; r < QN; ++r) {
-    const int u = threadIdx.x + r * 64 * NWV;
+    const int u = threadIdx.x + r * NT;
     const int j = u / QU, v = u - j * QU;
     int node, head;
     column_to_row(qt, j, G, g, node, head);
@@ -355,6 +437,8 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
     qv[r] = *reinterpret_cast<const uint4*>(
         a.q + (size_t)(sidx * a.nq + node) * 2 * HH + (size_t)half * HH + (size_t)head * HD + 8 * k8);
   }
+  uint4 kf[HD / 16], vf[HD / 32][2];
+  attend_prefetch<HD>(kf, vf, kbase, vbase, a.S, k0);
 #pragma unroll
   for (int r = 0; r < QN; ++r) sq[qi[r]] = qv[r];
   int node, head;
@@ -363,11 +447,12 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
   const uint64_t msk = a.mask[sidx * a.nq + node];
   AttnState<HD> st;
   init_state<HD>(st);
-  __syncthreads();
+  lds_barrier();
   const QShared<HD> qf{sq + (lane & 31) * QU, lane & 15, lane >> 5};
   attend_range<HD>(st, qf, kf, vf, kbase, vbase, a.S, k0, k1, Ltot, a.scale, [&](int key) {
     return (key < P) | (((msk >> ((key - P) & 63)) & 1ull) != 0);
   });
+  lds_barrier();  // every wave is done with the query tile
   // merge the waves' states
 #pragma unroll
   for (int dt = 0; dt < HD / 32; ++dt)
@@ -377,7 +462,7 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
     sml[w][lane][0] = st.m;
     sml[w][lane][1] = st.l;
   }
-  __syncthreads();
+  lds_barrier();
   // per-column merge weights: wgt[q][j] = exp(m_q - M_j)
   if (threadIdx.x < 32) {
     const int j = threadIdx.x;
@@ -395,11 +480,11 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
     colm[j][0] = M;
     colm[j][1] = l;
   }
-  __syncthreads();
+  lds_barrier();
   if (a.n_chunks == 1) {
     // thread -> (query column j, 8 consecutive dims): one 16-byte store each
     // for the hi and lo halves of the output row
-    for (int u = threadIdx.x; u < 32 * (HD / 8); u += 64 * NWV) {
+    for (int u = threadIdx.x; u < 32 * (HD / 8); u += NT) {
       const int j = u & 31, d0 = 8 * (u >> 5);
       int nd, hd_;
       column_to_row(qt, j, G, g, nd, hd_);
@@ -419,112 +504,46 @@ __global__ __launch_bounds__(64 * TREE_WAVES) void k_tree_attn(AttnArgs a) {
     }
     return;
   }
-  const size_t item = (((size_t)sidx * a.KV + g) * a.qtiles + qt) * a.n_chunks + c;
-  for (int e = 4 * threadIdx.x; e < E; e += 4 * 64 * NWV) {
-    const int j = e & 31;  // columns j .. j+3 (consecutive lanes of one register)
-    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  const size_t item = ((size_t)sidx * a.KV + g) * a.qtiles + qt;
+  const size_t item0 = item * a.n_chunks;
+  // the chunk's partial by units (column j, dims d0..d0+7) at 8 u with
+  // u = (d0 / 8) * 32 + j: consecutive threads take consecutive columns
+  // (distinct LDS banks) and write consecutive 32-byte units
+  for (int u = threadIdx.x; u < 32 * (HD / 8); u += NT) {
+    const int j = u & 31, d0 = 8 * (u >> 5);
+    float o[8];
 #pragma unroll
-    for (int q = 0; q < NWV; ++q) {
-      const float4 x = *reinterpret_cast<const float4*>(so + q * E + e);
-      o.x += wgt[q][j] * x.x;
-      o.y += wgt[q][j + 1] * x.y;
-      o.z += wgt[q][j + 2] * x.z;
-      o.w += wgt[q][j + 3] * x.w;
+    for (int i = 0; i < 8; ++i) {
+      const int e = state_index<HD>(j, d0 + i);
+      float x = 0.f;
+#pragma unroll
+      for (int q = 0; q < NWV; ++q) x += wgt[q][j] * so[q * E + e];
+      o[i] = x;
     }
-    *reinterpret_cast<float4*>(a.part_o + item * E + e) = o;
+    float* dst = a.part_o + (item0 + c) * E + 8 * u;
+    *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<float4*>(dst + 4) = make_float4(o[4], o[5], o[6], o[7]);
   }
   if (threadIdx.x < 32) {
-    a.part_ml[item * 64 + 2 * threadIdx.x] = colm[threadIdx.x][0];
-    a.part_ml[item * 64 + 2 * threadIdx.x + 1] = colm[threadIdx.x][1];
+    a.part_ml[(item0 + c) * 64 + 2 * threadIdx.x] = colm[threadIdx.x][0];
+    a.part_ml[(item0 + c) * 64 + 2 * threadIdx.x + 1] = colm[threadIdx.x][1];
   }
-}
-
-// Merges the chunks of one (sequence, kv head, query tile) in chunk order;
-// block (tile, dim tile dt) reads the dt slice of every chunk's state
-// (contiguous), one float4 per thread, and writes those output dims.
-// Chunks go in groups of CG with every load of a group in flight (indices
-// past the last chunk reload it and are not used).  The first group of
-// state loads is issued before the merge weights are known, and the weights
-// come from one read of the chunks' (max, sum) pairs, so a merge with at
-// most CG chunks waits for memory once.
-template <int HD>
-__global__ __launch_bounds__(256) void k_tree_combine(AttnArgs a) {
-  constexpr int E = 32 * HD;
-  constexpr int SL = E / (HD / 32);          // elements of one dim tile
-  static_assert(SL == 4 * 256, "one float4 of the dim tile per thread");
-  constexpr int CG = 8;
-  __shared__ float wgt[ATT_MAX_CHUNKS][32];  // chunk weights per column
-  __shared__ float inv_den[32];
-  const int dt = blockIdx.x % (HD / 32);
-  int t = blockIdx.x / (HD / 32);
-  const size_t item0 = (size_t)t * a.n_chunks;
-  const int qt = t % a.qtiles; t /= a.qtiles;
-  const int g = t % a.KV;
-  const int sidx = t / a.KV;
-  const int G = a.H / a.KV;
-  const int nc = a.n_chunks;
-  const int e = dt * SL + 4 * threadIdx.x;  // element index in the state
-  const int j0 = e & 31;                    // columns of e .. e+3 (consecutive lanes)
-  float4 v[CG];
-#pragma unroll
-  for (int q = 0; q < CG; ++q)
-    v[q] = *reinterpret_cast<const float4*>(a.part_o + (item0 + min(q, nc - 1)) * E + e);
-  if (threadIdx.x < 32) {
-    const int j = threadIdx.x;
-    float2 ml[CG];
-#pragma unroll
-    for (int q = 0; q < CG; ++q)
-      ml[q] = *reinterpret_cast<const float2*>(a.part_ml + (item0 + min(q, nc - 1)) * 64 + 2 * j);
-    float M = -INFINITY;
-#pragma unroll
-    for (int q = 0; q < CG; ++q)
-      if (q < nc) M = fmaxf(M, ml[q].x);
-    for (int c = CG; c < nc; ++c) M = fmaxf(M, a.part_ml[(item0 + c) * 64 + 2 * j]);
-    float den = 0.f;
-#pragma unroll
-    for (int q = 0; q < CG; ++q) {
-      if (q >= nc) continue;
-      const float wc = (M == -INFINITY || ml[q].x == -INFINITY) ? 0.f : __expf(ml[q].x - M);
-      wgt[q][j] = wc;
-      den += wc * ml[q].y;
-    }
-    for (int c = CG; c < nc; ++c) {
-      const float2 mc = *reinterpret_cast<const float2*>(a.part_ml + (item0 + c) * 64 + 2 * j);
-      const float wc = (M == -INFINITY || mc.x == -INFINITY) ? 0.f : __expf(mc.x - M);
-      wgt[c][j] = wc;
-      den += wc * mc.y;
-    }
-    inv_den[j] = den > 0.f ? 1.f / den : 0.f;
+  // The workgroup that finishes the item's last chunk merges them.  Every
+  // chunk of the item runs on this XCD, so its partial is in this XCD's L2
+  // once the stores are acknowledged: each thread waits for its own, the
+  // barrier for all, and the arrival count is taken after that.
+  __builtin_amdgcn_s_waitcnt(0);
+  lds_barrier();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(a.att_cnt + item, 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    last = prev == a.n_chunks - 1;
   }
-  __syncthreads();
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int c0 = 0;;) {
-#pragma unroll
-    for (int q = 0; q < CG; ++q) {
-      if (c0 + q >= nc) continue;
-      const int c = c0 + q;
-      acc.x += wgt[c][j0] * v[q].x;
-      acc.y += wgt[c][j0 + 1] * v[q].y;
-      acc.z += wgt[c][j0 + 2] * v[q].z;
-      acc.w += wgt[c][j0 + 3] * v[q].w;
-    }
-    c0 += CG;
-    if (c0 >= nc) break;
-#pragma unroll
-    for (int q = 0; q < CG; ++q)
-      v[q] = *reinterpret_cast<const float4*>(a.part_o + (item0 + min(c0 + q, nc - 1)) * E + e);
-  }
-  const int HH = a.H * HD;
-  const float vals[4] = {acc.x, acc.y, acc.z, acc.w};
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int j = j0 + q;
-    int nd, hd_;
-    column_to_row(qt, j, G, g, nd, hd_);
-    if (nd < a.nq)
-      put_split(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH, HH, hd_ * HD + dim_of<HD>(e + q),
-                vals[q] * inv_den[j]);
-  }
+  lds_barrier();
+  if (!last) return;
+  combine_chunks<HD, NWV>(a, item0, a.n_chunks, qt, g, sidx, wgt, &colm[0][0]);
+  if (threadIdx.x == 0)
+    __hip_atomic_store(a.att_cnt + item, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int HD>
@@ -570,21 +589,13 @@ size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd) 
 
 template <int HD>
 void launch_tree_hd(const AttnArgs& a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
-  const int items = a.n_seq * a.KV * a.qtiles;
-  const int units = a.n_seq * a.KV * a.n_chunks;
-  const dim3 grid(8 * a.qtiles * ((units + 7) / 8));
-  const bool comb = a.n_chunks > 1;
-  if (ev0) {
-    // events carried by the launches themselves bracket the kernels only
-    hipExtLaunchKernelGGL(k_tree_attn<HD>, grid, dim3(64 * TREE_WAVES), 0, st, ev0,
-                          comb ? nullptr : ev1, 0, a);
-    if (comb)
-      hipExtLaunchKernelGGL(k_tree_combine<HD>, dim3(items * (HD / 32)), dim3(256), 0, st,
-                            nullptr, ev1, 0, a);
-  } else {
-    hipLaunchKernelGGL(k_tree_attn<HD>, grid, dim3(64 * TREE_WAVES), 0, st, a);
-    if (comb) hipLaunchKernelGGL(k_tree_combine<HD>, dim3(items * (HD / 32)), dim3(256), 0, st, a);
-  }
+  const int pairs = a.n_seq * a.KV;
+  const dim3 grid(8 * ((pairs + 7) / 8) * a.qtiles * a.n_chunks);
+  if (ev0)  // events carried by the launch itself bracket the kernel only
+    hipExtLaunchKernelGGL((k_tree_attn<HD, TREE_WAVES>), grid, dim3(64 * TREE_WAVES), 0, st,
+                          ev0, ev1, 0, a);
+  else
+    hipLaunchKernelGGL((k_tree_attn<HD, TREE_WAVES>), grid, dim3(64 * TREE_WAVES), 0, st, a);
 }
 
 void launch_tree_attention(AttnArgs a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {

@@ -252,14 +252,6 @@ MSD_DEV void store_x(uint4* xs, const uint4 (&xh)[XB], const uint4 (&xl)[XB], in
   }
 }
 
-// Workgroup barrier that orders LDS accesses only: global loads issued
-// before it stay in flight.
-MSD_DEV void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 // The same product with two K chunks per workgroup, for 64-row passes (whose
 // X chunk fills LDS at 4 blocks) and the widest 32-row ones: each workgroup
 // covers chunks 2s and 2s+1

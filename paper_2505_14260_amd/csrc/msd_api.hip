@@ -124,6 +124,7 @@ struct Carver {
 
 struct Plan {
   int rows_max, lrows, ld_qkv;
+  int att_items;  // tree-attention items (sequence, kv head, query tile)
   size_t attn_floats, part_floats;
 };
 
@@ -134,6 +135,7 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
   p.ld_qkv = (m.n_heads + 2 * m.n_kv_heads) * m.head_dim;
   const int G = m.n_heads / m.n_kv_heads;
   const int qtiles = (MSD_MAX_TREE * G + 31) / 32;
+  p.att_items = lim.max_batch * m.n_kv_heads * qtiles;
   p.attn_floats =
       attn_partial_floats(lim.max_batch, m.n_kv_heads, qtiles, ATT_MAX_CHUNKS, m.head_dim);
   // GEMM partials of one 64-row launch, for the largest weight of the model
@@ -191,6 +193,7 @@ struct msd_ctx {
   DynPool pool;
   GemmScratch gs;
   float *att_po, *att_ml, *tk_scratch;
+  int* att_cnt;
   float2* rope;
   int device;            // the GPU current at msd_create
   float* noalloc_base;   // that GPU's copy of `scratch`
@@ -322,6 +325,7 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->pool.frontier = cv.take<int>((size_t)B * TOPK);
   t->att_po = cv.take<float>(p.attn_floats);
   t->att_ml = cv.take<float>(p.attn_floats / m.head_dim * 2 + 64);
+  t->att_cnt = cv.take<int>(p.att_items);
   t->rope = cv.take<float2>((size_t)lim.max_seq * (m.head_dim / 2));
   t->tk_scratch = cv.take<float>(topk_scratch_floats(p.lrows, m.vocab));
   return cv.off + 256;
@@ -428,10 +432,11 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
 
 // Key chunks of a tree-attention pass: each of a workgroup's TREE_WAVES
 // waves takes chunk_keys / TREE_WAVES keys (a multiple of 32); enough chunks
-// for about one workgroup per CU while every wave keeps at least one block
-// (a wave hides little latency behind its own blocks, so spreading the keys
-// over more CUs pays until the combine pass dominates), within the partial
-// buffer of cap floats.
+// for about ATT_TARGET_WGS workgroups while every wave keeps at least one
+// block (a wave hides little latency behind its own blocks, so spreading the
+// keys over more CUs pays), at most ATT_MAX_CHUNKS per item (their merge
+// reads every chunk's partial at once), within the partial buffer of cap
+// floats.
 struct TreeChunks {
   int qtiles, chunk_keys, n_chunks;
   size_t part_floats;
@@ -443,8 +448,9 @@ TreeChunks plan_tree_chunks(const msd_model_desc& m, int n_seq, int nq, int max_
   t.qtiles = (nq * G + 31) / 32;
   const int span = 32 * TREE_WAVES;
   const int base_items = n_seq * KV * t.qtiles;
-  const int max_chunks = std::max(1, (max_ltot + span - 1) / span);
-  const int chunks = std::min(max_chunks, std::max(1, (256 + base_items - 1) / base_items));
+  const int max_chunks = std::min(ATT_MAX_CHUNKS, std::max(1, (max_ltot + span - 1) / span));
+  const int chunks =
+      std::min(max_chunks, std::max(1, (ATT_TARGET_WGS + base_items - 1) / base_items));
   int ck = (max_ltot + chunks - 1) / chunks;
   ck = (ck + span - 1) / span * span;
   while ((max_ltot + ck - 1) / ck > ATT_MAX_CHUNKS ||
@@ -523,6 +529,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     a.scale = 1.0f / std::sqrt((float)hd);
     a.part_o = c->att_po;
     a.part_ml = c->att_ml;
+    a.att_cnt = c->att_cnt;
     if (tree_R < 0) {
       a.qtiles = (nq + 31) / 32;
       a.n_chunks = 1;
@@ -848,6 +855,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     HIPC(c, hipMemsetAsync(c->pend_n, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->d_root, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->tree_err, 0, sizeof(int) * lim->max_batch, c->st));
+    HIPC(c, hipMemsetAsync(c->att_cnt, 0, sizeof(int) * c->plan.att_items, c->st));
     HIPC(c, hipMemsetAsync(c->gemm_zero, 0, sizeof(uint16_t) * gemm_dummy_elems(), c->st));
     launch_rope_table(c->rope, lim->max_seq, m->head_dim, (double)m->rope_theta, c->st);
     LAUNCHED(c);

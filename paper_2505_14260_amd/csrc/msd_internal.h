@@ -36,6 +36,14 @@ MSD_DEV float get_split(const uint16_t* row, int K, int k) {
   return bf2f(row[k]) + bf2f(row[K + k]);
 }
 
+// Workgroup barrier that orders LDS accesses only: global loads issued
+// before it stay in flight.
+MSD_DEV void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // True when the verify of this call flagged any of its n_seq trees.
 MSD_DEV bool any_tree_err(const int* tree_err, int n_seq) {
   int e = 0;
@@ -124,8 +132,15 @@ struct RowNorm {
 
 // ----------------------------------------------------------- attention ----
 constexpr int ATT_MAX_SEQ = 8;
-constexpr int TREE_WAVES = 8;  // waves per tree-attention workgroup (32 keys each per block)
-constexpr int ATT_MAX_CHUNKS = 64;  // key chunks per (sequence, kv head, query tile)
+#ifndef MSD_TREE_WAVES
+#define MSD_TREE_WAVES 4
+#endif
+constexpr int TREE_WAVES = MSD_TREE_WAVES;  // waves per tree-attention workgroup
+// key chunks per (sequence, kv head, query tile): the workgroup that
+// finishes an item's last chunk merges at most this many partials
+constexpr int ATT_MAX_CHUNKS = 8;
+// tree-attention workgroups a pass aims for (about eight waves per CU)
+constexpr int ATT_TARGET_WGS = 256 * 8 / TREE_WAVES;
 struct AttnArgs {
   const uint16_t* q;      // [n_seq*nq] split rows of H*hd, rotated
   const uint16_t* kc;     // layer K cache  [B][KV][S][hd]
@@ -139,6 +154,7 @@ struct AttnArgs {
   int n_chunks, chunk_keys, qtiles;  // chunk_keys: multiple of 128 (tree mode)
   float* part_o;          // [items][32*hd] partial outputs (tree mode, n_chunks > 1)
   float* part_ml;         // [items][32][2]
+  int* att_cnt;           // [items] chunk arrivals (zero between launches)
   uint16_t* out;          // [n_seq*nq] split rows of H*hd
   float scale;
 };
