@@ -74,7 +74,9 @@ class PendingRow:
     is_visual: bool
     h: Optional[np.ndarray] = None         # target feature of the row (text)
     e_next: Optional[np.ndarray] = None    # embedding of the following token (text)
-    e_visual: Optional[np.ndarray] = None  # the row's own embedding (visual)
+    # the draft input of a visual row: its own embedding (Eq. decouple), or
+    # its target feature in the Visual Feature variant (Sec. 5.3)
+    e_visual: Optional[np.ndarray] = None
 
 
 @dataclass
@@ -94,8 +96,22 @@ class Models:
         return M.widen(self.w["embed"][int(token)])
 
 
-def prefill(m: Models, tokens, is_visual, visual, max_slots):
-    """Target forward over the prompt; returns (state, first generated token)."""
+VISUAL_INPUTS = ("embedding", "feature")
+
+
+def prefill(m: Models, tokens, is_visual, visual, max_slots, visual_input="embedding"):
+    """Target forward over the prompt; returns (state, first generated token).
+
+    visual_input selects the draft input of the visual rows.  "embedding" is
+    the method's decoupled input (Eq. decouple): a visual row enters the draft
+    as its own embedding e_v.  "feature" is the Visual Feature variant of the
+    input-decoupling ablation (Sec. 5.3, Table decouple_input): a visual row
+    enters as the target's feature h_v of that row (the final-norm output,
+    the same feature the text rows concatenate), with no next-token
+    concatenation and no f_down.
+    """
+    if visual_input not in VISUAL_INPUTS:
+        raise ValueError(f"visual_input must be one of {VISUAL_INPUTS}")
     dims = m.dims
     n = len(tokens)
     is_visual = np.asarray(is_visual, dtype=bool)
@@ -116,7 +132,8 @@ def prefill(m: Models, tokens, is_visual, visual, max_slots):
     st = SeqState(kv=kv, dkv=dkv, L=n, root=first)
     for i in range(n):
         if is_visual[i]:
-            st.pending.append(PendingRow(True, e_visual=x[i].copy()))
+            src = x[i] if visual_input == "embedding" else h[i]
+            st.pending.append(PendingRow(True, e_visual=src.copy()))
         else:
             e_next = x[i + 1].copy() if i + 1 < n else m.embed(first)
             st.pending.append(PendingRow(False, h=h[i].copy(), e_next=e_next))
@@ -348,12 +365,12 @@ def accept_and_compact(m: Models, st: SeqState, tree: Tree, h_tree, amax):
 
 
 def msd_generate(m: Models, prompt, shape, n_new, static_arrays=None, max_slots=None,
-                 record=False):
+                 record=False, visual_input="embedding"):
     """Speculative greedy decoding; returns (tokens[n_new], per-cycle records)."""
     tokens, is_visual, visual = prompt
     T = (shape.n_draft + 1)
     max_slots = max_slots or (len(tokens) + n_new + 2 * T + 8)
-    st, first, _, _ = prefill(m, tokens, is_visual, visual, max_slots)
+    st, first, _, _ = prefill(m, tokens, is_visual, visual, max_slots, visual_input)
     out = [first]
     cycles = []
     while len(out) < n_new:

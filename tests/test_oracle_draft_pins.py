@@ -13,7 +13,8 @@ definitions, not against the oracle's own code path:
   draft cache and the root feature must equal one causal draft forward over
   the whole committed sequence, with each row's input assembled here from a
   fresh target forward: text row i takes f_down(Concat(h_i, e_{i+1})),
-  visual row i takes e_i.
+  visual row i takes e_i, or h_i in the Visual Feature variant of the
+  input-decoupling ablation (Sec. 5.3).
 * Dynamic tree: the beam is defined breadth-wise by sets (each depth's
   frontier is the best K of its candidates by cumulative log-probability;
   the tree keeps the best N of the whole pool), and the canonical node order
@@ -108,14 +109,15 @@ def test_draft_nodes_equal_sequential_branch_decode(wl, kind):
     assert checked >= 3 * (shape.depth - 1)
 
 
-def decoupled_inputs(m, rows_x, is_visual, h, root):
-    """Draft input rows of Eq. decouple, assembled independently."""
+def decoupled_inputs(m, rows_x, is_visual, h, root, visual_input="embedding"):
+    """Draft input rows of Eq. decouple, assembled independently (visual rows:
+    the embedding, or the target feature for visual_input="feature")."""
     L = len(rows_x)
     f = np.empty_like(rows_x)
     e_root = M.widen(m.w["embed"][int(root)])
     for i in range(L):
         if is_visual[i]:
-            f[i] = rows_x[i]
+            f[i] = rows_x[i] if visual_input == "embedding" else h[i]
         else:
             e_next = rows_x[i + 1] if i + 1 < L else e_root
             f[i] = M.linear(np.concatenate([h[i], e_next])[None, :], m.draft["fc"])[0]
@@ -123,13 +125,14 @@ def decoupled_inputs(m, rows_x, is_visual, h, root):
 
 
 @pytest.mark.parametrize("wl", [MINI_GQA, TINY], ids=lambda w: w.name)
-@pytest.mark.parametrize("kind", ["static", "chain"])
-def test_draft_cache_equals_one_causal_draft_forward(wl, kind):
+@pytest.mark.parametrize("kind,visual_input", [("static", "embedding"), ("chain", "embedding"),
+                                               ("static", "feature")])
+def test_draft_cache_equals_one_causal_draft_forward(wl, kind, visual_input):
     m, prompt = setup(wl)
     tokens, vis_flags, visual = prompt
     shape = SHAPES[kind](wl)
     n = len(tokens)
-    st, first, _, _ = O.prefill(m, *prompt, max_slots=n + 96)
+    st, first, _, _ = O.prefill(m, *prompt, max_slots=n + 96, visual_input=visual_input)
     out = [first]
     for cycle in range(4):
         trace = {}
@@ -152,7 +155,7 @@ def test_draft_cache_equals_one_causal_draft_forward(wl, kind):
         kv = M.KVCache(m.dims.n_layers, L, m.dims.n_kv_heads, m.dims.head_dim)
         pos = np.arange(L, dtype=np.int32)
         h, _ = M.target_forward(m.dims, m.w, kv, x, pos, pos, 0, L, None, want_logits=False)
-        f = decoupled_inputs(m, x, is_vis, h, out[-1])
+        f = decoupled_inputs(m, x, is_vis, h, out[-1], visual_input)
         dkv = M.KVCache(1, L, m.dims.n_kv_heads, m.dims.head_dim)
         feats = M.layer_forward(m.dims, m.draft["layer"], dkv.k[0], dkv.v[0], f, pos, pos,
                                 0, L, None)

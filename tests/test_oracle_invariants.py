@@ -7,7 +7,9 @@
   target's plain greedy sequence, whatever the draft proposes.
 * Decoupled draft input (Eq. decouple): text rows use f_down(Concat(h, e_next))
   (the feature-level form of Eq. concat); visual rows use the visual
-  embedding itself and never touch f_down.
+  embedding itself and never touch f_down.  In the Visual Feature variant
+  of the input-decoupling ablation (Sec. 5.3) they use the target's feature
+  of the row instead, still without f_down.
 """
 import numpy as np
 import pytest
@@ -76,6 +78,20 @@ def test_speculative_equals_greedy(wl, kind, mode):
     assert all(1 <= len(c["emitted"]) <= shape.depth + 1 for c in cycles)
 
 
+@pytest.mark.parametrize("kind", ["static", "dynamic"])
+def test_speculative_equals_greedy_visual_feature_input(kind):
+    # the draft's input rule changes what it proposes, never what is emitted
+    wl = TINY
+    m, prompt = setup(wl, "hidden")
+    shape = SHAPES[kind](wl)
+    ref = O.greedy_generate(m, prompt, wl.new_tokens)
+    out, cycles = O.msd_generate(m, prompt, shape, wl.new_tokens, arrays(shape),
+                                 visual_input="feature")
+    assert out == ref
+    assert len(out) == wl.new_tokens
+    assert all(1 <= len(c["emitted"]) <= shape.depth + 1 for c in cycles)
+
+
 def test_speculative_accepts_something():
     # with the pass-through draft init, acceptance on the tiny model is nonzero,
     # so compaction with k > 0 is exercised by the losslessness test above
@@ -118,6 +134,23 @@ def test_visual_rows_bypass_fdown():
     # last visual row's predecessor is not needed; the last text row's next
     # embedding is the first generated token's
     assert not rows[-1].is_visual
+
+
+def test_visual_feature_rows_are_target_features():
+    wl = TINY
+    m, prompt = setup(wl, "random")
+    st, _, h, _ = O.prefill(m, *prompt, max_slots=wl.prompt_len + 8, visual_input="feature")
+    emb, _, _, _ = O.prefill(m, *prompt, max_slots=wl.prompt_len + 8)
+    vis = np.array([p.is_visual for p in st.pending])
+    assert vis.any() and (~vis).any()
+    ev = np.stack([p.e_visual for p in np.array(st.pending)[vis]])
+    assert np.array_equal(ev, h[vis])                     # bit-exact h_v
+    assert not np.array_equal(ev, M.widen(prompt[2]))     # not the embedding
+    for a, b in zip(st.pending, emb.pending):             # text rows unchanged
+        if not a.is_visual:
+            assert np.array_equal(a.h, b.h) and np.array_equal(a.e_next, b.e_next)
+    with pytest.raises(ValueError):
+        O.prefill(m, *prompt, max_slots=wl.prompt_len + 8, visual_input="concat")
 
 
 def test_prompt_must_end_in_text():

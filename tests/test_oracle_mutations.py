@@ -239,7 +239,12 @@ SOURCE_CASES = [
     # the draft catch-up rows are rotated one position too far
     ("catch_up_positions_shifted", O, "draft_catch_up",
      "np.arange(L0, L0 + r, dtype=np.int32)", "np.arange(L0 + 1, L0 + r + 1, dtype=np.int32)",
-     lambda: [lambda: PD.test_draft_cache_equals_one_causal_draft_forward(PI.TINY, "static")]),
+     lambda: [lambda: PD.test_draft_cache_equals_one_causal_draft_forward(PI.TINY, "static", "embedding")]),
+    # the Visual Feature variant feeds the visual embedding after all
+    ("visual_feature_input_ignored", O, "prefill",
+     'src = x[i] if visual_input == "embedding" else h[i]', "src = x[i]",
+     lambda: [lambda: PD.test_draft_cache_equals_one_causal_draft_forward(
+         PI.TINY, "static", "feature")]),
     # log-softmax without the log-sum-exp term
     ("log_softmax_without_lse", O, "log_softmax",
      "return logits - (m + np.log(np.sum(np.exp(logits - m))))", "return logits - m",
