@@ -181,8 +181,22 @@ int msd_prefill(msd_ctx* ctx, int seq, int n, const int32_t* tokens_h,
                 int32_t* first_token_h);
 
 /*
+ * Draft input of the visual prompt rows (the input-decoupling ablation,
+ * Sec. 5.3, Table decouple_input).  MSD_DRAFT_VISUAL_EMBEDDING (the default,
+ * the method's Eq. decouple): a visual row enters the draft as its own
+ * embedding e_v.  MSD_DRAFT_VISUAL_FEATURE: it enters as the target's feature
+ * h_v of that row (the final-norm output the text rows concatenate), again
+ * without f_down.  Text rows are f_down(Concat(h_i, e_{i+1})) either way.
+ * Applies to the msd_prefill calls that follow on this context (only prompt
+ * rows are visual).  MSD_ERR_INVALID_ARG for another value.
+ */
+enum { MSD_DRAFT_VISUAL_EMBEDDING = 0, MSD_DRAFT_VISUAL_FEATURE = 1 };
+int msd_set_draft_input(msd_ctx* ctx, int visual_input);
+
+/*
  * Draft phase for sequences seqs_h[0..n_seq): runs the pending rows through
- * the draft head (text: f_down(Concat(h_i, e_{i+1})); visual: e_i), then
+ * the draft head (text: f_down(Concat(h_i, e_{i+1})); visual: e_i, or h_i
+ * after msd_set_draft_input(MSD_DRAFT_VISUAL_FEATURE)), then
  * builds the tree of `spec` depth by depth.  Writes one msd_tree per
  * sequence to trees_d[0..n_seq).  All sequences use the same spec.
  */

@@ -54,6 +54,16 @@ __global__ __launch_bounds__(256) void k_visual_rows(const uint16_t* visual, con
   for (int e = threadIdx.x; e < d; e += 256) x[(size_t)row * d + e] = bf2f(visual[(size_t)v * d + e]);
 }
 
+// Overwrites the visual rows of x with the target's features of those rows
+// (h: split rows of d): the draft input of the Visual Feature variant.
+__global__ __launch_bounds__(256) void k_visual_feature_rows(const uint16_t* h, const int* vis_idx,
+                                                             int d, float* x) {
+  const int row = blockIdx.x;
+  if (vis_idx[row] < 0) return;
+  const uint16_t* hr = h + (size_t)row * 2 * d;
+  for (int e = threadIdx.x; e < d; e += 256) x[(size_t)row * d + e] = get_split(hr, d, e);
+}
+
 // cos/sin of pos * theta^(-2i/hd), evaluated in float64.
 __global__ void k_rope_table(float2* tab, int max_pos, int half, double theta) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
@@ -612,6 +622,12 @@ void launch_visual_rows(const uint16_t* visual, const int* vis_idx, int rows, in
                         hipStream_t st) {
   if (rows <= 0) return;
   hipLaunchKernelGGL(k_visual_rows, dim3(rows), dim3(256), 0, st, visual, vis_idx, d, x);
+}
+
+void launch_visual_feature_rows(const uint16_t* h, const int* vis_idx, int rows, int d, float* x,
+                                hipStream_t st) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(k_visual_feature_rows, dim3(rows), dim3(256), 0, st, h, vis_idx, d, x);
 }
 
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st) {

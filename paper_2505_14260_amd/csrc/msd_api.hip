@@ -195,6 +195,7 @@ struct msd_ctx {
   float *att_po, *att_ml, *tk_scratch;
   int* att_cnt;
   float2* rope;
+  int visual_input = MSD_DRAFT_VISUAL_EMBEDDING;  // draft input of visual prompt rows
   int device;            // the GPU current at msd_create
   float* noalloc_base;   // that GPU's copy of `scratch`
   // host
@@ -598,7 +599,10 @@ int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const ui
     LAUNCHED(c);
   }
   if (visual) {
-    launch_visual_rows(visual, c->rows.vis, rows, d, c->x, c->st);
+    if (c->visual_input == MSD_DRAFT_VISUAL_FEATURE)
+      launch_visual_feature_rows(c->h, c->rows.vis, rows, d, c->x, c->st);
+    else
+      launch_visual_rows(visual, c->rows.vis, rows, d, c->x, c->st);
     LAUNCHED(c);
     TRY(norm_rows(c, rows, c->dlayer.n1));
   }
@@ -972,7 +976,8 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
   launch_set_int(c->d_root, seq, c->tk_idx, 0, c->st);
   launch_set_int(c->nxt, n - 1, c->tk_idx, 0, c->st);
   LAUNCHED(c);
-  // draft over the prompt: text rows f_down(Concat(h_i, e_{i+1})), visual rows e_i
+  // draft over the prompt: text rows f_down(Concat(h_i, e_{i+1})), visual rows
+  // e_i (or h_i for the Visual Feature input)
   launch_fc_input(c->h, nullptr, c->rows.hrow, c->embed, c->nxt, (const uint16_t*)visual_d, n, d,
                   c->fcin, c->st);
   LAUNCHED(c);
@@ -986,6 +991,14 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
   c->L[seq] = n;
   c->pend[seq] = 0;
   c->ready[seq] = 1;
+  return MSD_OK;
+}
+
+int msd_set_draft_input(msd_ctx* c, int visual_input) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  if (visual_input != MSD_DRAFT_VISUAL_EMBEDDING && visual_input != MSD_DRAFT_VISUAL_FEATURE)
+    return fail(c, MSD_ERR_INVALID_ARG, "unknown draft input mode");
+  c->visual_input = visual_input;
   return MSD_OK;
 }
 

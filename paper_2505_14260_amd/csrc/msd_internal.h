@@ -195,6 +195,9 @@ void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const
                      hipStream_t st);
 void launch_visual_rows(const uint16_t* visual, const int* vis_idx, int rows, int d,
                         float* x, hipStream_t st);
+// x rows with vis_idx >= 0 = the split rows h (the target features).
+void launch_visual_feature_rows(const uint16_t* h, const int* vis_idx, int rows, int d, float* x,
+                                hipStream_t st);
 
 // -------------------------------------------------------- selection ----
 // scratch: topk_scratch_floats(rows, V) floats (8-byte aligned).  The

@@ -93,6 +93,7 @@ def lib():
                                         c_vp]
         L.msd_seq_len.argtypes = [c_vp, ctypes.c_int]
         L.msd_set_state.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, c_vp, c_i32]
+        L.msd_set_draft_input.argtypes = [c_vp, ctypes.c_int]
         L.msd_stream_read.argtypes = [c_vp, c_sz, ctypes.c_int, c_vp, c_vp]
         L.msd_trace_enable.argtypes = [c_vp, ctypes.c_int, ctypes.c_int]
         L.msd_trace_read.argtypes = [c_vp, ctypes.c_int, P(TraceRec)]
@@ -201,6 +202,14 @@ def msd_seq_len(ctx, seq):
     return lib().msd_seq_len(ctx, seq)
 
 
+# draft input of visual prompt rows (msd_set_draft_input)
+DRAFT_VISUAL_INPUTS = {"embedding": 0, "feature": 1}
+
+
+def msd_set_draft_input(ctx, visual_input):
+    _check(ctx, lib().msd_set_draft_input(ctx, visual_input))
+
+
 def msd_set_state(ctx, seq, L, h_ptr, next_token):
     _check(ctx, lib().msd_set_state(ctx, seq, L, h_ptr, next_token))
 
@@ -243,7 +252,7 @@ class Engine:
     """Owns device copies of the weights and the caller-side buffers."""
 
     def __init__(self, dims, target, draft, max_batch=1, max_seq=1024, max_tree=64,
-                 max_prompt=1024, device="cuda"):
+                 max_prompt=1024, device="cuda", visual_input="embedding"):
         import torch
         self.torch = torch
         self.dims = dims
@@ -267,6 +276,12 @@ class Engine:
         self.bufs = Buffers(*[b.data_ptr() for b in self.bufs_t])
         self.stream = torch.cuda.current_stream(self.dev).cuda_stream
         self.ctx = msd_create(self.desc, self.lim, self.tw, self.dw, self.bufs, self.stream)
+        self.set_draft_input(visual_input)
+
+    def set_draft_input(self, visual_input):
+        """Draft input of the visual prompt rows of later prefills: "embedding"
+        (the method) or "feature" (the Visual Feature variant)."""
+        msd_set_draft_input(self.ctx, DRAFT_VISUAL_INPUTS[visual_input])
 
     def _upload(self, a):
         a = np.ascontiguousarray(a)

@@ -345,6 +345,53 @@ def test_speculative_decode_matches_greedy(setup):
                                                               ref[first_bad])
 
 
+def test_visual_feature_draft_input_matches_oracle(setup):
+    # the Visual Feature variant of the draft input (Sec. 5.3): visual prompt
+    # rows enter the draft as the target's features h_v instead of e_v
+    wl, eng, m, prompt = setup
+    print("case: visual-feature draft input, tiny", flush=True)
+    n = wl.prompt_len
+    vis = np.asarray(prompt[1], dtype=bool)
+    eng.set_draft_input("feature")
+    try:
+        eng.prefill(0, *prompt)
+        st, _, _, _ = O.prefill(m, *prompt, max_slots=256, visual_input="feature")
+        tk, tv, dk, dv = eng.kv_views()
+        torch.cuda.synchronize()
+        kg = bits_to_f64(dk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        vg = bits_to_f64(dv[0, 0, :, :, :n].permute(2, 0, 1).reshape(n, -1))
+        emb, _, _, _ = O.prefill(m, *prompt, max_slots=256)
+        O.draft_catch_up(m, emb)
+        spec, _ = static_spec(wl.tree.paths)
+        ref, logs, rank = oracle_draft_static(m, st, wl.tree.paths)  # catch-up + tree
+        ok, err = row_close(kg, st.dkv.k[0, :n].reshape(n, -1))
+        assert ok, ("draft K", err)
+        ok, err = row_close(vg, st.dkv.v[0, :n].reshape(n, -1))
+        assert ok, ("draft V", err)
+        # the embedding-input cache differs at the visual rows: the mode took effect
+        ok_emb, _ = row_close(kg[vis], emb.dkv.k[0, :n][vis].reshape(int(vis.sum()), -1))
+        assert not ok_emb
+        dev = eng.new_trees(1)
+        eng.draft_tree([0], spec, dev)
+        g = eng.trees_to_host(dev, 1)[0]
+        checked = compare_static_tree(g, ref, logs, rank)
+        print(f"visual-feature draft tree: {checked}/{ref.n - 1} nodes compared equal")
+        assert checked >= (ref.n - 1) // 2
+        # the emitted tokens are still the target's greedy decode
+        toks, cycles = eng.generate(0, prompt, spec, wl.new_tokens)
+        want, rows = O.greedy_generate(m, prompt, wl.new_tokens, return_logits=True)
+        bad = next((i for i in range(len(want)) if toks[i] != want[i]), None)
+        print(f"visual-feature e2e: {bad if bad is not None else len(want)}/{len(want)} "
+              f"tokens equal; tau={np.mean(cycles):.2f}")
+        if bad is not None:
+            assert argmax_ok(toks[bad], rows[bad]), (bad, toks[bad], want[bad])
+    finally:
+        eng.set_draft_input("embedding")
+    from paper_2505_14260_amd import msd as B
+    with pytest.raises(B.MSDError):
+        B.msd_set_draft_input(eng.ctx, 2)
+
+
 def test_chain_n_alpha_matches_oracle(setup):
     """Chain drafts (one token per draft forward): the per-cycle accepted
     counts, and so the n-alpha acceptance rates, equal the oracle's MSD loop
