@@ -204,6 +204,89 @@ class Case:
             log(f"[{label} seq {b}] accepted path {path}, emitted {emitted}")
         log(f"[{label}] cycle checked in {time.perf_counter() - t0:.1f}s")
 
+    def natural_cycle(self, n_chain, label):
+        """One cycle whose tree holds the target's own greedy continuation.
+
+        The oracle decodes n_chain tokens greedily from the committed state;
+        they replace the tokens of the first-ranked chain of the GPU's draft
+        tree (siblings kept distinct), so the verify's own argmax accepts them
+        without any forcing.  Everything the GPU emits must equal the oracle's
+        acceptance on the oracle's logits wherever those are decided, and the
+        accepted path must reach the chain's depth when every step is decided.
+        """
+        from paper_2505_14260_amd.msd import MAX_TREE, Tree, msd_seq_len
+        wl, eng, m, T, dims = self.wl, self.eng, self.m, self.T, self.dims
+        assert len(self.states) == 1 and wl.tree.kind == "static"
+        st = self.states[0]
+        t0 = time.perf_counter()
+        trees = eng.new_trees(1)
+        eng.draft_tree([0], self.spec, trees)
+        g = eng.trees_to_host(trees, 1)[0]
+        # the target's greedy continuation of the root, one row at a time
+        kv = st.kv.copy()
+        cur, chain, margins = st.root, [], []
+        for j in range(n_chain):
+            x = M.embed_rows(m.w, [cur])
+            pos = np.array([st.L + j], dtype=np.int32)
+            _, lg1 = M.target_forward(dims, m.w, kv, x, pos, pos, st.L + j, 1, None)
+            cur = int(np.argmax(lg1[0]))
+            chain.append(cur)
+            margins.append(decided(lg1[0]))
+        # the first-ranked chain of the static shape: node 0 -> ... by rank 0
+        par = list(g.parent[:T])
+        rank = list(self.arrays[1])
+        u, nodes = 0, []
+        for _ in range(n_chain):
+            kids = [c for c in range(1, T) if par[c] == u and rank[c] == 0]
+            if not kids:
+                break
+            u = kids[0]
+            nodes.append(u)
+        tok = list(g.token[:T])
+        for u, t in zip(nodes, chain):
+            tok[u] = t
+        for u in nodes:  # a sibling holding the same token gets another one
+            for c in range(1, T):
+                if c != u and par[c] == par[u] and tok[c] == tok[u]:
+                    while tok[c] in [tok[x] for x in range(1, T) if par[x] == par[u] and x != c]:
+                        tok[c] = (tok[c] + 1) % dims.vocab
+        t = Tree()
+        t.n_nodes = T
+        for i in range(T):
+            t.token[i], t.parent[i], t.depth[i], t.anc[i] = tok[i], g.parent[i], g.depth[i], \
+                g.anc[i]
+        trees.copy_(torch.frombuffer(bytearray(bytes(t)), dtype=torch.uint8).cuda())
+        tree = oracle_tree_of(t)
+        amax, logits = eng.verify([0], trees, T, want_logits=True)
+        torch.cuda.synchronize()
+        lg = logits.cpu().numpy().reshape(T, -1)
+        am = amax.cpu().numpy().reshape(T)
+        h_ref, lg_ref = O.verify(m, st, tree)
+        ok, err = row_close(lg, lg_ref)
+        assert ok, err
+        for i in range(T):
+            assert argmax_ok(am[i], lg_ref[i]), i
+        em, slots = eng.accept([0], trees, T, amax, want_slots=True)
+        torch.cuda.synchronize()
+        sl = slots.cpu().numpy().reshape(1, MAX_TREE)[0]
+        L = st.L
+        ref_am = np.argmax(lg_ref, axis=1)
+        r_path, r_emit = O.greedy_accept(tree, ref_am)
+        g_path, g_emit = O.greedy_accept(tree, am)
+        assert em[0] == g_emit and list(sl[:len(g_path)]) == [L + j for j in g_path]
+        # the chain is accepted as far as the oracle's own decisions are decided
+        n_dec = next((j for j, d in enumerate(margins) if not d), n_chain)
+        assert len(g_path) - 1 >= min(n_dec, len(nodes)), (g_path, margins)
+        assert g_emit[:min(n_dec, len(nodes))] == chain[:min(n_dec, len(nodes))]
+        if all(decided(lg_ref[u]) for u in [0] + g_path[1:]):
+            assert g_path == r_path and g_emit == r_emit
+        O.accept_and_compact(m, st, tree, h_ref, am)
+        assert msd_seq_len(eng.ctx, 0) == st.L
+        log(f"[{label}] greedy chain {chain} (decided {margins}); accepted path {g_path}, "
+            f"emitted {g_emit}; logits max rel err {err:.2e}; "
+            f"checked in {time.perf_counter() - t0:.1f}s")
+        return len(g_path) - 1
+
     def sample_cycle(self, temperature, seed, label):
         """One cycle with speculative-sampling acceptance, checked against the
         oracle's rule on the GPU's own logits and draws (the state is not
@@ -249,6 +332,21 @@ def test_llava7b_two_cycles():
         c.cycle([3], "7b c1")
         c.cycle([0], "7b c2")
         c.sample_cycle(1.0, 2024, "7b c3")
+    finally:
+        c.close()
+
+
+@pytest.mark.timeout(300)
+def test_llava7b_natural_acceptance():
+    """7B-shaped: a tree carrying the target's greedy continuation is accepted
+    by the verify's own argmax (no forcing), then the draft catches up over
+    the accepted rows in the next cycle."""
+    log("case: full llava-1.5-7b-shaped, natural multi-token acceptance")
+    c = Case(LLAVA7B, [LLAVA7B.prompt_len])
+    try:
+        k = c.natural_cycle(LLAVA7B.tree.depth, "7b natural")
+        assert k >= 1
+        c.cycle([0], "7b after natural")
     finally:
         c.close()
 
