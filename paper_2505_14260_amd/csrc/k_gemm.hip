@@ -691,10 +691,12 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
   // Two K chunks per workgroup (the tiles' accumulators live in registers,
   // at most PAIR_MAX_TILES of them).  64-row passes: when at least three
   // quarters of the target workgroups stay busy.  32-row passes, whose
-  // partials are half as many per weight byte: only when the workgroup count
-  // stays within 5% and each workgroup has four tiles or more to amortise
-  // the mid-stream restage of X (the wide LM heads).
-  if ((p.MT == 4 || (p.MT == 2 && nw == 1)) && p.S >= 2) {
+  // partials are half as many per weight byte: the SwiGLU pair always (its
+  // 9.5 MB of partials at the 7B shape cost more than the idle CUs: gate+up
+  // 37.0 -> 36.1 us, its consumer about 1 us less), single weights only when
+  // the workgroup count stays within 5% and each workgroup has four tiles or
+  // more to amortise the mid-stream restage of X (the wide LM heads).
+  if ((p.MT == 4 || p.MT == 2) && p.S >= 2) {
     const int S2 = (p.S + 1) / 2;
     int G2 = (target_wgs + S2 - 1) / S2;
     if (G2 > p.n_tiles) G2 = p.n_tiles;
@@ -705,7 +707,7 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
       G2 = (p.n_tiles + per2 - 1) / per2;
     }
     const bool busy = p.MT == 4 ? 4 * S2 * G2 >= 3 * target_wgs
-                                : (per2 >= 4 && 20 * S2 * G2 >= 19 * p.S * p.G);
+                                : (nw == 2 || (per2 >= 4 && 20 * S2 * G2 >= 19 * p.S * p.G));
     if (per2 <= PAIR_MAX_TILES && busy) {
       p.pair = 1;
       p.S = S2;
@@ -748,8 +750,8 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
   a.dummy = dummy;
   const dim3 grid(pl.S * pl.G);
   if (pl.pair) {
-    // 32-row passes pair only single weights (the LM heads)
-    if (pl.MT == 2) launch_pair_nt<2, 1>(pl.per, grid, a, sc, st);
+    if (pl.MT == 2 && nw == 2) launch_pair_nt<2, 2>(pl.per, grid, a, sc, st);
+    else if (pl.MT == 2) launch_pair_nt<2, 1>(pl.per, grid, a, sc, st);
     else if (nw == 2) launch_pair_nt<4, 2>(pl.per, grid, a, sc, st);
     else launch_pair_nt<4, 1>(pl.per, grid, a, sc, st);
     return;
