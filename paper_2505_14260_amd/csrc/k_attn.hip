@@ -301,14 +301,29 @@ struct QShared {
   }
 };
 
+// A chunk's partial output is stored normalised by its own softmax sum (a
+// convex combination of value rows, so no larger in magnitude than the
+// largest of them) in float16, eight head dims per 16-byte unit; its
+// (max, sum) pair stays float32.
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+MSD_DEV uint4 pack_half8(const float (&o)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    w[i] = __builtin_bit_cast(uint32_t, half2v{(_Float16)o[2 * i], (_Float16)o[2 * i + 1]});
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+MSD_DEV float half_lo(uint32_t w) { return (float)__builtin_bit_cast(half2v, w).x; }
+MSD_DEV float half_hi(uint32_t w) { return (float)__builtin_bit_cast(half2v, w).y; }
+
 // Merges the key chunks of one item (sequence, kv head, query tile): run by
 // the workgroup that finishes the item's last chunk.  A chunk's partial is
 // stored by units of (query column j, 8 consecutive head dims d0..d0+7) at
 // ((d0 / 8) * 32 + j) * 8; a thread owns such units: it loads every chunk's
 // slices first, then the (max, sum) pairs, so the merge waits for memory
 // once, and writes each unit as one 16-byte hi and one 16-byte lo store.
-// Chunks merge in chunk order, so the result does not depend on which
-// workgroup merges.
+// Chunk q's weight is exp(max_q - max) * sum_q over the total; chunks merge
+// in chunk order, so the result does not depend on which workgroup merges.
 template <int HD, int NWV>
 MSD_DEV void combine_chunks(const AttnArgs& a, size_t item0, int nc, int qt, int g, int sidx,
                             float (*wgt)[32], float* inv_den) {
@@ -317,16 +332,14 @@ MSD_DEV void combine_chunks(const AttnArgs& a, size_t item0, int nc, int qt, int
   constexpr int UN = 32 * HD / 8;           // (column, 8 dims) units
   constexpr int IT = (UN + NT - 1) / NT;    // units per thread
   const int G = a.H / a.KV;
-  float4 v[IT][ATT_MAX_CHUNKS][2];
+  uint4 v[IT][ATT_MAX_CHUNKS];
+  const uint16_t* const po = reinterpret_cast<const uint16_t*>(a.part_o);
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const int u = min((int)threadIdx.x + NT * it, UN - 1);
 #pragma unroll
-    for (int q = 0; q < ATT_MAX_CHUNKS; ++q) {
-      const float* src = a.part_o + (item0 + min(q, nc - 1)) * E + 8 * u;
-      v[it][q][0] = *reinterpret_cast<const float4*>(src);
-      v[it][q][1] = *reinterpret_cast<const float4*>(src + 4);
-    }
+    for (int q = 0; q < ATT_MAX_CHUNKS; ++q)
+      v[it][q] = *reinterpret_cast<const uint4*>(po + (item0 + min(q, nc - 1)) * E + 8 * u);
   }
   if (threadIdx.x < 32) {
     const int j = threadIdx.x;
@@ -343,7 +356,7 @@ MSD_DEV void combine_chunks(const AttnArgs& a, size_t item0, int nc, int qt, int
     for (int q = 0; q < ATT_MAX_CHUNKS; ++q) {
       const float wc = (q >= nc || M == -INFINITY || ml[q].x == -INFINITY) ? 0.f
                                                                             : __expf(ml[q].x - M);
-      wgt[q][j] = wc;
+      wgt[q][j] = wc * ml[q].y;
       den += wc * ml[q].y;
     }
     inv_den[j] = den > 0.f ? 1.f / den : 0.f;
@@ -362,14 +375,15 @@ MSD_DEV void combine_chunks(const AttnArgs& a, size_t item0, int nc, int qt, int
 #pragma unroll
     for (int q = 0; q < ATT_MAX_CHUNKS; ++q) {
       const float wq = wgt[q][j];
-      o[0] += wq * v[it][q][0].x;
-      o[1] += wq * v[it][q][0].y;
-      o[2] += wq * v[it][q][0].z;
-      o[3] += wq * v[it][q][0].w;
-      o[4] += wq * v[it][q][1].x;
-      o[5] += wq * v[it][q][1].y;
-      o[6] += wq * v[it][q][1].z;
-      o[7] += wq * v[it][q][1].w;
+      const uint4 h = v[it][q];
+      o[0] += wq * half_lo(h.x);
+      o[1] += wq * half_hi(h.x);
+      o[2] += wq * half_lo(h.y);
+      o[3] += wq * half_hi(h.y);
+      o[4] += wq * half_lo(h.z);
+      o[5] += wq * half_hi(h.z);
+      o[6] += wq * half_lo(h.w);
+      o[7] += wq * half_hi(h.w);
     }
     const float inv = inv_den[j];
 #pragma unroll
@@ -511,6 +525,8 @@ __global__ __launch_bounds__(64 * NWV, 2) void k_tree_attn(AttnArgs a) {
   // (distinct LDS banks) and write consecutive 32-byte units
   for (int u = threadIdx.x; u < 32 * (HD / 8); u += NT) {
     const int j = u & 31, d0 = 8 * (u >> 5);
+    const float l = colm[j][1];
+    const float inv = l > 0.f ? 1.f / l : 0.f;
     float o[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -518,11 +534,10 @@ __global__ __launch_bounds__(64 * NWV, 2) void k_tree_attn(AttnArgs a) {
       float x = 0.f;
 #pragma unroll
       for (int q = 0; q < NWV; ++q) x += wgt[q][j] * so[q * E + e];
-      o[i] = x;
+      o[i] = x * inv;
     }
-    float* dst = a.part_o + (item0 + c) * E + 8 * u;
-    *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
-    *reinterpret_cast<float4*>(dst + 4) = make_float4(o[4], o[5], o[6], o[7]);
+    uint16_t* dst = reinterpret_cast<uint16_t*>(a.part_o) + (item0 + c) * E + 8 * u;
+    *reinterpret_cast<uint4*>(dst) = pack_half8(o);
   }
   if (threadIdx.x < 32) {
     a.part_ml[(item0 + c) * 64 + 2 * threadIdx.x] = colm[threadIdx.x][0];

@@ -152,7 +152,7 @@ struct AttnArgs {
   const uint64_t* mask;   // [n_seq*nq] region masks (tree mode)
   int S, H, KV, hd, nq, n_seq;
   int n_chunks, chunk_keys, qtiles;  // chunk_keys: multiple of 128 (tree mode)
-  float* part_o;          // [items][32*hd] partial outputs (tree mode, n_chunks > 1)
+  float* part_o;          // [items][32*hd] float16 partial outputs (tree mode, n_chunks > 1)
   float* part_ml;         // [items][32][2]
   int* att_cnt;           // [items] chunk arrivals (zero between launches)
   uint16_t* out;          // [n_seq*nq] split rows of H*hd
