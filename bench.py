@@ -135,8 +135,7 @@ def cpu_baseline(wl, w, dr, budget_s):
             break
     threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
     return {"value": emitted / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "precision": "float64 (the oracle's arithmetic, stricter than the float32 of the "
-                         "baseline plan)",
+            "precision": "float64 (the oracle's arithmetic)",
             "sample": f"{cycles} MSD cycle(s) of the same workload (draft tree + tree verify "
                       f"at L={L} + accept) from a seeded synthetic cache state; "
                       f"{el:.1f} s, {el / cycles * 1e3:.0f} ms/cycle"}

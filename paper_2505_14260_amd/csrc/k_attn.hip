@@ -546,13 +546,29 @@ __global__ __launch_bounds__(64 * NWV, 2) void k_tree_attn(AttnArgs a) {
   // The workgroup that finishes the item's last chunk merges them.  Every
   // chunk of the item runs on this XCD, so its partial is in this XCD's L2
   // once the stores are acknowledged: each thread waits for its own, the
-  // barrier for all, and the arrival count is taken after that.
+  // barrier for all, and the arrival count is taken after that.  The count
+  // keeps one 4-bit field per XCD (read from the XCC_ID hardware register),
+  // so the last arrival also sees whether every chunk ran on one XCD; if
+  // not, the merge may have read another L2's stale lines and place_err is
+  // raised for the host to report.
   __builtin_amdgcn_s_waitcnt(0);
   lds_barrier();
   if (threadIdx.x == 0) {
-    const int prev = __hip_atomic_fetch_add(a.att_cnt + item, 1, __ATOMIC_RELAXED,
-                                            __HIP_MEMORY_SCOPE_AGENT);
-    last = prev == a.n_chunks - 1;
+    unsigned xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const unsigned mine = 1u << (4 * (xcc & 7));
+    const unsigned now = __hip_atomic_fetch_add(reinterpret_cast<unsigned*>(a.att_cnt + item), mine,
+                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) +
+                         mine;
+    int total = 0, xcds = 0;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const int n = (now >> (4 * x)) & 15;
+      total += n;
+      xcds += n != 0;
+    }
+    last = total == a.n_chunks;
+    if (last && xcds != 1) __hip_atomic_store(a.place_err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   lds_barrier();
   if (!last) return;

@@ -194,6 +194,7 @@ struct msd_ctx {
   GemmScratch gs;
   float *att_po, *att_ml, *tk_scratch;
   int* att_cnt;
+  int* att_place;  // tree attention merged chunks that ran on different XCDs
   float2* rope;
   int visual_input = MSD_DRAFT_VISUAL_EMBEDDING;  // draft input of visual prompt rows
   int device;            // the GPU current at msd_create
@@ -327,6 +328,7 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->att_po = cv.take<float>(p.attn_floats);
   t->att_ml = cv.take<float>(p.attn_floats / m.head_dim * 2 + 64);
   t->att_cnt = cv.take<int>(p.att_items);
+  t->att_place = cv.take<int>(1);
   t->rope = cv.take<float2>((size_t)lim.max_seq * (m.head_dim / 2));
   t->tk_scratch = cv.take<float>(topk_scratch_floats(p.lrows, m.vocab));
   return cv.off + 256;
@@ -531,6 +533,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     a.part_o = c->att_po;
     a.part_ml = c->att_ml;
     a.att_cnt = c->att_cnt;
+    a.place_err = c->att_place;
     if (tree_R < 0) {
       a.qtiles = (nq + 31) / 32;
       a.n_chunks = 1;
@@ -742,8 +745,18 @@ int finish_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, int T, int32_t* 
                          hipMemcpyDeviceToHost, c->st));
   HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8 + 8, c->tree_err, sizeof(int) * n_seq,
                          hipMemcpyDeviceToHost, c->st));
+  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8 + 16, c->att_place, sizeof(int),
+                         hipMemcpyDeviceToHost, c->st));
   HIPC(c, hipStreamSynchronize(c->st));
   c->verified_T = 0;
+  if (back[MSD_MAX_TREE * 8 + 16]) {
+    HIPC(c, hipMemsetAsync(c->att_place, 0, sizeof(int), c->st));
+    HIPC(c, hipStreamSynchronize(c->st));
+    return fail(c, MSD_ERR_HIP,
+                "tree attention found the key chunks of one item on different XCDs (the "
+                "workgroup placement its in-L2 merge relies on); results since the last "
+                "acceptance are unreliable");
+  }
   for (int i = 0; i < n_seq; ++i)
     if (back[MSD_MAX_TREE * 8 + 8 + i]) {
       // the kernels accepted nothing for any sequence of the call
@@ -860,6 +873,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     HIPC(c, hipMemsetAsync(c->d_root, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->tree_err, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->att_cnt, 0, sizeof(int) * c->plan.att_items, c->st));
+    HIPC(c, hipMemsetAsync(c->att_place, 0, sizeof(int), c->st));
     HIPC(c, hipMemsetAsync(c->gemm_zero, 0, sizeof(uint16_t) * gemm_dummy_elems(), c->st));
     launch_rope_table(c->rope, lim->max_seq, m->head_dim, (double)m->rope_theta, c->st);
     LAUNCHED(c);

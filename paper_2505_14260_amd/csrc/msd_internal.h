@@ -154,7 +154,8 @@ struct AttnArgs {
   int n_chunks, chunk_keys, qtiles;  // chunk_keys: multiple of 128 (tree mode)
   float* part_o;          // [items][32*hd] float16 partial outputs (tree mode, n_chunks > 1)
   float* part_ml;         // [items][32][2]
-  int* att_cnt;           // [items] chunk arrivals (zero between launches)
+  int* att_cnt;           // [items] chunk arrivals per XCD (zero between launches)
+  int* place_err;         // set to 1 when an item's chunks ran on more than one XCD
   uint16_t* out;          // [n_seq*nq] split rows of H*hd
   float scale;
 };
