@@ -263,7 +263,17 @@ MSD_DEV void store_x(uint4* xs, const uint4 (&xh)[XB], const uint4 (&xl)[XB], in
 // workgroup restages X in LDS; waiting for those loads also waits for the
 // ring's, once per workgroup.  Slots for tiles past the workgroup's last and
 // blocks past K read the zero block.
-template <int MT, int NW, int NKB, int P, int NT>
+//
+// BO (block outer): within each chunk the sequence runs block by block over
+// the tiles, so a block's X fragments are read from LDS once for all of the
+// workgroup's tiles instead of once per tile.  Every output element sums the
+// same products in the same order either way.  It pays at 64 rows, where
+// the per-tile fragment reads (eight 16-byte LDS reads per MFMA row tile and
+// K step) held the kernel back: 61-row q/k/v 30.5 -> 25.2 us, down
+// 30.4 -> 24.9 us, gate+up 44.8 -> 41.5 us (7B-shaped), 64-row down
+// 43.8 -> 34.7 us (Qwen-shaped); the fragments' registers make the SwiGLU
+// pair spill from four tiles per workgroup on.
+template <int MT, int NW, int NKB, int P, int NT, bool BO>
 __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
   static_assert(NKB % P == 0, "ring slots must divide the chunk");
   extern __shared__ uint4 xs[];
@@ -281,9 +291,12 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
   const uint16_t* const W2 = a.W2;
   const size_t lane_off = (size_t)wave * (BLOCK_ELEMS / 4) + lane * 8;
   const uint16_t* const dummy = a.dummy + lane_off;
-  // element offset of sequence block q, or -1 for the zero block
+  // element offset of sequence block q, or -1 for the zero block; the
+  // sequence of chunk half h is tile by tile (q = (h NT + j) NKB + p), or
+  // block by block with BO (q = (h NKB + p) NT + j)
   auto block_off = [&](int q) -> long long {
-    const int h = q / (NT * NKB), j = (q / NKB) % NT, p = q % NKB;
+    const int h = q / (NT * NKB);
+    const int j = BO ? q % NT : (q / NKB) % NT, p = BO ? (q / NT) % NKB : q % NKB;
     const int kb = kb0 + h * NKB + p;
     if (q >= SEQ || j >= n_my || kb >= nkt) return -1;
     return ((long long)(gi + j * G) * nkt + kb) * BLOCK_ELEMS + (long long)lane_off;
@@ -330,45 +343,54 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
       }
       lds_barrier();
     }
-#pragma unroll
-    for (int j = 0; j < NT; ++j)
+#define MSD_GEMM2_STEP(Q, J)                                                                  \
+  {                                                                                          \
+    const int q_ = (Q), j_ = (J), r_ = q_ % P;                                               \
+    _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                          \
+      _Pragma("unroll") for (int w = 0; w < NW; ++w)                                         \
+      _Pragma("unroll") for (int t = 0; t < MT; ++t)                                         \
+        acc[j_][w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(                             \
+            as_bf16x8(ring[r_][w][c]), as_bf16x8(fh[t][c]), acc[j_][w][t], 0, 0, 0);         \
+      _Pragma("unroll") for (int w = 0; w < NW; ++w)                                         \
+      _Pragma("unroll") for (int t = 0; t < MT; ++t)                                         \
+        acc[j_][w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(                             \
+            as_bf16x8(ring[r_][w][c]), as_bf16x8(fl[t][c]), acc[j_][w][t], 0, 0, 0);         \
+    }                                                                                        \
+    const long long o_ = block_off(q_ + P);                                                  \
+    const uint16_t* const b1 = o_ >= 0 ? W + o_ : dummy;                                     \
+    const uint16_t* const b2 = o_ >= 0 ? W2 + o_ : dummy;                                    \
+    _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                          \
+      ring[r_][0][c] = load_stream(b1 + c * 512);                                            \
+      if (NW == 2) ring[r_][NW - 1][c] = load_stream(b2 + c * 512);                          \
+    }                                                                                        \
+  }
+#define MSD_GEMM2_FRAGS(PB)                                                                  \
+  _Pragma("unroll") for (int t = 0; t < MT; ++t)                                             \
+  _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                            \
+    const int xi = xs_index(t * 16 + i, (PB) * 16 + 4 * g + c, UPR);                         \
+    fh[t][c] = xs[xi];                                                                       \
+    fl[t][c] = xs[LO + xi];                                                                  \
+  }
+    if constexpr (BO) {
 #pragma unroll
       for (int p = 0; p < NKB; ++p) {
-        const int q = (h * NT + j) * NKB + p;
-        const int r = q % P;
         uint4 fh[MT][4], fl[MT][4];
+        MSD_GEMM2_FRAGS(p)
 #pragma unroll
-        for (int t = 0; t < MT; ++t)
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const int xi = xs_index(t * 16 + i, p * 16 + 4 * g + c, UPR);
-            fh[t][c] = xs[xi];
-            fl[t][c] = xs[LO + xi];
-          }
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-#pragma unroll
-          for (int w = 0; w < NW; ++w)
-#pragma unroll
-            for (int t = 0; t < MT; ++t)
-              acc[j][w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  as_bf16x8(ring[r][w][c]), as_bf16x8(fh[t][c]), acc[j][w][t], 0, 0, 0);
-#pragma unroll
-          for (int w = 0; w < NW; ++w)
-#pragma unroll
-            for (int t = 0; t < MT; ++t)
-              acc[j][w][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  as_bf16x8(ring[r][w][c]), as_bf16x8(fl[t][c]), acc[j][w][t], 0, 0, 0);
-        }
-        const long long o = block_off(q + P);
-        const uint16_t* const b1 = o >= 0 ? W + o : dummy;
-        const uint16_t* const b2 = o >= 0 ? W2 + o : dummy;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          ring[r][0][c] = load_stream(b1 + c * 512);
-          if (NW == 2) ring[r][NW - 1][c] = load_stream(b2 + c * 512);
-        }
+        for (int j = 0; j < NT; ++j) MSD_GEMM2_STEP((h * NKB + p) * NT + j, j)
       }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int p = 0; p < NKB; ++p) {
+          uint4 fh[MT][4], fl[MT][4];
+          MSD_GEMM2_FRAGS(p)
+          MSD_GEMM2_STEP((h * NT + j) * NKB + p, j)
+        }
+    }
+#undef MSD_GEMM2_STEP
+#undef MSD_GEMM2_FRAGS
   }
   const int ldp = a.ldp, off2 = a.off2;
   float* const part = a.part + (size_t)s * a.part_split;
@@ -599,12 +621,14 @@ template <int MT, int NW, int NT>
 void launch_pair(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
   constexpr int P = RING;
   constexpr int NKB = chunk_blocks(MT);
+  // block outer at 64 rows, but for the SwiGLU pair from four tiles on
+  constexpr bool BO = MT == 4 && (NW == 1 || NT <= 3);
   const size_t lds = (size_t)MT * 16 * NKB * KB * 4;
   if (sc.ev_start)
-    hipExtLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT>), grid, dim3(256), lds, st, sc.ev_start,
+    hipExtLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT, BO>), grid, dim3(256), lds, st, sc.ev_start,
                           sc.ev_stop, 0, a);
   else
-    hipLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT>), grid, dim3(256), lds, st, a);
+    hipLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT, BO>), grid, dim3(256), lds, st, a);
 }
 
 template <int MT, int NW>
