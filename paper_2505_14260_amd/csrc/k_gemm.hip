@@ -45,6 +45,9 @@ constexpr int BLOCK_ELEMS = TILE_ROWS * KB;
 constexpr int RING = 4;
 __host__ __device__ constexpr int chunk_blocks(int MT) { return MT <= 2 ? 8 : 4; }
 constexpr int PAIR_MAX_TILES = 5;  // tiles per workgroup of the two-chunk kernel
+// tiles per workgroup of the full-K kernel (k_gemm_fk): launched with 8 or
+// 10 (the registers of twelve tiles' accumulators spill)
+constexpr int FK_MIN_TILES = 8, FK_MAX_TILES = 10;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 MSD_DEV uint4 load_stream(const uint16_t* p) {
@@ -410,6 +413,133 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
   }
 }
 
+// Full-K variant for the widest single weights at 64 rows (LM heads of large
+// vocabularies, many tiles per workgroup): every workgroup covers all of K
+// for NT tiles, chunk by chunk, restaging X in LDS at each chunk and keeping
+// the tiles' accumulators in registers throughout.  It writes one partial
+// per tile (S = 1), where the chunked kernels write one per K chunk: at the
+// Qwen2-VL-7B-shaped LM head that is 39 MB instead of 272 MB per 64 rows,
+// and as much less for the consumer to read.
+//
+// With ten tiles' accumulators the X fragments of a whole block no longer
+// fit beside them, so a block is taken in two halves of its K steps (MFMA
+// steps c = 0, 1 and c = 2, 3), and the register ring holds half blocks:
+// 2P of them, as many bytes in flight as P whole blocks.  The ring runs
+// half by half over the tiles, q = ((c NKB + p) 2 + hf) NT + j, so one half's
+// fragments are read from LDS once for all NT tiles; 2 NKB NT is a multiple
+// of 2P, so every chunk uses the same ring slots.  A half block is two
+// 1 KB contiguous loads per wave.  Each restage waits for the ring's loads
+// in flight (loads complete in order), once per chunk.
+template <int MT, int NKB, int P, int NT>
+__global__ __launch_bounds__(256) void k_gemm_fk(GemmArgs a) {
+  constexpr int PH = 2 * P;           // half-block ring slots
+  constexpr int CSEQ = 2 * NKB * NT;  // half blocks per chunk
+  static_assert(CSEQ % PH == 0, "every chunk must start at ring slot 0");
+  extern __shared__ uint4 xs[];
+  constexpr int UPR = NKB * KB / 8;
+  constexpr int LO = MT * 16 * UPR;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane & 15, g = lane >> 4;
+  const int G = a.G, M = a.M, nkt = a.nkt, n_tiles = a.n_tiles;
+  const int gi = blockIdx.x;
+  const int n_my = gi < n_tiles ? min(NT, (n_tiles - gi + G - 1) / G) : 0;
+  if (n_my == 0) return;
+  const int n_ch = (nkt + NKB - 1) / NKB;
+  const uint16_t* const W = a.W;
+  const size_t lane_off = (size_t)wave * (BLOCK_ELEMS / 4) + lane * 8;
+  const uint16_t* const dummy = a.dummy + lane_off;
+  // element offset of sequence half block q, or -1 for the zero block
+  auto half_off = [&](int q) -> long long {
+    const int c = q / CSEQ, r = q - c * CSEQ;
+    const int ph = r / NT, j = r - ph * NT;
+    const int kb = c * NKB + (ph >> 1);
+    if (j >= n_my || kb >= nkt) return -1;
+    return ((long long)(gi + j * G) * nkt + kb) * BLOCK_ELEMS + (long long)lane_off +
+           (ph & 1) * 1024;
+  };
+  constexpr int NX = MT * 16 * UPR / 256;
+  static_assert(NX == 16, "X staging assumes 16 units per thread");
+  uint4 xh[NX], xl[NX];
+  load_x<MT, NKB, NX>(xh, xl, a.X, a.ldx, M, a.K, 0, 0);
+  uint4 ring[PH][2];
+#pragma unroll
+  for (int q = 0; q < PH; ++q) {
+    const long long o = half_off(q);
+    const uint16_t* const b = o >= 0 ? W + o : dummy;
+    ring[q][0] = load_stream(b);
+    ring[q][1] = load_stream(b + 512);
+  }
+  store_x<MT, NKB, NX>(xs, xh, xl, 0);
+  __syncthreads();
+  f32x4 acc[NT][MT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+  for (int ch = 0; ch < n_ch; ++ch) {
+    if (ch > 0) {
+      // the chunk's X: loads before the barrier (every wave done with the
+      // previous chunk), LDS writes after
+      constexpr int XB = NX / 2;
+#pragma unroll
+      for (int q0 = 0; q0 < NX; q0 += XB) {
+        uint4 yh[XB], yl[XB];
+        load_x<MT, NKB, XB>(yh, yl, a.X, a.ldx, M, a.K, ch * NKB, q0);
+        if (q0 == 0) lds_barrier();
+        store_x<MT, NKB, XB>(xs, yh, yl, q0);
+      }
+      lds_barrier();
+    }
+#pragma unroll
+    for (int ph = 0; ph < 2 * NKB; ++ph) {
+      const int p = ph >> 1, hf = ph & 1;
+      uint4 fh[MT][2], fl[MT][2];
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int xi = xs_index(t * 16 + i, p * 16 + 4 * g + 2 * hf + c, UPR);
+          fh[t][c] = xs[xi];
+          fl[t][c] = xs[LO + xi];
+        }
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int r = (ph * NT + j) % PH;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+#pragma unroll
+          for (int t = 0; t < MT; ++t)
+            acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                as_bf16x8(ring[r][c]), as_bf16x8(fh[t][c]), acc[j][t], 0, 0, 0);
+#pragma unroll
+          for (int t = 0; t < MT; ++t)
+            acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                as_bf16x8(ring[r][c]), as_bf16x8(fl[t][c]), acc[j][t], 0, 0, 0);
+        }
+        const long long o = half_off(ch * CSEQ + ph * NT + j + PH);
+        const uint16_t* const b = o >= 0 ? W + o : dummy;
+        ring[r][0] = load_stream(b);
+        ring[r][1] = load_stream(b + 512);
+      }
+    }
+  }
+  const int ldp = a.ldp;
+  float* const part = a.part;
+  float* const sink = a.sink + lane * 4;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int n = (gi + j * G) * TILE_ROWS + wave * 16 + 4 * g;
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const int m = t * 16 + i;
+      float* dst = (m < M && j < n_my) ? part + (size_t)m * ldp + n : sink;
+      *reinterpret_cast<float4*>(dst) =
+          make_float4(acc[j][t][0], acc[j][t][1], acc[j][t][2], acc[j][t][3]);
+    }
+  }
+}
+
 // Many-row GEMM (prompt rows, large batches): a (64 NB) x 128 output tile
 // per workgroup over all of K, both operands staged through LDS.
 //
@@ -631,6 +761,18 @@ void launch_pair(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_
     hipLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT, BO>), grid, dim3(256), lds, st, a);
 }
 
+template <int NT>
+void launch_fk(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
+  constexpr int MT = 4, P = RING;
+  constexpr int NKB = chunk_blocks(MT);
+  const size_t lds = (size_t)MT * 16 * NKB * KB * 4;
+  if (sc.ev_start)
+    hipExtLaunchKernelGGL((k_gemm_fk<MT, NKB, P, NT>), grid, dim3(256), lds, st, sc.ev_start,
+                          sc.ev_stop, 0, a);
+  else
+    hipLaunchKernelGGL((k_gemm_fk<MT, NKB, P, NT>), grid, dim3(256), lds, st, a);
+}
+
 template <int MT, int NW>
 void launch_pair_nt(int nt, dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
   if (nt == 1) launch_pair<MT, NW, 1>(grid, a, sc, st);
@@ -739,6 +881,21 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
       p.per = per2;
     }
   }
+  // Full K per workgroup for the widest single weights at 64 rows: when
+  // every workgroup would take FK_MIN_TILES tiles or more at one chunk each,
+  // the X restage per chunk costs less than the chunk partials it saves
+  p.fk = 0;
+  if (p.MT == 4 && nw == 1) {
+    int nt = (p.n_tiles + target_wgs - 1) / target_wgs;
+    nt = (nt + 1) / 2 * 2;  // launched tile counts are even
+    if (nt >= FK_MIN_TILES && nt <= FK_MAX_TILES) {
+      p.fk = nt;
+      p.pair = 0;
+      p.S = 1;
+      p.G = (p.n_tiles + nt - 1) / nt;
+      p.per = nt;
+    }
+  }
   p.nw = nw;
   p.ldp = p.n_tiles * TILE_ROWS * nw;
   p.off2 = p.n_tiles * TILE_ROWS;
@@ -773,6 +930,11 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
   a.sink = sink;
   a.dummy = dummy;
   const dim3 grid(pl.S * pl.G);
+  if (pl.fk) {
+    if (pl.fk == 8) launch_fk<8>(grid, a, sc, st);
+    else launch_fk<10>(grid, a, sc, st);
+    return;
+  }
   if (pl.pair) {
     if (pl.MT == 2 && nw == 2) launch_pair_nt<2, 2>(pl.per, grid, a, sc, st);
     else if (pl.MT == 2) launch_pair_nt<2, 1>(pl.per, grid, a, sc, st);

@@ -75,6 +75,7 @@ struct GemmArgs {
 struct GemmPlan {
   int MT, nkb, S, G, nw, n_tiles, nkt, ldp, off2;
   int pair;  // two K chunks per workgroup (S counts chunk pairs)
+  int fk;    // > 0: all of K per workgroup for fk tiles (S = 1)
   int per;   // tiles per workgroup
 };
 
