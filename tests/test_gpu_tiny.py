@@ -130,6 +130,51 @@ def test_prefill_many_rows_wide(n_visual):
         eng.close()
 
 
+def test_wide_vocab_lm_head_full_k():
+    """A 152,064-word vocabulary at d_model 1024: three sequences' 15-node
+    trees make a 45-row verify whose LM head takes the full-K GEMM (ten
+    tiles per workgroup, X restaged for each of two K chunks, one partial per
+    tile); its logits and argmax against the oracle on the GPU's trees."""
+    import dataclasses
+    from paper_2505_14260_amd.msd import Engine
+    from parity import oracle_tree_of
+    wl = dataclasses.replace(WIDE, dims=dataclasses.replace(WIDE.dims, vocab=152064),
+                             n_visual=24, n_text=12)
+    dims = wl.dims
+    print(f"case: verify {wl.name} vocab {dims.vocab}, batch 3", flush=True)
+    w = synth.make_target_weights(dims, wl.seed)
+    dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
+    prompts = [synth.make_prompt(wl, seq=b) for b in range(3)]
+    m = O.Models(dims, w, dr)
+    spec, _ = static_spec(wl.tree.paths)
+    T = spec.n_nodes + 1
+    max_seq = 256
+    eng = Engine(dims, w, dr, max_batch=3, max_seq=max_seq, max_tree=64,
+                 max_prompt=wl.prompt_len)
+    try:
+        for b in range(3):
+            eng.prefill(b, *prompts[b])
+        trees = eng.new_trees(3)
+        eng.draft_tree([0, 1, 2], spec, trees)
+        amax, logits = eng.verify([0, 1, 2], trees, T, want_logits=True)
+        torch.cuda.synchronize()
+        lg = logits.cpu().numpy().reshape(3, T, -1)
+        am = amax.cpu().numpy().reshape(3, T)
+        gts = eng.trees_to_host(trees, 3)
+        worst = 0.0
+        for b in range(3):
+            st, _, _, _ = O.prefill(m, *prompts[b], max_slots=max_seq)
+            _, lg_ref = O.verify(m, st, oracle_tree_of(gts[b]))
+            ok, err = row_close(lg[b], lg_ref)
+            assert ok, (b, err)
+            for i in range(T):
+                assert argmax_ok(am[b, i], lg_ref[i]), (b, i)
+            worst = max(worst, err)
+        print(f"logits max rel err {worst:.2e}")
+    finally:
+        eng.close()
+
+
 def test_max_width_model():
     """d_model 8192, the library's limit (whole-row kernels at two 16-byte
     units per thread), with 8-way GQA: the prompt forward's K/V, first token
