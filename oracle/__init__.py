@@ -21,6 +21,10 @@ order the paper gives them:
             SplitMix64 draws.
   metrics.py the expected-tokens closed form omega(gamma, alpha) and the
             speedup model of Sec. 5.1.3.
+  train.py  the draft-head training step of Sec. 4.2 (teacher-forced draft
+            forward, feature-regression + token loss, AdamW, cosine schedule,
+            the progressive data mix of Eq. progressive_data), in float64
+            PyTorch on the CPU with autograd gradients.
 """
 import ctypes
 import os

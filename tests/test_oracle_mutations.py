@@ -22,11 +22,13 @@ from oracle import metrics as MET  # noqa: E402
 from oracle import model as M  # noqa: E402
 from oracle import msd as O  # noqa: E402
 from oracle import sampling as S  # noqa: E402
+from oracle import train as TR  # noqa: E402
 
 import test_oracle_draft_pins as PD  # noqa: E402
 import test_oracle_invariants as PI  # noqa: E402
 import test_oracle_primitives as PP  # noqa: E402
 import test_oracle_sampling as PS  # noqa: E402
+import test_oracle_train as PTR  # noqa: E402
 import test_oracle_trees as PT  # noqa: E402
 
 
@@ -257,6 +259,32 @@ SOURCE_CASES = [
     ("final_order_by_score", O, "select_dynamic_tree",
      "key=lambda i: (pool[i][2], i))", "key=lambda i: (pool[i][2], -pool[i][3]))",
      beam_pins),
+    # training: the draft output is regressed on its own position's feature
+    ("train_target_not_shifted", TR, "row_losses",
+     "diff = d - h[1:]", "diff = d - h[:-1]",
+     lambda: [PTR.test_loss_assembly_closed_form]),
+    # training: the token term against the distribution of the wrong row
+    ("train_labels_not_shifted", TR, "row_losses",
+     "pt[1:]", "pt[:-1]", lambda: [PTR.test_loss_assembly_closed_form]),
+    # training: SmoothL1 without its one-half in the quadratic zone
+    ("train_smooth_l1_quadratic", TR, "row_losses",
+     "0.5 * diff * diff", "diff * diff", lambda: [PTR.test_loss_assembly_closed_form]),
+    # training: the token term at full weight
+    ("train_token_weight", TR, "sequence_loss_sum",
+     "reg + CLS_WEIGHT * cls", "reg + cls", lambda: [PTR.test_batch_loss_weights_and_means]),
+    # training: text rows concatenate their own embedding, not the next one
+    ("train_input_embedding", TR, "draft_inputs",
+     "torch.cat([h[:R], e[1:]], dim=1)", "torch.cat([h[:R], e[:R]], dim=1)",
+     lambda: [PTR.test_draft_inputs_follow_decoupled_rule]),
+    # AdamW without bias correction
+    ("adam_without_bias_correction", TR, "AdamW",
+     "(self.m[k] / c1) / (np.sqrt(self.v[k] / c2) + ADAM_EPS)",
+     "self.m[k] / (np.sqrt(self.v[k]) + ADAM_EPS)",
+     lambda: [PTR.test_adamw_first_step_and_schedule]),
+    # the progressive mix runs backwards (visual share (T - t) / T)
+    ("mix_reversed", TR, "progressive_counts",
+     "n_per_epoch * epoch / n_epochs", "n_per_epoch * (n_epochs - epoch) / n_epochs",
+     lambda: [lambda: PTR.test_progressive_mix_counts(5)]),
 ]
 
 
