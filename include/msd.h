@@ -317,6 +317,54 @@ int msd_set_state(msd_ctx* ctx, int seq, int L, const void* h_d, int32_t next_to
  * n = key slots of the longest sequence including the tree, k = key chunks).
  */
 /*
+ * Draft-head training (Sec. 4.2: the one-layer draft learns from the frozen
+ * target; the data schedule is Eq. progressive_data).  The paper leaves the
+ * loss and optimiser to the feature-level draft it builds on; this library
+ * reads them as follows.  On a training sequence of n positions (tokens,
+ * visual flags and visual rows as for msd_prefill) the target's features
+ * h_0..h_{n-1} (final-norm outputs) are computed; the draft's input rows
+ * i = 0..n-2 follow the decoupled rule (Eq. decouple: text rows
+ * f_down(Concat(h_i, e_{i+1})), visual rows e_i) and the draft layer runs
+ * causally over them at positions i; its output d_i is trained toward
+ * h_{i+1}:
+ *   loss_i = mean_k SmoothL1(d_i - h_{i+1})_k
+ *            + 0.1 CE(softmax(W_lm h_{i+1}), softmax(W_lm d_i)),
+ * with SmoothL1's beta = 1 and the cross-entropy against the target's full
+ * next-token distribution.  A batch's loss is the mean of loss_i over all
+ * rows of its sequences.  Trained: f_down, the draft layer's seven matrices
+ * and two norm gains (float32 master copies); the embedding table and the
+ * LM head stay frozen.  Arithmetic in float32 (the contractions on rocBLAS).
+ *
+ * msd_train_accumulate adds one sequence's gradient sums and writes its
+ * loss sums to loss_h[3] (total, regression part, token part, each summed
+ * over its n - 1 rows).  It runs the target over the sequence in slot `seq`
+ * (2 <= n <= max_prompt): the slot's cache is overwritten and the slot must
+ * be prefilled again before decoding.  The first training call allocates
+ * the training state (device memory of its own, freed by msd_destroy).
+ * msd_train_apply performs one AdamW step (beta1 0.9, beta2 0.999, eps 1e-8,
+ * no weight decay) with the mean gradient over the accumulated rows and
+ * learning rate lr, refreshes the draft the decoder uses (its packed
+ * weights, and from the first training call on the draft's norm gains are
+ * read from the library's copy), and clears the sums; MSD_ERR_INVALID_ARG
+ * when nothing was accumulated.  msd_train_read copies the float32 gradient
+ * sums (what = 0) or master parameters (what = 1), concatenated row-major in
+ * the order f_down [d][2d], wq [H hd][d], wk [KV hd][d], wv [KV hd][d],
+ * wo [d][H hd], w_gate [F][d], w_up [F][d], w_down [d][F], attn_norm [d],
+ * ffn_norm [d], to the device buffer out_d of exactly that many floats.
+ * msd_train_lr gives the cosine schedule lr_max (1 + cos(pi step / total)) / 2
+ * (0 <= step <= total); msd_train_mix gives the text-only and visual sample
+ * counts of epoch t of T in stage 2 (Eq. progressive_data: a visual share of
+ * t / T of n_per_epoch, rounded to the nearest integer, ties to even).
+ * Errors: MSD_ERR_INVALID_ARG (arguments), MSD_ERR_HIP (device or rocBLAS).
+ */
+int msd_train_accumulate(msd_ctx* ctx, int seq, int n, const int32_t* tokens_h,
+                         const uint8_t* is_visual_h, const void* visual_d, double* loss_h);
+int msd_train_apply(msd_ctx* ctx, double lr);
+int msd_train_read(msd_ctx* ctx, int what, float* out_d, size_t n_floats);
+int msd_train_lr(int step, int total_steps, double lr_max, double* lr_out);
+int msd_train_mix(int epoch, int n_epochs, int n_per_epoch, int* n_text_out, int* n_visual_out);
+
+/*
  * Diagnostic for measurement tools: one kernel that reads `bytes` of the
  * device buffer buf_d (16-byte aligned, zero-filled, bytes a multiple of
  * 64 KiB) with the access pattern of the library's weight stream (every wave

@@ -5,7 +5,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["msd_api.hip", "k_gemm.hip", "k_attn.hip", "k_rows.hip", "k_tree.hip", "k_sample.hip"]
+SOURCES = ["msd_api.hip", "k_gemm.hip", "k_attn.hip", "k_rows.hip", "k_tree.hip", "k_sample.hip",
+           "k_train.hip"]
 LIB = os.path.join(HERE, "libmsd.so")
 ARCH = os.environ.get("MSD_OFFLOAD_ARCH", "gfx950")
 
@@ -22,7 +23,7 @@ def build(verbose=False):
         subprocess.check_call(cmd, stderr=None if verbose else subprocess.DEVNULL
                               if os.environ.get("MSD_QUIET_BUILD") else None)
         objs.append(obj)
-    cmd = ["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", LIB] + objs
+    cmd = ["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", LIB] + objs + ["-lrocblas"]
     subprocess.check_call(cmd)
     return LIB
 

@@ -733,6 +733,23 @@ __global__ void k_pack(const uint16_t* src, int N, int K, int nkt, size_t units,
   *reinterpret_cast<uint4*>(dst + q * 8) = v;
 }
 
+// The inverse of k_pack: row-major bf16 [N][K] from the packed layout.
+__global__ void k_unpack(const uint16_t* src, int N, int K, int nkt, size_t units, uint16_t* dst) {
+  const size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= units) return;
+  const int lane = (int)(q & 63);
+  const size_t r = q >> 6;
+  const int c = (int)(r & 3), wave = (int)((r >> 2) & 3);
+  const size_t blk = r >> 4;
+  const int kb = (int)(blk % nkt);
+  const int t = (int)(blk / nkt);
+  const int row = t * TILE_ROWS + wave * 16 + (lane & 15);
+  const int col = kb * KB + 32 * (lane >> 4) + 8 * c;
+  if (row < N && col < K)
+    *reinterpret_cast<uint4*>(dst + (size_t)row * K + col) =
+        *reinterpret_cast<const uint4*>(src + q * 8);
+}
+
 // With timing events the launch carries them in its dispatch packet, so they
 // bracket the kernel's execution only.
 template <int MT, int NW>
@@ -818,6 +835,13 @@ void launch_stream_read(const uint16_t* buf, size_t spans, int wgs, unsigned* si
 }
 
 size_t gemm_dummy_elems() { return (size_t)BLOCK_ELEMS; }
+
+void launch_unpack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t st) {
+  const int nkt = (K + KB - 1) / KB;
+  const size_t units = packed_elems(N, K) / 8;
+  hipLaunchKernelGGL(k_unpack, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, st, src, N, K,
+                     nkt, units, dst);
+}
 
 size_t packed_elems(int N, int K) {
   return (size_t)((N + TILE_ROWS - 1) / TILE_ROWS) * ((K + KB - 1) / KB) * BLOCK_ELEMS;

@@ -10,6 +10,8 @@
 #include <string>
 #include <vector>
 
+#include <rocblas/rocblas.h>
+
 #include "../../include/msd.h"
 #include "msd_internal.h"
 
@@ -161,6 +163,31 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
 
 }  // namespace
 
+// Draft-head training state (Sec. 4.2).  Float32 master copies of the
+// draft's parameters (f_down, the layer's seven matrices, its two norm gains,
+// in that order), their gradient sums and AdamW moments; float32 activations
+// of one training pass of up to max_prompt - 1 rows; a float32 copy of the
+// frozen LM head.  The contractions run as rocBLAS float32 GEMMs on the
+// context's stream, everything else in k_train.hip.
+constexpr int TRAIN_PARAMS = 10;
+constexpr float TRAIN_CLS_WEIGHT = 0.1f;  // weight of the token term
+constexpr float ADAM_B1 = 0.9f, ADAM_B2 = 0.999f, ADAM_EPS = 1e-8f;
+
+struct TrainState {
+  rocblas_handle blas = nullptr;
+  int Rmax = 0;
+  size_t off[TRAIN_PARAMS + 1] = {};  // float offsets of the parameters
+  float *w = nullptr, *g = nullptr, *m = nullptr, *v = nullptr;
+  uint16_t* wb = nullptr;             // bf16 copy of w (inference packing, norm gains)
+  float* lm = nullptr;                // [V][d]
+  float *H, *X0, *E0, *F, *A1, *r1, *Q, *K, *V, *S, *dP, *O, *X1, *A2, *r2, *G, *U, *Mx, *D;
+  float *Ld, *Lt, *dD, *dMx, *dG, *dU, *dA2, *dX1, *dO, *dQ, *dK, *dV, *dA1, *dF;
+  float *reg, *ce;
+  std::vector<void*> allocs;
+  double rows = 0;                    // rows accumulated since the last update
+  int steps = 0;                      // updates applied
+};
+
 struct msd_ctx {
   msd_model_desc m;
   msd_limits lim;
@@ -197,6 +224,7 @@ struct msd_ctx {
   int* att_place;  // tree attention merged chunks that ran on different XCDs
   float2* rope;
   int visual_input = MSD_DRAFT_VISUAL_EMBEDDING;  // draft input of visual prompt rows
+  TrainState* tr = nullptr;  // draft-head training state (from the first training call)
   int device;            // the GPU current at msd_create
   float* noalloc_base;   // that GPU's copy of `scratch`
   // host
@@ -614,6 +642,47 @@ int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const ui
                         c->rows.dst, c->dfeat);
 }
 
+// The target over a prompt (or training sequence) of n rows in sequence slot
+// seq: row descriptors (the draft's next-token rows included), the slot's
+// KV cache rows [0, n) and the final features of every row in c->h.
+int prompt_target(msd_ctx* c, int seq, int n, const int32_t* tokens_h,
+                  const uint8_t* is_visual_h, const void* visual_d) {
+  const int d = c->m.d_model;
+  // row descriptors: tok, vis, pos, slot, seq, hrow, dst, nxt
+  std::vector<int> a(8 * (size_t)n);
+  int* tok = a.data();
+  int* vis = tok + n;
+  int* pos = vis + n;
+  int* slot = pos + n;
+  int* sq = slot + n;
+  int* hrow = sq + n;
+  int* dst = hrow + n;
+  int* nxt = dst + n;
+  for (int i = 0, v = 0; i < n; ++i) {
+    tok[i] = is_visual_h[i] ? 0 : tokens_h[i];
+    vis[i] = is_visual_h[i] ? v++ : -1;
+    pos[i] = slot[i] = i;
+    sq[i] = seq;
+    hrow[i] = i;
+    dst[i] = (i == n - 1) ? seq * FEAT : -1;
+  }
+  for (int i = 0; i < n; ++i)
+    nxt[i] = (i + 1 < n) ? (is_visual_h[i + 1] ? -1 - vis[i + 1] : tokens_h[i + 1]) : 0;
+  int hdr[2] = {0, seq};
+  const size_t nb = sizeof(int) * (size_t)n;
+  TRY(upload_many(c, {{c->rows.tok, tok, nb}, {c->rows.vis, vis, nb}, {c->rows.pos, pos, nb},
+                      {c->rows.slot, slot, nb}, {c->rows.seq, sq, nb}, {c->rows.hrow, hrow, nb},
+                      {c->rows.dst, dst, nb}, {c->nxt, nxt, nb}, {c->prefix, hdr, sizeof(int)},
+                      {c->seq_ids, hdr + 1, sizeof(int)}}));
+  c->seq_ids_h.assign(1, seq);
+  c->att_pre[0] = 0;
+  c->att_keys[0] = n;
+  launch_embed(c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, c->x, c->st);
+  LAUNCHED(c);
+  TRY(norm_rows(c, n, c->layers[0].n1));
+  return forward_layers(c, false, 1, n, -1, n, c->final_norm, c->h, nullptr);
+}
+
 // LM head + top-k (and log-sum-exp) over the rows of c->xb: no final norm.
 int draft_head(msd_ctx* c, int rows, int k) {
   const int d = c->m.d_model, V = c->m.vocab;
@@ -776,6 +845,257 @@ int finish_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, int T, int32_t* 
   return MSD_OK;
 }
 
+// ------------------------------------------------------------------------
+// Draft-head training (Sec. 4.2; the state is TrainState).
+void train_free(TrainState* t) {
+  if (!t) return;
+  for (void* p : t->allocs) (void)hipFree(p);
+  if (t->blas) (void)rocblas_destroy_handle(t->blas);
+  delete t;
+}
+
+// Row-major C[M][N] = alpha op(A) op(B) + beta C (ta: A stored [K][M];
+// tb: B stored [N][K]); rocBLAS is column-major, so it computes the
+// transposed product C^T = op(B)^T op(A)^T.
+int sgemm_rm(msd_ctx* c, bool ta, bool tb, int M, int N, int K, float alpha, const float* A,
+             int lda, const float* B, int ldb, float beta, float* C, int ldc) {
+  const rocblas_status st = rocblas_sgemm(
+      c->tr->blas, tb ? rocblas_operation_transpose : rocblas_operation_none,
+      ta ? rocblas_operation_transpose : rocblas_operation_none, N, M, K, &alpha, B, ldb, A, lda,
+      &beta, C, ldc);
+  if (st != rocblas_status_success)
+    return fail(c, MSD_ERR_HIP, std::string("rocblas_sgemm: ") + rocblas_status_to_string(st));
+  return MSD_OK;
+}
+
+// Shapes [rows][cols] of the draft parameters in training order.
+void train_shapes(const msd_model_desc& m, int (*sh)[2]) {
+  const int d = m.d_model, F = m.ffn_dim, qd = m.n_heads * m.head_dim;
+  const int kd = m.n_kv_heads * m.head_dim;
+  const int s[TRAIN_PARAMS][2] = {{d, 2 * d}, {qd, d}, {kd, d}, {kd, d}, {d, qd},
+                                  {F, d},     {F, d},  {d, F},  {1, d},  {1, d}};
+  for (int i = 0; i < TRAIN_PARAMS; ++i) sh[i][0] = s[i][0], sh[i][1] = s[i][1];
+}
+
+int train_init(msd_ctx* c) {
+  if (c->tr) return MSD_OK;
+  const msd_model_desc& m = c->m;
+  const int d = m.d_model, F = m.ffn_dim, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim;
+  const int V = m.vocab, R = c->lim.max_prompt - 1;
+  TrainState* t = new TrainState;
+  t->Rmax = R;
+  int sh[TRAIN_PARAMS][2];
+  train_shapes(m, sh);
+  for (int i = 0; i < TRAIN_PARAMS; ++i) t->off[i + 1] = t->off[i] + (size_t)sh[i][0] * sh[i][1];
+  const size_t np = t->off[TRAIN_PARAMS];
+  auto take = [&](size_t bytes) -> void* {
+    void* p = nullptr;
+    if (hipMalloc(&p, std::max<size_t>(bytes, 256)) != hipSuccess) return nullptr;
+    t->allocs.push_back(p);
+    return p;
+  };
+  auto f32 = [&](size_t n) { return static_cast<float*>(take(n * sizeof(float))); };
+  t->w = f32(np);
+  t->g = f32(np);
+  t->m = f32(np);
+  t->v = f32(np);
+  t->wb = static_cast<uint16_t*>(take(np * sizeof(uint16_t)));
+  t->lm = f32((size_t)V * d);
+  const size_t Rd = (size_t)R * d, RF = (size_t)R * F, RV = (size_t)R * V;
+  t->H = f32((size_t)(R + 1) * d);
+  t->X0 = f32(2 * Rd);
+  t->E0 = f32(Rd);
+  t->F = f32(Rd);
+  t->A1 = f32(Rd);
+  t->r1 = f32(R);
+  t->Q = f32((size_t)R * H * hd);
+  t->K = f32((size_t)R * KV * hd);
+  t->V = f32((size_t)R * KV * hd);
+  t->S = f32((size_t)H * R * R);
+  t->dP = f32((size_t)H * R * R);
+  t->O = f32((size_t)R * H * hd);
+  t->X1 = f32(Rd);
+  t->A2 = f32(Rd);
+  t->r2 = f32(R);
+  t->G = f32(RF);
+  t->U = f32(RF);
+  t->Mx = f32(RF);
+  t->D = f32(Rd);
+  t->Ld = f32(RV);
+  t->Lt = f32(RV);
+  t->dD = f32(Rd);
+  t->dMx = f32(RF);
+  t->dG = f32(RF);
+  t->dU = f32(RF);
+  t->dA2 = f32(Rd);
+  t->dX1 = f32(Rd);
+  t->dO = f32((size_t)R * H * hd);
+  t->dQ = f32((size_t)R * H * hd);
+  t->dK = f32((size_t)R * KV * hd);
+  t->dV = f32((size_t)R * KV * hd);
+  t->dA1 = f32(Rd);
+  t->dF = f32(Rd);
+  t->reg = f32(R);
+  t->ce = f32(R);
+  for (void* p : t->allocs)
+    if (!p) {
+      train_free(t);
+      return fail(c, MSD_ERR_HIP, "training buffers: hipMalloc failed");
+    }
+  if (rocblas_create_handle(&t->blas) != rocblas_status_success ||
+      rocblas_set_stream(t->blas, c->st) != rocblas_status_success) {
+    train_free(t);
+    return fail(c, MSD_ERR_HIP, "rocblas handle");
+  }
+  c->tr = t;
+  // the draft's parameters from the packed copies the decoder uses (and the
+  // norm gains); from here on the decoder reads the gains from wb
+  const PackedLayer& pl = c->pdlayer;
+  const size_t pq = packed_elems(H * hd, d), pk = packed_elems(KV * hd, d);
+  const uint16_t* packed[7] = {c->fc_p, pl.qkv, pl.qkv + pq, pl.qkv + pq + pk, pl.o, pl.g, pl.u};
+  for (int i = 0; i < 7; ++i) launch_unpack(packed[i], sh[i][0], sh[i][1], t->wb + t->off[i], c->st);
+  launch_unpack(pl.d, sh[7][0], sh[7][1], t->wb + t->off[7], c->st);
+  HIPC(c, hipMemcpyAsync(t->wb + t->off[8], c->dlayer.n1, sizeof(uint16_t) * d,
+                         hipMemcpyDeviceToDevice, c->st));
+  HIPC(c, hipMemcpyAsync(t->wb + t->off[9], c->dlayer.n2, sizeof(uint16_t) * d,
+                         hipMemcpyDeviceToDevice, c->st));
+  LAUNCHED(c);
+  tr_widen(t->wb, np, t->w, c->st);
+  tr_fill(t->g, np, 0.f, c->st);
+  tr_fill(t->m, np, 0.f, c->st);
+  tr_fill(t->v, np, 0.f, c->st);
+  uint16_t* lm16 = static_cast<uint16_t*>(take((size_t)V * d * sizeof(uint16_t)));
+  if (!lm16) return fail(c, MSD_ERR_HIP, "training buffers: hipMalloc failed");
+  launch_unpack(c->lm_p, V, d, lm16, c->st);
+  tr_widen(lm16, (size_t)V * d, t->lm, c->st);
+  LAUNCHED(c);
+  c->dlayer.n1 = t->wb + t->off[8];
+  c->dlayer.n2 = t->wb + t->off[9];
+  HIPC(c, hipStreamSynchronize(c->st));
+  return MSD_OK;
+}
+
+// One training sequence: forward, loss and gradient sums (see
+// msd_train_accumulate).  c->h holds the target features of its n rows,
+// c->rows.tok / .vis its tokens and visual row indices.
+int train_pass(msd_ctx* c, int n, const void* visual_d, double* loss3) {
+  TrainState* t = c->tr;
+  const msd_model_desc& m = c->m;
+  const int d = m.d_model, F = m.ffn_dim, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim;
+  const int V = m.vocab, R = n - 1, Gq = H / KV, qd = H * hd, kd = KV * hd;
+  const float eps = m.norm_eps, scale = 1.f / std::sqrt((float)hd);
+  hipStream_t st = c->st;
+  const size_t* o = t->off;
+  float* w = t->w;
+  float* g = t->g;
+  const float *Wfc = w + o[0], *Wq = w + o[1], *Wk = w + o[2], *Wv = w + o[3], *Wo = w + o[4];
+  const float *Wg = w + o[5], *Wu = w + o[6], *Wd = w + o[7], *n1 = w + o[8], *n2 = w + o[9];
+  const size_t Rd = (size_t)R * d;
+  // ---- forward
+  tr_inputs(c->h, c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, t->H,
+            t->X0, t->E0, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, false, true, R, d, 2 * d, 1.f, t->X0, 2 * d, Wfc, 2 * d, 0.f, t->F, d));
+  tr_visual_rows(t->F, t->E0, c->rows.vis, R, d, st);
+  tr_rmsnorm(t->F, n1, eps, R, d, t->A1, t->r1, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, false, true, R, qd, d, 1.f, t->A1, d, Wq, d, 0.f, t->Q, qd));
+  TRY(sgemm_rm(c, false, true, R, kd, d, 1.f, t->A1, d, Wk, d, 0.f, t->K, kd));
+  TRY(sgemm_rm(c, false, true, R, kd, d, 1.f, t->A1, d, Wv, d, 0.f, t->V, kd));
+  tr_rope(t->Q, R, H, hd, c->rope, 1, st);
+  tr_rope(t->K, R, KV, hd, c->rope, 1, st);
+  LAUNCHED(c);
+  const size_t RR = (size_t)R * R;
+  for (int h = 0; h < H; ++h)
+    TRY(sgemm_rm(c, false, true, R, R, hd, 1.f, t->Q + h * hd, qd, t->K + (h / Gq) * hd, kd, 0.f,
+                 t->S + h * RR, R));
+  tr_softmax(t->S, R, H, scale, st);
+  LAUNCHED(c);
+  for (int h = 0; h < H; ++h)
+    TRY(sgemm_rm(c, false, false, R, hd, R, 1.f, t->S + h * RR, R, t->V + (h / Gq) * hd, kd, 0.f,
+                 t->O + h * hd, qd));
+  HIPC(c, hipMemcpyAsync(t->X1, t->F, Rd * 4, hipMemcpyDeviceToDevice, st));
+  TRY(sgemm_rm(c, false, true, R, d, qd, 1.f, t->O, qd, Wo, qd, 1.f, t->X1, d));
+  tr_rmsnorm(t->X1, n2, eps, R, d, t->A2, t->r2, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, false, true, R, F, d, 1.f, t->A2, d, Wg, d, 0.f, t->G, F));
+  TRY(sgemm_rm(c, false, true, R, F, d, 1.f, t->A2, d, Wu, d, 0.f, t->U, F));
+  tr_silu(t->G, t->U, (size_t)R * F, t->Mx, st);
+  LAUNCHED(c);
+  HIPC(c, hipMemcpyAsync(t->D, t->X1, Rd * 4, hipMemcpyDeviceToDevice, st));
+  TRY(sgemm_rm(c, false, true, R, d, F, 1.f, t->Mx, F, Wd, F, 1.f, t->D, d));
+  // ---- loss: regression toward h_{i+1}, token term against softmax(W_lm h_{i+1})
+  tr_reg(t->D, t->H, R, d, t->dD, t->reg, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, false, true, R, V, d, 1.f, t->D, d, t->lm, d, 0.f, t->Ld, V));
+  TRY(sgemm_rm(c, false, true, R, V, d, 1.f, t->H + d, d, t->lm, d, 0.f, t->Lt, V));
+  tr_ce(t->Ld, t->Lt, R, V, TRAIN_CLS_WEIGHT, t->ce, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, false, false, R, d, V, 1.f, t->Ld, V, t->lm, d, 1.f, t->dD, d));
+  // ---- backward (gradient sums over the rows, accumulated into g)
+  TRY(sgemm_rm(c, true, false, d, F, R, 1.f, t->dD, d, t->Mx, F, 1.f, g + o[7], F));
+  TRY(sgemm_rm(c, false, false, R, F, d, 1.f, t->dD, d, Wd, F, 0.f, t->dMx, F));
+  tr_silu_bwd(t->G, t->U, t->dMx, (size_t)R * F, t->dG, t->dU, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, true, false, F, d, R, 1.f, t->dG, F, t->A2, d, 1.f, g + o[5], d));
+  TRY(sgemm_rm(c, true, false, F, d, R, 1.f, t->dU, F, t->A2, d, 1.f, g + o[6], d));
+  TRY(sgemm_rm(c, false, false, R, d, F, 1.f, t->dG, F, Wg, d, 0.f, t->dA2, d));
+  TRY(sgemm_rm(c, false, false, R, d, F, 1.f, t->dU, F, Wu, d, 1.f, t->dA2, d));
+  HIPC(c, hipMemcpyAsync(t->dX1, t->dD, Rd * 4, hipMemcpyDeviceToDevice, st));
+  tr_rmsnorm_bwd(t->X1, n2, t->r2, t->dA2, R, d, t->dX1, g + o[9], st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, true, false, d, qd, R, 1.f, t->dX1, d, t->O, qd, 1.f, g + o[4], qd));
+  TRY(sgemm_rm(c, false, false, R, qd, d, 1.f, t->dX1, d, Wo, qd, 0.f, t->dO, qd));
+  tr_fill(t->dK, (size_t)R * kd, 0.f, st);
+  tr_fill(t->dV, (size_t)R * kd, 0.f, st);
+  LAUNCHED(c);
+  for (int h = 0; h < H; ++h) {
+    const int kv = h / Gq;
+    TRY(sgemm_rm(c, true, false, R, hd, R, 1.f, t->S + h * RR, R, t->dO + h * hd, qd, 1.f,
+                 t->dV + kv * hd, kd));
+    TRY(sgemm_rm(c, false, true, R, R, hd, 1.f, t->dO + h * hd, qd, t->V + kv * hd, kd, 0.f,
+                 t->dP + h * RR, R));
+  }
+  tr_softmax_bwd(t->S, t->dP, R, H, scale, st);
+  LAUNCHED(c);
+  for (int h = 0; h < H; ++h) {
+    const int kv = h / Gq;
+    TRY(sgemm_rm(c, false, false, R, hd, R, 1.f, t->dP + h * RR, R, t->K + kv * hd, kd, 0.f,
+                 t->dQ + h * hd, qd));
+    TRY(sgemm_rm(c, true, false, R, hd, R, 1.f, t->dP + h * RR, R, t->Q + h * hd, qd, 1.f,
+                 t->dK + kv * hd, kd));
+  }
+  tr_rope(t->dQ, R, H, hd, c->rope, -1, st);
+  tr_rope(t->dK, R, KV, hd, c->rope, -1, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, true, false, qd, d, R, 1.f, t->dQ, qd, t->A1, d, 1.f, g + o[1], d));
+  TRY(sgemm_rm(c, true, false, kd, d, R, 1.f, t->dK, kd, t->A1, d, 1.f, g + o[2], d));
+  TRY(sgemm_rm(c, true, false, kd, d, R, 1.f, t->dV, kd, t->A1, d, 1.f, g + o[3], d));
+  TRY(sgemm_rm(c, false, false, R, d, qd, 1.f, t->dQ, qd, Wq, d, 0.f, t->dA1, d));
+  TRY(sgemm_rm(c, false, false, R, d, kd, 1.f, t->dK, kd, Wk, d, 1.f, t->dA1, d));
+  TRY(sgemm_rm(c, false, false, R, d, kd, 1.f, t->dV, kd, Wv, d, 1.f, t->dA1, d));
+  HIPC(c, hipMemcpyAsync(t->dF, t->dX1, Rd * 4, hipMemcpyDeviceToDevice, st));
+  tr_rmsnorm_bwd(t->F, n1, t->r1, t->dA1, R, d, t->dF, g + o[8], st);
+  tr_zero_visual(t->dF, c->rows.vis, R, d, st);
+  LAUNCHED(c);
+  TRY(sgemm_rm(c, true, false, d, 2 * d, R, 1.f, t->dF, d, t->X0, 2 * d, 1.f, g + o[0], 2 * d));
+  // the rows' loss terms, summed in row order on the host
+  std::vector<float> rc(2 * (size_t)R);
+  HIPC(c, hipMemcpyAsync(rc.data(), t->reg, sizeof(float) * R, hipMemcpyDeviceToHost, st));
+  HIPC(c, hipMemcpyAsync(rc.data() + R, t->ce, sizeof(float) * R, hipMemcpyDeviceToHost, st));
+  HIPC(c, hipStreamSynchronize(st));
+  double reg = 0, ce = 0;
+  for (int i = 0; i < R; ++i) {
+    reg += rc[i];
+    ce += rc[R + i];
+  }
+  loss3[0] = reg + TRAIN_CLS_WEIGHT * ce;
+  loss3[1] = reg;
+  loss3[2] = ce;
+  t->rows += R;
+  return MSD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -912,6 +1232,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
 int msd_destroy(msd_ctx* c) {
   if (!c) return MSD_OK;
   const hipError_t e1 = hipStreamSynchronize(c->st);
+  train_free(c->tr);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   const hipError_t e2 = hipHostFree(c->stage);
   delete c;
@@ -947,41 +1268,8 @@ int msd_prefill(msd_ctx* c, int seq, int n, const int32_t* tokens_h, const uint8
     n_vis += is_visual_h[i] ? 1 : 0;
   }
   if (n_vis && !visual_d) return fail(c, MSD_ERR_INVALID_ARG, "visual rows missing");
+  TRY(prompt_target(c, seq, n, tokens_h, is_visual_h, visual_d));
   const int d = m.d_model;
-  // row descriptors: tok, vis, pos, slot, seq, hrow, dst, nxt
-  std::vector<int> a(8 * (size_t)n);
-  int* tok = a.data();
-  int* vis = tok + n;
-  int* pos = vis + n;
-  int* slot = pos + n;
-  int* sq = slot + n;
-  int* hrow = sq + n;
-  int* dst = hrow + n;
-  int* nxt = dst + n;
-  for (int i = 0, v = 0; i < n; ++i) {
-    tok[i] = is_visual_h[i] ? 0 : tokens_h[i];
-    vis[i] = is_visual_h[i] ? v++ : -1;
-    pos[i] = slot[i] = i;
-    sq[i] = seq;
-    hrow[i] = i;
-    dst[i] = (i == n - 1) ? seq * FEAT : -1;
-  }
-  for (int i = 0; i < n; ++i)
-    nxt[i] = (i + 1 < n) ? (is_visual_h[i + 1] ? -1 - vis[i + 1] : tokens_h[i + 1]) : 0;
-  int hdr[2] = {0, seq};
-  const size_t nb = sizeof(int) * (size_t)n;
-  TRY(upload_many(c, {{c->rows.tok, tok, nb}, {c->rows.vis, vis, nb}, {c->rows.pos, pos, nb},
-                      {c->rows.slot, slot, nb}, {c->rows.seq, sq, nb}, {c->rows.hrow, hrow, nb},
-                      {c->rows.dst, dst, nb}, {c->nxt, nxt, nb}, {c->prefix, hdr, sizeof(int)},
-                      {c->seq_ids, hdr + 1, sizeof(int)}}));
-  c->seq_ids_h.assign(1, seq);
-  c->att_pre[0] = 0;
-  c->att_keys[0] = n;
-  // target over the prompt
-  launch_embed(c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, c->x, c->st);
-  LAUNCHED(c);
-  TRY(norm_rows(c, n, c->layers[0].n1));
-  TRY(forward_layers(c, false, 1, n, -1, n, c->final_norm, c->h, nullptr));
   Parts pt;
   TRY(gemm(c, GK_LMHEAD, c->h + (size_t)(n - 1) * 2 * d, 2 * d, 1, c->lm_p, nullptr, m.vocab, d,
            &pt));
@@ -1312,6 +1600,95 @@ int msd_stream_read(const void* buf_d, size_t bytes, int workgroups, void* sink_
                      static_cast<unsigned*>(sink_d), (hipStream_t)stream);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(nullptr, MSD_ERR_HIP, hipGetErrorString(e));
+  return MSD_OK;
+}
+
+int msd_train_accumulate(msd_ctx* c, int seq, int n, const int32_t* tokens_h,
+                         const uint8_t* is_visual_h, const void* visual_d, double* loss_h) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  const msd_model_desc& m = c->m;
+  if (seq < 0 || seq >= c->lim.max_batch) return fail(c, MSD_ERR_INVALID_ARG, "bad sequence");
+  if (n < 2 || n > c->lim.max_prompt || n > c->lim.max_seq || !tokens_h || !is_visual_h ||
+      !loss_h)
+    return fail(c, MSD_ERR_INVALID_ARG, "bad training sequence");
+  int n_vis = 0;
+  for (int i = 0; i < n; ++i) {
+    if (!is_visual_h[i] && (tokens_h[i] < 0 || tokens_h[i] >= m.vocab))
+      return fail(c, MSD_ERR_INVALID_ARG, "token id out of range");
+    n_vis += is_visual_h[i] ? 1 : 0;
+  }
+  if (n_vis && !visual_d) return fail(c, MSD_ERR_INVALID_ARG, "visual rows missing");
+  TRY(train_init(c));
+  c->verified_T = 0;
+  // the slot's cache now holds the training sequence: no longer a decode state
+  c->ready[seq] = 0;
+  c->L[seq] = 0;
+  TRY(prompt_target(c, seq, n, tokens_h, is_visual_h, visual_d));
+  return train_pass(c, n, visual_d, loss_h);
+}
+
+int msd_train_apply(msd_ctx* c, double lr) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  TrainState* t = c->tr;
+  if (!t || t->rows <= 0) return fail(c, MSD_ERR_INVALID_ARG, "no accumulated gradients");
+  if (!(lr >= 0.0)) return fail(c, MSD_ERR_INVALID_ARG, "bad learning rate");
+  const msd_model_desc& m = c->m;
+  const int d = m.d_model, F = m.ffn_dim, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim;
+  const size_t np = t->off[TRAIN_PARAMS];
+  t->steps += 1;
+  const float c1 = (float)(1.0 - std::pow((double)ADAM_B1, t->steps));
+  const float c2 = (float)(1.0 - std::pow((double)ADAM_B2, t->steps));
+  tr_adamw(t->w, t->g, t->m, t->v, np, (float)(1.0 / t->rows), (float)lr, c1, c2, ADAM_B1, ADAM_B2,
+           ADAM_EPS, t->wb, c->st);
+  LAUNCHED(c);
+  // the decoder's packed copies (the norm gains it reads from wb directly)
+  const PackedLayer& pl = c->pdlayer;
+  const size_t pq = packed_elems(H * hd, d), pk = packed_elems(KV * hd, d);
+  uint16_t* qkv = const_cast<uint16_t*>(pl.qkv);
+  launch_pack(t->wb + t->off[0], d, 2 * d, const_cast<uint16_t*>(c->fc_p), c->st);
+  launch_pack(t->wb + t->off[1], H * hd, d, qkv, c->st);
+  launch_pack(t->wb + t->off[2], KV * hd, d, qkv + pq, c->st);
+  launch_pack(t->wb + t->off[3], KV * hd, d, qkv + pq + pk, c->st);
+  launch_pack(t->wb + t->off[4], d, H * hd, const_cast<uint16_t*>(pl.o), c->st);
+  launch_pack(t->wb + t->off[5], F, d, const_cast<uint16_t*>(pl.g), c->st);
+  launch_pack(t->wb + t->off[6], F, d, const_cast<uint16_t*>(pl.u), c->st);
+  launch_pack(t->wb + t->off[7], d, F, const_cast<uint16_t*>(pl.d), c->st);
+  tr_fill(t->g, np, 0.f, c->st);
+  LAUNCHED(c);
+  t->rows = 0;
+  HIPC(c, hipStreamSynchronize(c->st));
+  return MSD_OK;
+}
+
+int msd_train_read(msd_ctx* c, int what, float* out_d, size_t n_floats) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  TRY(train_init(c));
+  TrainState* t = c->tr;
+  const size_t np = t->off[TRAIN_PARAMS];
+  if (!out_d || n_floats != np)
+    return fail(c, MSD_ERR_INVALID_ARG, "msd_train_read wants " + std::to_string(np) + " floats");
+  const float* src = what == 0 ? t->g : what == 1 ? t->w : nullptr;
+  if (!src) return fail(c, MSD_ERR_INVALID_ARG, "unknown training buffer");
+  HIPC(c, hipMemcpyAsync(out_d, src, np * sizeof(float), hipMemcpyDeviceToDevice, c->st));
+  HIPC(c, hipStreamSynchronize(c->st));
+  return MSD_OK;
+}
+
+int msd_train_lr(int step, int total_steps, double lr_max, double* lr_out) {
+  if (total_steps <= 0 || step < 0 || step > total_steps || !lr_out)
+    return fail(nullptr, MSD_ERR_INVALID_ARG, "bad schedule arguments");
+  *lr_out = 0.5 * lr_max * (1.0 + std::cos(M_PI * (double)step / (double)total_steps));
+  return MSD_OK;
+}
+
+int msd_train_mix(int epoch, int n_epochs, int n_per_epoch, int* n_text_out,
+                  int* n_visual_out) {
+  if (n_epochs <= 0 || epoch < 0 || epoch > n_epochs || n_per_epoch < 0 || !n_text_out ||
+      !n_visual_out)
+    return fail(nullptr, MSD_ERR_INVALID_ARG, "bad mix arguments");
+  const int nv = (int)std::nearbyint((double)n_per_epoch * epoch / n_epochs);
+  *n_visual_out = nv;
+  *n_text_out = n_per_epoch - nv;
   return MSD_OK;
 }
 

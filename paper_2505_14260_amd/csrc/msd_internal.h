@@ -88,6 +88,8 @@ struct GemmScratch {
 size_t packed_elems(int N, int K);
 // Packs the row-major bf16 [N][K] src into dst (packed_elems(N, K) elements).
 void launch_pack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t st);
+// Row-major bf16 [N][K] back from the packed layout (K a multiple of 8).
+void launch_unpack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t st);
 GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs);
 // floats of partials for M rows (M <= 64 per launch)
 size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs);
@@ -296,5 +298,31 @@ void launch_commit(int n_seq, const int* seq_ids, const int* path, const int* n_
 // dst = split row of the bf16 row src[0..n) (lo = 0): an imported feature
 void launch_import_row(const uint16_t* src, int n, uint16_t* dst, hipStream_t st);
 void launch_set_int(int* p, int idx, const int* src, int src_idx, hipStream_t st);
+
+// ------------------------------------------------------------ training ----
+// Kernels of the draft-head training step (k_train.hip), float32, row-major,
+// R = n - 1 rows.
+void tr_inputs(const uint16_t* h, const uint16_t* E, const int* tok, const int* vis_idx,
+               const uint16_t* visual, int n, int d, float* H, float* X0, float* E0,
+               hipStream_t st);
+void tr_visual_rows(float* F, const float* E0, const int* vis_idx, int R, int d, hipStream_t st);
+void tr_zero_visual(float* dF, const int* vis_idx, int R, int d, hipStream_t st);
+void tr_rmsnorm(const float* X, const float* g, float eps, int R, int d, float* Y, float* rstd,
+                hipStream_t st);
+// dX += the input gradient, dg += the gain gradient
+void tr_rmsnorm_bwd(const float* X, const float* g, const float* rstd, const float* dY, int R,
+                    int d, float* dX, float* dg, hipStream_t st);
+void tr_rope(float* X, int R, int nh, int hd, const float2* tab, int dir, hipStream_t st);
+void tr_softmax(float* S, int R, int heads, float scale, hipStream_t st);
+void tr_softmax_bwd(const float* P, float* dP, int R, int heads, float scale, hipStream_t st);
+void tr_silu(const float* G, const float* U, size_t n, float* Mx, hipStream_t st);
+void tr_silu_bwd(const float* G, const float* U, const float* dM, size_t n, float* dG, float* dU,
+                 hipStream_t st);
+void tr_reg(const float* D, const float* H, int R, int d, float* dD, float* reg, hipStream_t st);
+void tr_ce(float* Ld, const float* Lt, int R, int V, float w, float* ce, hipStream_t st);
+void tr_adamw(float* w, const float* gsum, float* m, float* v, size_t n, float gscale, float lr,
+              float c1, float c2, float b1, float b2, float eps, uint16_t* wb, hipStream_t st);
+void tr_widen(const uint16_t* src, size_t n, float* dst, hipStream_t st);
+void tr_fill(float* p, size_t n, float v, hipStream_t st);
 
 }  // namespace msd

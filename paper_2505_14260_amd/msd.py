@@ -95,6 +95,13 @@ def lib():
         L.msd_set_state.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, c_vp, c_i32]
         L.msd_set_draft_input.argtypes = [c_vp, ctypes.c_int]
         L.msd_stream_read.argtypes = [c_vp, c_sz, ctypes.c_int, c_vp, c_vp]
+        L.msd_train_accumulate.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, P(c_i32),
+                                           P(ctypes.c_uint8), c_vp, P(ctypes.c_double)]
+        L.msd_train_apply.argtypes = [c_vp, ctypes.c_double]
+        L.msd_train_read.argtypes = [c_vp, ctypes.c_int, c_vp, c_sz]
+        L.msd_train_lr.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                   P(ctypes.c_double)]
+        L.msd_train_mix.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, P(c_i32), P(c_i32)]
         L.msd_trace_enable.argtypes = [c_vp, ctypes.c_int, ctypes.c_int]
         L.msd_trace_read.argtypes = [c_vp, ctypes.c_int, P(TraceRec)]
         _lib = L
@@ -210,6 +217,48 @@ def msd_set_draft_input(ctx, visual_input):
     _check(ctx, lib().msd_set_draft_input(ctx, visual_input))
 
 
+def msd_train_accumulate(ctx, seq, tokens, is_visual, visual_ptr):
+    """Loss sums (total, regression, token) of one training sequence; its
+    gradient sums are added to the context's."""
+    tok, ptok = _i32(tokens)
+    vis = np.ascontiguousarray(is_visual, dtype=np.uint8)
+    loss = (ctypes.c_double * 3)()
+    _check(ctx, lib().msd_train_accumulate(ctx, seq, len(tok), ptok,
+                                           vis.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+                                           visual_ptr, loss))
+    return tuple(loss)
+
+
+def msd_train_apply(ctx, lr):
+    _check(ctx, lib().msd_train_apply(ctx, lr))
+
+
+def msd_train_read(ctx, what, out_ptr, n_floats):
+    _check(ctx, lib().msd_train_read(ctx, what, out_ptr, n_floats))
+
+
+def msd_train_lr(step, total_steps, lr_max):
+    out = ctypes.c_double()
+    _check(None, lib().msd_train_lr(step, total_steps, lr_max, ctypes.byref(out)))
+    return out.value
+
+
+def msd_train_mix(epoch, n_epochs, n_per_epoch):
+    nt, nv = c_i32(), c_i32()
+    _check(None, lib().msd_train_mix(epoch, n_epochs, n_per_epoch, ctypes.byref(nt),
+                                     ctypes.byref(nv)))
+    return nt.value, nv.value
+
+
+def train_param_shapes(dims):
+    """Shapes of the trained draft parameters in msd_train_read's order."""
+    d, F = dims.d_model, dims.ffn_dim
+    qd, kd = dims.n_heads * dims.head_dim, dims.n_kv_heads * dims.head_dim
+    return [("fc", (d, 2 * d)), ("wq", (qd, d)), ("wk", (kd, d)), ("wv", (kd, d)),
+            ("wo", (d, qd)), ("wg", (F, d)), ("wu", (F, d)), ("wd", (d, F)),
+            ("attn_norm", (d,)), ("ffn_norm", (d,))]
+
+
 def msd_set_state(ctx, seq, L, h_ptr, next_token):
     _check(ctx, lib().msd_set_state(ctx, seq, L, h_ptr, next_token))
 
@@ -282,6 +331,33 @@ class Engine:
         """Draft input of the visual prompt rows of later prefills: "embedding"
         (the method) or "feature" (the Visual Feature variant)."""
         msd_set_draft_input(self.ctx, DRAFT_VISUAL_INPUTS[visual_input])
+
+    def train_accumulate(self, seq, tokens, is_visual, visual_bits):
+        """Gradient sums of one training sequence; returns its loss sums."""
+        vis_t = None
+        ptr = None
+        if visual_bits is not None and len(visual_bits):
+            vis_t = self.torch.from_numpy(np.ascontiguousarray(visual_bits).view(np.int16)).to(self.dev)
+            ptr = vis_t.data_ptr()
+        return msd_train_accumulate(self.ctx, seq, tokens, is_visual, ptr)
+
+    def train_apply(self, lr):
+        msd_train_apply(self.ctx, lr)
+
+    def train_read(self, what):
+        """{name: float32 numpy array} of the gradient sums (what 0) or the
+        master parameters (what 1)."""
+        shapes = train_param_shapes(self.dims)
+        n = sum(int(np.prod(s)) for _, s in shapes)
+        buf = self.torch.empty(n, dtype=self.torch.float32, device=self.dev)
+        msd_train_read(self.ctx, what, buf.data_ptr(), n)
+        flat = buf.cpu().numpy()
+        out, o = {}, 0
+        for name, s in shapes:
+            k = int(np.prod(s))
+            out[name] = flat[o:o + k].reshape(s)
+            o += k
+        return out
 
     def _upload(self, a):
         a = np.ascontiguousarray(a)

@@ -61,3 +61,24 @@ def test_buffer_sizes_and_errors_without_gpu():
         msd.msd_buffer_sizes(msd.ModelDesc(2, 128, 4, 2, 96, 256, 512, 1e4, 1e-5), lim)
     with pytest.raises(msd.MSDError):
         msd.msd_buffer_sizes(d, msd.Limits(1, 256, 65, 64))
+
+
+def test_training_schedule_and_mix_match_oracle():
+    # host-side arithmetic of the training calls (no GPU): the cosine
+    # schedule and the progressive mix of Eq. progressive_data
+    from paper_2505_14260_amd import msd
+    from oracle import train as TR
+    if not os.path.exists(msd.LIB_PATH):
+        pytest.skip("libmsd.so not built")
+    for total in (1, 7, 100):
+        for step in range(total + 1):
+            assert abs(msd.msd_train_lr(step, total, 5e-5) - TR.cosine_lr(step, total, 5e-5)) \
+                <= 1e-20
+    for T in (1, 4, 5, 20):
+        for t in range(T + 1):
+            for n in (0, 3, 40, 68000):
+                assert msd.msd_train_mix(t, T, n) == TR.progressive_counts(t, T, n)
+    with pytest.raises(msd.MSDError):
+        msd.msd_train_lr(5, 4, 1.0)
+    with pytest.raises(msd.MSDError):
+        msd.msd_train_mix(6, 5, 10)
