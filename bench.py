@@ -195,6 +195,92 @@ def host_tree(B, wl, first_token=1):
     return bytes(t), T
 
 
+FP32_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
+
+
+def train_flops(dims, n):
+    """Matrix work of one draft training pass over an n-row sequence (R = n - 1
+    rows): the draft layer, f_down and both LM-head products forward, and
+    twice the layer's and f_down's forward work (input and weight gradients)
+    plus the draft logits' input gradient backward; the target's forward over
+    the n rows (its bf16 hi + lo products, the inference GEMMs) separately."""
+    d, F, V = dims.d_model, dims.ffn_dim, dims.vocab
+    qd, kd, H, hd = dims.n_heads * dims.head_dim, dims.n_kv_heads * dims.head_dim, \
+        dims.n_heads, dims.head_dim
+    R = n - 1
+    mats = 2 * R * (2 * d * d + d * (qd + 2 * kd) + qd * d + 3 * d * F)
+    attn = 2 * 2 * H * R * R * hd
+    lm = 2 * 2 * R * V * d
+    fwd = mats + attn + lm
+    bwd = 2 * mats + 2 * attn + 2 * R * V * d
+    layer = d * (qd + 2 * kd) + qd * d + 3 * d * F
+    target = 2 * 2 * n * dims.n_layers * layer
+    return fwd + bwd, target
+
+
+def train_step_bench(args, wl, w, dr):
+    """Timed draft training steps (msd_train_accumulate on one sequence of the
+    workload's prompt shape, then msd_train_apply) after two warm-up steps."""
+    import torch
+    import synth
+    from paper_2505_14260_amd import msd as B
+    dims = wl.dims
+    prompt = synth.make_prompt(wl)
+    n = len(prompt[0])
+    eng = B.Engine(dims, w, dr, max_batch=1, max_seq=(n + 64 + 255) // 256 * 256, max_tree=64,
+                   max_prompt=n)
+    vis_t = torch.from_numpy(np.ascontiguousarray(prompt[2]).view(np.int16)).cuda()
+    stream = torch.cuda.current_stream()
+    acc, app, losses = [], [], []
+    for it in range(args.warmup + args.steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        loss = B.msd_train_accumulate(eng.ctx, 0, prompt[0], prompt[1], vis_t.data_ptr())
+        e[1].record(stream)
+        B.msd_train_apply(eng.ctx, B.msd_train_lr(it, args.warmup + args.steps, 5e-5))
+        e[2].record(stream)
+        torch.cuda.synchronize()
+        if it >= args.warmup:
+            acc.append(e[0].elapsed_time(e[1]))
+            app.append(e[1].elapsed_time(e[2]))
+            losses.append(loss[0] / (n - 1))
+    # the target's share: a prefill of the same sequence (target forward, its
+    # LM-head row and the draft pass over the prompt)
+    pre = []
+    for _ in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        eng.prefill(0, *prompt)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pre.append(e0.elapsed_time(e1))
+    eng.close()
+    tf, tgt = train_flops(dims, n)
+    a_ms, p_ms = float(np.median(acc)), float(np.median(app))
+    step_ms = a_ms + p_ms
+    achieved = (tf + tgt) / (step_ms * 1e-3) / 1e12
+    # the step's mix of work at the two peaks: the draft's fp32 training
+    # products and the target's bf16 forward
+    t_peak = tf / (FP32_PEAK_TFLOPS * 1e12) + tgt / (BF16_PEAK_TFLOPS * 1e12)
+    peak = (tf + tgt) / t_peak / 1e12
+    print(json.dumps({
+        "metric": "draft training step (Sec. 4.2), one sequence",
+        "workload": wl.name, "rows": n, "steps": args.steps, "warmup": args.warmup,
+        "step_ms": round(step_ms, 3), "accumulate_ms": round(a_ms, 3),
+        "apply_ms": round(p_ms, 3), "prefill_ms_same_sequence": round(float(np.median(pre)), 3),
+        "loss_per_row": [round(x, 5) for x in losses],
+        "draft_train_tflop": round(tf / 1e12, 3), "target_forward_tflop": round(tgt / 1e12, 3),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": round(peak, 2),
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "note": "all matrix work of the step over its time; the peak is the rate "
+                             "of this work mix with the draft's fp32 training products at the "
+                             "fp32 peak (157.3) and the target's bf16 forward (hi + lo "
+                             "products) at the bf16 peak (2500)"},
+        "dtype": "f32 (training), bf16 hi+lo (target forward)", "data": "synthetic",
+    }), flush=True)
+
+
 def verify_only(args, wl, w, dr):
     """N verify calls on a fixed static tree from an imported cache state
     (no prompt, no draft): the dispatches after set-up belong to the verifies."""
@@ -258,6 +344,8 @@ def main():
                     help="only time plain HBM streaming (read reduction, copy)")
     ap.add_argument("--verify-only", type=int, default=0, metavar="N",
                     help="only run N verify calls on a fixed tree (counter runs)")
+    ap.add_argument("--train-step", action="store_true",
+                    help="only time the draft training step (accumulate + AdamW apply)")
     ap.add_argument("--late-L", type=int, default=1152,
                     help="cache length of the end-of-generation verify sample")
     args = ap.parse_args()
@@ -297,6 +385,9 @@ def main():
           flush=True)
     if args.verify_only:
         verify_only(args, wl, w, dr)
+        return
+    if args.train_step:
+        train_step_bench(args, wl, w, dr)
         return
     T = wl.tree.n_draft + 1
     max_seq = wl.prompt_len + (args.steps + args.warmup + 18) * (wl.tree.depth + 1) + 2 * T + 32
