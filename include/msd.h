@@ -324,7 +324,8 @@ int msd_set_state(msd_ctx* ctx, int seq, int L, const void* h_d, int32_t next_to
  * visual flags and visual rows as for msd_prefill) the target's features
  * h_0..h_{n-1} (final-norm outputs) are computed; the draft's input rows
  * i = 0..n-2 follow the decoupled rule (Eq. decouple: text rows
- * f_down(Concat(h_i, e_{i+1})), visual rows e_i) and the draft layer runs
+ * f_down(Concat(h_i, e_{i+1})), visual rows e_i, or h_i after
+ * msd_set_draft_input(..., MSD_DRAFT_VISUAL_FEATURE)) and the draft layer runs
  * causally over them at positions i; its output d_i is trained toward
  * h_{i+1}:
  *   loss_i = mean_k SmoothL1(d_i - h_{i+1})_k

@@ -114,13 +114,15 @@ def sequence_inputs(m, tokens, is_visual, visual):
     return h, e, pt
 
 
-def draft_inputs(p, h, e, is_visual):
+def draft_inputs(p, h, e, is_visual, visual_input="embedding"):
     """Input rows i = 0..n-2 of the draft (Eq. decouple): text rows
-    f_down(Concat(h_i, e_{i+1})), visual rows e_i."""
+    f_down(Concat(h_i, e_{i+1})), visual rows e_i, or h_i in the Visual
+    Feature variant of the input-decoupling ablation (Sec. 5.3)."""
     R = h.shape[0] - 1
     vis = torch.as_tensor(np.asarray(is_visual, dtype=bool)[:R])
     cat = torch.cat([h[:R], e[1:]], dim=1)
-    return torch.where(vis[:, None], e[:R], cat @ p["fc"].T)
+    src = e[:R] if visual_input == "embedding" else h[:R]
+    return torch.where(vis[:, None], src, cat @ p["fc"].T)
 
 
 def row_losses(d, h, pt, lm_head):
@@ -136,32 +138,35 @@ def row_losses(d, h, pt, lm_head):
     return reg, cls
 
 
-def sequence_loss_sum(dims, p, lm_head, h, e, is_visual, pt):
+def sequence_loss_sum(dims, p, lm_head, h, e, is_visual, pt, visual_input="embedding"):
     """Sum over rows i = 0..n-2 of loss_i for one sequence, with its parts
     (sum of the regression terms, sum of the cross-entropy terms)."""
     h = torch.as_tensor(h, dtype=torch.float64)
     e = torch.as_tensor(e, dtype=torch.float64)
     R = h.shape[0] - 1
-    d = layer_forward_t(dims, p, draft_inputs(p, h, e, is_visual), torch.arange(R))
+    d = layer_forward_t(dims, p, draft_inputs(p, h, e, is_visual, visual_input),
+                        torch.arange(R))
     reg, cls = row_losses(d, h, pt, lm_head)
     return reg + CLS_WEIGHT * cls, reg, cls
 
 
-def batch_loss(m, params, seqs):
+def batch_loss(m, params, seqs, visual_input="embedding"):
     """The batch loss alone (no gradients)."""
     lm = torch.as_tensor(M.widen(m.w["lm_head"]), dtype=torch.float64)
     rows = sum(s[0].shape[0] - 1 for s in seqs)
     with torch.no_grad():
-        tot = sum(sequence_loss_sum(m.dims, params, lm, h, e, vis, pt)[0]
+        tot = sum(sequence_loss_sum(m.dims, params, lm, h, e, vis, pt, visual_input)[0]
                   for h, e, vis, pt in seqs)
     return float(tot) / rows
 
 
-def batch_grads(m, params, seqs):
+def batch_grads(m, params, seqs, visual_input="embedding"):
     """Loss (mean over every row of the batch's sequences) and its gradients.
 
     seqs: list of (h, e, is_visual, pt) from sequence_inputs.  Returns
     (loss, reg, cls, {key: grad ndarray}) with reg and cls the row means.
+    visual_input: the draft input rule of visual rows ("embedding", the
+    method, or "feature", the Visual Feature variant).
     """
     lm = torch.as_tensor(M.widen(m.w["lm_head"]), dtype=torch.float64)
     for t in params.values():
@@ -169,7 +174,7 @@ def batch_grads(m, params, seqs):
     rows = sum(s[0].shape[0] - 1 for s in seqs)
     tot = reg = cls = 0.0
     for h, e, vis, pt in seqs:
-        l, r, c = sequence_loss_sum(m.dims, params, lm, h, e, vis, pt)
+        l, r, c = sequence_loss_sum(m.dims, params, lm, h, e, vis, pt, visual_input)
         tot = tot + l
         reg += r.item()
         cls += c.item()

@@ -32,12 +32,15 @@ MSD_DEV float bmax(float v, float* sh) {
 }
 
 // Row i < n: H[i] = target feature (split row hi + lo); for i < R also
-// X0[i] = [h_i | e_{i+1}] and E0[i] = e_i, where e is the token embedding
-// (text) or the visual row vis_idx (visual).  Grid (n), block TB.
+// X0[i] = [h_i | e_{i+1}] and E0[i] = the draft input of a visual row i:
+// e_i, or h_i with visual_feature (the Visual Feature variant), where e is
+// the token embedding (text) or the visual row vis_idx (visual).  Grid (n),
+// block TB.
 __global__ __launch_bounds__(TB) void k_tr_inputs(const uint16_t* h, const uint16_t* E,
                                                   const int* tok, const int* vis_idx,
-                                                  const uint16_t* visual, int n, int d, float* H,
-                                                  float* X0, float* E0) {
+                                                  const uint16_t* visual, int n, int d,
+                                                  int visual_feature, float* H, float* X0,
+                                                  float* E0) {
   const int i = blockIdx.x;
   const int R = n - 1;
   const uint16_t* hr = h + (size_t)i * 2 * d;
@@ -48,13 +51,14 @@ __global__ __launch_bounds__(TB) void k_tr_inputs(const uint16_t* h, const uint1
     H[(size_t)i * d + k] = hv;
     if (i < R) {
       X0[(size_t)i * 2 * d + k] = hv;
-      E0[(size_t)i * d + k] = bf2f(er[k]);
+      E0[(size_t)i * d + k] = visual_feature ? hv : bf2f(er[k]);
     }
     if (i > 0) X0[(size_t)(i - 1) * 2 * d + d + k] = bf2f(er[k]);
   }
 }
 
-// Visual rows take their embedding as the draft input (Eq. decouple).
+// Visual rows take E0 as the draft input (Eq. decouple: their embedding, or
+// their target feature in the Visual Feature variant).
 __global__ __launch_bounds__(TB) void k_tr_visual_rows(float* F, const float* E0,
                                                        const int* vis_idx, int d) {
   const int i = blockIdx.x;
@@ -258,10 +262,10 @@ unsigned blocks(size_t n) { return (unsigned)((n + TB - 1) / TB); }
 }  // namespace
 
 void tr_inputs(const uint16_t* h, const uint16_t* E, const int* tok, const int* vis_idx,
-               const uint16_t* visual, int n, int d, float* H, float* X0, float* E0,
-               hipStream_t st) {
-  hipLaunchKernelGGL(k_tr_inputs, dim3(n), dim3(TB), 0, st, h, E, tok, vis_idx, visual, n, d, H,
-                     X0, E0);
+               const uint16_t* visual, int n, int d, int visual_feature, float* H, float* X0,
+               float* E0, hipStream_t st) {
+  hipLaunchKernelGGL(k_tr_inputs, dim3(n), dim3(TB), 0, st, h, E, tok, vis_idx, visual, n, d,
+                     visual_feature, H, X0, E0);
 }
 void tr_visual_rows(float* F, const float* E0, const int* vis_idx, int R, int d, hipStream_t st) {
   hipLaunchKernelGGL(k_tr_visual_rows, dim3(R), dim3(TB), 0, st, F, E0, vis_idx, d);

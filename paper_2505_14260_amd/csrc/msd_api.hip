@@ -992,8 +992,8 @@ int train_pass(msd_ctx* c, int n, const void* visual_d, double* loss3) {
   const float *Wg = w + o[5], *Wu = w + o[6], *Wd = w + o[7], *n1 = w + o[8], *n2 = w + o[9];
   const size_t Rd = (size_t)R * d;
   // ---- forward
-  tr_inputs(c->h, c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d, t->H,
-            t->X0, t->E0, st);
+  tr_inputs(c->h, c->embed, c->rows.tok, c->rows.vis, (const uint16_t*)visual_d, n, d,
+            c->visual_input == MSD_DRAFT_VISUAL_FEATURE, t->H, t->X0, t->E0, st);
   LAUNCHED(c);
   TRY(sgemm_rm(c, false, true, R, d, 2 * d, 1.f, t->X0, 2 * d, Wfc, 2 * d, 0.f, t->F, d));
   tr_visual_rows(t->F, t->E0, c->rows.vis, R, d, st);

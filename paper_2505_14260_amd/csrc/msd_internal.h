@@ -302,9 +302,11 @@ void launch_set_int(int* p, int idx, const int* src, int src_idx, hipStream_t st
 // ------------------------------------------------------------ training ----
 // Kernels of the draft-head training step (k_train.hip), float32, row-major,
 // R = n - 1 rows.
+// visual_feature: visual rows take the target feature (the Visual Feature
+// variant) instead of their embedding
 void tr_inputs(const uint16_t* h, const uint16_t* E, const int* tok, const int* vis_idx,
-               const uint16_t* visual, int n, int d, float* H, float* X0, float* E0,
-               hipStream_t st);
+               const uint16_t* visual, int n, int d, int visual_feature, float* H, float* X0,
+               float* E0, hipStream_t st);
 void tr_visual_rows(float* F, const float* E0, const int* vis_idx, int R, int d, hipStream_t st);
 void tr_zero_visual(float* dF, const int* vis_idx, int R, int d, hipStream_t st);
 void tr_rmsnorm(const float* X, const float* g, float eps, int R, int d, float* Y, float* rstd,

@@ -53,11 +53,14 @@ def oracle_batch(m, prompts):
     return seqs
 
 
-@pytest.mark.parametrize("wl", [TINY, WIDE_SHORT], ids=lambda w: w.name)
-def test_gradients_match_oracle(wl):
-    print(f"case: training gradients {wl.name}, two sequences", flush=True)
+@pytest.mark.parametrize("wl,visual_input", [(TINY, "embedding"), (WIDE_SHORT, "embedding"),
+                                             (TINY, "feature")],
+                         ids=["tiny", "wide-gqa", "tiny-visual-feature"])
+def test_gradients_match_oracle(wl, visual_input):
+    print(f"case: training gradients {wl.name} ({visual_input} input), two sequences", flush=True)
     eng, m, w, dr = make(wl)
     try:
+        eng.set_draft_input(visual_input)
         p0 = synth.make_prompt(wl, seq=0)
         p1 = synth.make_prompt(wl, seq=1)
         cut = wl.n_visual + 7
@@ -67,7 +70,7 @@ def test_gradients_match_oracle(wl):
         g = eng.train_read(0)
         rows = len(p0[0]) - 1 + len(p1[0]) - 1
         params = TR.draft_params(m.draft)
-        loss, reg, cls, gref = TR.batch_grads(m, params, oracle_batch(m, [p0, p1]))
+        loss, reg, cls, gref = TR.batch_grads(m, params, oracle_batch(m, [p0, p1]), visual_input)
         got = (l0[0] + l1[0]) / rows
         print(f"loss {got:.6f} oracle {loss:.6f} (reg {reg:.5f}, token {cls:.5f})")
         assert abs(got - loss) <= 1e-2 * abs(loss)

@@ -275,7 +275,11 @@ SOURCE_CASES = [
     # training: text rows concatenate their own embedding, not the next one
     ("train_input_embedding", TR, "draft_inputs",
      "torch.cat([h[:R], e[1:]], dim=1)", "torch.cat([h[:R], e[:R]], dim=1)",
-     lambda: [PTR.test_draft_inputs_follow_decoupled_rule]),
+     lambda: [lambda: PTR.test_draft_inputs_follow_decoupled_rule("embedding")]),
+    # training: the Visual Feature input ignored (visual rows keep e_i)
+    ("train_visual_feature_ignored", TR, "draft_inputs",
+     'src = e[:R] if visual_input == "embedding" else h[:R]', "src = e[:R]",
+     lambda: [lambda: PTR.test_draft_inputs_follow_decoupled_rule("feature")]),
     # AdamW without bias correction
     ("adam_without_bias_correction", TR, "AdamW",
      "(self.m[k] / c1) / (np.sqrt(self.v[k] / c2) + ADAM_EPS)",

@@ -123,13 +123,16 @@ def test_batch_loss_weights_and_means():
     assert abs(got - want / rows) <= 1e-12 * abs(got)
 
 
-def test_draft_inputs_follow_decoupled_rule():
+@pytest.mark.parametrize("visual_input", ["embedding", "feature"])
+def test_draft_inputs_follow_decoupled_rule(visual_input):
     wl, m, (tokens, vis, visual) = setup()
     h, e, pt = TR.sequence_inputs(m, tokens, vis, visual)
-    x = TR.draft_inputs(TR.draft_params(m.draft), torch.tensor(h), torch.tensor(e), vis)
+    x = TR.draft_inputs(TR.draft_params(m.draft), torch.tensor(h), torch.tensor(e), vis,
+                        visual_input)
     n = len(tokens)
     v = np.asarray(vis, dtype=bool)[:n - 1]
-    want = M.draft_input(m.draft, h[:n - 1], e[1:], v, e[:n - 1])
+    src = e[:n - 1] if visual_input == "embedding" else h[:n - 1]
+    want = M.draft_input(m.draft, h[:n - 1], e[1:], v, src)
     assert np.allclose(x.detach().numpy(), want, rtol=1e-12, atol=1e-14)
     assert v.any() and (~v).any()
 
