@@ -418,7 +418,7 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
 // for NT tiles, chunk by chunk, restaging X in LDS at each chunk and keeping
 // the tiles' accumulators in registers throughout.  It writes one partial
 // per tile (S = 1), where the chunked kernels write one per K chunk: at the
-// Qwen2-VL-7B-shaped LM head that is 39 MB instead of 272 MB per 64 rows,
+// Qwen2.5-VL-7B-shaped LM head that is 39 MB instead of 272 MB per 64 rows,
 // and as much less for the consumer to read.
 //
 // With ten tiles' accumulators the X fragments of a whole block no longer
