@@ -60,7 +60,11 @@ MSD_DEV uint4 load_stream(const uint16_t* p) {
 // MFMA operand load hit different banks.
 MSD_DEV int xs_index(int m, int u, int upr) { return m * upr + (u ^ (m & 15)); }
 
-template <int MT, int NW, int NKB, int P>
+// MS (row split): a pass of 33-64 rows runs as two 32-row halves.  Workgroups
+// b and b + 8 (same XCD) take the two halves of one (chunk, tile set), so
+// the second one's weight blocks are L2 hits, and each workgroup streams its
+// weight blocks against a 32-row X chunk twice as long as a 64-row one.
+template <int MT, int NW, int NKB, int P, bool MS = false>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   static_assert(NKB % P == 0, "ring slots must divide the chunk");
   extern __shared__ uint4 xs[];
@@ -70,8 +74,15 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int XB = NX < 16 ? NX : 16;  // staging batch (loads in flight)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
-  const int S = a.S, G = a.G, K = a.K, M = a.M, nkt = a.nkt, n_tiles = a.n_tiles;
-  const int s = blockIdx.x % S, gi = blockIdx.x / S;
+  const int S = a.S, G = a.G, K = a.K, nkt = a.nkt, n_tiles = a.n_tiles;
+  int unit = blockIdx.x, half = 0;
+  if (MS) {
+    half = (unit >> 3) & 1;
+    unit = ((unit >> 4) << 3) | (unit & 7);
+    if (unit >= S * G) return;
+  }
+  const int M = MS ? min(MT * 16, a.M - MT * 16 * half) : a.M;
+  const int s = unit % S, gi = unit / S;
   const int n_my = gi < n_tiles ? (n_tiles - gi + G - 1) / G : 0;
   if (n_my == 0) return;
   const int kb0 = s * NKB;
@@ -88,8 +99,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   // zero.  The first batch's loads are issued before the weight ring's, so
   // the ring's prefetch overlaps the staging.
   uint4 xh[XB], xl[XB];
-  const uint16_t* const X = a.X;
   const int ldx = a.ldx;
+  const uint16_t* const X = a.X + (MS ? (size_t)half * MT * 16 * ldx : 0);
 #pragma unroll
   for (int q = 0; q < XB; ++q) {
     const int e = threadIdx.x + 256 * q;
@@ -144,7 +155,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   __syncthreads();
 
   const int ldp = a.ldp, off2 = a.off2;
-  float* const part = a.part + (size_t)s * a.part_split;
+  float* const part =
+      a.part + (size_t)s * a.part_split + (MS ? (size_t)half * MT * 16 * ldp : 0);
   float* const sink = a.sink + lane * 4;
   for (int j = 0; j < n_my; ++j) {
     const int tile = gi + j * G;
@@ -923,6 +935,22 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
   p.nw = nw;
   p.ldp = p.n_tiles * TILE_ROWS * nw;
   p.off2 = p.n_tiles * TILE_ROWS;
+  p.ms = 0;
+  // 33-64 rows, single weights with at most two tiles per workgroup: the X
+  // chunk costs as much as the weight blocks streamed against it, so the
+  // pass runs as two 32-row halves with 8-block chunks (each workgroup
+  // streaming twice the weight bytes per X byte; the output projection at
+  // 61 rows 14.7 -> 12.0 us, Qwen2.5-VL-7B-shaped).  Wider weights stay
+  // whole: there the doubled weight stream per CU (the partner's blocks are
+  // L2 hits, but they still pass through the CU) costs more than the
+  // halved partials save.
+  if (p.MT == 4 && nw == 1 && !p.fk && p.per <= 2) {
+    const GemmPlan h = plan_gemm(32, N, K, nw, target_wgs / 2);
+    if (!h.pair && !h.fk) {
+      p = h;  // same ldp and off2: they depend on N and nw only
+      p.ms = 1;
+    }
+  }
   return p;
 }
 
@@ -953,6 +981,17 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
   a.off2 = pl.off2;
   a.sink = sink;
   a.dummy = dummy;
+  if (pl.ms) {
+    const dim3 grid(16 * ((pl.S * pl.G + 7) / 8));
+    constexpr int NKB = chunk_blocks(2);
+    const size_t lds = (size_t)2 * 16 * NKB * KB * 4;
+    if (sc.ev_start)
+      hipExtLaunchKernelGGL((k_gemm<2, 1, NKB, RING, true>), grid, dim3(256), lds, st, sc.ev_start,
+                            sc.ev_stop, 0, a);
+    else
+      hipLaunchKernelGGL((k_gemm<2, 1, NKB, RING, true>), grid, dim3(256), lds, st, a);
+    return;
+  }
   const dim3 grid(pl.S * pl.G);
   if (pl.fk) {
     if (pl.fk == 8) launch_fk<8>(grid, a, sc, st);

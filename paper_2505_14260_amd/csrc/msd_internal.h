@@ -77,6 +77,7 @@ struct GemmPlan {
   int pair;  // two K chunks per workgroup (S counts chunk pairs)
   int fk;    // > 0: all of K per workgroup for fk tiles (S = 1)
   int per;   // tiles per workgroup
+  int ms;    // 33-64 rows as two 32-row halves (MT, S and G of one half)
 };
 
 struct GemmScratch {
