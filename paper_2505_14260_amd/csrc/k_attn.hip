@@ -23,6 +23,8 @@
 // are split rows (the O projection's input).
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+
 #include "msd_internal.h"
 
 namespace msd {
@@ -409,16 +411,23 @@ __global__ __launch_bounds__(64 * NWV, 2) void k_tree_attn(AttnArgs a) {
   __shared__ int last;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   // Workgroup -> (sequence, kv head) pair, key chunk c and query tile qt.
-  // Every workgroup of one pair runs on one XCD (workgroup i runs on XCD
-  // i mod 8): the chunks of an item meet in that XCD's L2 for the merge,
-  // and the query tiles of one chunk (consecutive slots) read the same K/V
-  // blocks, fetched from HBM once.  Grid: 8 * ceil(pairs / 8) * chunks * qtiles.
-  const int per_pair = a.qtiles * a.n_chunks;
+  // Every workgroup of one item (pair, qt) runs on one XCD (workgroup i runs
+  // on XCD i mod 8): its chunks meet in that XCD's L2 for the merge.  With
+  // fewer pairs than XCDs a pair's query tiles are dealt over a.xrep XCDs
+  // (virtual pair pair * xrep + qt mod xrep), so that every XCD works; the
+  // tiles on one XCD (consecutive slots) read the same K/V blocks, fetched
+  // from HBM once per XCD.  Grid: 8 * ceil(pairs * xrep / 8) * chunks *
+  // ceil(qtiles / xrep).
+  const int D = a.xrep;
+  const int QD = (a.qtiles + D - 1) / D;  // query tiles per virtual pair
+  const int per_pair = QD * a.n_chunks;
   const int slot = blockIdx.x >> 3;
   const int pp = slot / per_pair, rem = slot - pp * per_pair;
-  const int pair = pp * 8 + (blockIdx.x & 7);
-  if (pair >= a.n_seq * a.KV) return;
-  const int c = rem / a.qtiles, qt = rem - c * a.qtiles;
+  const int vpair = pp * 8 + (blockIdx.x & 7);
+  if (vpair >= a.n_seq * a.KV * D) return;
+  const int pair = vpair / D;
+  const int c = rem / QD, qt = (rem - c * QD) * D + vpair % D;
+  if (qt >= a.qtiles) return;
   const int g = pair % a.KV;
   const int sidx = pair / a.KV;
   const int b = a.seq[sidx];
@@ -619,9 +628,13 @@ size_t attn_partial_floats(int n_seq, int KV, int qtiles, int n_chunks, int hd) 
 }
 
 template <int HD>
-void launch_tree_hd(const AttnArgs& a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+void launch_tree_hd(AttnArgs a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   const int pairs = a.n_seq * a.KV;
-  const dim3 grid(8 * ((pairs + 7) / 8) * a.qtiles * a.n_chunks);
+  // XCDs per pair: the query tiles of fewer than eight pairs are dealt over
+  // the idle XCDs (their K/V is then read from HBM once per XCD)
+  a.xrep = std::max(1, std::min(8 / pairs, a.qtiles));
+  const int QD = (a.qtiles + a.xrep - 1) / a.xrep;
+  const dim3 grid(8 * ((pairs * a.xrep + 7) / 8) * QD * a.n_chunks);
   if (ev0)  // events carried by the launch itself bracket the kernel only
     hipExtLaunchKernelGGL((k_tree_attn<HD, TREE_WAVES>), grid, dim3(64 * TREE_WAVES), 0, st,
                           ev0, ev1, 0, a);

@@ -156,6 +156,7 @@ struct AttnArgs {
   const uint64_t* mask;   // [n_seq*nq] region masks (tree mode)
   int S, H, KV, hd, nq, n_seq;
   int n_chunks, chunk_keys, qtiles;  // chunk_keys: multiple of 128 (tree mode)
+  int xrep;               // XCDs per (sequence, kv head) pair (set by the launcher)
   float* part_o;          // [items][32*hd] float16 partial outputs (tree mode, n_chunks > 1)
   float* part_ml;         // [items][32][2]
   int* att_cnt;           // [items] chunk arrivals per XCD (zero between launches)
