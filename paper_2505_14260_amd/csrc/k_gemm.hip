@@ -279,6 +279,9 @@ MSD_DEV void store_x(uint4* xs, const uint4 (&xh)[XB], const uint4 (&xl)[XB], in
 // ring's, once per workgroup.  Slots for tiles past the workgroup's last and
 // blocks past K read the zero block.
 //
+// NC (3 or 4 instead of 2): more K chunks per workgroup, for 64-row passes
+// whose partials would otherwise cost more than the extra X restages.
+//
 // BO (block outer): within each chunk the sequence runs block by block over
 // the tiles, so a block's X fragments are read from LDS once for all of the
 // workgroup's tiles instead of once per tile.  Every output element sums the
@@ -288,20 +291,20 @@ MSD_DEV void store_x(uint4* xs, const uint4 (&xh)[XB], const uint4 (&xl)[XB], in
 // 30.4 -> 24.9 us, gate+up 44.8 -> 41.5 us (7B-shaped), 64-row down
 // 43.8 -> 34.7 us (Qwen-shaped); the fragments' registers make the SwiGLU
 // pair spill from four tiles per workgroup on.
-template <int MT, int NW, int NKB, int P, int NT, bool BO>
+template <int MT, int NW, int NKB, int P, int NT, bool BO, int NC = 2>
 __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
   static_assert(NKB % P == 0, "ring slots must divide the chunk");
   extern __shared__ uint4 xs[];
   constexpr int UPR = NKB * KB / 8;
   constexpr int LO = MT * 16 * UPR;
-  constexpr int SEQ = 2 * NT * NKB;  // blocks of the workgroup's sequence
+  constexpr int SEQ = NC * NT * NKB;  // blocks of the workgroup's sequence
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
   const int S = a.S, G = a.G, M = a.M, nkt = a.nkt, n_tiles = a.n_tiles;
   const int s = blockIdx.x % S, gi = blockIdx.x / S;
   const int n_my = gi < n_tiles ? min(NT, (n_tiles - gi + G - 1) / G) : 0;
   if (n_my == 0) return;
-  const int kb0 = 2 * s * NKB;
+  const int kb0 = NC * s * NKB;
   const uint16_t* const W = a.W;
   const uint16_t* const W2 = a.W2;
   const size_t lane_off = (size_t)wave * (BLOCK_ELEMS / 4) + lane * 8;
@@ -344,15 +347,15 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
 #pragma unroll
       for (int t = 0; t < MT; ++t) acc[j][w][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    if (h == 1) {
-      // the second X chunk: its loads go out before the barrier (every wave
-      // done with the first chunk), its LDS writes after
+  for (int h = 0; h < NC; ++h) {
+    if (h >= 1) {
+      // the next X chunk: its loads go out before the barrier (every wave
+      // done with the previous chunk), its LDS writes after
       constexpr int XB = NX / 2;
 #pragma unroll
       for (int q0 = 0; q0 < NX; q0 += XB) {
         uint4 yh[XB], yl[XB];
-        load_x<MT, NKB, XB>(yh, yl, a.X, a.ldx, M, a.K, kb0 + NKB, q0);
+        load_x<MT, NKB, XB>(yh, yl, a.X, a.ldx, M, a.K, kb0 + h * NKB, q0);
         if (q0 == 0) lds_barrier();
         store_x<MT, NKB, XB>(xs, yh, yl, q0);
       }
@@ -776,7 +779,7 @@ void launch_mt(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t 
     hipLaunchKernelGGL((k_gemm<MT, NW, NKB, P>), grid, dim3(256), lds, st, a);
 }
 
-template <int MT, int NW, int NT>
+template <int MT, int NW, int NT, int NC = 2>
 void launch_pair(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
   constexpr int P = RING;
   constexpr int NKB = chunk_blocks(MT);
@@ -784,10 +787,10 @@ void launch_pair(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_
   constexpr bool BO = MT == 4 && (NW == 1 || NT <= 3);
   const size_t lds = (size_t)MT * 16 * NKB * KB * 4;
   if (sc.ev_start)
-    hipExtLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT, BO>), grid, dim3(256), lds, st, sc.ev_start,
-                          sc.ev_stop, 0, a);
+    hipExtLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT, BO, NC>), grid, dim3(256), lds, st,
+                          sc.ev_start, sc.ev_stop, 0, a);
   else
-    hipLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT, BO>), grid, dim3(256), lds, st, a);
+    hipLaunchKernelGGL((k_gemm2<MT, NW, NKB, P, NT, BO, NC>), grid, dim3(256), lds, st, a);
 }
 
 template <int NT>
@@ -802,13 +805,13 @@ void launch_fk(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t 
     hipLaunchKernelGGL((k_gemm_fk<MT, NKB, P, NT>), grid, dim3(256), lds, st, a);
 }
 
-template <int MT, int NW>
+template <int MT, int NW, int NC = 2>
 void launch_pair_nt(int nt, dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
-  if (nt == 1) launch_pair<MT, NW, 1>(grid, a, sc, st);
-  else if (nt == 2) launch_pair<MT, NW, 2>(grid, a, sc, st);
-  else if (nt == 3) launch_pair<MT, NW, 3>(grid, a, sc, st);
-  else if (nt == 4) launch_pair<MT, NW, 4>(grid, a, sc, st);
-  else launch_pair<MT, NW, 5>(grid, a, sc, st);
+  if (nt == 1) launch_pair<MT, NW, 1, NC>(grid, a, sc, st);
+  else if (nt == 2) launch_pair<MT, NW, 2, NC>(grid, a, sc, st);
+  else if (nt == 3) launch_pair<MT, NW, 3, NC>(grid, a, sc, st);
+  else if (nt == 4) launch_pair<MT, NW, 4, NC>(grid, a, sc, st);
+  else launch_pair<MT, NW, 5, NC>(grid, a, sc, st);
 }
 
 // Streaming read of a buffer with the weight stream's access pattern: every
@@ -911,7 +914,7 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
     const bool busy = p.MT == 4 ? 4 * S2 * G2 >= 3 * target_wgs
                                 : (nw == 2 || (per2 >= 4 && 20 * S2 * G2 >= 19 * p.S * p.G));
     if (per2 <= PAIR_MAX_TILES && busy) {
-      p.pair = 1;
+      p.pair = 2;
       p.S = S2;
       p.G = G2;
       p.per = per2;
@@ -949,6 +952,36 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
     if (!h.pair && !h.fk) {
       p = h;  // same ldp and off2: they depend on N and nw only
       p.ms = 1;
+    }
+  }
+  // 64-row passes of single weights: four or three K chunks per workgroup
+  // where that writes fewer partials on about as many workgroups, each with
+  // four tiles or more to amortise the X restage between chunks (the 7B LM
+  // head at 61 rows: 8 -> 2 partials, 66.6 -> 55.9 us).  Not with fewer
+  // tiles (7B down on 256 workgroups of two tiles: 24.9 -> 26.8 us), fewer
+  // workgroups (7B q/k/v 27.2 -> 31.0 us on 192 instead of 256), nor for
+  // the SwiGLU pair, whose accumulators then spill (Qwen-shaped gate+up
+  // 59.3 -> 77.2 us).
+  if (p.MT == 4 && nw == 1 && !p.fk && !p.ms) {
+    const int S1 = (p.nkt + p.nkb - 1) / p.nkb;
+    for (int nc = 4; nc >= 3; --nc) {
+      const int Sn = (S1 + nc - 1) / nc;
+      if (Sn >= p.S) continue;
+      int Gn = (target_wgs + Sn - 1) / Sn;
+      if (Gn > p.n_tiles) Gn = p.n_tiles;
+      int pern = (p.n_tiles + Gn - 1) / Gn;
+      Gn = (p.n_tiles + pern - 1) / pern;
+      while (Sn * Gn > target_wgs && Gn > 1) {
+        ++pern;
+        Gn = (p.n_tiles + pern - 1) / pern;
+      }
+      if (pern >= 4 && pern <= PAIR_MAX_TILES && 20 * Sn * Gn >= 19 * p.S * p.G) {
+        p.pair = nc;
+        p.S = Sn;
+        p.G = Gn;
+        p.per = pern;
+        break;
+      }
     }
   }
   return p;
@@ -998,7 +1031,15 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
     else launch_fk<10>(grid, a, sc, st);
     return;
   }
-  if (pl.pair) {
+  if (pl.pair == 4) {
+    launch_pair_nt<4, 1, 4>(pl.per, grid, a, sc, st);
+    return;
+  }
+  if (pl.pair == 3) {
+    launch_pair_nt<4, 1, 3>(pl.per, grid, a, sc, st);
+    return;
+  }
+  if (pl.pair == 2) {
     if (pl.MT == 2 && nw == 2) launch_pair_nt<2, 2>(pl.per, grid, a, sc, st);
     else if (pl.MT == 2) launch_pair_nt<2, 1>(pl.per, grid, a, sc, st);
     else if (nw == 2) launch_pair_nt<4, 2>(pl.per, grid, a, sc, st);

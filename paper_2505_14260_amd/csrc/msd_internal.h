@@ -74,7 +74,7 @@ struct GemmArgs {
 
 struct GemmPlan {
   int MT, nkb, S, G, nw, n_tiles, nkt, ldp, off2;
-  int pair;  // two K chunks per workgroup (S counts chunk pairs)
+  int pair;  // 2, 3 or 4: K chunks per workgroup (S counts their groups); 0: one
   int fk;    // > 0: all of K per workgroup for fk tiles (S = 1)
   int per;   // tiles per workgroup
   int ms;    // 33-64 rows as two 32-row halves (MT, S and G of one half)
