@@ -1,6 +1,8 @@
 // Row-wise kernels of the decode path: embedding gather, RMSNorm, rotary
 // embedding with the KV-cache write, the draft input builder and the
 // vocabulary top-k / logsumexp.
+#include <algorithm>
+
 #include "msd_internal.h"
 
 namespace msd {
@@ -76,11 +78,16 @@ __global__ void k_rope_table(float2* tab, int max_pos, int half, double theta) {
 }
 
 // Sum over the K chunks of one partial-product element, in chunk order.
-// The chunks are loaded in groups of PART_GROUP, all loads of a group in
-// flight at once (indices past the last chunk reload the last one and are
-// not added): a loop over a runtime count would otherwise wait for each load
-// of its remainder before issuing the next.
+// The chunks are loaded in groups of PG, all loads of a group in flight at
+// once (indices past the last chunk reload the last one and are not added):
+// a loop over a runtime count would otherwise wait for each load of its
+// remainder before issuing the next.  The launchers take PG = the chunk
+// count rounded up to a power of two, at most MAX_PART_GROUP, so that most
+// sums wait for memory once and few loads are repeats.  PART_GROUP: the
+// group of the per-row sums of squares (at most eight blocks).
 constexpr int PART_GROUP = 8;
+constexpr int MAX_PART_GROUP = 16;
+inline int part_group(int S) { return S <= 2 ? 2 : S <= 4 ? 4 : S <= 8 ? 8 : MAX_PART_GROUP; }
 
 // Sums over the K chunks of N elements of one row (N columns; every load of a
 // chunk group, for all N, in flight at once), in chunk order per element.
@@ -89,44 +96,44 @@ constexpr int PART_GROUP = 8;
 // are masked to +0 bitwise rather than skipped: a branch per entry would also
 // make the compiler wait at each branch.
 MSD_DEV float keep_if(float v, uint32_t m) { return __uint_as_float(__float_as_uint(v) & m); }
-template <int N>
+template <int N, int PG>
 MSD_DEV void part_sums_group(const Parts& pt, const float* p, int s0, const int (&col)[N],
                              float (&out)[N]) {
-  float q[N][PART_GROUP];
+  float q[N][PG];
 #pragma unroll
   for (int n = 0; n < N; ++n)
 #pragma unroll
-    for (int j = 0; j < PART_GROUP; ++j)
+    for (int j = 0; j < PG; ++j)
       q[n][j] = p[col[n] + (size_t)min(s0 + j, pt.S - 1) * pt.split];
 #pragma unroll
-  for (int j = 0; j < PART_GROUP; ++j) {
+  for (int j = 0; j < PG; ++j) {
     const uint32_t m = s0 + j < pt.S ? 0xFFFFFFFFu : 0u;
 #pragma unroll
     for (int n = 0; n < N; ++n) out[n] += keep_if(q[n][j], m);
   }
 }
 
-template <int N>
+template <int N, int PG>
 MSD_DEV void part_sums(const Parts& pt, int row, const int (&col)[N], float (&out)[N]) {
   const float* p = pt.p + (size_t)row * pt.ld;
 #pragma unroll
   for (int n = 0; n < N; ++n) out[n] = 0.f;
-  part_sums_group<N>(pt, p, 0, col, out);
-  for (int s0 = PART_GROUP; s0 < pt.S; s0 += PART_GROUP) part_sums_group<N>(pt, p, s0, col, out);
+  part_sums_group<N, PG>(pt, p, 0, col, out);
+  for (int s0 = PG; s0 < pt.S; s0 += PG) part_sums_group<N, PG>(pt, p, s0, col, out);
 }
 
-template <int N>
+template <int N, int PG>
 MSD_DEV void part_sums4_group(const Parts& pt, const float* p, int s0, const int (&col)[N],
                               float4 (&out)[N]) {
-  float4 q[N][PART_GROUP];
+  float4 q[N][PG];
 #pragma unroll
   for (int n = 0; n < N; ++n)
 #pragma unroll
-    for (int j = 0; j < PART_GROUP; ++j)
+    for (int j = 0; j < PG; ++j)
       q[n][j] = *reinterpret_cast<const float4*>(p + col[n] +
                                                  (size_t)min(s0 + j, pt.S - 1) * pt.split);
 #pragma unroll
-  for (int j = 0; j < PART_GROUP; ++j) {
+  for (int j = 0; j < PG; ++j) {
     const uint32_t m = s0 + j < pt.S ? 0xFFFFFFFFu : 0u;
 #pragma unroll
     for (int n = 0; n < N; ++n)
@@ -135,28 +142,21 @@ MSD_DEV void part_sums4_group(const Parts& pt, const float* p, int s0, const int
   }
 }
 
-template <int N>
+template <int N, int PG>
 MSD_DEV void part_sums4(const Parts& pt, int row, const int (&col)[N], float4 (&out)[N]) {
   const float* p = pt.p + (size_t)row * pt.ld;
 #pragma unroll
   for (int n = 0; n < N; ++n) out[n] = make_float4(0.f, 0.f, 0.f, 0.f);
-  part_sums4_group<N>(pt, p, 0, col, out);
-  for (int s0 = PART_GROUP; s0 < pt.S; s0 += PART_GROUP)
-    part_sums4_group<N>(pt, p, s0, col, out);
-}
-
-MSD_DEV float part_sum(const Parts& pt, int row, int col) {
-  const int c[1] = {col};
-  float o[1];
-  part_sums<1>(pt, row, c, o);
-  return o[0];
+  part_sums4_group<N, PG>(pt, p, 0, col, out);
+  for (int s0 = PG; s0 < pt.S; s0 += PG) part_sums4_group<N, PG>(pt, p, s0, col, out);
 }
 
 // The same for four consecutive elements (col a multiple of 4).
+template <int PG>
 MSD_DEV float4 part_sum4(const Parts& pt, int row, int col) {
   const int c[1] = {col};
   float4 o[1];
-  part_sums4<1>(pt, row, c, o);
+  part_sums4<1, PG>(pt, row, c, o);
   return o[0];
 }
 
@@ -209,6 +209,7 @@ MSD_DEV float row_rstd(const RowNorm& rn, int row) {
 // (row, head, rotation pair i): a block of ROPE_THREADS threads covers
 // ROPE_THREADS / (hd/2) heads of one row (hd/2 divides ROPE_THREADS).
 constexpr int ROPE_THREADS = 256;
+template <int PG>
 __global__ __launch_bounds__(ROPE_THREADS) void k_rope_kv(Parts qkv, RowNorm rn, int H, int KV,
                                                           int hd, const int* pos,
                                                           const int* row_seq,
@@ -229,7 +230,7 @@ __global__ __launch_bounds__(ROPE_THREADS) void k_rope_kv(Parts qkv, RowNorm rn,
   const float2 t = tab[(size_t)pos[row] * half + i];
   const int cols[2] = {head * hd + i, head * hd + i + half};
   float ac[2];
-  part_sums<2>(qkv, row, cols, ac);
+  part_sums<2, PG>(qkv, row, cols, ac);
   const float r = ssq_end(rn, row, sq);
   const float a = r * ac[0];
   const float c = r * ac[1];
@@ -268,6 +269,7 @@ MSD_DEV float block_sum_1024(float v, float* sh) {
 // x = sum of parts (RN_SET), x + sum (RN_ADD) or x (RN_KEEP); then the
 // RMSNorm of the new x (gain g) and/or a copy of x, as split rows.  One
 // block of 1024 threads per row.
+template <int PG>
 __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, int mode, float* x,
                                                      const uint16_t* g, float eps, uint16_t* xn,
                                                      uint16_t* xb) {
@@ -286,7 +288,7 @@ __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, 
     cols[k] = col0 + min(e, d - 4);
     v[k] = e < d ? *reinterpret_cast<const float4*>(xr + e) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  if (mode != RN_KEEP) part_sums4<U>(pt, row, cols, p);
+  if (mode != RN_KEEP) part_sums4<U, PG>(pt, row, cols, p);
   float ss = 0.f;
 #pragma unroll
   for (int k = 0; k < U; ++k) {
@@ -322,6 +324,7 @@ __global__ __launch_bounds__(1024) void k_resid_norm(Parts pt, int col0, int d, 
 // ssq[row][block].  Grid (ceil(d/256), rows).
 // Four consecutive features per thread; a block covers SSQ_BLOCK features of
 // one row and writes their sum of squares.  d is a multiple of 4.
+template <int PG>
 __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float* x,
                                                const uint16_t* g, uint16_t* xg, uint16_t* xb,
                                                float* ssq, const int* dst, float* feat) {
@@ -333,7 +336,7 @@ __global__ __launch_bounds__(256) void k_resid(Parts pt, int d, int mode, float*
     float* const xr = x + (size_t)row * d + e;
     float4 x4 = *reinterpret_cast<const float4*>(xr);
     if (mode != RN_KEEP) {
-      const float4 p = part_sum4(pt, row, e);
+      const float4 p = part_sum4<PG>(pt, row, e);
       x4 = (mode == RN_SET) ? p : make_float4(x4.x + p.x, x4.y + p.y, x4.z + p.z, x4.w + p.w);
       *reinterpret_cast<float4*>(xr) = x4;
     }
@@ -376,6 +379,7 @@ __global__ __launch_bounds__(256) void k_root_feat(const int* seq_ids, const flo
 // act = silu(gate) * up (split rows) with gate at columns [0, F), up at
 // [off2, off2 + F), both scaled by the row's 1/rms (the GEMM read the
 // un-normalised input).
+template <int PG>
 __global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint16_t* act) {
   const int row = blockIdx.y;
   const int f = blockIdx.x * 1024 + 4 * threadIdx.x;  // F is a multiple of 4
@@ -384,7 +388,7 @@ __global__ __launch_bounds__(256) void k_silu(Parts pt, RowNorm rn, int F, uint1
   ssq_begin(rn, row, sq);
   const int cols[2] = {f, pt.off2 + f};
   float4 gu[2];
-  part_sums4<2>(pt, row, cols, gu);
+  part_sums4<2, PG>(pt, row, cols, gu);
   const float r = ssq_end(rn, row, sq);
   const float4 gt = gu[0], up = gu[1];
   const float g4[4] = {gt.x, gt.y, gt.z, gt.w}, u4[4] = {up.x, up.y, up.z, up.w};
@@ -493,6 +497,7 @@ MSD_DEV void block_merge(const float (*wv)[TOPK_MAX], const int (*wi)[TOPK_MAX],
   wave_select<1>(c, ci, k, out_v, out_i);
 }
 
+template <int PG>
 __global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, int n_slices,
                                                     float* cand_v, int* cand_i, float2* stats,
                                                     float* logits_out) {
@@ -510,7 +515,7 @@ __global__ __launch_bounds__(256) void k_topk_slice(Parts logits, int V, int k, 
 #pragma unroll
   for (int e = 0; e < TOPK_PER; ++e) cols[e] = min(v0 + threadIdx.x + 256 * e, V - 1);
   float raws[TOPK_PER];
-  part_sums<TOPK_PER>(logits, row, cols, raws);
+  part_sums<TOPK_PER, PG>(logits, row, cols, raws);
 #pragma unroll
   for (int e = 0; e < TOPK_PER; ++e) {
     const int v = v0 + threadIdx.x + 256 * e;
@@ -612,6 +617,17 @@ __global__ __launch_bounds__(256) void k_topk_merge(int k, int n_slices, const f
 
 }  // namespace
 
+// Launches kernel template K<PG> with PG = part_group(S).
+#define PG_DISPATCH(S, K, ...)                                       \
+  do {                                                               \
+    switch (part_group(S)) {                                         \
+      case 2: hipLaunchKernelGGL(K<2>, __VA_ARGS__); break;          \
+      case 4: hipLaunchKernelGGL(K<4>, __VA_ARGS__); break;          \
+      case 8: hipLaunchKernelGGL(K<8>, __VA_ARGS__); break;          \
+      default: hipLaunchKernelGGL(K<MAX_PART_GROUP>, __VA_ARGS__);   \
+    }                                                                \
+  } while (0)
+
 void launch_embed(const uint16_t* E, const int* tokens, const int* vis_idx,
                   const uint16_t* visual, int rows, int d, float* x, hipStream_t st) {
   if (rows <= 0) return;
@@ -641,16 +657,25 @@ void launch_rope_kv(Parts qkv, RowNorm rn, int rows, int H, int KV, int hd, cons
                     uint16_t* q, uint16_t* kc, uint16_t* vc, int S, hipStream_t st) {
   if (rows <= 0) return;
   const int per_block = ROPE_THREADS / (hd / 2);
-  hipLaunchKernelGGL(k_rope_kv, dim3(rows, (H + 2 * KV + per_block - 1) / per_block),
-                     dim3(ROPE_THREADS), 0, st, qkv, rn, H, KV, hd, pos,
-                     row_seq, row_slot, rope_tab, q, kc, vc, S);
+  const dim3 grid(rows, (H + 2 * KV + per_block - 1) / per_block);
+  PG_DISPATCH(qkv.S, k_rope_kv, grid, dim3(ROPE_THREADS), 0, st, qkv, rn, H, KV, hd, pos, row_seq,
+              row_slot, rope_tab, q, kc, vc, S);
 }
 
 void launch_resid_norm(Parts pt, int col0, int rows, int d, int mode, float* x,
                        const uint16_t* g, float eps, uint16_t* xn, uint16_t* xb, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_resid_norm, dim3(rows), dim3(1024), 0, st, pt, col0, d, mode, x, g, eps, xn,
-                     xb);
+  // groups of at most 8: at 16 the 1024-thread blocks' registers spill
+  const int pg = part_group(std::min(pt.S, 8));
+  if (pg == 2)
+    hipLaunchKernelGGL(k_resid_norm<2>, dim3(rows), dim3(1024), 0, st, pt, col0, d, mode, x, g,
+                       eps, xn, xb);
+  else if (pg == 4)
+    hipLaunchKernelGGL(k_resid_norm<4>, dim3(rows), dim3(1024), 0, st, pt, col0, d, mode, x, g,
+                       eps, xn, xb);
+  else
+    hipLaunchKernelGGL(k_resid_norm<8>, dim3(rows), dim3(1024), 0, st, pt, col0, d, mode, x, g,
+                       eps, xn, xb);
 }
 
 void launch_root_feat(int n_seq, const int* seq_ids, const float* feat, int feat_stride, int d,
@@ -662,14 +687,14 @@ void launch_root_feat(int n_seq, const int* seq_ids, const float* feat, int feat
 
 void launch_silu(Parts pt, RowNorm rn, int rows, int F, uint16_t* act, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_silu, dim3((F + 1023) / 1024, rows), dim3(256), 0, st, pt, rn, F, act);
+  PG_DISPATCH(pt.S, k_silu, dim3((F + 1023) / 1024, rows), dim3(256), 0, st, pt, rn, F, act);
 }
 
 void launch_resid(Parts pt, int rows, int d, int mode, float* x, const uint16_t* g, uint16_t* xg,
                   uint16_t* xb, float* ssq, hipStream_t st, const int* dst, float* feat) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_resid, dim3(ssq_blocks(d), rows), dim3(256), 0, st, pt, d, mode, x, g, xg,
-                     xb, ssq, dst, feat);
+  PG_DISPATCH(pt.S, k_resid, dim3(ssq_blocks(d), rows), dim3(256), 0, st, pt, d, mode, x, g, xg,
+              xb, ssq, dst, feat);
 }
 
 void launch_fc_input(const uint16_t* h, const float* hf, const int* h_row, const uint16_t* E,
@@ -692,8 +717,8 @@ void launch_topk(Parts logits, int rows, int V, int k, int* idx, float* val, flo
   float* cand_v = scratch;
   int* cand_i = reinterpret_cast<int*>(cand_v + (size_t)rows * n_slices * TOPK_MAX);
   float2* stats = reinterpret_cast<float2*>(cand_i + (size_t)rows * n_slices * TOPK_MAX);
-  hipLaunchKernelGGL(k_topk_slice, dim3(rows * n_slices), dim3(256), 0, st, logits, V, k, n_slices,
-                     cand_v, cand_i, stats, logits_out);
+  PG_DISPATCH(logits.S, k_topk_slice, dim3(rows * n_slices), dim3(256), 0, st, logits, V, k,
+              n_slices, cand_v, cand_i, stats, logits_out);
   hipLaunchKernelGGL(k_topk_merge, dim3(rows), dim3(256), 0, st, k, n_slices, cand_v, cand_i,
                      stats, idx, val, lse);
 }
