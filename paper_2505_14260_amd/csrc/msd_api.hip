@@ -140,16 +140,21 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
   p.att_items = lim.max_batch * m.n_kv_heads * qtiles;
   p.attn_floats =
       attn_partial_floats(lim.max_batch, m.n_kv_heads, qtiles, ATT_MAX_CHUNKS, m.head_dim);
-  // GEMM partials of one 64-row launch, for the largest weight of the model
-  const int mm = std::min(64, p.rows_max);
+  // GEMM partials of one launch of up to 64 rows, for the largest weight of
+  // the model (the plans change at 16, 32 and 64 rows; within each class the
+  // partials grow with the rows)
   const int d = m.d_model, F = m.ffn_dim, hh = m.n_heads * m.head_dim;
-  const size_t cand[6] = {gemm_part_floats(mm, p.ld_qkv, d, 1, GEMM_WGS),
-                          gemm_part_floats(mm, d, hh, 1, GEMM_WGS),
-                          gemm_part_floats(mm, F, d, 2, GEMM_WGS),
-                          gemm_part_floats(mm, d, F, 1, GEMM_WGS),
-                          gemm_part_floats(mm, d, 2 * d, 1, GEMM_WGS),
-                          gemm_part_floats(mm, m.vocab, d, 1, GEMM_WGS)};
-  p.part_floats = *std::max_element(cand, cand + 6);
+  p.part_floats = 0;
+  for (int mm : {16, 32, 64}) {
+    mm = std::min(mm, p.rows_max);
+    const size_t cand[6] = {gemm_part_floats(mm, p.ld_qkv, d, 1, GEMM_WGS),
+                            gemm_part_floats(mm, d, hh, 1, GEMM_WGS),
+                            gemm_part_floats(mm, F, d, 2, GEMM_WGS),
+                            gemm_part_floats(mm, d, F, 1, GEMM_WGS),
+                            gemm_part_floats(mm, d, 2 * d, 1, GEMM_WGS),
+                            gemm_part_floats(mm, m.vocab, d, 1, GEMM_WGS)};
+    p.part_floats = std::max(p.part_floats, *std::max_element(cand, cand + 6));
+  }
   // full products of one many-row launch (every GEMM but the LM head, which
   // always runs in CHUNK-row launches)
   if (p.rows_max > BIG_MIN_ROWS) {
@@ -205,7 +210,7 @@ struct msd_ctx {
   uint16_t *xn, *xb, *fcin, *q, *ao, *act, *h;
   float* part;
   float* sink;          // GEMM rows past M
-  uint16_t* gemm_zero;  // zero block the GEMM ring reads after its last tile
+  uint16_t* gemm_zero;  // zero block the many-row GEMM reads for tiles past N
   float* ssq;
   Rows rows;
   int *nxt, *prefix, *seq_ids;
@@ -451,11 +456,13 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
     *out = Parts{c->part, S, (size_t)M * nt * 64 * nw, nt * 64 * nw, nt * 64};
     return MSD_OK;
   }
+  const GemmPlan pl = plan_gemm(M, N, K, W2 ? 2 : 1, c->gs.target_wgs);
+  if ((size_t)pl.S * M * pl.ldp > c->plan.part_floats)
+    return fail(c, MSD_ERR_INVALID_ARG, "internal: GEMM partials exceed their buffer");
   GemmScratch gs = c->gs;
   trace_events(c, kind, M, N, K, &gs.ev_start, &gs.ev_stop);
-  launch_gemm(X, ldx, M, W, W2, N, K, c->part, c->sink, c->gemm_zero, gs, c->st);
+  launch_gemm(X, ldx, M, W, W2, N, K, c->part, c->sink, gs, c->st);
   LAUNCHED(c);
-  const GemmPlan pl = plan_gemm(M, N, K, W2 ? 2 : 1, c->gs.target_wgs);
   *out = Parts{c->part, pl.S, (size_t)M * pl.ldp, pl.ldp, pl.off2};
   return MSD_OK;
 }

@@ -69,7 +69,6 @@ struct GemmArgs {
   size_t part_split;        // floats between consecutive chunks (M * ldp)
   int ldp, off2;            // floats between rows; column offset of W2's products
   float* sink;              // 1 KB written by padded rows
-  const uint16_t* dummy;    // gemm_dummy_elems() zeros read by the ring after the last tile
 };
 
 struct GemmPlan {
@@ -108,8 +107,7 @@ size_t stream_span_bytes();
 void launch_stream_read(const uint16_t* buf, size_t spans, int wgs, unsigned* sink,
                         hipStream_t st);
 void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2, int N,
-                 int K, float* part, float* sink, const uint16_t* dummy, const GemmScratch& sc,
-                 hipStream_t st);
+                 int K, float* part, float* sink, const GemmScratch& sc, hipStream_t st);
 
 // Partial sums as seen by a consumer: value(m, n) = sum_s p[s*split + m*ld + n];
 // the second weight's products are at column n + off2.
