@@ -99,6 +99,7 @@ constexpr int TOPK = 16;
 constexpr int MAX_VOCAB = 262144;  // 128 top-k slices of 2048 logits
 constexpr int POOL = 1024;              // dynamic-tree candidates per sequence
 constexpr int STAGE_INTS = 1 << 16;
+constexpr int ACC_BACK_INTS = 8 * MSD_MAX_TREE + 8 + 8 + 1;
 // GEMM launch shape: about one workgroup per CU streams best (more
 // concurrent weight streams per CU lower the achieved HBM bandwidth).
 constexpr int GEMM_WGS = 256;
@@ -333,11 +334,16 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->pend_h = cv.take<uint16_t>((size_t)B * PEND * 2 * d);
   t->dfeat = cv.take<float>((size_t)B * FEAT * d);
   t->acc_path = cv.take<int>((size_t)B * MSD_MAX_TREE);
-  t->acc_n = cv.take<int>(B);
-  t->acc_emit = cv.take<int>((size_t)B * MSD_MAX_TREE);
+  // what the host reads after an acceptance, back to back so that one copy
+  // brings it: acc_emit [8][MSD_MAX_TREE], acc_n [8], tree_err [8],
+  // att_place [1] (at most eight sequences per context)
+  int* const accb = cv.take<int>(ACC_BACK_INTS);
+  t->acc_emit = accb;
+  t->acc_n = accb + 8 * MSD_MAX_TREE;
+  t->tree_err = t->acc_n + 8;
+  t->att_place = t->tree_err + 8;
   t->acc_slot = cv.take<int>((size_t)B * MSD_MAX_TREE);
   t->feat_idx = cv.take<int>(B);
-  t->tree_err = cv.take<int>(B);
   t->tk_idx = cv.take<int>((size_t)p.lrows * TOPK);
   t->tk_val = cv.take<float>((size_t)p.lrows * TOPK);
   t->tk_lse = cv.take<float>(p.lrows);
@@ -361,7 +367,6 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->att_po = cv.take<float>(p.attn_floats);
   t->att_ml = cv.take<float>(p.attn_floats / m.head_dim * 2 + 64);
   t->att_cnt = cv.take<int>(p.att_items);
-  t->att_place = cv.take<int>(1);
   t->rope = cv.take<float2>((size_t)lim.max_seq * (m.head_dim / 2));
   t->tk_scratch = cv.take<float>(topk_scratch_floats(p.lrows, m.vocab));
   return cv.off + 256;
@@ -814,15 +819,11 @@ int finish_accept(msd_ctx* c, int n_seq, const int32_t* seqs_h, int T, int32_t* 
   launch_commit(n_seq, c->seq_ids, c->acc_path, c->acc_n, c->acc_emit, c->h, T, d, c->pend_h,
                 c->pend_next, c->pend_n, PEND, c->d_len, c->d_root, c->st);
   LAUNCHED(c);
-  int* back = c->stage + STAGE_INTS - (MSD_MAX_TREE + 2) * 8 - 64;
-  HIPC(c, hipMemcpyAsync(back, c->acc_emit, sizeof(int) * MSD_MAX_TREE * n_seq,
-                         hipMemcpyDeviceToHost, c->st));
-  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8, c->acc_n, sizeof(int) * n_seq,
-                         hipMemcpyDeviceToHost, c->st));
-  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8 + 8, c->tree_err, sizeof(int) * n_seq,
-                         hipMemcpyDeviceToHost, c->st));
-  HIPC(c, hipMemcpyAsync(back + MSD_MAX_TREE * 8 + 16, c->att_place, sizeof(int),
-                         hipMemcpyDeviceToHost, c->st));
+  // the staging block's last 64 ints take other small read-backs
+  static_assert(ACC_BACK_INTS <= 544, "acceptance read-back block");
+  int* back = c->stage + STAGE_INTS - 64 - 544;
+  HIPC(c, hipMemcpyAsync(back, c->acc_emit, sizeof(int) * ACC_BACK_INTS, hipMemcpyDeviceToHost,
+                         c->st));
   HIPC(c, hipStreamSynchronize(c->st));
   c->verified_T = 0;
   if (back[MSD_MAX_TREE * 8 + 16]) {
