@@ -155,7 +155,14 @@ int msd_workspace_size(const msd_model_desc* m, const msd_limits* lim, size_t* b
  * caches (enqueued on the stream, waited for before returning).  After it
  * returns, the library reads the embedding table, the norm gains and the
  * packed copies only: the row-major matrices may be released; every other
- * pointer must stay valid until msd_destroy. */
+ * pointer must stay valid until msd_destroy.
+ * When lim->max_prompt allows prompt GEMMs of 512 rows or more, those run on
+ * rocBLAS (bf16 inputs, float32 results) against a row-major copy of one
+ * weight at a time that the library unpacks into the workspace: msd_create
+ * then also creates a rocBLAS handle on the stream, gives it a 32 MB
+ * workspace carved from bufs->workspace, and runs the prompt GEMM shapes
+ * once so that rocBLAS loads their kernels here rather than in the first
+ * msd_prefill.  MSD_ERR_HIP if the handle cannot be set up. */
 int msd_create(const msd_model_desc* m, const msd_limits* lim,
                const msd_target_weights* tw, const msd_draft_weights* dw,
                const msd_buffers* bufs, void* stream, msd_ctx** out);

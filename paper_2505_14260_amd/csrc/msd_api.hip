@@ -105,6 +105,10 @@ constexpr int ACC_BACK_INTS = 8 * MSD_MAX_TREE + 8 + 8 + 1;
 constexpr int GEMM_WGS = 256;
 constexpr int CHUNK = 64;         // rows per weight-streaming GEMM launch
 constexpr int BIG_CHUNK = 1024;   // rows per many-row GEMM launch
+// many-row launches of at least this many rows run on rocBLAS (bf16 GEMMs
+// with float32 results, the weight unpacked to row-major in the workspace)
+constexpr int BLAS_MIN_ROWS = 512;
+constexpr size_t BLAS_WS_BYTES = (size_t)32 << 20;  // rocBLAS's workspace
 // Passes over more rows than this use the many-row GEMM (below it, a few
 // weight-streaming launches of CHUNK rows are faster).
 constexpr int BIG_MIN_ROWS = 256;
@@ -129,6 +133,7 @@ struct Plan {
   int rows_max, lrows, ld_qkv;
   int att_items;  // tree-attention items (sequence, kv head, query tile)
   size_t attn_floats, part_floats;
+  size_t wrm_elems;  // row-major copy of the largest layer weight (0: no rocBLAS path)
 };
 
 Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
@@ -164,6 +169,9 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
     const size_t w = std::max({ldp(p.ld_qkv, 1), ldp(d, 1), ldp(F, 2)});
     p.part_floats = std::max(p.part_floats, big * w);
   }
+  p.wrm_elems = 0;
+  if (std::min(BIG_CHUNK, p.rows_max) >= BLAS_MIN_ROWS)
+    p.wrm_elems = std::max({(size_t)p.ld_qkv * d, (size_t)d * hh, (size_t)F * d, (size_t)d * 2 * d});
   return p;
 }
 
@@ -212,6 +220,13 @@ struct msd_ctx {
   float* part;
   float* sink;          // GEMM rows past M
   uint16_t* gemm_zero;  // zero block the many-row GEMM reads for tiles past N
+  uint16_t* wrm;        // two row-major bf16 weight slots (rocBLAS prompt GEMMs)
+  const uint16_t* wrm_src[2] = {nullptr, nullptr};  // packed weight each slot holds
+  void* blas_ws;        // rocBLAS's workspace (BLAS_WS_BYTES)
+  rocblas_handle blas = nullptr;  // prompt GEMMs, when plan.wrm_elems > 0
+  ~msd_ctx() {
+    if (blas) (void)rocblas_destroy_handle(blas);
+  }
   float* ssq;
   Rows rows;
   int *nxt, *prefix, *seq_ids;
@@ -311,6 +326,8 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->part = cv.take<float>(p.part_floats);
   t->sink = cv.take<float>(256);
   t->gemm_zero = cv.take<uint16_t>(gemm_dummy_elems());
+  t->wrm = p.wrm_elems ? cv.take<uint16_t>(2 * p.wrm_elems) : nullptr;
+  t->blas_ws = p.wrm_elems ? (void*)cv.take<char>(BLAS_WS_BYTES) : nullptr;
   t->ssq = cv.take<float>((size_t)R * ssq_blocks(d));
   t->q = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
   t->ao = cv.take<uint16_t>((size_t)R * 2 * m.n_heads * m.head_dim);
@@ -446,6 +463,41 @@ void trace_events(msd_ctx* c, int kind, int M, int N, int K, hipEvent_t* e0, hip
   c->trace.push_back(r);
 }
 
+// A many-row product on rocBLAS: each weight is unpacked from the streaming
+// layout to row-major bf16 in a workspace slot (slot w for the pass's
+// weight w; kept for the pass's further row chunks, forgotten at the start
+// of every layer pass), then
+//   C[m][w * off2 + n] = X_hi[m] . W[n] + X_lo[m] . W[n]   (float32, row stride ldp)
+// as two bf16 GEMMs with float32 accumulation and results (the second adds
+// to the first), issued column-major: C^T = W X^T.  The split rows' hi and
+// lo halves are the strided views X and X + K (row stride ldx).
+int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
+              const uint16_t* W2, int N, int K, int ldp, int off2) {
+  if ((size_t)N * K > c->plan.wrm_elems || (size_t)M * ldp > c->plan.part_floats)
+    return fail(c, MSD_ERR_INVALID_ARG, "internal: prompt GEMM exceeds its buffers");
+  const float one = 1.f, zero = 0.f;
+  for (int w = 0; w < (W2 ? 2 : 1); ++w) {
+    const uint16_t* src = w ? W2 : W;
+    uint16_t* wrm = c->wrm + (size_t)w * c->plan.wrm_elems;
+    if (c->wrm_src[w] != src) {
+      launch_unpack(src, N, K, wrm, c->st);
+      LAUNCHED(c);
+      c->wrm_src[w] = src;
+    }
+    float* C = c->part + (size_t)w * off2;
+    for (int h = 0; h < 2; ++h) {
+      const rocblas_status st = rocblas_gemm_ex(
+          c->blas, rocblas_operation_transpose, rocblas_operation_none, N, M, K, &one, wrm,
+          rocblas_datatype_bf16_r, K, X + (size_t)h * K, rocblas_datatype_bf16_r, ldx,
+          h ? &one : &zero, C, rocblas_datatype_f32_r, ldp, C, rocblas_datatype_f32_r, ldp,
+          rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+      if (st != rocblas_status_success)
+        return fail(c, MSD_ERR_HIP, std::string("rocblas_gemm_ex: ") + rocblas_status_to_string(st));
+    }
+  }
+  return MSD_OK;
+}
+
 // Partial products of rows [0, M) (M <= 64) of the split rows X (row stride
 // ldx = 2K) against the packed weight W [N][K] (and W2); returns the view the
 // consumer sums.
@@ -454,6 +506,12 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
   if (M > CHUNK) {
     if (kind == GK_LMHEAD || M > BIG_CHUNK)
       return fail(c, MSD_ERR_INVALID_ARG, "internal: GEMM launch with too many rows");
+    if (c->blas && M >= BLAS_MIN_ROWS) {
+      const int nt = (N + 63) / 64, nw = W2 ? 2 : 1;
+      TRY(blas_gemm(c, X, ldx, M, W, W2, N, K, nt * 64 * nw, nt * 64));
+      *out = Parts{c->part, 1, (size_t)M * nt * 64 * nw, nt * 64 * nw, nt * 64};
+      return MSD_OK;
+    }
     const int S = launch_gemm_big(X, ldx, M, W, W2, N, K, c->part, c->plan.part_floats,
                                   c->gemm_zero, c->st);
     LAUNCHED(c);
@@ -536,6 +594,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
   const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim, F = m.ffn_dim;
   const int nl = draft ? 1 : m.n_layers;
   const int ch = row_chunk(rows);
+  c->wrm_src[0] = c->wrm_src[1] = nullptr;
   const int B = c->lim.max_batch, S = c->lim.max_seq;
   const size_t layer_kv = (size_t)B * KV * S * hd;
   for (int l = 0; l < nl; ++l) {
@@ -1104,6 +1163,35 @@ int train_pass(msd_ctx* c, int n, const void* visual_d, double* loss3) {
   return MSD_OK;
 }
 
+// rocBLAS loads the kernels of a GEMM shape on its first use (about 0.2 s
+// for a context's first prompt).  Run once here, on layer 0's weights and
+// whatever the activation buffers hold, each prompt GEMM shape at the row
+// counts this context's prompts will use: full BIG_CHUNK launches and the
+// launch of a max_prompt-row prompt's last chunk.  The results are
+// discarded.
+int warm_blas(msd_ctx* c) {
+  if (!c->blas) return MSD_OK;
+  const msd_model_desc& m = c->m;
+  const int d = m.d_model, F = m.ffn_dim, hh = m.n_heads * m.head_dim;
+  const int rows = c->lim.max_prompt;
+  std::vector<int> ms;
+  if (rows >= BIG_CHUNK) ms.push_back(BIG_CHUNK);
+  const int tail = rows % BIG_CHUNK;
+  if (tail >= BLAS_MIN_ROWS) ms.push_back(tail);
+  const PackedLayer& p = c->players[0];
+  for (int M : ms) {
+    Parts pt;
+    TRY(gemm(c, GK_QKV, c->xn, 2 * d, M, p.qkv, nullptr, c->plan.ld_qkv, d, &pt));
+    TRY(gemm(c, GK_O, c->ao, 2 * hh, M, p.o, nullptr, d, hh, &pt));
+    TRY(gemm(c, GK_GATEUP, c->xn, 2 * d, M, p.g, p.u, F, d, &pt));
+    TRY(gemm(c, GK_DOWN, c->act, 2 * F, M, p.d, nullptr, d, F, &pt));
+    TRY(gemm(c, GK_FC, c->fcin, 4 * d, M, c->fc_p, nullptr, d, 2 * d, &pt));
+  }
+  c->wrm_src[0] = c->wrm_src[1] = nullptr;
+  HIPC(c, hipStreamSynchronize(c->st));
+  return MSD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1167,6 +1255,18 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
   c->dk = (uint16_t*)bufs->draft_k;
   c->dv = (uint16_t*)bufs->draft_v;
   carve(c, *m, *lim, (char*)bufs->workspace);
+  if (c->plan.wrm_elems) {
+    // prompt GEMMs on rocBLAS, on the context's stream, in a workspace carved
+    // from the caller's buffer (the context's destructor frees the handle)
+    rocblas_handle hb = nullptr;
+    const bool ok = rocblas_create_handle(&hb) == rocblas_status_success;
+    if (ok) c->blas = hb;
+    if (!ok || rocblas_set_stream(c->blas, c->st) != rocblas_status_success ||
+        rocblas_set_workspace(c->blas, c->blas_ws, BLAS_WS_BYTES) != rocblas_status_success) {
+      delete c;
+      return fail(nullptr, MSD_ERR_HIP, "rocBLAS handle for the prompt GEMMs");
+    }
+  }
   {
     hipError_t e = hipGetDevice(&c->device);
     void* sp = nullptr;
@@ -1227,6 +1327,7 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     return MSD_OK;
   };
   r = init();
+  if (r == MSD_OK) r = warm_blas(c);
   if (r != MSD_OK) {
     g_err = c->err;
     (void)hipHostFree(c->stage);
