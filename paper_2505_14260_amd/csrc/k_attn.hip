@@ -10,8 +10,9 @@
 // their states through LDS into one partial per workgroup; a combine kernel
 // merges the chunks in fixed order.  Query rows of a tile are (node,
 // head-in-group) pairs so a GQA group shares every K/V load.
-// Causal mode (prompt processing): one wave per (sequence, head, 32
-// consecutive query rows) over all keys up to the diagonal.
+// Causal mode (prompt processing): one workgroup per (sequence, head, 32
+// consecutive query rows); its waves split the keys up to the diagonal and
+// merge through LDS.
 //
 // Per 32-key block: S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows,
 // B = Q^T), then O^T += V^T P^T (A = V^T rows of the transposed V cache,
@@ -586,16 +587,27 @@ __global__ __launch_bounds__(64 * NWV, 2) void k_tree_attn(AttnArgs a) {
     __hip_atomic_store(a.att_cnt + item, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Causal attention of a prompt: one workgroup of CAUSAL_WAVES waves per
+// (sequence, head, 32-row query tile).  The tile's key blocks [0, end of its
+// last row) are split into contiguous quarters, one per wave, each with its
+// own online softmax; the waves' states merge through LDS (weights
+// exp(m_w - max)) and the workgroup writes the tile's output rows.  Tiles
+// are dealt longest first (the last query tiles see the most keys).
+constexpr int CAUSAL_WAVES = 4;
 template <int HD>
-__global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int n_items = a.n_seq * a.H * a.qtiles;
-  if (wid >= n_items) return;
-  int t = wid;
-  const int qt = t % a.qtiles; t /= a.qtiles;
-  const int head = t % a.H;
-  const int sidx = t / a.H;
+__global__ __launch_bounds__(64 * CAUSAL_WAVES, 2) void k_causal_attn(AttnArgs a) {
+  constexpr int NWV = CAUSAL_WAVES;
+  constexpr int E = 32 * HD;  // state elements of one wave
+  __shared__ float so[NWV * E];
+  __shared__ float sml[NWV][32][2];
+  __shared__ float wgt[NWV][32];
+  __shared__ float colm[32];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n_sh = a.n_seq * a.H;
+  const int qt = a.qtiles - 1 - (int)blockIdx.x / n_sh;  // longest tiles first
+  const int sh = (int)blockIdx.x % n_sh;
+  const int head = sh % a.H;
+  const int sidx = sh / a.H;
   const int b = a.seq[sidx];
   const int P = a.prefix[sidx];
   const int g = head / (a.H / a.KV);
@@ -608,17 +620,62 @@ __global__ __launch_bounds__(256) void k_causal_attn(AttnArgs a) {
   load_q<HD>(qh, ql, a.q + (size_t)(sidx * a.nq + node) * 2 * HH + (size_t)head * HD, HH);
   const uint16_t* kbase = a.kc + (size_t)(b * a.KV + g) * a.S * HD;
   const uint16_t* vbase = a.vc + (size_t)(b * a.KV + g) * HD * a.S;
+  const int last = min(qt * 32 + 32, a.nq);
+  const int k1 = P + last;  // keys of the tile: [0, k1)
+  const int nb = (k1 + 31) / 32;
+  const int per = (nb + NWV - 1) / NWV;
+  const int kb0 = min(w * per, nb) * 32;
+  const int kb1 = min(kb0 + per * 32, k1);
+  const int my_last = P + node;
   AttnState<HD> st;
   init_state<HD>(st);
-  const int last = min(qt * 32 + 32, a.nq);
-  const int k1 = P + last;
-  const int my_last = P + node;
   uint4 kf[HD / 16], vf[HD / 32][2];
-  attend_prefetch<HD>(kf, vf, kbase, vbase, a.S, 0);
-  attend_range<HD>(st, QRegs<HD>{qh, ql}, kf, vf, kbase, vbase, a.S, 0, k1, k1, a.scale,
+  attend_prefetch<HD>(kf, vf, kbase, vbase, a.S, min(kb0, ((k1 - 1) / 32) * 32));
+  attend_range<HD>(st, QRegs<HD>{qh, ql}, kf, vf, kbase, vbase, a.S, kb0, kb1, k1, a.scale,
                    [&](int key) { return key <= my_last; });
-  store_final<HD>(st, a.out + (size_t)(sidx * a.nq + node) * 2 * a.H * HD + (size_t)head * HD,
-                  a.H * HD, valid);
+  // merge the waves' states
+#pragma unroll
+  for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) so[w * E + (dt * 16 + r) * 64 + lane] = st.o[dt][r];
+  if (lane < 32) {
+    sml[w][lane][0] = st.m;
+    sml[w][lane][1] = st.l;
+  }
+  lds_barrier();
+  if (threadIdx.x < 32) {
+    const int jj = threadIdx.x;
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < NWV; ++q) M = fmaxf(M, sml[q][jj][0]);
+    float l = 0.f;
+#pragma unroll
+    for (int q = 0; q < NWV; ++q) {
+      const float mq = sml[q][jj][0];
+      const float wq = (M == -INFINITY || mq == -INFINITY) ? 0.f : __expf(mq - M);
+      wgt[q][jj] = wq;
+      l += wq * sml[q][jj][1];
+    }
+    colm[jj] = l > 0.f ? 1.f / l : 0.f;
+  }
+  lds_barrier();
+  // thread -> (query column jj, 8 consecutive dims): one 16-byte store each
+  // for the hi and lo halves of the output row
+  for (int u = threadIdx.x; u < 32 * (HD / 8); u += 64 * NWV) {
+    const int jj = u & 31, d0 = 8 * (u >> 5);
+    const int nd = qt * 32 + jj;
+    if (nd >= a.nq) continue;
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int e = state_index<HD>(jj, d0 + i);
+      float o = 0.f;
+#pragma unroll
+      for (int q = 0; q < NWV; ++q) o += wgt[q][jj] * so[q * E + e];
+      v[i] = o * colm[jj];
+    }
+    store_split8(a.out + (size_t)(sidx * a.nq + nd) * 2 * HH + (size_t)head * HD + d0, HH, v);
+  }
 }
 
 }  // namespace
@@ -649,7 +706,7 @@ void launch_tree_attention(AttnArgs a, hipStream_t st, hipEvent_t ev0, hipEvent_
 
 void launch_causal_attention(AttnArgs a, hipStream_t st) {
   const int items = a.n_seq * a.H * a.qtiles;
-  dim3 grid((items + 3) / 4);
+  dim3 grid(items);
   if (a.hd == 128)
     hipLaunchKernelGGL(k_causal_attn<128>, grid, dim3(256), 0, st, a);
   else
