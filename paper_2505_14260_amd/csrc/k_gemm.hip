@@ -368,7 +368,12 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
     for (int w = 0; w < NW; ++w)
 #pragma unroll
       for (int t = 0; t < MT; ++t) acc[j][w][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
+  // the ring slot of sequence block q is q % P whatever the chunk h (a
+  // chunk holds NT * NKB blocks, a multiple of P), so the chunk loop of the
+  // SwiGLU pair over more than two chunks stays rolled: unrolled, its
+  // registers spill (single weights keep it unrolled: 3 us faster on the 7B
+  // LM head at 61 rows)
+#pragma unroll((NC == 2 || NW == 1) ? NC : 1)
   for (int h = 0; h < NC; ++h) {
     if (h >= 1) {
       // the next X chunk: its loads go out before the barrier (every wave
@@ -383,9 +388,9 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
       }
       lds_barrier();
     }
-#define MSD_GEMM2_STEP(Q, J)                                                                  \
+#define MSD_GEMM2_STEP(Q, J, R)                                                               \
   {                                                                                          \
-    const int q_ = (Q), j_ = (J), r_ = q_ % P;                                               \
+    const int q_ = (Q), j_ = (J), r_ = (R);                                                  \
     _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                          \
       _Pragma("unroll") for (int w = 0; w < NW; ++w)                                         \
       _Pragma("unroll") for (int t = 0; t < MT; ++t)                                         \
@@ -416,7 +421,7 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
         uint4 fh[MT][4], fl[MT][4];
         MSD_GEMM2_FRAGS(p)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) MSD_GEMM2_STEP((h * NKB + p) * NT + j, j)
+        for (int j = 0; j < NT; ++j) MSD_GEMM2_STEP((h * NKB + p) * NT + j, j, (p * NT + j) % P)
       }
     } else {
 #pragma unroll
@@ -425,7 +430,7 @@ __global__ __launch_bounds__(256) void k_gemm2(GemmArgs a) {
         for (int p = 0; p < NKB; ++p) {
           uint4 fh[MT][4], fl[MT][4];
           MSD_GEMM2_FRAGS(p)
-          MSD_GEMM2_STEP((h * NT + j) * NKB + p, j)
+          MSD_GEMM2_STEP((h * NT + j) * NKB + p, j, p % P)
         }
     }
 #undef MSD_GEMM2_STEP
@@ -824,13 +829,16 @@ void launch_fk(dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t 
     hipLaunchKernelGGL((k_gemm_fk<MT, NKB, P, NT>), grid, dim3(256), lds, st, a);
 }
 
+// The SwiGLU pair over more than two chunks takes at most four tiles per
+// workgroup (PAIR_NC_MAX_TILES): at five its registers spill.
+constexpr int PAIR_NC_MAX_TILES = 4;
 template <int MT, int NW, int NC = 2>
 void launch_pair_nt(int nt, dim3 grid, const GemmArgs& a, const GemmScratch& sc, hipStream_t st) {
   if (nt == 1) launch_pair<MT, NW, 1, NC>(grid, a, sc, st);
   else if (nt == 2) launch_pair<MT, NW, 2, NC>(grid, a, sc, st);
   else if (nt == 3) launch_pair<MT, NW, 3, NC>(grid, a, sc, st);
   else if (nt == 4) launch_pair<MT, NW, 4, NC>(grid, a, sc, st);
-  else launch_pair<MT, NW, 5, NC>(grid, a, sc, st);
+  else if constexpr (NW == 1 || NC == 2) launch_pair<MT, NW, 5, NC>(grid, a, sc, st);
 }
 
 // Streaming read of a buffer with the weight stream's access pattern: every
@@ -973,15 +981,16 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
       p.ms = 1;
     }
   }
-  // 64-row passes of single weights: four or three K chunks per workgroup
-  // where that writes fewer partials on about as many workgroups, each with
+  // 64-row passes: four or three K chunks per workgroup where that writes
+  // fewer partials.  Single weights: on about as many workgroups, each with
   // four tiles or more to amortise the X restage between chunks (the 7B LM
-  // head at 61 rows: 8 -> 2 partials, 66.6 -> 55.9 us).  Not with fewer
-  // tiles (7B down on 256 workgroups of two tiles: 24.9 -> 26.8 us), fewer
-  // workgroups (7B q/k/v 27.2 -> 31.0 us on 192 instead of 256), nor for
-  // the SwiGLU pair, whose accumulators then spill (Qwen-shaped gate+up
-  // 59.3 -> 77.2 us).
-  if (p.MT == 4 && nw == 1 && !p.fk && !p.ms) {
+  // head at 61 rows: 8 -> 2 partials, 66.6 -> 55.9 us); not with fewer
+  // tiles (7B down on 256 workgroups of two tiles: 24.9 -> 26.8 us) or
+  // fewer workgroups (7B q/k/v 27.2 -> 31.0 us on 192 instead of 256).  The
+  // SwiGLU pair: while three quarters of the target workgroups stay busy,
+  // since its consumer reads every partial of both weights (Qwen-shaped
+  // 61-row verify 4.71 -> 4.59 ms with 2 partials instead of 4).
+  if (p.MT == 4 && !p.fk && !p.ms) {
     const int S1 = (p.nkt + p.nkb - 1) / p.nkb;
     for (int nc = 4; nc >= 3; --nc) {
       const int Sn = (S1 + nc - 1) / nc;
@@ -994,7 +1003,9 @@ GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs) {
         ++pern;
         Gn = (p.n_tiles + pern - 1) / pern;
       }
-      if (pern >= 4 && pern <= PAIR_MAX_TILES && 20 * Sn * Gn >= 19 * p.S * p.G) {
+      const bool keep = nw == 2 ? 4 * Sn * Gn >= 3 * target_wgs : 20 * Sn * Gn >= 19 * p.S * p.G;
+      const int max_tiles = nw == 2 ? PAIR_NC_MAX_TILES : PAIR_MAX_TILES;
+      if ((nw == 2 || pern >= 4) && pern <= max_tiles && keep) {
         p.pair = nc;
         p.S = Sn;
         p.G = Gn;
@@ -1050,11 +1061,13 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
     return;
   }
   if (pl.pair == 4) {
-    launch_pair_nt<4, 1, 4>(pl.per, grid, a, sc, st);
+    if (nw == 2) launch_pair_nt<4, 2, 4>(pl.per, grid, a, sc, st);
+    else launch_pair_nt<4, 1, 4>(pl.per, grid, a, sc, st);
     return;
   }
   if (pl.pair == 3) {
-    launch_pair_nt<4, 1, 3>(pl.per, grid, a, sc, st);
+    if (nw == 2) launch_pair_nt<4, 2, 3>(pl.per, grid, a, sc, st);
+    else launch_pair_nt<4, 1, 3>(pl.per, grid, a, sc, st);
     return;
   }
   if (pl.pair == 2) {
