@@ -15,8 +15,10 @@
  * msd_prefill processes the interleaved visual + text prompt (Sec. 3.1).
  *
  * Conventions
- *  - Every pointer named *_d is device memory owned by the caller; the
- *    library never allocates or frees device memory.  *_h pointers are host.
+ *  - Every pointer named *_d is device memory owned by the caller.  The
+ *    library allocates device memory of its own only for the draft-training
+ *    state (msd_train_*); the rocBLAS handle of the prompt GEMMs works in
+ *    workspace carved from the caller's buffer.  *_h pointers are host.
  *  - Weights are bfloat16 (raw 16-bit patterns), row-major [out][in], no
  *    biases.  Norm gains are bfloat16 [d].
  *  - All device work is enqueued on the stream given to msd_create, in order.
@@ -56,6 +58,9 @@ typedef struct msd_model_desc {
   float rope_theta;
   float norm_eps;
 } msd_model_desc;
+/* Every weight matrix (q, k and v stacked, o, gate, up, down, f_down, the LM
+ * head) must stay under 2 GiB in the library's padded layout (64-row x
+ * 128-column blocks of bf16). */
 
 typedef struct msd_limits {
   int32_t max_batch;   /* sequences decoded together (<= 8) */

@@ -402,6 +402,16 @@ int check_desc(const msd_model_desc* m, const msd_limits* lim, msd_ctx* c) {
   if (m->d_model > MAX_D_MODEL) return fail(c, MSD_ERR_INVALID_ARG, "d_model larger than 8192");
   if (m->n_heads / m->n_kv_heads > 16)
     return fail(c, MSD_ERR_INVALID_ARG, "query group larger than 16");
+  {
+    // the weight-streaming GEMMs address a packed matrix with 32-bit byte
+    // offsets
+    const int d = m->d_model, hd = m->head_dim, F = m->ffn_dim;
+    const int qkv = (m->n_heads + 2 * m->n_kv_heads) * hd, hh = m->n_heads * hd;
+    const int shapes[6][2] = {{qkv, d}, {d, hh}, {F, d}, {d, F}, {d, 2 * d}, {m->vocab, d}};
+    for (const auto& sh : shapes)
+      if (packed_elems(sh[0], sh[1]) * sizeof(uint16_t) >= ((size_t)1 << 31))
+        return fail(c, MSD_ERR_INVALID_ARG, "a weight matrix of 2 GiB or more (packed)");
+  }
   if (lim->max_batch <= 0 || lim->max_batch > 8 || lim->max_tree <= 0 ||
       lim->max_tree > MSD_MAX_TREE || lim->max_prompt <= 0 || lim->max_seq <= 0 ||
       lim->max_seq % 8)

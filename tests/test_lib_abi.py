@@ -61,6 +61,14 @@ def test_buffer_sizes_and_errors_without_gpu():
         msd.msd_buffer_sizes(msd.ModelDesc(2, 128, 4, 2, 96, 256, 512, 1e4, 1e-5), lim)
     with pytest.raises(msd.MSDError):
         msd.msd_buffer_sizes(d, msd.Limits(1, 256, 65, 64))
+    # a packed matrix of 2 GiB or more is refused (the weight stream's 32-bit
+    # byte offsets): the LM head 131072 x 8192 is exactly 2^31 bytes, one
+    # 64-row tile fewer fits
+    with pytest.raises(msd.MSDError) as e:
+        msd.msd_buffer_sizes(msd.ModelDesc(1, 8192, 64, 8, 128, 8192, 131072, 1e4, 1e-5), lim)
+    assert e.value.code == msd.MSD_ERR_INVALID_ARG
+    assert packed(131072, 8192) == 1 << 31 and packed(131008, 8192) < 1 << 31
+    msd.msd_buffer_sizes(msd.ModelDesc(1, 8192, 64, 8, 128, 8192, 131008, 1e4, 1e-5), lim)
 
 
 def test_training_schedule_and_mix_match_oracle():
