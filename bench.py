@@ -230,6 +230,7 @@ def train_step_bench(args, wl, w, dr):
     n = len(prompt[0])
     eng = B.Engine(dims, w, dr, max_batch=1, max_seq=(n + 64 + 255) // 256 * 256, max_tree=64,
                    max_prompt=n)
+    eng.use_caller_weights(True)  # the target forward's rocBLAS products, as in the decode bench
     vis_t = torch.from_numpy(np.ascontiguousarray(prompt[2]).view(np.int16)).cuda()
     stream = torch.cuda.current_stream()
     acc, app, losses = [], [], []
@@ -395,6 +396,9 @@ def main():
     max_seq = (max_seq + 255) // 256 * 256
     eng = B.Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64,
                    max_prompt=wl.prompt_len)
+    # the engine keeps the row-major target weights it uploaded: the prompt's
+    # rocBLAS products read them in place instead of unpacking the packed copies
+    eng.use_caller_weights(True)
     if wl.tree.kind == "static":
         parent, rank, _ = synth.static_tree_arrays(wl.tree.paths)
         spec = B.make_static_spec(parent[1:], rank[1:])
@@ -576,6 +580,7 @@ def main():
                      "accept no drafted token here",
         },
         "prefill_ms": round(prefill_ms, 2),
+        "prefill_weights": "row-major target matrices read in place (msd_use_caller_weights)",
         "cpu_baseline": None,
     }
     eng.close()

@@ -206,6 +206,25 @@ enum { MSD_DRAFT_VISUAL_EMBEDDING = 0, MSD_DRAFT_VISUAL_FEATURE = 1 };
 int msd_set_draft_input(msd_ctx* ctx, int visual_input);
 
 /*
+ * Where msd_prefill's many-row products find the target's weights (the
+ * prompt forward of Sec. 3.1; msd_train_accumulate's target forward takes
+ * the same path).  enable != 0: the rocBLAS products of 512 rows or more
+ * (see msd_create) read the row-major matrices given to msd_create (wo,
+ * w_gate, w_up and w_down of every target layer) in place, instead of first
+ * unpacking each packed copy into a workspace slot (a 640-row
+ * LLaVA-1.5-7B-shaped prefill: 29.3 -> 25.1 ms).  Those matrices must then
+ * stay valid and unchanged until msd_destroy or a call with enable = 0.
+ * The q|k|v product keeps its unpacked, stacked copy (one product over all
+ * three fills the GPU better than three), and so do the draft layer and
+ * f_down (draft training rewrites their packed copies).  Results equal the
+ * default path's bit for bit: the same rocBLAS products of the same
+ * shapes on the same values.  Takes effect at the next prompt; enqueues no
+ * device work.  Default: disabled.  Errors: MSD_ERR_INVALID_ARG for a NULL
+ * ctx.
+ */
+int msd_use_caller_weights(msd_ctx* ctx, int enable);
+
+/*
  * Draft phase for sequences seqs_h[0..n_seq): runs the pending rows through
  * the draft head (text: f_down(Concat(h_i, e_{i+1})); visual: e_i, or h_i
  * after msd_set_draft_input(MSD_DRAFT_VISUAL_FEATURE)), then

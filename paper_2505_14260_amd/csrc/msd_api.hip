@@ -224,6 +224,9 @@ struct msd_ctx {
   const uint16_t* wrm_src[2] = {nullptr, nullptr};  // packed weight each slot holds
   void* blas_ws;        // rocBLAS's workspace (BLAS_WS_BYTES)
   rocblas_handle blas = nullptr;  // prompt GEMMs, when plan.wrm_elems > 0
+  // the target's prompt GEMMs read the caller's row-major matrices (layers)
+  // instead of unpacking their packed copies (msd_use_caller_weights)
+  bool caller_w = false;
   ~msd_ctx() {
     if (blas) (void)rocblas_destroy_handle(blas);
   }
@@ -473,31 +476,44 @@ void trace_events(msd_ctx* c, int kind, int M, int N, int K, hipEvent_t* e0, hip
   c->trace.push_back(r);
 }
 
-// A many-row product on rocBLAS: each weight is unpacked from the streaming
-// layout to row-major bf16 in a workspace slot (slot w for the pass's
-// weight w; kept for the pass's further row chunks, forgotten at the start
-// of every layer pass), then
+// The caller's row-major matrices of one many-row product (w2: the second
+// weight of the SwiGLU pair).
+struct RowMajorW {
+  const uint16_t *w, *w2;
+};
+
+// A many-row product on rocBLAS against row-major bf16 weights: the
+// caller's matrices (rm), or else each weight unpacked from the streaming
+// layout into a workspace slot (slot w for the pass's weight w; kept for the
+// pass's further row chunks, forgotten at the start of every layer pass).
+// Then
 //   C[m][w * off2 + n] = X_hi[m] . W[n] + X_lo[m] . W[n]   (float32, row stride ldp)
 // as two bf16 GEMMs with float32 accumulation and results (the second adds
 // to the first), issued column-major: C^T = W X^T.  The split rows' hi and
 // lo halves are the strided views X and X + K (row stride ldx).
 int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
-              const uint16_t* W2, int N, int K, int ldp, int off2) {
-  if ((size_t)N * K > c->plan.wrm_elems || (size_t)M * ldp > c->plan.part_floats)
+              const uint16_t* W2, int N, int K, int ldp, int off2, const RowMajorW* rm) {
+  if ((!rm && (size_t)N * K > c->plan.wrm_elems) || (size_t)M * ldp > c->plan.part_floats)
     return fail(c, MSD_ERR_INVALID_ARG, "internal: prompt GEMM exceeds its buffers");
   const float one = 1.f, zero = 0.f;
   for (int w = 0; w < (W2 ? 2 : 1); ++w) {
-    const uint16_t* src = w ? W2 : W;
-    uint16_t* wrm = c->wrm + (size_t)w * c->plan.wrm_elems;
-    if (c->wrm_src[w] != src) {
-      launch_unpack(src, N, K, wrm, c->st);
-      LAUNCHED(c);
-      c->wrm_src[w] = src;
+    const uint16_t* A = nullptr;
+    if (rm) {
+      A = w ? rm->w2 : rm->w;
+    } else {
+      const uint16_t* src = w ? W2 : W;
+      uint16_t* wrm = c->wrm + (size_t)w * c->plan.wrm_elems;
+      if (c->wrm_src[w] != src) {
+        launch_unpack(src, N, K, wrm, c->st);
+        LAUNCHED(c);
+        c->wrm_src[w] = src;
+      }
+      A = wrm;
     }
     float* C = c->part + (size_t)w * off2;
     for (int h = 0; h < 2; ++h) {
       const rocblas_status st = rocblas_gemm_ex(
-          c->blas, rocblas_operation_transpose, rocblas_operation_none, N, M, K, &one, wrm,
+          c->blas, rocblas_operation_transpose, rocblas_operation_none, N, M, K, &one, A,
           rocblas_datatype_bf16_r, K, X + (size_t)h * K, rocblas_datatype_bf16_r, ldx,
           h ? &one : &zero, C, rocblas_datatype_f32_r, ldp, C, rocblas_datatype_f32_r, ldp,
           rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
@@ -508,17 +524,31 @@ int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
   return MSD_OK;
 }
 
-// Partial products of rows [0, M) (M <= 64) of the split rows X (row stride
+// The target layer's row-major matrices that the prompt products read in
+// place.  q, k and v stay unpacked: one product over the stacked q|k|v rows
+// keeps more of the GPU busy than three over the caller's separate matrices
+// (LLaVA-1.5-7B-shaped 640-row prefill 25.1 ms against 25.9 ms, 3,136 rows
+// 109.7 against 114.6 ms).
+struct LayerRowMajor {
+  RowMajorW o, gu, d;
+};
+LayerRowMajor layer_row_major(const msd_ctx* c, int l) {
+  const LayerW& w = c->layers[l];
+  return LayerRowMajor{{w.wo, nullptr}, {w.wg, w.wu}, {w.wd, nullptr}};
+}
+
+// Partial products of rows [0, M) of the split rows X (row stride
 // ldx = 2K) against the packed weight W [N][K] (and W2); returns the view the
-// consumer sums.
+// consumer sums.  Passes of BLAS_MIN_ROWS rows or more run on rocBLAS, against
+// rm's row-major matrices when given.
 int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t* W,
-         const uint16_t* W2, int N, int K, Parts* out) {
+         const uint16_t* W2, int N, int K, Parts* out, const RowMajorW* rm = nullptr) {
   if (M > CHUNK) {
     if (kind == GK_LMHEAD || M > BIG_CHUNK)
       return fail(c, MSD_ERR_INVALID_ARG, "internal: GEMM launch with too many rows");
     if (c->blas && M >= BLAS_MIN_ROWS) {
       const int nt = (N + 63) / 64, nw = W2 ? 2 : 1;
-      TRY(blas_gemm(c, X, ldx, M, W, W2, N, K, nt * 64 * nw, nt * 64));
+      TRY(blas_gemm(c, X, ldx, M, W, W2, N, K, nt * 64 * nw, nt * 64, rm));
       *out = Parts{c->part, 1, (size_t)M * nt * 64 * nw, nt * 64 * nw, nt * 64};
       return MSD_OK;
     }
@@ -610,6 +640,8 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
   for (int l = 0; l < nl; ++l) {
     const LayerW& w = draft ? c->dlayer : c->layers[l];
     const PackedLayer& pw = draft ? c->pdlayer : c->players[l];
+    const bool rmw = c->caller_w && !draft;
+    const LayerRowMajor rl = rmw ? layer_row_major(c, l) : LayerRowMajor{};
     uint16_t* kc = (draft ? c->dk : c->tk) + (size_t)l * layer_kv;
     uint16_t* vc = (draft ? c->dv : c->tv) + (size_t)l * layer_kv;
     Parts pt;
@@ -660,14 +692,15 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     for (int m0 = 0; m0 < rows; m0 += ch) {
       const int mc = std::min(ch, rows - m0);
       TRY(gemm(c, GK_O, c->ao + (size_t)m0 * 2 * H * hd, 2 * H * hd, mc, pw.o, nullptr, d, H * hd,
-               &pt));
+               &pt, rmw ? &rl.o : nullptr));
       launch_resid(pt, mc, d, RN_ADD, c->x + (size_t)m0 * d, w.n2, c->xn + (size_t)m0 * 2 * d, nullptr,
                    c->ssq + (size_t)m0 * ssq_blocks(d), c->st);
       LAUNCHED(c);
     }
     for (int m0 = 0; m0 < rows; m0 += ch) {
       const int mc = std::min(ch, rows - m0);
-      TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, pw.g, pw.u, F, d, &pt));
+      TRY(gemm(c, GK_GATEUP, c->xn + (size_t)m0 * 2 * d, 2 * d, mc, pw.g, pw.u, F, d, &pt,
+               rmw ? &rl.gu : nullptr));
       launch_silu(pt, row_norm(c, m0), mc, F, c->act + (size_t)m0 * 2 * F, c->st);
       LAUNCHED(c);
     }
@@ -675,7 +708,8 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
     const uint16_t* g_next = last ? final_g : c->layers[l + 1].n1;
     for (int m0 = 0; m0 < rows; m0 += ch) {
       const int mc = std::min(ch, rows - m0);
-      TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * 2 * F, 2 * F, mc, pw.d, nullptr, d, F, &pt));
+      TRY(gemm(c, GK_DOWN, c->act + (size_t)m0 * 2 * F, 2 * F, mc, pw.d, nullptr, d, F, &pt,
+               rmw ? &rl.d : nullptr));
       if (last && final_g) {
         // the final feature h is materialised (LM head input, draft input)
         launch_resid_norm(pt, 0, mc, d, RN_ADD, c->x + (size_t)m0 * d, final_g, m.norm_eps,
@@ -1420,6 +1454,12 @@ int msd_set_draft_input(msd_ctx* c, int visual_input) {
   if (visual_input != MSD_DRAFT_VISUAL_EMBEDDING && visual_input != MSD_DRAFT_VISUAL_FEATURE)
     return fail(c, MSD_ERR_INVALID_ARG, "unknown draft input mode");
   c->visual_input = visual_input;
+  return MSD_OK;
+}
+
+int msd_use_caller_weights(msd_ctx* c, int enable) {
+  if (!c) return fail(nullptr, MSD_ERR_INVALID_ARG, "null context");
+  c->caller_w = enable != 0;
   return MSD_OK;
 }
 

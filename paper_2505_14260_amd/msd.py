@@ -94,6 +94,7 @@ def lib():
         L.msd_seq_len.argtypes = [c_vp, ctypes.c_int]
         L.msd_set_state.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, c_vp, c_i32]
         L.msd_set_draft_input.argtypes = [c_vp, ctypes.c_int]
+        L.msd_use_caller_weights.argtypes = [c_vp, ctypes.c_int]
         L.msd_stream_read.argtypes = [c_vp, c_sz, ctypes.c_int, c_vp, c_vp]
         L.msd_train_accumulate.argtypes = [c_vp, ctypes.c_int, ctypes.c_int, P(c_i32),
                                            P(ctypes.c_uint8), c_vp, P(ctypes.c_double)]
@@ -217,6 +218,10 @@ def msd_set_draft_input(ctx, visual_input):
     _check(ctx, lib().msd_set_draft_input(ctx, visual_input))
 
 
+def msd_use_caller_weights(ctx, enable):
+    _check(ctx, lib().msd_use_caller_weights(ctx, 1 if enable else 0))
+
+
 def msd_train_accumulate(ctx, seq, tokens, is_visual, visual_ptr):
     """Loss sums (total, regression, token) of one training sequence; its
     gradient sums are added to the context's."""
@@ -331,6 +336,12 @@ class Engine:
         """Draft input of the visual prompt rows of later prefills: "embedding"
         (the method) or "feature" (the Visual Feature variant)."""
         msd_set_draft_input(self.ctx, DRAFT_VISUAL_INPUTS[visual_input])
+
+    def use_caller_weights(self, enable=True):
+        """Prompt products read the row-major target weights this engine
+        uploaded (it keeps them until it is closed) instead of unpacking the
+        packed copies."""
+        msd_use_caller_weights(self.ctx, enable)
 
     def train_accumulate(self, seq, tokens, is_visual, visual_bits):
         """Gradient sums of one training sequence; returns its loss sums."""

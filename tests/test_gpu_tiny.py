@@ -130,6 +130,65 @@ def test_prefill_many_rows_wide(n_visual):
         eng.close()
 
 
+def test_prefill_caller_row_major_weights():
+    """msd_use_caller_weights: a 1100-row prompt (one 1024-row rocBLAS pass
+    plus a 76-row one) whose output, gate, up and down products read the
+    uploaded row-major matrices: every layer's K/V, the first token and the
+    draft cache against the oracle, and the K/V bit for bit against the
+    default (unpacking) engine's, before and after switching back."""
+    import dataclasses
+    from paper_2505_14260_amd.msd import Engine
+    wl = dataclasses.replace(WIDE, n_visual=1036)
+    dims = wl.dims
+    print(f"case: prefill on caller weights {wl.name} n={wl.prompt_len}", flush=True)
+    w = synth.make_target_weights(dims, wl.seed)
+    dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
+    prompt = synth.make_prompt(wl)
+    m = O.Models(dims, w, dr)
+    n = wl.prompt_len
+    max_seq = (n + 64 + 255) // 256 * 256
+    st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=max_seq)
+    O.draft_catch_up(m, st)
+    engines = [Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64, max_prompt=n)
+               for _ in range(2)]
+    try:
+        engines[1].use_caller_weights(True)
+        firsts = [e.prefill(0, *prompt) for e in engines]
+        torch.cuda.synchronize()
+        assert argmax_ok(firsts[1], logits[-1]), (firsts, f_ref)
+        assert firsts[1] == firsts[0]
+        views = [e.kv_views() for e in engines]
+        worst = 0.0
+        for l in range(dims.n_layers):
+            for which in ("K", "V"):
+                got = []
+                for tk, tv, _, _ in views:
+                    if which == "K":
+                        got.append(bits_to_f64(tk[l, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1)))
+                    else:
+                        got.append(bits_to_f64(tv[l, 0, :, :, :n].permute(2, 0, 1).reshape(n, -1)))
+                ref = (st.kv.k if which == "K" else st.kv.v)[l, :n].reshape(n, -1)
+                ok, err = row_close(got[1], ref)
+                assert ok, (l, which, err)
+                assert np.array_equal(got[1], got[0]), (l, which, "differs from the unpacking path")
+                worst = max(worst, err)
+        dk = views[1][2]
+        kg = bits_to_f64(dk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        ok, err = row_close(kg, st.dkv.k[0, :n].reshape(n, -1))
+        assert ok, ("draft K", err)
+        print(f"caller weights: target K/V max rel err {worst:.2e}, draft K {err:.2e}")
+        # back to unpacking: the same prompt again gives the default engine's
+        # cache bit for bit
+        engines[1].use_caller_weights(False)
+        assert engines[1].prefill(0, *prompt) == firsts[0]
+        torch.cuda.synchronize()
+        tk0, tk1 = views[0][0], views[1][0]
+        assert torch.equal(tk0[:, 0, :, :n, :], tk1[:, 0, :, :n, :])
+    finally:
+        for e in engines:
+            e.close()
+
+
 def test_wide_vocab_lm_head_full_k():
     """A 152,064-word vocabulary at d_model 1024: three sequences' 15-node
     trees make a 45-row verify whose LM head takes the full-K GEMM (ten
