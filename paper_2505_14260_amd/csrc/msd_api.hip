@@ -109,6 +109,10 @@ constexpr int BIG_CHUNK = 1024;   // rows per many-row GEMM launch
 // with float32 results, the weight unpacked to row-major in the workspace)
 constexpr int BLAS_MIN_ROWS = 512;
 constexpr size_t BLAS_WS_BYTES = (size_t)32 << 20;  // rocBLAS's workspace
+// rocBLAS prompt products of fewer than BIG_CHUNK rows whose hi and lo
+// results together take at most this many bytes run as one product over 2M
+// interleaved rows (see blas_gemm)
+constexpr size_t BLAS_ONE_PRODUCT_BYTES = (size_t)192 << 20;
 // Passes over more rows than this use the many-row GEMM (below it, a few
 // weight-streaming launches of CHUNK rows are faster).
 constexpr int BIG_MIN_ROWS = 256;
@@ -168,6 +172,10 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
     auto ldp = [](int N, int nw) { return (size_t)(N + 63) / 64 * 64 * nw; };
     const size_t w = std::max({ldp(p.ld_qkv, 1), ldp(d, 1), ldp(F, 2)});
     p.part_floats = std::max(p.part_floats, big * w);
+    // the rocBLAS products' one-product form: hi and lo rows
+    if (big >= (size_t)BLAS_MIN_ROWS)
+      p.part_floats = std::max(p.part_floats,
+                               std::min(2 * big * w, BLAS_ONE_PRODUCT_BYTES / sizeof(float)));
   }
   p.wrm_elems = 0;
   if (std::min(BIG_CHUNK, p.rows_max) >= BLAS_MIN_ROWS)
@@ -486,14 +494,29 @@ struct RowMajorW {
 // caller's matrices (rm), or else each weight unpacked from the streaming
 // layout into a workspace slot (slot w for the pass's weight w; kept for the
 // pass's further row chunks, forgotten at the start of every layer pass).
-// Then
-//   C[m][w * off2 + n] = X_hi[m] . W[n] + X_lo[m] . W[n]   (float32, row stride ldp)
-// as two bf16 GEMMs with float32 accumulation and results (the second adds
-// to the first), issued column-major: C^T = W X^T.  The split rows' hi and
-// lo halves are the strided views X and X + K (row stride ldx).
+// Then bf16 GEMMs with float32 accumulation and results, issued column-major
+// (C^T = W X^T), give the consumer X_hi[m] . W[n] + X_lo[m] . W[n] (at
+// column w * off2 + n) in one of two forms:
+//  - one product over the 2M rows of K elements that the split rows are
+//    (row 2m the hi half of row m, row 2m + 1 its lo half; X's row stride
+//    must be 2K): C'[2m + h][n], two partials per row that the consumer
+//    sums in hi, lo order;
+//  - two products over the strided views X and X + K, the second adding to
+//    the first: C[m][n], one partial.
+// Either way the sum is hi + lo rounded once.  The one-product form runs
+// passes of fewer than BIG_CHUNK rows with results of at most
+// BLAS_ONE_PRODUCT_BYTES: its doubled row count tiles better (prefills of
+// 640 rows, LLaVA-1.5-7B-shaped, 25.3 -> 20.8 ms; 704 rows, 13B-shaped,
+// 46.8 -> 43.2 ms).  At 1024 rows it lost: 7B-shaped gate+up (180 MB of
+// results) over 3,136 rows 111.7 -> 123.4 ms, and every Qwen2.5-VL-7B-shaped
+// product, 1,152 rows 49.1 -> 52.7 ms even with the pair left out.
 int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
-              const uint16_t* W2, int N, int K, int ldp, int off2, const RowMajorW* rm) {
-  if ((!rm && (size_t)N * K > c->plan.wrm_elems) || (size_t)M * ldp > c->plan.part_floats)
+              const uint16_t* W2, int N, int K, int ldp, int off2, const RowMajorW* rm,
+              Parts* out) {
+  const bool one_product = ldx == 2 * K && M < BIG_CHUNK &&
+                           2 * (size_t)M * ldp * sizeof(float) <= BLAS_ONE_PRODUCT_BYTES;
+  const size_t rows = one_product ? 2 * (size_t)M : (size_t)M;
+  if ((!rm && (size_t)N * K > c->plan.wrm_elems) || rows * ldp > c->plan.part_floats)
     return fail(c, MSD_ERR_INVALID_ARG, "internal: prompt GEMM exceeds its buffers");
   const float one = 1.f, zero = 0.f;
   for (int w = 0; w < (W2 ? 2 : 1); ++w) {
@@ -511,16 +534,18 @@ int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
       A = wrm;
     }
     float* C = c->part + (size_t)w * off2;
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < (one_product ? 1 : 2); ++h) {
       const rocblas_status st = rocblas_gemm_ex(
-          c->blas, rocblas_operation_transpose, rocblas_operation_none, N, M, K, &one, A,
-          rocblas_datatype_bf16_r, K, X + (size_t)h * K, rocblas_datatype_bf16_r, ldx,
-          h ? &one : &zero, C, rocblas_datatype_f32_r, ldp, C, rocblas_datatype_f32_r, ldp,
-          rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+          c->blas, rocblas_operation_transpose, rocblas_operation_none, N, (int)rows, K, &one, A,
+          rocblas_datatype_bf16_r, K, X + (size_t)h * K, rocblas_datatype_bf16_r,
+          one_product ? K : ldx, h ? &one : &zero, C, rocblas_datatype_f32_r, ldp, C,
+          rocblas_datatype_f32_r, ldp, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
       if (st != rocblas_status_success)
         return fail(c, MSD_ERR_HIP, std::string("rocblas_gemm_ex: ") + rocblas_status_to_string(st));
     }
   }
+  *out = one_product ? Parts{c->part, 2, (size_t)ldp, 2 * ldp, off2}
+                     : Parts{c->part, 1, (size_t)M * ldp, ldp, off2};
   return MSD_OK;
 }
 
@@ -548,9 +573,7 @@ int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t
       return fail(c, MSD_ERR_INVALID_ARG, "internal: GEMM launch with too many rows");
     if (c->blas && M >= BLAS_MIN_ROWS) {
       const int nt = (N + 63) / 64, nw = W2 ? 2 : 1;
-      TRY(blas_gemm(c, X, ldx, M, W, W2, N, K, nt * 64 * nw, nt * 64, rm));
-      *out = Parts{c->part, 1, (size_t)M * nt * 64 * nw, nt * 64 * nw, nt * 64};
-      return MSD_OK;
+      return blas_gemm(c, X, ldx, M, W, W2, N, K, nt * 64 * nw, nt * 64, rm, out);
     }
     const int S = launch_gemm_big(X, ldx, M, W, W2, N, K, c->part, c->plan.part_floats,
                                   c->gemm_zero, c->st);
