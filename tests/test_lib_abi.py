@@ -90,3 +90,14 @@ def test_training_schedule_and_mix_match_oracle():
         msd.msd_train_lr(5, 4, 1.0)
     with pytest.raises(msd.MSDError):
         msd.msd_train_mix(6, 5, 10)
+
+
+def test_context_calls_reject_a_null_context_without_gpu():
+    from paper_2505_14260_amd import msd
+    if not os.path.exists(msd.LIB_PATH):
+        pytest.skip("libmsd.so not built")
+    for call in (lambda: msd.msd_use_caller_weights(None, 1),
+                 lambda: msd.msd_set_draft_input(None, 0)):
+        with pytest.raises(msd.MSDError) as e:
+            call()
+        assert e.value.code == msd.MSD_ERR_INVALID_ARG
