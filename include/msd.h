@@ -161,13 +161,16 @@ int msd_workspace_size(const msd_model_desc* m, const msd_limits* lim, size_t* b
  * returns, the library reads the embedding table, the norm gains and the
  * packed copies only: the row-major matrices may be released; every other
  * pointer must stay valid until msd_destroy.
- * When lim->max_prompt allows prompt GEMMs of 512 rows or more, those run on
- * rocBLAS (bf16 inputs, float32 results) against a row-major copy of one
- * weight at a time that the library unpacks into the workspace: msd_create
- * then also creates a rocBLAS handle on the stream, gives it a 32 MB
- * workspace carved from bufs->workspace, and runs the prompt GEMM shapes
- * once so that rocBLAS loads their kernels here rather than in the first
- * msd_prefill.  MSD_ERR_HIP if the handle cannot be set up. */
+ * When the limits allow passes over more than 256 rows (a prompt of
+ * max_prompt rows, or max_batch trees of max_tree nodes), the GEMMs of such
+ * passes run on rocBLAS (bf16 inputs, float32 results) in launches of up to
+ * 1024 rows (a last launch of 64 rows or fewer takes the library's own
+ * kernels), against a row-major copy of one weight at a time that the
+ * library unpacks into the workspace: msd_create then also creates a rocBLAS
+ * handle on the stream, gives it a 32 MB workspace carved from
+ * bufs->workspace, and runs the prompt GEMM shapes once so that rocBLAS
+ * loads their kernels here rather than in the first msd_prefill.
+ * MSD_ERR_HIP if the handle cannot be set up. */
 int msd_create(const msd_model_desc* m, const msd_limits* lim,
                const msd_target_weights* tw, const msd_draft_weights* dw,
                const msd_buffers* bufs, void* stream, msd_ctx** out);
@@ -208,10 +211,10 @@ int msd_set_draft_input(msd_ctx* ctx, int visual_input);
 /*
  * Where msd_prefill's many-row products find the target's weights (the
  * prompt forward of Sec. 3.1; msd_train_accumulate's target forward takes
- * the same path).  enable != 0: the rocBLAS products of 512 rows or more
- * (see msd_create) read the row-major matrices given to msd_create (wo,
- * w_gate, w_up and w_down of every target layer) in place, instead of first
- * unpacking each packed copy into a workspace slot (a 640-row
+ * the same path).  enable != 0: the rocBLAS products (see msd_create)
+ * read the row-major matrices given to msd_create (wo, w_gate, w_up and
+ * w_down of every target layer) in place, instead of first unpacking each
+ * packed copy into a workspace slot (a 640-row
  * LLaVA-1.5-7B-shaped prefill: 29.3 -> 25.1 ms).  Those matrices must then
  * stay valid and unchanged until msd_destroy or a call with enable = 0.
  * The q|k|v product keeps its unpacked, stacked copy (one product over all

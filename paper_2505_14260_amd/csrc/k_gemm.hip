@@ -579,182 +579,6 @@ __global__ __launch_bounds__(256) void k_gemm_fk(GemmArgs a) {
   }
 }
 
-// Many-row GEMM (prompt rows, large batches): a (64 NB) x 128 output tile
-// per workgroup over all of K, both operands staged through LDS.
-//
-// Per 128-column block of K the workgroup holds NB packed weight blocks
-// (tiles NB t .. NB t + NB - 1, 16 KB each, in their packed order) and the X
-// block of its 128 rows (hi and lo halves, 64 KB, XOR-swizzled as in
-// k_gemm).  Waves form a 2 x 2 grid: wave (wn, wm) multiplies packed blocks
-// NB/2 wn .. NB/2 wn + NB/2 - 1 with X rows 64 wm .. 64 wm + 63, in 16 x 16
-// MFMA tiles, hi and lo.  Wider tiles reuse each X fragment read from LDS
-// for more MFMAs.
-//
-// Global loads run P blocks ahead through a ring of register stages; the
-// ring has no branch on its loads (past the last block a stage reloads the
-// last one, a cache hit), and the barriers order LDS only, so loads stay in
-// flight across them.  Tiles are dealt XCD by XCD (a workgroup runs on XCD
-// blockIdx % 8), the M tiles of one (N tile, K split) consecutively, so a
-// weight tile is fetched once into that XCD's L2 and reused by its M tiles.
-// Narrow outputs split K so that the grid still covers the chip; each split
-// writes its own partial, summed in split order by the consumer.
-struct BigArgs {
-  const uint16_t* X;
-  int ldx, M, K;
-  const uint16_t* W;
-  const uint16_t* dummy;
-  int n_tiles, nkt, n_nt, n_mt, per_xcd;
-  int ks, kbs;         // K splits, 128-column blocks per split
-  float* part;
-  size_t part_split;   // floats between the partials of consecutive K splits
-  int ldp;
-};
-
-constexpr int BIG_M = 128;
-// Launched configurations: four packed blocks per N tile with one register
-// stage (the registers of a second stage would spill) from 512 rows on; two
-// blocks with two stages below, where the wider tiles leave too few
-// workgroups for the chip.
-constexpr int BIG_WIDE_ROWS = 512;
-constexpr int BIG_XU = 2 * KB / 8;                  // 16-byte units per X row (hi + lo)
-constexpr int BIG_X_UNITS = BIG_M * BIG_XU;
-constexpr int BIG_XQ = BIG_X_UNITS / 256;           // X units per thread
-__host__ __device__ constexpr int big_w_units(int NB) { return NB * BLOCK_ELEMS / 8; }
-__host__ __device__ constexpr size_t big_lds(int NB) {
-  return (size_t)(big_w_units(NB) + BIG_X_UNITS) * 16;
-}
-
-// hi units 0..15 and lo units 16..31 of row m, each half swizzled by m & 15
-MSD_DEV int big_xs_index(int m, int u) { return m * BIG_XU + (u & 16) + ((u & 15) ^ (m & 15)); }
-
-
-MSD_DEV bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-// One block of K (kb counts from the split's first block kbeg): the weight
-// units and the X units of this thread.  wt[j] is packed tile j of the
-// workgroup's N tile at block kbeg (the zero block for tiles past N, which
-// then takes no block offset).
-template <int NB>
-MSD_DEV void big_load(const BigArgs& a, int kbeg, int kb, int m0,
-                      const uint16_t* const (&wt)[NB], u32x4 (&wq)[NB * 4],
-                      u32x4 (&xq)[BIG_XQ]) {
-#pragma unroll
-  for (int q = 0; q < NB * 4; ++q) {
-    const int j = q / 4;  // packed block of this unit
-    const int ue = threadIdx.x + 256 * (q % 4);
-    const uint16_t* src = wt[j] + (wt[j] == a.dummy ? 0 : (size_t)kb * BLOCK_ELEMS);
-    wq[q] = *reinterpret_cast<const u32x4*>(src + (size_t)ue * 8);
-  }
-#pragma unroll
-  for (int q = 0; q < BIG_XQ; ++q) {
-    const int e = threadIdx.x + 256 * q;
-    const int m = e / BIG_XU, u = e - m * BIG_XU;
-    const int col = (kbeg + kb) * KB + 8 * (u & 15);
-    const bool ok = m0 + m < a.M && col < a.K;
-    const uint16_t* src = a.X + (ok ? (size_t)(m0 + m) * a.ldx + (u >= 16 ? a.K : 0) + col : 0);
-    const u32x4 v = *reinterpret_cast<const u32x4*>(src);
-    xq[q] = ok ? v : u32x4{0u, 0u, 0u, 0u};
-  }
-}
-
-template <int NB, int P>
-__global__ __launch_bounds__(256) void k_gemm_big(BigArgs a) {
-  static_assert(NB == 2 || NB == 4, "two or four packed blocks per N tile");
-  constexpr int WB = NB / 2;      // packed blocks per wave
-  constexpr int SL = 4 * WB;      // 16-row weight slabs per wave
-  constexpr int WU = big_w_units(NB);
-  extern __shared__ u32x4 lds_big[];
-  u32x4* const ws = lds_big;
-  u32x4* const xs = lds_big + WU;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wn = wave & 1, wm = wave >> 1;
-  const int i = lane & 15, g = lane >> 4;
-  const int flat = (blockIdx.x & 7) * a.per_xcd + (blockIdx.x >> 3);
-  if (flat >= a.n_nt * a.ks * a.n_mt) return;
-  const int mt = flat % a.n_mt, nk = flat / a.n_mt;
-  const int nt = nk / a.ks, ksp = nk - nt * a.ks;
-  const int m0 = mt * BIG_M;
-  // this split's blocks [kbeg, kbeg + nkt) of the weight's a.nkt
-  const int kbeg = ksp * a.kbs;
-  const int nkt = min(a.kbs, a.nkt - kbeg);
-  const uint16_t* wt[NB];
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int tile = NB * nt + j;
-    wt[j] = tile < a.n_tiles ? a.W + ((size_t)tile * a.nkt + kbeg) * BLOCK_ELEMS : a.dummy;
-  }
-  float* const part = a.part + (size_t)ksp * a.part_split;
-
-  u32x4 wr[P][NB * 4], xr[P][BIG_XQ];
-#pragma unroll
-  for (int p = 0; p < P; ++p) big_load<NB>(a, kbeg, min(p, nkt - 1), m0, wt, wr[p], xr[p]);
-
-  f32x4 acc[SL][4];
-#pragma unroll
-  for (int s = 0; s < SL; ++s)
-#pragma unroll
-    for (int t = 0; t < 4; ++t) acc[s][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll 1
-  for (int kb0 = 0; kb0 < nkt; kb0 += P) {
-#pragma unroll
-    for (int r = 0; r < P; ++r) {
-      const int kb = kb0 + r;
-      lds_barrier();  // the previous block's MFMAs are done with the LDS
-#pragma unroll
-      for (int q = 0; q < NB * 4; ++q) ws[(q / 4) * 1024 + threadIdx.x + 256 * (q % 4)] = wr[r][q];
-#pragma unroll
-      for (int q = 0; q < BIG_XQ; ++q) {
-        const int e = threadIdx.x + 256 * q;
-        const int m = e / BIG_XU, u = e - m * BIG_XU;
-        xs[big_xs_index(m, u)] = xr[r][q];
-      }
-      lds_barrier();
-      big_load<NB>(a, kbeg, min(kb + P, nkt - 1), m0, wt, wr[r], xr[r]);
-      if (kb < nkt) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          u32x4 bh[4], bl[4];
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const int m = wm * 64 + t * 16 + i;
-            bh[t] = xs[big_xs_index(m, 4 * g + c)];
-            bl[t] = xs[big_xs_index(m, 16 + 4 * g + c)];
-          }
-#pragma unroll
-          for (int s = 0; s < SL; ++s) {
-            // slab s: packed block WB wn + s / 4, wave-slab s % 4
-            const u32x4 af = ws[(WB * wn + s / 4) * 1024 + ((s % 4) * 4 + c) * 64 + lane];
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(af), as_bf16x8(bh[t]),
-                                                                   acc[s][t], 0, 0, 0);
-              acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(af), as_bf16x8(bl[t]),
-                                                                   acc[s][t], 0, 0, 0);
-            }
-          }
-        }
-      }
-    }
-  }
-  // lane holds output row m = (lane & 15) of its M group and four consecutive
-  // weight rows 4 * (lane >> 4) + r of its 16-row slab; slabs of tiles past
-  // N are not stored
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int m = m0 + wm * 64 + t * 16 + i;
-    if (m >= a.M) continue;
-#pragma unroll
-    for (int s = 0; s < SL; ++s) {
-      const int tile = NB * nt + WB * wn + s / 4;
-      if (tile >= a.n_tiles) continue;
-      const int n = tile * TILE_ROWS + (s % 4) * 16 + 4 * g;
-      *reinterpret_cast<float4*>(part + (size_t)m * a.ldp + n) =
-          make_float4(acc[s][t][0], acc[s][t][1], acc[s][t][2], acc[s][t][3]);
-    }
-  }
-}
-
 // One thread per 16-byte unit of the packed layout.
 __global__ void k_pack(const uint16_t* src, int N, int K, int nkt, size_t units, uint16_t* dst) {
   const size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -875,8 +699,6 @@ void launch_stream_read(const uint16_t* buf, size_t spans, int wgs, unsigned* si
                         hipStream_t st) {
   hipLaunchKernelGGL(k_stream_read, dim3(wgs), dim3(256), 0, st, buf, spans, sink);
 }
-
-size_t gemm_dummy_elems() { return (size_t)BLOCK_ELEMS; }
 
 void launch_unpack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t st) {
   const int nkt = (K + KB - 1) / KB;
@@ -1086,47 +908,6 @@ void launch_gemm(const uint16_t* X, int ldx, int M, const uint16_t* W, const uin
     else if (pl.MT == 2) launch_mt<2, 1>(grid, a, sc, st);
     else launch_mt<4, 1>(grid, a, sc, st);
   }
-}
-
-int launch_gemm_big(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2,
-                    int N, int K, float* part, size_t part_cap, const uint16_t* dummy,
-                    hipStream_t st) {
-  const int nw = W2 ? 2 : 1;
-  BigArgs a{};
-  a.X = X;
-  a.ldx = ldx;
-  a.M = M;
-  a.K = K;
-  a.dummy = dummy;
-  a.n_tiles = (N + TILE_ROWS - 1) / TILE_ROWS;
-  a.nkt = (K + KB - 1) / KB;
-  const bool wide = M >= BIG_WIDE_ROWS;
-  const int NB = wide ? 4 : 2;
-  a.n_nt = (a.n_tiles + NB - 1) / NB;
-  a.n_mt = (M + BIG_M - 1) / BIG_M;
-  a.ldp = a.n_tiles * TILE_ROWS * nw;
-  a.part_split = (size_t)M * a.ldp;
-  // K splits for grids that would leave most CUs idle (single weights only;
-  // the partials of every split must fit the buffer).  With half the CUs
-  // busy or more, the extra partials cost more than the extra workgroups gain.
-  int ks = 1;
-  if (nw == 1)
-    while (ks < 4 && a.n_nt * a.n_mt * ks < 128 && a.nkt >= 8 * (ks + 1) &&
-           (size_t)(ks + 1) * a.part_split <= part_cap)
-      ++ks;
-  a.kbs = (a.nkt + ks - 1) / ks;
-  a.ks = (a.nkt + a.kbs - 1) / a.kbs;
-  a.per_xcd = (a.n_nt * a.ks * a.n_mt + 7) / 8;
-  const dim3 grid(8 * a.per_xcd);
-  for (int w = 0; w < nw; ++w) {
-    a.W = w ? W2 : W;
-    a.part = part + (size_t)w * a.n_tiles * TILE_ROWS;
-    if (wide)
-      hipLaunchKernelGGL((k_gemm_big<4, 1>), grid, dim3(256), big_lds(4), st, a);
-    else
-      hipLaunchKernelGGL((k_gemm_big<2, 2>), grid, dim3(256), big_lds(2), st, a);
-  }
-  return a.ks;
 }
 
 }  // namespace msd

@@ -104,17 +104,16 @@ constexpr int ACC_BACK_INTS = 8 * MSD_MAX_TREE + 8 + 8 + 1;
 // concurrent weight streams per CU lower the achieved HBM bandwidth).
 constexpr int GEMM_WGS = 256;
 constexpr int CHUNK = 64;         // rows per weight-streaming GEMM launch
-constexpr int BIG_CHUNK = 1024;   // rows per many-row GEMM launch
-// many-row launches of at least this many rows run on rocBLAS (bf16 GEMMs
-// with float32 results, the weight unpacked to row-major in the workspace)
-constexpr int BLAS_MIN_ROWS = 512;
+constexpr int BIG_CHUNK = 1024;   // rows per many-row (rocBLAS) GEMM launch
 constexpr size_t BLAS_WS_BYTES = (size_t)32 << 20;  // rocBLAS's workspace
 // rocBLAS prompt products of fewer than BIG_CHUNK rows whose hi and lo
 // results together take at most this many bytes run as one product over 2M
 // interleaved rows (see blas_gemm)
 constexpr size_t BLAS_ONE_PRODUCT_BYTES = (size_t)192 << 20;
-// Passes over more rows than this use the many-row GEMM (below it, a few
-// weight-streaming launches of CHUNK rows are faster).
+// Passes over more rows than this run their GEMMs on rocBLAS in launches of
+// up to BIG_CHUNK rows (bf16 products with float32 results against row-major
+// weights; a last launch of CHUNK rows or fewer takes the weight-streaming
+// kernels).  Below it, a few weight-streaming launches of CHUNK rows.
 constexpr int BIG_MIN_ROWS = 256;
 
 // Rows per GEMM launch for a pass over `rows` rows.
@@ -165,21 +164,18 @@ Plan make_plan(const msd_model_desc& m, const msd_limits& lim) {
                             gemm_part_floats(mm, m.vocab, d, 1, GEMM_WGS)};
     p.part_floats = std::max(p.part_floats, *std::max_element(cand, cand + 6));
   }
-  // full products of one many-row launch (every GEMM but the LM head, which
-  // always runs in CHUNK-row launches)
+  // full products of one rocBLAS launch (every GEMM but the LM head, which
+  // always runs in CHUNK-row launches), in either form of blas_gemm
+  p.wrm_elems = 0;
   if (p.rows_max > BIG_MIN_ROWS) {
     const size_t big = std::min(BIG_CHUNK, p.rows_max);
     auto ldp = [](int N, int nw) { return (size_t)(N + 63) / 64 * 64 * nw; };
     const size_t w = std::max({ldp(p.ld_qkv, 1), ldp(d, 1), ldp(F, 2)});
     p.part_floats = std::max(p.part_floats, big * w);
-    // the rocBLAS products' one-product form: hi and lo rows
-    if (big >= (size_t)BLAS_MIN_ROWS)
-      p.part_floats = std::max(p.part_floats,
-                               std::min(2 * big * w, BLAS_ONE_PRODUCT_BYTES / sizeof(float)));
-  }
-  p.wrm_elems = 0;
-  if (std::min(BIG_CHUNK, p.rows_max) >= BLAS_MIN_ROWS)
+    p.part_floats = std::max(p.part_floats,
+                             std::min(2 * big * w, BLAS_ONE_PRODUCT_BYTES / sizeof(float)));
     p.wrm_elems = std::max({(size_t)p.ld_qkv * d, (size_t)d * hh, (size_t)F * d, (size_t)d * 2 * d});
+  }
   return p;
 }
 
@@ -227,7 +223,6 @@ struct msd_ctx {
   uint16_t *xn, *xb, *fcin, *q, *ao, *act, *h;
   float* part;
   float* sink;          // GEMM rows past M
-  uint16_t* gemm_zero;  // zero block the many-row GEMM reads for tiles past N
   uint16_t* wrm;        // two row-major bf16 weight slots (rocBLAS prompt GEMMs)
   const uint16_t* wrm_src[2] = {nullptr, nullptr};  // packed weight each slot holds
   void* blas_ws;        // rocBLAS's workspace (BLAS_WS_BYTES)
@@ -336,7 +331,6 @@ size_t carve(msd_ctx* c, const msd_model_desc& m, const msd_limits& lim, char* b
   t->fcin = cv.take<uint16_t>((size_t)R * 4 * d);
   t->part = cv.take<float>(p.part_floats);
   t->sink = cv.take<float>(256);
-  t->gemm_zero = cv.take<uint16_t>(gemm_dummy_elems());
   t->wrm = p.wrm_elems ? cv.take<uint16_t>(2 * p.wrm_elems) : nullptr;
   t->blas_ws = p.wrm_elems ? (void*)cv.take<char>(BLAS_WS_BYTES) : nullptr;
   t->ssq = cv.take<float>((size_t)R * ssq_blocks(d));
@@ -564,23 +558,16 @@ LayerRowMajor layer_row_major(const msd_ctx* c, int l) {
 
 // Partial products of rows [0, M) of the split rows X (row stride
 // ldx = 2K) against the packed weight W [N][K] (and W2); returns the view the
-// consumer sums.  Passes of BLAS_MIN_ROWS rows or more run on rocBLAS, against
+// consumer sums.  Launches of more than CHUNK rows run on rocBLAS, against
 // rm's row-major matrices when given.
 int gemm(msd_ctx* c, int kind, const uint16_t* X, int ldx, int M, const uint16_t* W,
          const uint16_t* W2, int N, int K, Parts* out, const RowMajorW* rm = nullptr) {
   if (M > CHUNK) {
     if (kind == GK_LMHEAD || M > BIG_CHUNK)
       return fail(c, MSD_ERR_INVALID_ARG, "internal: GEMM launch with too many rows");
-    if (c->blas && M >= BLAS_MIN_ROWS) {
-      const int nt = (N + 63) / 64, nw = W2 ? 2 : 1;
-      return blas_gemm(c, X, ldx, M, W, W2, N, K, nt * 64 * nw, nt * 64, rm, out);
-    }
-    const int S = launch_gemm_big(X, ldx, M, W, W2, N, K, c->part, c->plan.part_floats,
-                                  c->gemm_zero, c->st);
-    LAUNCHED(c);
+    if (!c->blas) return fail(c, MSD_ERR_INVALID_ARG, "internal: many-row GEMM without rocBLAS");
     const int nt = (N + 63) / 64, nw = W2 ? 2 : 1;
-    *out = Parts{c->part, S, (size_t)M * nt * 64 * nw, nt * 64 * nw, nt * 64};
-    return MSD_OK;
+    return blas_gemm(c, X, ldx, M, W, W2, N, K, nt * 64 * nw, nt * 64, rm, out);
   }
   const GemmPlan pl = plan_gemm(M, N, K, W2 ? 2 : 1, c->gs.target_wgs);
   if ((size_t)pl.S * M * pl.ldp > c->plan.part_floats)
@@ -1244,7 +1231,7 @@ int warm_blas(msd_ctx* c) {
   std::vector<int> ms;
   if (rows >= BIG_CHUNK) ms.push_back(BIG_CHUNK);
   const int tail = rows % BIG_CHUNK;
-  if (tail >= BLAS_MIN_ROWS) ms.push_back(tail);
+  if (rows > BIG_MIN_ROWS && tail > CHUNK) ms.push_back(tail);
   const PackedLayer& p = c->players[0];
   for (int M : ms) {
     Parts pt;
@@ -1369,7 +1356,6 @@ int msd_create(const msd_model_desc* m, const msd_limits* lim, const msd_target_
     HIPC(c, hipMemsetAsync(c->tree_err, 0, sizeof(int) * lim->max_batch, c->st));
     HIPC(c, hipMemsetAsync(c->att_cnt, 0, sizeof(int) * c->plan.att_items, c->st));
     HIPC(c, hipMemsetAsync(c->att_place, 0, sizeof(int), c->st));
-    HIPC(c, hipMemsetAsync(c->gemm_zero, 0, sizeof(uint16_t) * gemm_dummy_elems(), c->st));
     launch_rope_table(c->rope, lim->max_seq, m->head_dim, (double)m->rope_theta, c->st);
     LAUNCHED(c);
     const int d = m->d_model, hd = m->head_dim, H = m->n_heads, KV = m->n_kv_heads;

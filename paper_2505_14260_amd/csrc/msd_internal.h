@@ -93,13 +93,6 @@ void launch_unpack(const uint16_t* src, int N, int K, uint16_t* dst, hipStream_t
 GemmPlan plan_gemm(int M, int N, int K, int nw, int target_wgs);
 // floats of partials for M rows (M <= 64 per launch)
 size_t gemm_part_floats(int M, int N, int K, int nw, int target_wgs);
-// Many-row GEMM: products of rows [0, M) into part [S][M][ldp] (same ldp and
-// W2 column offset as the thin plan; S K splits, part_cap floats available);
-// returns S.
-int launch_gemm_big(const uint16_t* X, int ldx, int M, const uint16_t* W, const uint16_t* W2,
-                    int N, int K, float* part, size_t part_cap, const uint16_t* dummy,
-                    hipStream_t st);
-size_t gemm_dummy_elems();
 // Diagnostic: reads spans * stream_span_bytes() bytes of buf with the weight
 // stream's access pattern on wgs workgroups (sink: wgs words, never written
 // for zero-filled buffers).
