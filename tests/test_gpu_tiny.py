@@ -90,10 +90,11 @@ def test_prefill_kv_and_first_token(setup):
 
 @pytest.mark.parametrize("n_visual", [256, 480, 1036])
 def test_prefill_many_rows_wide(n_visual):
-    """320-, 544- and 1100-row prompts through the many-row GEMM path (both
-    tile widths, K splits, an odd FFN tile count, a partial last K block,
-    tiles past N; 1100 rows = one 1024-row launch plus a 76-row one): every
-    layer's K/V, the first token and the draft cache against the oracle."""
+    """320-, 544- and 1100-row prompts through the rocBLAS path (single
+    hi+lo products of 640 and 1088 rows; 1100 rows = one 1024-row launch of
+    two products plus a 76-row one; an odd FFN tile count and a partial
+    last K block of the packed layout): every layer's K/V, the first token
+    and the draft cache against the oracle."""
     import dataclasses
     from paper_2505_14260_amd.msd import Engine
     wl = dataclasses.replace(WIDE, n_visual=n_visual)
