@@ -88,13 +88,13 @@ def test_prefill_kv_and_first_token(setup):
     assert ok, ("draft K", err)
 
 
-@pytest.mark.parametrize("n_visual", [256, 480, 1036])
+@pytest.mark.parametrize("n_visual", [136, 256, 480, 1036])
 def test_prefill_many_rows_wide(n_visual):
-    """320-, 544- and 1100-row prompts through the rocBLAS path (single
-    hi+lo products of 640 and 1088 rows; 1100 rows = one 1024-row launch of
-    two products plus a 76-row one; an odd FFN tile count and a partial
-    last K block of the packed layout): every layer's K/V, the first token
-    and the draft cache against the oracle."""
+    """200-, 320-, 544- and 1100-row prompts through the rocBLAS path (single
+    hi+lo products of 400, 640 and 1088 rows; 1100 rows = one 1024-row
+    launch of two products plus a 76-row one; an odd FFN tile count and a
+    partial last K block of the packed layout): every layer's K/V, the first
+    token and the draft cache against the oracle."""
     import dataclasses
     from paper_2505_14260_amd.msd import Engine
     wl = dataclasses.replace(WIDE, n_visual=n_visual)
