@@ -117,15 +117,19 @@ constexpr size_t BLAS_ONE_PRODUCT_BYTES = (size_t)192 << 20;
 // CHUNK rows or fewer takes the weight-streaming kernels).  Shorter passes
 // run as weight-streaming launches of CHUNK rows.  7B-shaped prompts: 128
 // rows 9.0 ms streamed against 10.0 ms on rocBLAS, 192 rows 13.5 against
-// 11.1 ms, 256 rows 17.9 against 12.5 ms.  The 244-row batch-4 verify stays
-// on the weight-streaming kernels, which beat the library's earlier
-// many-row kernel there.
+// 11.1 ms, 256 rows 17.9 against 12.5 ms.  Target tree passes take the
+// prompt threshold when their output, gate, up and down products can read
+// the caller's row-major matrices in place (msd_use_caller_weights): the
+// Qwen2.5-VL-7B-shaped batch-4 verify (244 rows), whose 64-row launches
+// stream every weight four times, 17.2 -> 12.4 ms; unpacking the
+// weights on every verify instead would cost more than it saves (17.9 ms).
 constexpr int BIG_MIN_ROWS = 256;
 constexpr int PROMPT_BIG_MIN_ROWS = 128;
 
-// Rows per GEMM launch for a pass over `rows` rows (causal: a prompt pass).
-int row_chunk(int rows, bool causal) {
-  return rows > (causal ? PROMPT_BIG_MIN_ROWS : BIG_MIN_ROWS) ? BIG_CHUNK : CHUNK;
+// Rows per GEMM launch for a pass over `rows` rows (causal: a prompt pass;
+// in_place: the target's row-major matrices are readable in place).
+int row_chunk(int rows, bool causal, bool in_place) {
+  return rows > (causal || in_place ? PROMPT_BIG_MIN_ROWS : BIG_MIN_ROWS) ? BIG_CHUNK : CHUNK;
 }
 
 // Bump allocator over the workspace (also used to size it).
@@ -652,7 +656,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
   const int rows = n_seq * nq;
   const int d = m.d_model, H = m.n_heads, KV = m.n_kv_heads, hd = m.head_dim, F = m.ffn_dim;
   const int nl = draft ? 1 : m.n_layers;
-  const int ch = row_chunk(rows, tree_R < 0);
+  const int ch = row_chunk(rows, tree_R < 0, c->caller_w && !draft && c->blas);
   c->wrm_src[0] = c->wrm_src[1] = nullptr;
   const int B = c->lim.max_batch, S = c->lim.max_seq;
   const size_t layer_kv = (size_t)B * KV * S * hd;
@@ -753,7 +757,7 @@ int forward_layers(msd_ctx* c, bool draft, int n_seq, int nq, int tree_R, int ma
 int draft_pass(msd_ctx* c, int n_seq, int nq, int tree_R, int max_ltot, const uint16_t* visual) {
   const int d = c->m.d_model;
   const int rows = n_seq * nq;
-  const int ch = row_chunk(rows, tree_R < 0);
+  const int ch = row_chunk(rows, tree_R < 0, false);
   Parts pt;
   for (int m0 = 0; m0 < rows; m0 += ch) {
     const int mc = std::min(ch, rows - m0);

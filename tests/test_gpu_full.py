@@ -61,7 +61,7 @@ def bits64(t):
 class Case:
     """Engine + oracle models + per-sequence synthetic states of one workload."""
 
-    def __init__(self, wl, lengths, cycles=2):
+    def __init__(self, wl, lengths, cycles=2, caller_weights=False):
         from paper_2505_14260_amd.msd import Engine, msd_set_state, make_static_spec, \
             make_dynamic_spec
         t0 = time.perf_counter()
@@ -74,6 +74,8 @@ class Case:
         self.max_seq = (max(lengths) + cycles * T + 255) // 256 * 256
         self.eng = Engine(dims, self.w, self.dr, max_batch=len(lengths), max_seq=self.max_seq,
                           max_tree=64, max_prompt=wl.prompt_len)
+        if caller_weights:
+            self.eng.use_caller_weights(True)
         self.m = O.Models(dims, self.w, self.dr)
         if wl.tree.kind == "static":
             self.arrays = synth.static_tree_arrays(wl.tree.paths)
@@ -372,13 +374,16 @@ def test_llava7b_long_prefix_dynamic_cycle():
 
 
 @pytest.mark.timeout(300)
-def test_qwen7b_gqa_batch4_ragged():
+@pytest.mark.parametrize("caller_weights", [False, True])
+def test_qwen7b_gqa_batch4_ragged(caller_weights):
     """Qwen-shaped GQA (28 query / 4 KV heads, vocab 152064), four sequences
-    at different lengths, dynamic 60-node trees, different accepted depths."""
+    at different lengths, dynamic 60-node trees, different accepted depths.
+    The 244-row verify runs as 64-row weight-streaming launches, or with
+    msd_use_caller_weights as rocBLAS products on the row-major weights."""
     n = QWEN7B.prompt_len
     lengths = [n, n - 37, n + 5, n - 100]
-    log(f"case: full qwen2.5-vl-7b-shaped, batch 4, L={lengths}")
-    c = Case(QWEN7B, lengths, cycles=2)
+    log(f"case: full qwen2.5-vl-7b-shaped, batch 4, L={lengths}, caller weights {caller_weights}")
+    c = Case(QWEN7B, lengths, cycles=2, caller_weights=caller_weights)
     try:
         c.cycle([0, 1, 3, 6], "qwen")
         c.sample_cycle(0.8, 99, "qwen sampled")
