@@ -517,6 +517,12 @@ struct RowMajorW {
 // 46.8 -> 43.2 ms).  At 1024 rows it lost: 7B-shaped gate+up (180 MB of
 // results) over 3,136 rows 111.7 -> 123.4 ms, and every Qwen2.5-VL-7B-shaped
 // product, 1,152 rows 49.1 -> 52.7 ms even with the pair left out.
+// A one-product launch with few output tiles is split along K into ns
+// slices, one strided batch each (2 ns partials per row: the hi rows of
+// every slice, then the lo rows), so that the batches fill the GPU.
+#ifndef MAX_K_SLICES
+#define MAX_K_SLICES 8
+#endif
 int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
               const uint16_t* W2, int N, int K, int ldp, int off2, const RowMajorW* rm,
               Parts* out) {
@@ -525,6 +531,17 @@ int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
   const size_t rows = one_product ? 2 * (size_t)M : (size_t)M;
   if ((!rm && (size_t)N * K > c->plan.wrm_elems) || rows * ldp > c->plan.part_floats)
     return fail(c, MSD_ERR_INVALID_ARG, "internal: prompt GEMM exceeds its buffers");
+  // K slices: output tiles counted at 256 x 256; each slice at least 1024
+  // columns, a multiple of 8 (16-byte aligned slice starts), within the buffer
+  int ns = 1;
+  if (one_product) {
+    const int tiles = (int)((rows + 255) / 256) * ((N + 255) / 256);
+    ns = std::max(1, std::min({MAX_K_SLICES, 256 / std::max(tiles, 1), K / 1024}));
+    while (ns > 1 && (K % ns != 0 || (K / ns) % 8 != 0 ||
+                      rows * ldp * ns > c->plan.part_floats))
+      --ns;
+  }
+  const int nw = W2 ? 2 : 1, npad = off2;
   const float one = 1.f, zero = 0.f;
   for (int w = 0; w < (W2 ? 2 : 1); ++w) {
     const uint16_t* A = nullptr;
@@ -541,6 +558,19 @@ int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
       A = wrm;
     }
     float* C = c->part + (size_t)w * off2;
+    if (ns > 1) {
+      // slice s of weight w at column (s nw + w) npad of rows of nw ns npad
+      const int ks = K / ns, ldc = nw * ns * npad;
+      const rocblas_status st = rocblas_gemm_strided_batched_ex(
+          c->blas, rocblas_operation_transpose, rocblas_operation_none, N, (int)rows, ks, &one,
+          A, rocblas_datatype_bf16_r, K, ks, X, rocblas_datatype_bf16_r, K, ks, &zero, C,
+          rocblas_datatype_f32_r, ldc, (rocblas_stride)nw * npad, C, rocblas_datatype_f32_r, ldc,
+          (rocblas_stride)nw * npad, ns, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+      if (st != rocblas_status_success)
+        return fail(c, MSD_ERR_HIP,
+                    std::string("rocblas_gemm_strided_batched_ex: ") + rocblas_status_to_string(st));
+      continue;
+    }
     for (int h = 0; h < (one_product ? 1 : 2); ++h) {
       const rocblas_status st = rocblas_gemm_ex(
           c->blas, rocblas_operation_transpose, rocblas_operation_none, N, (int)rows, K, &one, A,
@@ -551,8 +581,11 @@ int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
         return fail(c, MSD_ERR_HIP, std::string("rocblas_gemm_ex: ") + rocblas_status_to_string(st));
     }
   }
-  *out = one_product ? Parts{c->part, 2, (size_t)ldp, 2 * ldp, off2}
-                     : Parts{c->part, 1, (size_t)M * ldp, ldp, off2};
+  if (ns > 1)
+    *out = Parts{c->part, 2 * ns, (size_t)nw * npad, 2 * nw * ns * npad, npad};
+  else
+    *out = one_product ? Parts{c->part, 2, (size_t)ldp, 2 * ldp, off2}
+                       : Parts{c->part, 1, (size_t)M * ldp, ldp, off2};
   return MSD_OK;
 }
 
