@@ -235,6 +235,54 @@ def test_wide_vocab_lm_head_full_k():
         eng.close()
 
 
+@pytest.mark.timeout(240)
+def test_prefill_k_sliced_products_max_width():
+    """A 224-row prompt at d_model 8192 (one layer, FFN 2048): its rocBLAS
+    products take one GEMM over the 448 hi and lo rows, split along K into
+    strided batches (the gate+up pair into eight slices, q|k|v and down into
+    two, the output into four), on the uploaded row-major weights.  Layer
+    0's K/V, the first token and the draft cache (whose text rows carry the
+    whole target layer) against the oracle, and bit for bit against an
+    engine that unpacks the weights instead."""
+    import dataclasses
+    from paper_2505_14260_amd.msd import Engine
+    wl = dataclasses.replace(MAXW, n_visual=200)
+    dims = wl.dims
+    n = wl.prompt_len
+    print(f"case: {wl.name} prefill of {n} rows, K-sliced rocBLAS products", flush=True)
+    w = synth.make_target_weights(dims, wl.seed)
+    dr = synth.make_draft_weights(dims, w, wl.seed, wl.draft_fc_mode)
+    prompt = synth.make_prompt(wl)
+    m = O.Models(dims, w, dr)
+    max_seq = 512
+    st, f_ref, _, logits = O.prefill(m, *prompt, max_slots=max_seq)
+    O.draft_catch_up(m, st)
+    engines = [Engine(dims, w, dr, max_batch=1, max_seq=max_seq, max_tree=64, max_prompt=n)
+               for _ in range(2)]
+    try:
+        engines[1].use_caller_weights(True)
+        firsts = [e.prefill(0, *prompt) for e in engines]
+        torch.cuda.synchronize()
+        assert argmax_ok(firsts[1], logits[-1]), (firsts, f_ref)
+        assert firsts[0] == firsts[1]
+        views = [e.kv_views() for e in engines]
+        tk, tv, dk, _ = views[1]
+        kg = bits_to_f64(tk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        vg = bits_to_f64(tv[0, 0, :, :, :n].permute(2, 0, 1).reshape(n, -1))
+        ok, ek = row_close(kg, st.kv.k[0, :n].reshape(n, -1))
+        ok2, ev = row_close(vg, st.kv.v[0, :n].reshape(n, -1))
+        assert ok and ok2, (ek, ev)
+        dkg = bits_to_f64(dk[0, 0, :, :n, :].permute(1, 0, 2).reshape(n, -1))
+        ok3, ed = row_close(dkg, st.dkv.k[0, :n].reshape(n, -1))
+        assert ok3, ed
+        for a_, b_ in zip(views[0], views[1]):
+            assert torch.equal(a_, b_)
+        print(f"K-sliced prefill: K/V rel err {ek:.2e} / {ev:.2e}, draft K {ed:.2e}")
+    finally:
+        for e in engines:
+            e.close()
+
+
 def test_max_width_model():
     """d_model 8192, the library's limit (whole-row kernels at two 16-byte
     units per thread), with 8-way GQA: the prompt forward's K/V, first token
