@@ -106,10 +106,12 @@ constexpr int GEMM_WGS = 256;
 constexpr int CHUNK = 64;         // rows per weight-streaming GEMM launch
 constexpr int BIG_CHUNK = 1024;   // rows per many-row (rocBLAS) GEMM launch
 constexpr size_t BLAS_WS_BYTES = (size_t)32 << 20;  // rocBLAS's workspace
-// rocBLAS prompt products of fewer than BIG_CHUNK rows whose hi and lo
-// results together take at most this many bytes run as one product over 2M
-// interleaved rows (see blas_gemm)
+// rocBLAS products whose hi and lo results together take at most this many
+// bytes (fewer than BIG_CHUNK rows), or BLAS_ONE_PRODUCT_FULL_BYTES (launches
+// of BIG_CHUNK rows), run as one product over 2M interleaved rows (see
+// blas_gemm)
 constexpr size_t BLAS_ONE_PRODUCT_BYTES = (size_t)192 << 20;
+constexpr size_t BLAS_ONE_PRODUCT_FULL_BYTES = (size_t)128 << 20;
 // Tree passes (verify, draft) over more rows than BIG_MIN_ROWS, and causal
 // passes (prompts, training sequences) over more than PROMPT_BIG_MIN_ROWS,
 // run their GEMMs on rocBLAS in launches of up to BIG_CHUNK rows (bf16
@@ -511,12 +513,14 @@ struct RowMajorW {
 //  - two products over the strided views X and X + K, the second adding to
 //    the first: C[m][n], one partial.
 // Either way the sum is hi + lo rounded once.  The one-product form runs
-// passes of fewer than BIG_CHUNK rows with results of at most
+// launches of fewer than BIG_CHUNK rows with results of at most
 // BLAS_ONE_PRODUCT_BYTES: its doubled row count tiles better (prefills of
 // 640 rows, LLaVA-1.5-7B-shaped, 25.3 -> 20.8 ms; 704 rows, 13B-shaped,
-// 46.8 -> 43.2 ms).  At 1024 rows it lost: 7B-shaped gate+up (180 MB of
-// results) over 3,136 rows 111.7 -> 123.4 ms, and every Qwen2.5-VL-7B-shaped
-// product, 1,152 rows 49.1 -> 52.7 ms even with the pair left out.
+// 46.8 -> 43.2 ms).  Full BIG_CHUNK launches take it for results of at most
+// BLAS_ONE_PRODUCT_FULL_BYTES, with the K slices below: 3,136 rows 7B-shaped
+// 107.9 -> 100.8 ms, 1,152 rows Qwen2.5-VL-7B-shaped 44.2 -> 37.8 ms.  Their
+// SwiGLU pairs (180 and 310 MB of results) keep two products: with the pair
+// included, before the K slices, 3,136 rows took 123.4 instead of 111.7 ms.
 // A one-product launch with few output tiles is split along K into ns
 // slices, one strided batch each (2 ns partials per row: the hi rows of
 // every slice, then the lo rows), so that the batches fill the GPU.
@@ -526,8 +530,9 @@ struct RowMajorW {
 int blas_gemm(msd_ctx* c, const uint16_t* X, int ldx, int M, const uint16_t* W,
               const uint16_t* W2, int N, int K, int ldp, int off2, const RowMajorW* rm,
               Parts* out) {
-  const bool one_product = ldx == 2 * K && M < BIG_CHUNK &&
-                           2 * (size_t)M * ldp * sizeof(float) <= BLAS_ONE_PRODUCT_BYTES;
+  const bool one_product =
+      ldx == 2 * K && 2 * (size_t)M * ldp * sizeof(float) <=
+                          (M < BIG_CHUNK ? BLAS_ONE_PRODUCT_BYTES : BLAS_ONE_PRODUCT_FULL_BYTES);
   const size_t rows = one_product ? 2 * (size_t)M : (size_t)M;
   if ((!rm && (size_t)N * K > c->plan.wrm_elems) || rows * ldp > c->plan.part_floats)
     return fail(c, MSD_ERR_INVALID_ARG, "internal: prompt GEMM exceeds its buffers");
